@@ -1,0 +1,23 @@
+"""Slow, plain fp64 CPU reference of the large-sparse-target output-layer step.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call, link or
+execute anything in this package: only the test suite, the smoke check of the
+entry module and the CPU-baseline leg of the benchmark use it.  It shares no
+code with the GPU library; both sides receive their inputs from the `synth`
+generators, which hold none of the method's arithmetic.
+
+Modules
+  explicit  the plain definition: W kept explicit, O(Dd) per example
+            (sections 2.3, 3.1 and 3.2 of the paper, and its loss-family
+            extension in section 3.6 for the spherical softmax).
+  factored  the paper's factored algorithm in fp64 (Algorithm 1, the minibatch
+            algorithm of Appendix A, the pristine restore of Appendix C), used
+            only to check the paper's identities against the explicit
+            definition: W = VU, Q = W^T W, U (U^{-T})^T = I.
+
+Pin status (what fixes each function other than itself) is listed in each
+function's docstring; the only function without a pin by the paper is the
+minibatch form of the spherical-softmax factored step, which is pinned by the
+explicit definition and by finite differences instead.
+"""
+from . import explicit, factored  # noqa: F401

@@ -1,0 +1,142 @@
+"""Explicit-W fp64 reference: the plain definition of the output-layer step.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+Notation follows the paper (section 2.1): W is the D x d output weight matrix,
+h a d-dimensional last hidden representation, o = W h the D-dimensional output
+and y the K-sparse target.  A minibatch stacks m examples as the columns of H
+(d x m) and Y (D x m) (Appendix A).  The arrays handed in are row-major with
+one example per row (H_rows = H^T), which is the same memory as the paper's
+column layout; this module transposes them back to the paper's notation.
+
+Every function widens its fp32 inputs to fp64 exactly and computes the naive
+O(Dd)-per-example quantities the factored method must reproduce exactly
+(section 3, and the experimental check of section 4 that VU equals the
+explicitly trained W).
+
+Readings of the paper taken here:
+  * learning rate: W <- W - lr * dL/dW with L the SUM of the per-example
+    losses of the minibatch, so squared error uses 2*lr (section 3.2 and the
+    minibatch algorithm of Appendix A, whose L = Tr M is a sum);
+  * a target is a list of (index, value) pairs (section 2.1); index -1 marks an
+    unused slot and a repeated index adds its values;
+  * spherical softmax: L_i = -log((o_c^2 + eps) / sum_k (o_k^2 + eps)) with one
+    target class c per example, eps = 1e-3; this is a member of the family of
+    section 3.6 (a function of o_c and ||o||^2 only).
+"""
+from __future__ import annotations
+
+from typing import Iterable, Iterator, Tuple
+
+import numpy as np
+
+
+def widen(x) -> np.ndarray:
+    """fp32 (or any) array -> fp64 copy; exact for fp32 inputs."""
+    return np.array(x, dtype=np.float64, copy=True)
+
+
+def dense_targets(D: int, idx: np.ndarray, val: np.ndarray, one_hot: bool = False) -> np.ndarray:
+    """Dense Y (D x m) from the (index, value) pairs of each example (section 2.1).
+
+    Column i is example i's target vector: y[idx[i,k]] += val[i,k] for every
+    slot k with idx[i,k] >= 0 (a repeated index adds up).  With one_hot the
+    value of each pair is taken as 1 (classification targets).
+    Raises IndexError for an index outside [-1, D).
+    """
+    idx = np.asarray(idx)
+    m, K = idx.shape
+    Y = np.zeros((D, m), dtype=np.float64)
+    for i in range(m):
+        for k in range(K):
+            r = int(idx[i, k])
+            if r == -1:
+                continue
+            if r < -1 or r >= D:
+                raise IndexError(f"target index {r} outside [-1, {D})")
+            Y[r, i] += 1.0 if one_hot else float(val[i, k])
+    return Y
+
+
+def touched_rows(idx: np.ndarray) -> np.ndarray:
+    """Sorted distinct target indices of a minibatch: the rows of W that the
+    sparse part of the update visits (section 3.2, the O(Kd) update of V)."""
+    idx = np.asarray(idx).ravel()
+    return np.unique(idx[idx >= 0]).astype(np.int64)
+
+
+def target_gram(D: int, idx: np.ndarray, val: np.ndarray, one_hot: bool = False) -> np.ndarray:
+    """Y^T Y (m x m), the target term of M in the minibatch algorithm (Appendix A, step 5)."""
+    Y = dense_targets(D, idx, val, one_hot)
+    return Y.T @ Y
+
+
+def squared_error_step(W, H_rows, idx, val, lr: float):
+    """One minibatch step of the naive linear output + squared error layer.
+
+    Section 2.3 / 3.1 / 3.2: o = W h, L = ||o - y||^2, grad_h = 2 W^T (o - y),
+    W_new = W - 2 lr (o - y) h^T, summed over the m examples.
+
+    Returns (loss[m], grad_H[m x d] (row i = grad wrt h_i), W_new[D x d]), fp64.
+    """
+    W = widen(W)
+    D = W.shape[0]
+    H = widen(H_rows).T                     # d x m, columns are examples
+    Y = dense_targets(D, idx, val)          # D x m
+    O = W @ H                               # outputs, D x m   -- O(Dd) per example
+    R = O - Y                               # residuals
+    loss = np.einsum("jm,jm->m", R, R)      # ||o_i - y_i||^2
+    grad_H = 2.0 * (W.T @ R)                # d x m
+    grad_W = 2.0 * (R @ H.T)                # dL/dW = sum_i 2 (o_i - y_i) h_i^T
+    W_new = W - lr * grad_W
+    return loss, grad_H.T.copy(), W_new
+
+
+def spherical_softmax_step(W, H_rows, idx, lr: float, eps: float = 1e-3):
+    """One minibatch step of the naive spherical-softmax output layer.
+
+    Section 3.6 loss family, in the form
+        L_i = -log((o_c^2 + eps) / sum_j (o_j^2 + eps)),   o = W h_i,
+    with c = idx[i, 0] the target class.  Its output gradient is
+        dL_i/do = 2 o / S_i - 2 o_c e_c / (o_c^2 + eps),   S_i = sum_j (o_j^2 + eps),
+    back-propagated as grad_h = W^T dL/do and applied as W_new = W - lr dL/dW.
+
+    Returns (loss[m], grad_H[m x d], W_new[D x d]), fp64.
+    """
+    W = widen(W)
+    D = W.shape[0]
+    H = widen(H_rows).T                     # d x m
+    m = H.shape[1]
+    c = np.asarray(idx)[:, 0].astype(np.int64)
+    if np.any(c < 0) or np.any(c >= D):
+        raise IndexError("spherical softmax needs one target class in [0, D) per example")
+    O = W @ H                               # D x m
+    cols = np.arange(m)
+    S = np.sum(O * O + eps, axis=0)         # sum_j (o_j^2 + eps)
+    oc = O[c, cols]
+    loss = -np.log((oc * oc + eps) / S)
+    G = 2.0 * O / S                         # dL/dO, dense part
+    G[c, cols] -= 2.0 * oc / (oc * oc + eps)  # sparse part at the target classes
+    grad_H = W.T @ G
+    W_new = W - lr * (G @ H.T)
+    return loss, grad_H.T.copy(), W_new
+
+
+def step(W, H_rows, idx, val, lr: float, loss_kind: str = "squared", eps: float = 1e-3):
+    """Dispatch on the loss: 'squared' or 'spherical'."""
+    if loss_kind == "squared":
+        return squared_error_step(W, H_rows, idx, val, lr)
+    if loss_kind == "spherical":
+        return spherical_softmax_step(W, H_rows, idx, lr, eps)
+    raise ValueError(f"unknown loss {loss_kind!r}")
+
+
+def trajectory(
+    W0, batches: Iterable[Tuple[np.ndarray, np.ndarray, np.ndarray]], lr: float,
+    loss_kind: str = "squared", eps: float = 1e-3,
+) -> Iterator[Tuple[np.ndarray, np.ndarray, np.ndarray]]:
+    """Run consecutive steps from W0; yields (loss, grad_H, W_after) per step."""
+    W = widen(W0)
+    for H, idx, val in batches:
+        loss, grad_H, W = step(W, H, idx, val, lr, loss_kind, eps)
+        yield loss, grad_H, W
