@@ -1,0 +1,248 @@
+"""Throughput of the exact factored output-layer step on one MI355X.
+
+Default workload: D = 200,000 outputs, d = 500 hidden units, minibatches of
+m = 128 examples with K = 10 (index, value) targets each, squared error,
+lr = 1e-3 (the paper's typical sizes).  A step is one call of lst_step: loss,
+grad_H and the exact update of W = V U, Q and U^{-T}.  Inputs are synthetic,
+seeded and resident in HBM before timing: a pool of 16 minibatches cycled
+through.
+
+Printed on stdout (one JSON line): examples/s over exactly --steps timed
+steps, the roofline of the dominant kernel (per-phase times come from a
+second, event-profiled pass over the same steps), the in-library naive
+explicit-W step and its measured speedup, and the fp64 CPU oracle timed on a
+bounded sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+REPO = os.path.dirname(os.path.abspath(__file__))
+if REPO not in sys.path:
+    sys.path.insert(0, REPO)
+
+METRIC = "examples/sec, exact sparse-target step D=200k d=500 m=128; % MFMA/HBM peak"
+PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix
+PEAK_FP64_TFLOPS = 78.6         # MI355X fp64 vector
+PEAK_HBM_GBS = 8000.0           # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def phase_work(name, cfg, u, nnz):
+    """(bound, algorithmic amount per launch, unit) of one phase of the step."""
+    D, d, m, K = cfg.D, cfg.d, cfg.m, cfg.K
+    if name == "gather":
+        return "hbm", float(u * d * 4), "bytes"           # each distinct target row of V read once
+    if name == "scatter":
+        return "hbm", float(2 * u * d * 4), "bytes"       # each distinct row read and written once
+    if name == "gemm_stack":
+        return "mfma", 2.0 * m * d * (3 * d + m), "flop"  # [Q; U; U^-T; H^T] H
+    if name == "gemm_yhat":
+        return "mfma", 2.0 * m * d * d, "flop"            # U^T (V^T Y)
+    if name == "gemm_m":
+        return "mfma", 2.0 * m * (2 * m) * d, "flop"      # H^T H^, H^T Y^
+    if name == "gemm_xt":
+        return "mfma", 2.0 * 2 * m * m * d, "flop"        # S^-1 P^T, N H^T
+    if name == "gemm_update":
+        return "mfma", 2.0 * d * d * m * 2 + 2.0 * (d * (d + 1) / 2) * 2 * m, "flop"
+    if name == "inverse":
+        return "alu", 2.0 * m ** 3, "flop"                # Gauss-Jordan, fp64
+    return None, 0.0, None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="c2")
+    ap.add_argument("--naive-steps", type=int, default=10)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-naive", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the step has no "
+              "multi-GPU path in this build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_1412_7091_amd as lst
+    from synth import Workload, get_config
+
+    if not torch.cuda.is_available():
+        log("no GPU visible")
+        sys.exit(1)
+    lst.load_library()
+    cfg = get_config(args.config)
+    wl = Workload(cfg)
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    V0 = wl.init_V()
+    V0_t = torch.from_numpy(V0).to(dev)
+    pool = []
+    for s in range(16):
+        H, idx, val = wl.batch(s)
+        pool.append(tuple(torch.from_numpy(x).to(dev) for x in (H, idx, val)))
+    loss_t = torch.empty(cfg.m, dtype=torch.float32, device=dev)
+    grad_t = torch.empty((cfg.m, cfg.d), dtype=torch.float32, device=dev)
+    log(f"workload {cfg.name}: D={cfg.D} d={cfg.d} m={cfg.m} K={cfg.K} loss={cfg.loss} "
+        f"(inputs ready in {time.time() - t0:.1f}s)")
+
+    layer = lst.FactoredOutputLayer(V0_t, loss=cfg.loss, sph_eps=cfg.sph_eps, m_max=cfg.m,
+                                    K_max=cfg.K)
+
+    def run(n, offset=0):
+        for s in range(n):
+            H, idx, val = pool[(s + offset) % len(pool)]
+            layer.step(H, idx, val, cfg.lr, out=(loss_t, grad_t))
+
+    run(args.warmup)
+    torch.cuda.synchronize()
+    if layer.sync() != 0:
+        log("device error during warmup")
+        sys.exit(1)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    run(args.steps, args.warmup)
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop)
+    code = layer.sync()
+    if code != 0:
+        log(f"device error in timed steps: {lst.lst_strerror(code)}")
+        sys.exit(1)
+    ms_per_step = ms / args.steps
+    value = cfg.m * args.steps / (ms / 1e3)
+    log(f"factored: {ms_per_step * 1e3:.1f} us/step, {value:.4g} examples/s")
+
+    # profiled pass: per-phase durations from HIP events on the library's stream
+    layer.profile(True)
+    run(args.steps, args.warmup)
+    phases, nsteps = layer.profile_read()
+    layer.profile(False)
+    st = layer.stats()
+    u, nnz = st.last_unique, st.last_nnz
+    kernels = {}
+    best = None
+    for name, tot in phases.items():
+        avg_us = 1e3 * tot / max(nsteps, 1)
+        bound, amount, unit = phase_work(name, cfg, u, nnz)
+        entry = {"avg_us": round(avg_us, 3)}
+        if bound is not None and avg_us > 0:
+            if bound == "hbm":
+                ach = amount / (avg_us * 1e-6) / 1e9
+                peak, punit = PEAK_HBM_GBS, "GB/s"
+            elif bound == "mfma":
+                ach = amount / (avg_us * 1e-6) / 1e12
+                peak, punit = PEAK_FP32_MFMA_TFLOPS, "TFLOP/s"
+            else:
+                ach = amount / (avg_us * 1e-6) / 1e12
+                peak, punit = PEAK_FP64_TFLOPS, "TFLOP/s"
+            entry.update(bound=bound, achieved=round(ach, 4), peak=peak, unit=punit,
+                         frac=round(ach / peak, 5))
+        kernels[name] = entry
+        if best is None or avg_us > kernels[best]["avg_us"]:
+            best = name
+    log("per-phase us: " + ", ".join(f"{k}={v['avg_us']:.1f}" for k, v in kernels.items()))
+    dom = kernels[best]
+    roofline = {"kernel": best, "bound": dom.get("bound"), "achieved": dom.get("achieved"),
+                "peak": dom.get("peak"), "unit": dom.get("unit"), "frac": dom.get("frac"),
+                "traffic": None}
+    layer.close()
+    del layer
+
+    naive = None
+    if not args.no_naive:
+        nl = lst.NaiveOutputLayer(V0_t, loss=cfg.loss, sph_eps=cfg.sph_eps, m_max=cfg.m,
+                                  K_max=cfg.K)
+        for s in range(2):
+            H, idx, val = pool[s]
+            nl.step(H, idx, val, cfg.lr, out=(loss_t, grad_t))
+        torch.cuda.synchronize()
+        start.record()
+        for s in range(args.naive_steps):
+            H, idx, val = pool[s % len(pool)]
+            nl.step(H, idx, val, cfg.lr, out=(loss_t, grad_t))
+        stop.record()
+        torch.cuda.synchronize()
+        nms = start.elapsed_time(stop) / args.naive_steps
+        if nl.sync() != 0:
+            log("device error in naive steps")
+            sys.exit(1)
+        nl.close()
+        naive = {"ms_per_step": round(nms, 4), "speedup": round(nms / ms_per_step, 2),
+                 "D_over_4d": round(cfg.D / (4 * cfg.d), 2), "steps": args.naive_steps}
+        log(f"naive: {nms:.3f} ms/step, speedup {nms / ms_per_step:.1f} (D/4d = {cfg.D / (4 * cfg.d):.0f})")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, wl, V0, args.cpu_seconds)
+        log(f"cpu oracle: {cpu['value']:.4g} examples/s on {cpu['cores']} threads")
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "examples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "D": cfg.D, "d": cfg.d, "m": cfg.m, "K": cfg.K,
+                   "loss": cfg.loss, "lr": cfg.lr, "global_batch": cfg.m,
+                   "parallelism": "none"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "naive": naive,
+        "kernels": kernels,
+        "last_step": {"distinct_rows": u, "pairs": nnz},
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(cfg, wl, V0, seconds):
+    """The fp64 oracle (explicit W, O(D d) per example) on a bounded prefix of the same steps."""
+    from oracle import explicit
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()
+                       if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl missing
+        threads = len(os.sched_getaffinity(0))
+    W = V0.astype(np.float64)
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        H, idx, val = wl.batch(n)
+        _, _, W = explicit.step(W, H, idx, val, cfg.lr, cfg.loss, cfg.sph_eps)
+        n += 1
+        el = time.perf_counter() - t0
+        if (el >= seconds and n >= 2) or n >= 1000:
+            break
+    return {"value": round(cfg.m * n / el, 3), "unit": "examples/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{n} consecutive steps of {cfg.name} from its initial W, fp64 numpy, "
+                      f"{el:.1f}s wall"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,204 @@
+/*
+ * lst.h -- C ABI of the exact large-sparse-target output-layer step on MI355X.
+ *
+ * The method (Vincent, de Brebisson, Bouthillier, "Efficient Exact Gradient
+ * Update for training Deep Networks with Very Large Sparse Targets"):
+ * a linear output layer o = W h with W of size D x d (D very large, d small),
+ * trained against K-sparse targets y, is stepped WITHOUT forming the
+ * D-dimensional output.  W is kept factored as W = V U (V: D x d, U: d x d,
+ * section 3.2) together with Q = W^T W and U^{-T} (section 3.3), so that each
+ * minibatch costs O(m d^2 + m^2 d + m^3) plus O(m K d) for the sparse rows of V
+ * (minibatch algorithm, Appendix A), instead of O(m D d).
+ *
+ * Conventions shared by every entry point
+ *   - All matrices are float32, row-major, densely packed (leading dimension =
+ *     number of columns).  Indices are int32.
+ *   - H is m x d: row i is the last hidden representation h_i of example i
+ *     (the paper stores it as the i-th column of a d x m matrix; same bytes).
+ *   - A target is given as K (index, value) pairs per example (section 2.1):
+ *     Y_idx and Y_val are m x K; index -1 marks an unused slot (its value is
+ *     ignored); an index that repeats inside one example adds its values.
+ *   - Pointers documented "device" must be device memory of the GPU that was
+ *     current when the state was created; "host" pointers are host memory.
+ *   - Every call is asynchronous on the HIP stream given at creation, unless
+ *     documented otherwise.  Caller-owned buffers must stay valid until that
+ *     stream has executed the work.
+ *   - Argument errors detected on the host are returned immediately and leave
+ *     the state untouched.  Errors only the device can see (a target index
+ *     outside [-1, D), a singular Woodbury matrix, a non-finite loss) are
+ *     recorded in a sticky device flag: the step that raised it still writes
+ *     loss and grad_H but skips every update of the state, and so does every
+ *     later step until lst_sync() reports the error and clears the flag.
+ *   - A state is not thread-safe; distinct states are independent.
+ */
+#ifndef LST_H
+#define LST_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+enum {
+  LST_OK = 0,
+  LST_EINVAL = -1,      /* bad argument (null pointer, size, learning rate ...)   */
+  LST_EINDEX = -2,      /* a target index outside [-1, D) (or -1 with the
+                           spherical loss, which needs one class per example)    */
+  LST_ESINGULAR = -3,   /* the m x m Woodbury matrix H^T H - A^{-1}/lr is
+                           singular to working precision                          */
+  LST_ENOMEM = -4,      /* device allocation failed                               */
+  LST_EHIP = -5,        /* a HIP runtime call failed                              */
+  LST_ENONFINITE = -6,  /* the loss of the minibatch is not finite                */
+  LST_ESTATE = -7       /* call not valid for this kind of state                  */
+};
+
+/* Loss functions (sections 3.1 and 3.6). */
+enum {
+  LST_LOSS_SQUARED = 0,   /* L_i = ||W h_i - y_i||^2                                    */
+  LST_LOSS_SPHERICAL = 1  /* L_i = -log((o_c^2 + eps) / sum_j (o_j^2 + eps)), o = W h_i,
+                             c = Y_idx[i][0] the target class; requires K == 1 and
+                             ignores Y_val                                           */
+};
+
+typedef struct lst_config {
+  int32_t loss;      /* LST_LOSS_SQUARED or LST_LOSS_SPHERICAL                         */
+  float sph_eps;     /* eps of the spherical softmax (> 0); unused for squared error   */
+  int32_t m_max;     /* largest minibatch any lst_step call will pass (1..4096)        */
+  int32_t K_max;     /* largest K any lst_step call will pass (1..1024); m_max*K_max
+                        must not exceed 16384 (the target pairs of one step are
+                        ordered in one workgroup's LDS)                                */
+  float cond_max;    /* drift control (Appendix C, pristine restore): after a step, if
+                        ||U||_F * ||U^{-T}||_F > cond_max * d, set V <- V U, U <- I,
+                        U^{-T} <- I (W and Q unchanged).  0 disables the check.      */
+} lst_config;
+
+typedef struct lst_state lst_state;
+
+/* Statistics of a state (host copy; lst_stats synchronises the stream). */
+typedef struct lst_stats_t {
+  int64_t steps;           /* lst_step calls that were enqueued                        */
+  int64_t restores;        /* pristine restores performed by drift control             */
+  int32_t last_unique;     /* distinct target rows of the last factored step           */
+  int32_t last_nnz;        /* valid (index, value) pairs of the last factored step     */
+} lst_stats_t;
+
+/*
+ * lst_init -- create the factored state of section 3.2 / Appendix A.
+ *   out   (host)   receives the new state; unchanged on error.
+ *   D, d           output dimension (rows of W) and hidden size, D >= 1, 1 <= d <= 4096.
+ *   V     (device) D x d initial V; copied, the caller keeps ownership.
+ *   U     (device) d x d initial U, or NULL for the identity (the paper's
+ *                  initialisation: V = W0, U = I).  Must be invertible.
+ *   cfg   (host)   configuration, copied.
+ *   hip_stream     hipStream_t every later call of this state is ordered on
+ *                  (NULL = the default stream).
+ * Computes U^{-T} (the identity when U is NULL) and Q = (V U)^T (V U).
+ * Synchronous: returns after the state is ready.
+ */
+int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float* U,
+             const lst_config* cfg, void* hip_stream);
+
+/*
+ * lst_step -- one exact minibatch step (Appendix A, steps 1-10; for the
+ * spherical softmax the same steps with the per-example loss derivatives).
+ *   m, K            minibatch size (1..m_max) and pairs per example (1..K_max).
+ *   H      (device) m x d hidden representations.
+ *   Y_idx  (device) m x K target indices in [-1, D).
+ *   Y_val  (device) m x K target values (ignored for the spherical loss).
+ *   lr              learning rate eta > 0, finite.  The update is
+ *                   W <- W - lr * dL/dW with L the SUM of the m per-example
+ *                   losses (squared error: W <- W - 2 lr (W H - Y) H^T).
+ *   loss   (device) m floats: per-example loss L_i.
+ *   grad_H (device) m x d: row i = dL/dh_i (no 1/m factor).
+ * Never forms W H.  State is updated in place unless the sticky error flag is set.
+ */
+int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* Y_idx,
+             const float* Y_val, float lr, float* loss, float* grad_H);
+
+/*
+ * lst_materialize_W -- debug: W = V U into W (device, D x d).  O(D d^2).
+ * For a naive state, copies its explicit W.
+ */
+int lst_materialize_W(lst_state* s, float* W);
+
+/*
+ * lst_get_state -- debug: copy Q, U and U^{-T} (each d x d, device; any may be
+ * NULL) of a factored state.
+ */
+int lst_get_state(lst_state* s, float* Q, float* U, float* UinvT);
+
+/* lst_get_V -- debug: copy V (device, D x d) of a factored state. */
+int lst_get_V(lst_state* s, float* V);
+
+/*
+ * lst_touched_rows -- debug: the distinct target rows of the last factored
+ * step in ascending order (the rows of V that step 9 of Appendix A updates).
+ *   rows   (host) capacity m*K ints; receives the rows.
+ *   count  (host) receives how many were written.
+ * Synchronises the stream.
+ */
+int lst_touched_rows(lst_state* s, int32_t* rows, int32_t capacity, int32_t* count);
+
+/*
+ * lst_restore -- Appendix C pristine restore now: V <- V U, U <- I, U^{-T} <- I.
+ * W = V U and Q are unchanged (up to rounding of V U).
+ */
+int lst_restore(lst_state* s);
+
+/*
+ * lst_naive_init -- explicit-W baseline state (sections 2.3 and 3.1: the
+ * O(D d) per example computation the method avoids), same library, same GEMM
+ * kernels.  W (device, D x d) is copied.  Synchronous.
+ */
+int lst_naive_init(lst_state** out, int64_t D, int32_t d, const float* W,
+                   const lst_config* cfg, void* hip_stream);
+
+/*
+ * lst_naive_step -- same contract as lst_step, computed explicitly:
+ * O = W H (D x m), residual / loss derivatives, grad_H = W^T dL/dO,
+ * W <- W - lr dL/dO H^T.
+ */
+int lst_naive_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* Y_idx,
+                   const float* Y_val, float lr, float* loss, float* grad_H);
+
+/*
+ * lst_sync -- wait for the state's stream; return and clear the sticky device
+ * error (LST_OK if none).
+ */
+int lst_sync(lst_state* s);
+
+/* lst_stats -- synchronise and fill *st. */
+int lst_stats(lst_state* s, lst_stats_t* st);
+
+/*
+ * Profiling support for benchmarks.  While enabled, every lst_step brackets
+ * each of its phases on the state's stream with a pair of HIP events (the
+ * phases are listed by lst_profile_phase_name).  This adds event records to
+ * the stream, so steps timed for throughput should run with profiling off.
+ *   lst_profile_enable  enable != 0 turns it on, 0 off; either discards what
+ *                       was recorded so far.
+ *   lst_profile_read    synchronises, then writes the summed milliseconds of
+ *                       each phase over the profiled steps into ms_total
+ *                       (host, capacity doubles), the number of phases into
+ *                       *nphases and of profiled steps into *nsteps; the
+ *                       records are then discarded.
+ */
+int lst_profile_enable(lst_state* s, int32_t enable);
+int lst_profile_read(lst_state* s, double* ms_total, int32_t capacity, int32_t* nphases,
+                     int64_t* nsteps);
+/* Name of phase i of lst_step (NULL when out of range). */
+const char* lst_profile_phase_name(int32_t phase);
+
+/* lst_strerror -- static description of a status code. */
+const char* lst_strerror(int status);
+
+/* lst_free -- synchronise and release all device memory of the state (NULL ok). */
+void lst_free(lst_state* s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LST_H */

@@ -1,0 +1,631 @@
+// C ABI of the library: state ownership, argument checks and the order of the
+// kernels of one step.
+//
+// Factored step (Appendix A), with H^T as the m x d row-major input:
+//   side stream : validate + sort each example's targets -> Y^T Y ; global
+//                 (row, slot) sort -> distinct rows and their segments
+//   main stream : gather  G = (V^T Y)^T                                   (step 2, sparse part)
+//                 GEMM 1  [Q; U; U^{-T}; H^T] H -> H^, U H, P = U^{-T} H, H^T H  (steps 1, 7, 8)
+//                 GEMM 2  Y^ = U^T (V^T Y)                                 (step 2)
+//                 GEMM 3  H^T H^, H^T Y^                                   (step 5)
+//                 scalars: loss_i, a_i, b_i, N = (dL/dO)^T dL/dO, S = H^T H - A^{-1}/lr
+//                 S^{-1} (Gauss-Jordan)                                    (step 8, m x m inverse)
+//                 GEMM 4  X = S^{-1} P^T ; grad_H = H^ A + Y^ diag(b),
+//                         T = grad_H - (lr/2) N H^T                        (steps 3-4)
+//                 GEMM 5  U -= lr (U H) A H^T ; U^{-T} -= X^T H^T ;
+//                         Q -= lr (H T^T + T H^T)                          (steps 7, 8, 10)
+//                 scatter V[r] += sum_(i,k): idx=r of c_ik X_i           (step 9)
+//                 [drift control: Appendix C pristine restore]
+// Derivation of the shortcuts (exact in real arithmetic):
+//   U_new^{-T} H = -(1/lr) P S^{-1} A^{-1}, so with X = S^{-1} P^T (m x d):
+//   U_new^{-T} = U^{-T} - X^T H^T and V_new = V - lr G (U_new^{-T} H)^T
+//   = V + sum_i (g_i / a_i) X_i, i.e. c = -val (squared) or b_i / a_i (spherical);
+//   Q_new = Q - lr (H grad_H^T + grad_H H^T) + lr^2 H N H^T
+//         = Q - lr (H T^T + T H^T) with T = grad_H - (lr/2) H N.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "lst_internal.h"
+
+using namespace lst;
+
+struct lst_state {
+  int kind = 0;  // 0 factored, 1 naive
+  int64_t D = 0;
+  int d = 0;
+  lst_config cfg{};
+  int device = 0;
+  hipStream_t stream = nullptr;
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_yy = nullptr, ev_sort = nullptr;
+  float* V = nullptr;      // V (factored) or W (naive), D x d
+  float* state = nullptr;  // [Q; U; U^{-T}], 3d x d
+  float* Vtmp = nullptr;   // D x d copy for the pristine restore
+  int* flags = nullptr;
+  // factored workspace
+  float *G = nullptr, *Z0 = nullptr, *Yh = nullptr, *C12 = nullptr, *Nm = nullptr,
+        *Sm = nullptr, *Sinv = nullptr, *a = nullptr, *b = nullptr, *cs = nullptr,
+        *T = nullptr, *X = nullptr;
+  double* gjwork = nullptr;
+  SparseWs sp{};
+  int ld0 = 0, ldc12 = 0;
+  // naive workspace
+  float* O = nullptr;
+  float* wsplit = nullptr;
+  int naive_ksplit = 1;
+  int64_t steps = 0;
+  std::vector<void*> allocs;
+  // profiling: two events per phase per profiled step
+  int prof = 0;
+  std::vector<hipEvent_t> prof_events;
+  size_t prof_used = 0;
+  int64_t prof_steps = 0;
+};
+
+namespace {
+
+struct DeviceGuard {
+  int prev = -1;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) (void)hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+#define HIPCHK(x)                               \
+  do {                                          \
+    if ((x) != hipSuccess) return LST_EHIP;     \
+  } while (0)
+
+template <class T>
+int dalloc(lst_state* s, T** p, size_t count) {
+  if (count == 0) count = 1;
+  void* q = nullptr;
+  if (hipMalloc(&q, count * sizeof(T)) != hipSuccess) return LST_ENOMEM;
+  s->allocs.push_back(q);
+  *p = static_cast<T*>(q);
+  return LST_OK;
+}
+
+#define OK_OR_RETURN(x)            \
+  do {                             \
+    int rc_ = (x);                 \
+    if (rc_ != LST_OK) return rc_; \
+  } while (0)
+
+enum Phase {
+  PH_GATHER = 0, PH_GEMM_STACK, PH_GEMM_YHAT, PH_GEMM_M, PH_SCALARS, PH_INVERSE, PH_GEMM_XT,
+  PH_GEMM_UPDATE, PH_SCATTER, PH_DRIFT, PH_COUNT
+};
+const char* const kPhaseNames[PH_COUNT] = {
+    "gather", "gemm_stack", "gemm_yhat", "gemm_m", "scalars", "inverse", "gemm_xt",
+    "gemm_update", "scatter", "drift"};
+
+// Records the begin (end = 0) or end (end = 1) event of a phase when profiling.
+int prof_mark(lst_state* s, int phase, int end) {
+  if (!s->prof) return LST_OK;
+  const size_t slot = (size_t)(s->prof_steps - 1) * (2 * PH_COUNT) + 2 * phase + end;
+  while (s->prof_events.size() <= slot) {
+    hipEvent_t e;
+    HIPCHK(hipEventCreate(&e));
+    s->prof_events.push_back(e);
+  }
+  HIPCHK(hipEventRecord(s->prof_events[slot], s->stream));
+  if (slot + 1 > s->prof_used) s->prof_used = slot + 1;
+  return LST_OK;
+}
+
+void release(lst_state* s) {
+  if (!s) return;
+  if (s->stream || s->side) {
+    (void)hipStreamSynchronize(s->stream);
+    if (s->side) (void)hipStreamSynchronize(s->side);
+  }
+  for (void* p : s->allocs) (void)hipFree(p);
+  s->allocs.clear();
+  if (s->ev_fork) (void)hipEventDestroy(s->ev_fork);
+  if (s->ev_yy) (void)hipEventDestroy(s->ev_yy);
+  if (s->ev_sort) (void)hipEventDestroy(s->ev_sort);
+  if (s->side) (void)hipStreamDestroy(s->side);
+  for (hipEvent_t e : s->prof_events) (void)hipEventDestroy(e);
+  delete s;
+}
+
+float* Qp(lst_state* s) { return s->state; }
+float* Up(lst_state* s) { return s->state + (size_t)s->d * s->d; }
+float* Uitp(lst_state* s) { return s->state + 2 * (size_t)s->d * s->d; }
+
+int check_config(const lst_config* cfg) {
+  if (!cfg) return LST_EINVAL;
+  if (cfg->loss != LST_LOSS_SQUARED && cfg->loss != LST_LOSS_SPHERICAL) return LST_EINVAL;
+  if (cfg->loss == LST_LOSS_SPHERICAL && !(cfg->sph_eps > 0.f && isfinite(cfg->sph_eps)))
+    return LST_EINVAL;
+  if (cfg->m_max < 1 || cfg->m_max > 4096) return LST_EINVAL;
+  if (cfg->K_max < 1 || cfg->K_max > 1024) return LST_EINVAL;
+  if ((int64_t)cfg->m_max * cfg->K_max > 16384) return LST_EINVAL;
+  if (!(cfg->cond_max >= 0.f) || !isfinite(cfg->cond_max)) return LST_EINVAL;
+  return LST_OK;
+}
+
+int common_init(lst_state* s, int64_t D, int32_t d, const lst_config* cfg, void* hip_stream) {
+  s->D = D;
+  s->d = d;
+  s->cfg = *cfg;
+  HIPCHK(hipGetDevice(&s->device));
+  s->stream = static_cast<hipStream_t>(hip_stream);
+  HIPCHK(hipStreamCreateWithFlags(&s->side, hipStreamNonBlocking));
+  HIPCHK(hipEventCreateWithFlags(&s->ev_fork, hipEventDisableTiming));
+  HIPCHK(hipEventCreateWithFlags(&s->ev_yy, hipEventDisableTiming));
+  HIPCHK(hipEventCreateWithFlags(&s->ev_sort, hipEventDisableTiming));
+  OK_OR_RETURN(dalloc(s, &s->flags, F_COUNT));
+  HIPCHK(hipMemsetAsync(s->flags, 0, F_COUNT * sizeof(int), s->stream));
+  OK_OR_RETURN(dalloc(s, &s->V, (size_t)D * d));
+  return LST_OK;
+}
+
+// Split-K C = alpha A^T B with A, B: K x n (rows K), C n x n symmetric, K large.
+int gram_splitk(lst_state* s, const float* A, int64_t Krows, int n, float* C, float alpha) {
+  const int tiles = ((n + 63) / 64) * ((n + 63) / 64);
+  int64_t ks = (2048 + tiles - 1) / tiles;
+  const int64_t max_by_k = (Krows + 255) / 256;
+  if (ks > max_by_k) ks = max_by_k;
+  if (ks < 1) ks = 1;
+  if (ks > 256) ks = 256;
+  float* ws = nullptr;
+  if (hipMalloc((void**)&ws, (size_t)ks * n * n * sizeof(float)) != hipSuccess) return LST_ENOMEM;
+  GemmBatch bt{};
+  bt.np = 1;
+  bt.p[0] = gemm_problem(n, n, (int)Krows, vmat(A, n, (int)Krows), vmat(A, n, (int)Krows), ws, n,
+                         1.f, 0.f, EPI_PARTIAL);
+  bt.p[0].ksplit = (int)ks;
+  int rc = LST_OK;
+  if (gemm_launch(L_TN, bt, s->stream) != hipSuccess) rc = LST_EHIP;
+  if (rc == LST_OK &&
+      gemm_splitk_reduce(ws, (int)ks, n, n, C, n, alpha, 0.f, 1, nullptr, s->stream) != hipSuccess)
+    rc = LST_EHIP;
+  (void)hipStreamSynchronize(s->stream);
+  (void)hipFree(ws);
+  return rc;
+}
+
+// W = Vsrc U into Wdst (D x d), optionally gated on a device flag.
+int vu_product(lst_state* s, const float* Vsrc, float* Wdst, const int* run_if,
+               const int* skip_if) {
+  GemmBatch bt{};
+  bt.np = 1;
+  bt.p[0] = gemm_problem((int)s->D, s->d, s->d, vmat(Vsrc, s->d, (int)s->D), vmat(Up(s), s->d, s->d),
+                         Wdst, s->d, 1.f, 0.f, EPI_STORE);
+  bt.run_if = run_if;
+  bt.skip_if = skip_if;
+  HIPCHK(gemm_launch(L_NN, bt, s->stream));
+  return LST_OK;
+}
+
+int ensure_vtmp(lst_state* s) {
+  if (s->Vtmp) return LST_OK;
+  return dalloc(s, &s->Vtmp, (size_t)s->D * s->d);
+}
+
+int read_flag(lst_state* s, int which, int* out) {
+  HIPCHK(hipStreamSynchronize(s->stream));
+  HIPCHK(hipMemcpy(out, s->flags + which, sizeof(int), hipMemcpyDeviceToHost));
+  return LST_OK;
+}
+
+int check_step_args(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* Y_idx,
+                    const float* Y_val, float lr, float* loss, float* grad_H) {
+  if (!s) return LST_EINVAL;
+  if (m < 1 || m > s->cfg.m_max || K < 1 || K > s->cfg.K_max) return LST_EINVAL;
+  if (!H || !Y_idx || !loss || !grad_H) return LST_EINVAL;
+  if (s->cfg.loss == LST_LOSS_SQUARED && !Y_val) return LST_EINVAL;
+  if (s->cfg.loss == LST_LOSS_SPHERICAL && K != 1) return LST_EINVAL;
+  if (!(lr > 0.f) || !isfinite(lr)) return LST_EINVAL;
+  return LST_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* lst_strerror(int status) {
+  switch (status) {
+    case LST_OK: return "ok";
+    case LST_EINVAL: return "invalid argument";
+    case LST_EINDEX: return "target index outside [-1, D) (or missing class for the spherical loss)";
+    case LST_ESINGULAR: return "Woodbury matrix H^T H - A^{-1}/lr is singular";
+    case LST_ENOMEM: return "device allocation failed";
+    case LST_EHIP: return "HIP runtime error";
+    case LST_ENONFINITE: return "non-finite loss";
+    case LST_ESTATE: return "call not valid for this kind of state";
+    default: return "unknown status";
+  }
+}
+
+int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float* U,
+             const lst_config* cfg, void* hip_stream) {
+  if (!out || !V || D < 1 || d < 1 || d > 4096 || D > (int64_t)0x7fffffff) return LST_EINVAL;
+  if ((int64_t)D * d > ((int64_t)1 << 40)) return LST_EINVAL;
+  int rc = check_config(cfg);
+  if (rc != LST_OK) return rc;
+  lst_state* s = new lst_state();
+  s->kind = 0;
+  rc = common_init(s, D, d, cfg, hip_stream);
+  const int m = cfg->m_max, K = cfg->K_max;
+  auto fail = [&](int code) {
+    release(s);
+    return code;
+  };
+  if (rc != LST_OK) return fail(rc);
+  s->ld0 = 3 * d + m;
+  s->ldc12 = 2 * m;
+  const size_t md = (size_t)m * d;
+  if ((rc = dalloc(s, &s->state, 3 * (size_t)d * d)) ||
+      (rc = dalloc(s, &s->G, md)) || (rc = dalloc(s, &s->Z0, (size_t)m * s->ld0)) ||
+      (rc = dalloc(s, &s->Yh, md)) || (rc = dalloc(s, &s->C12, (size_t)m * s->ldc12)) ||
+      (rc = dalloc(s, &s->Nm, (size_t)m * m)) || (rc = dalloc(s, &s->Sm, (size_t)m * m)) ||
+      (rc = dalloc(s, &s->Sinv, (size_t)m * m)) || (rc = dalloc(s, &s->a, m)) ||
+      (rc = dalloc(s, &s->b, m)) || (rc = dalloc(s, &s->cs, m)) || (rc = dalloc(s, &s->T, md)) ||
+      (rc = dalloc(s, &s->X, md)) ||
+      (rc = dalloc(s, &s->gjwork, (size_t)(m > 128 ? m : 1) * (m > 128 ? m : 1))) ||
+      (rc = dalloc(s, &s->sp.ex_row, (size_t)m * K)) ||
+      (rc = dalloc(s, &s->sp.ex_val, (size_t)m * K)) || (rc = dalloc(s, &s->sp.ex_cnt, m)) ||
+      (rc = dalloc(s, &s->sp.keys, (size_t)m * K)) ||
+      (rc = dalloc(s, &s->sp.srt_slot, (size_t)m * K)) ||
+      (rc = dalloc(s, &s->sp.seg_row, (size_t)m * K)) ||
+      (rc = dalloc(s, &s->sp.seg_beg, (size_t)m * K + 1)) ||
+      (rc = dalloc(s, &s->sp.yy, (size_t)m * m)))
+    return fail(rc);
+  if (cfg->cond_max > 0.f && (rc = ensure_vtmp(s))) return fail(rc);
+  if (hipMemcpyAsync(s->V, V, (size_t)D * d * sizeof(float), hipMemcpyDeviceToDevice, s->stream) !=
+      hipSuccess)
+    return fail(LST_EHIP);
+  if (!U) {
+    if (set_identity_if(Up(s), d, nullptr, s->stream) != hipSuccess ||
+        set_identity_if(Uitp(s), d, nullptr, s->stream) != hipSuccess)
+      return fail(LST_EHIP);
+    if ((rc = gram_splitk(s, s->V, D, d, Qp(s), 1.f))) return fail(rc);
+  } else {
+    if (hipMemcpyAsync(Up(s), U, (size_t)d * d * sizeof(float), hipMemcpyDeviceToDevice,
+                       s->stream) != hipSuccess)
+      return fail(LST_EHIP);
+    // U^{-T}: invert U (fp64 Gauss-Jordan), then transpose
+    double* work = nullptr;
+    float* inv = nullptr;
+    if ((rc = dalloc(s, &work, (size_t)d * d)) || (rc = dalloc(s, &inv, (size_t)d * d)))
+      return fail(rc);
+    if (invert_small(Up(s), d, inv, d, d, work, s->flags, 0, s->stream) != hipSuccess ||
+        transpose_square(inv, Uitp(s), d, s->stream) != hipSuccess)
+      return fail(LST_EHIP);
+    // Q = (V U)^T (V U); the product goes through the restore buffer
+    if ((rc = ensure_vtmp(s))) return fail(rc);
+    if ((rc = vu_product(s, s->V, s->Vtmp, nullptr, nullptr))) return fail(rc);
+    if ((rc = gram_splitk(s, s->Vtmp, D, d, Qp(s), 1.f))) return fail(rc);
+  }
+  int err = 0;
+  if ((rc = read_flag(s, F_ERR, &err))) return fail(rc);
+  if (err) return fail(err);
+  *out = s;
+  return LST_OK;
+}
+
+int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* Y_idx,
+             const float* Y_val, float lr, float* loss, float* grad_H) {
+  int rc = check_step_args(s, m, K, H, Y_idx, Y_val, lr, loss, grad_H);
+  if (rc != LST_OK) return rc;
+  if (s->kind != 0) return LST_ESTATE;
+  DeviceGuard dg(s->device);
+  const int d = s->d;
+  const int64_t D = s->D;
+  const int one_hot = s->cfg.loss == LST_LOSS_SPHERICAL;
+  hipStream_t st = s->stream;
+  int* fl = s->flags;
+  float* U = Up(s);
+
+  if (s->prof) s->prof_steps += 1;
+  // side stream: target ordering and Y^T Y
+  HIPCHK(hipEventRecord(s->ev_fork, st));
+  HIPCHK(hipStreamWaitEvent(s->side, s->ev_fork, 0));
+  HIPCHK(prep_examples(Y_idx, Y_val, m, K, D, one_hot, s->sp, fl, s->side));
+  HIPCHK(prep_target_gram(m, K, s->sp, s->side));
+  HIPCHK(hipEventRecord(s->ev_yy, s->side));
+  HIPCHK(prep_global_sort(m, K, s->sp, fl, s->side));
+  HIPCHK(hipEventRecord(s->ev_sort, s->side));
+
+  // step 2, sparse part: G = (V^T Y)^T
+  OK_OR_RETURN(prof_mark(s, PH_GATHER, 0));
+  HIPCHK(gather_rows(s->V, D, d, Y_idx, Y_val, m, K, one_hot, s->G, d, st));
+  OK_OR_RETURN(prof_mark(s, PH_GATHER, 1));
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_STACK, 0));
+  {  // GEMM 1: Z0 = H^T [Q; U; U^{-T}; H^T]^T   (m x (3d + m))
+    GemmBatch bt{};
+    bt.np = 1;
+    bt.p[0] = gemm_problem(m, 3 * d + m, d, vmat(H, d, m), vmat2(s->state, d, 3 * d, H, d, m),
+                           s->Z0, s->ld0, 1.f, 0.f, EPI_STORE);
+    HIPCHK(gemm_launch(L_NT, bt, st));
+  }
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_STACK, 1));
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_YHAT, 0));
+  {  // GEMM 2: Y^ (rows) = G U
+    GemmBatch bt{};
+    bt.np = 1;
+    bt.p[0] = gemm_problem(m, d, d, vmat(s->G, d, m), vmat(U, d, d), s->Yh, d, 1.f, 0.f,
+                           EPI_STORE);
+    HIPCHK(gemm_launch(L_NN, bt, st));
+  }
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_YHAT, 1));
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_M, 0));
+  {  // GEMM 3: C12 = [H^T H^ | H^T Y^]
+    GemmBatch bt{};
+    bt.np = 1;
+    bt.p[0] = gemm_problem(m, 2 * m, d, vmat(H, d, m), vmat2(s->Z0, s->ld0, m, s->Yh, d, m),
+                           s->C12, s->ldc12, 1.f, 0.f, EPI_STORE);
+    HIPCHK(gemm_launch(L_NT, bt, st));
+  }
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_M, 1));
+  HIPCHK(hipStreamWaitEvent(st, s->ev_yy, 0));
+  OK_OR_RETURN(prof_mark(s, PH_SCALARS, 0));
+  HIPCHK(minibatch_scalars(s->cfg.loss, s->cfg.sph_eps, D, lr, m, s->C12, s->ldc12,
+                           s->Z0 + 3 * d, s->ld0, s->sp.yy, loss, s->a, s->b, s->cs, s->Nm, s->Sm,
+                           fl, st));
+  OK_OR_RETURN(prof_mark(s, PH_SCALARS, 1));
+  OK_OR_RETURN(prof_mark(s, PH_INVERSE, 0));
+  HIPCHK(invert_small(s->Sm, m, s->Sinv, m, m, s->gjwork, fl, 1, st));
+  OK_OR_RETURN(prof_mark(s, PH_INVERSE, 1));
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_XT, 0));
+  {  // GEMM 4: X = S^{-1} P^T ; grad_H and T
+    GemmBatch bt{};
+    bt.np = 2;
+    bt.p[0] = gemm_problem(m, d, m, vmat(s->Sinv, m, m), vmat(s->Z0 + 2 * d, s->ld0, m), s->X, d,
+                           1.f, 0.f, EPI_STORE);
+    GemmProblem& pt = bt.p[1];
+    pt = gemm_problem(m, d, m, vmat(s->Nm, m, m), vmat(H, d, m), s->T, d, -0.5f * lr, 0.f,
+                      EPI_GRADT);
+    pt.e1 = s->Z0;
+    pt.lde1 = s->ld0;
+    pt.e2 = s->Yh;
+    pt.lde2 = d;
+    pt.s1 = s->a;
+    pt.s2 = s->b;
+    pt.g = grad_H;
+    pt.ldg = d;
+    HIPCHK(gemm_launch(L_NN, bt, st));
+  }
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_XT, 1));
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_UPDATE, 0));
+  {  // GEMM 5: rank-m updates of U, U^{-T} and the symmetric rank-2m update of Q
+    GemmBatch bt{};
+    bt.np = 3;
+    bt.skip_if = fl + F_ERR;
+    bt.p[0] = gemm_problem(d, d, m, vmat(s->Z0 + d, s->ld0, m, s->a), vmat(H, d, m), U, d, -lr,
+                           1.f, EPI_STORE);
+    bt.p[1] = gemm_problem(d, d, m, vmat(s->X, d, m), vmat(H, d, m), Uitp(s), d, -1.f, 1.f,
+                           EPI_STORE);
+    bt.p[2] = gemm_problem(d, d, 2 * m, vmat2(H, d, m, s->T, d, m), vmat2(s->T, d, m, H, d, m),
+                           Qp(s), d, -lr, 1.f, EPI_SYM);
+    HIPCHK(gemm_launch(L_TN, bt, st));
+  }
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_UPDATE, 1));
+  HIPCHK(hipStreamWaitEvent(st, s->ev_sort, 0));
+  OK_OR_RETURN(prof_mark(s, PH_SCATTER, 0));
+  HIPCHK(scatter_rows(s->V, d, s->X, d, Y_val, one_hot ? s->cs : nullptr, m, K, s->sp, fl, st));
+  OK_OR_RETURN(prof_mark(s, PH_SCATTER, 1));
+  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 0));
+  if (s->cfg.cond_max > 0.f) {
+    HIPCHK(drift_check(U, Uitp(s), d, s->cfg.cond_max * (float)d, fl, st));
+    HIPCHK(copy_if(s->V, s->Vtmp, (size_t)D * d, fl + F_RESTORE, st));
+    OK_OR_RETURN(vu_product(s, s->Vtmp, s->V, fl + F_RESTORE, fl + F_ERR));
+    HIPCHK(set_identity_if(U, d, fl + F_RESTORE, st));
+    HIPCHK(set_identity_if(Uitp(s), d, fl + F_RESTORE, st));
+  }
+  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 1));
+  s->steps += 1;
+  return LST_OK;
+}
+
+int lst_materialize_W(lst_state* s, float* W) {
+  if (!s || !W) return LST_EINVAL;
+  DeviceGuard dg(s->device);
+  if (s->kind == 1) {
+    HIPCHK(hipMemcpyAsync(W, s->V, (size_t)s->D * s->d * sizeof(float), hipMemcpyDeviceToDevice,
+                          s->stream));
+    return LST_OK;
+  }
+  return vu_product(s, s->V, W, nullptr, nullptr);
+}
+
+int lst_get_state(lst_state* s, float* Q, float* U, float* UinvT) {
+  if (!s) return LST_EINVAL;
+  if (s->kind != 0) return LST_ESTATE;
+  DeviceGuard dg(s->device);
+  const size_t bytes = (size_t)s->d * s->d * sizeof(float);
+  if (Q) HIPCHK(hipMemcpyAsync(Q, Qp(s), bytes, hipMemcpyDeviceToDevice, s->stream));
+  if (U) HIPCHK(hipMemcpyAsync(U, Up(s), bytes, hipMemcpyDeviceToDevice, s->stream));
+  if (UinvT) HIPCHK(hipMemcpyAsync(UinvT, Uitp(s), bytes, hipMemcpyDeviceToDevice, s->stream));
+  return LST_OK;
+}
+
+int lst_get_V(lst_state* s, float* V) {
+  if (!s || !V) return LST_EINVAL;
+  if (s->kind != 0) return LST_ESTATE;
+  DeviceGuard dg(s->device);
+  HIPCHK(hipMemcpyAsync(V, s->V, (size_t)s->D * s->d * sizeof(float), hipMemcpyDeviceToDevice,
+                        s->stream));
+  return LST_OK;
+}
+
+int lst_touched_rows(lst_state* s, int32_t* rows, int32_t capacity, int32_t* count) {
+  if (!s || !count || (capacity > 0 && !rows) || capacity < 0) return LST_EINVAL;
+  if (s->kind != 0) return LST_ESTATE;
+  DeviceGuard dg(s->device);
+  int u = 0;
+  OK_OR_RETURN(read_flag(s, F_UNIQUE, &u));
+  if (s->steps == 0) u = 0;
+  if (u > capacity) return LST_EINVAL;
+  if (u > 0) HIPCHK(hipMemcpy(rows, s->sp.seg_row, (size_t)u * sizeof(int), hipMemcpyDeviceToHost));
+  *count = u;
+  return LST_OK;
+}
+
+int lst_restore(lst_state* s) {
+  if (!s) return LST_EINVAL;
+  if (s->kind != 0) return LST_ESTATE;
+  DeviceGuard dg(s->device);
+  OK_OR_RETURN(ensure_vtmp(s));
+  HIPCHK(hipMemcpyAsync(s->Vtmp, s->V, (size_t)s->D * s->d * sizeof(float),
+                        hipMemcpyDeviceToDevice, s->stream));
+  OK_OR_RETURN(vu_product(s, s->Vtmp, s->V, nullptr, nullptr));
+  HIPCHK(set_identity_if(Up(s), s->d, nullptr, s->stream));
+  HIPCHK(set_identity_if(Uitp(s), s->d, nullptr, s->stream));
+  return LST_OK;
+}
+
+int lst_naive_init(lst_state** out, int64_t D, int32_t d, const float* W, const lst_config* cfg,
+                   void* hip_stream) {
+  if (!out || !W || D < 1 || d < 1 || d > 4096 || D > (int64_t)0x7fffffff) return LST_EINVAL;
+  int rc = check_config(cfg);
+  if (rc != LST_OK) return rc;
+  lst_state* s = new lst_state();
+  s->kind = 1;
+  rc = common_init(s, D, d, cfg, hip_stream);
+  auto fail = [&](int code) {
+    release(s);
+    return code;
+  };
+  if (rc != LST_OK) return fail(rc);
+  const int m = cfg->m_max;
+  const int tiles = ((m + 63) / 64) * ((d + 63) / 64);
+  int64_t ks = (1024 + tiles - 1) / tiles;
+  const int64_t max_by_k = (D + 255) / 256;
+  if (ks > max_by_k) ks = max_by_k;
+  if (ks > 256) ks = 256;
+  if (ks < 1) ks = 1;
+  s->naive_ksplit = (int)ks;
+  if ((rc = dalloc(s, &s->O, (size_t)m * D)) ||
+      (rc = dalloc(s, &s->wsplit, (size_t)ks * m * d)))
+    return fail(rc);
+  if (hipMemcpyAsync(s->V, W, (size_t)D * d * sizeof(float), hipMemcpyDeviceToDevice, s->stream) !=
+      hipSuccess)
+    return fail(LST_EHIP);
+  if (hipStreamSynchronize(s->stream) != hipSuccess) return fail(LST_EHIP);
+  *out = s;
+  return LST_OK;
+}
+
+int lst_naive_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* Y_idx,
+                   const float* Y_val, float lr, float* loss, float* grad_H) {
+  int rc = check_step_args(s, m, K, H, Y_idx, Y_val, lr, loss, grad_H);
+  if (rc != LST_OK) return rc;
+  if (s->kind != 1) return LST_ESTATE;
+  DeviceGuard dg(s->device);
+  const int d = s->d;
+  const int64_t D = s->D;
+  hipStream_t st = s->stream;
+  const bool sq = s->cfg.loss == LST_LOSS_SQUARED;
+  {  // O (m x D) = H^T W^T: every output of every example, O(D d) each
+    GemmBatch bt{};
+    bt.np = 1;
+    bt.p[0] = gemm_problem(m, (int)D, d, vmat(H, d, m), vmat(s->V, d, (int)D), s->O, (int)D, 1.f,
+                           0.f, EPI_STORE);
+    HIPCHK(gemm_launch(L_NT, bt, st));
+  }
+  HIPCHK(naive_rowstats(s->O, D, D, m, Y_idx, Y_val, K, s->cfg.loss, s->cfg.sph_eps, loss,
+                        s->flags, st));
+  {  // grad_H = (dL/dO) W  (K = D, split over K)
+    GemmBatch bt{};
+    bt.np = 1;
+    bt.p[0] = gemm_problem(m, d, (int)D, vmat(s->O, (int)D, m), vmat(s->V, d, (int)D), s->wsplit,
+                           d, 1.f, 0.f, EPI_PARTIAL);
+    bt.p[0].ksplit = s->naive_ksplit;
+    HIPCHK(gemm_launch(L_NN, bt, st));
+    HIPCHK(gemm_splitk_reduce(s->wsplit, s->naive_ksplit, m, d, grad_H, d, sq ? 2.f : 1.f, 0.f, 0,
+                              nullptr, st));
+  }
+  {  // W -= lr (dL/dO)^T H^T
+    GemmBatch bt{};
+    bt.np = 1;
+    bt.skip_if = s->flags + F_ERR;
+    bt.p[0] = gemm_problem((int)D, d, m, vmat(s->O, (int)D, m), vmat(H, d, m), s->V, d,
+                           sq ? -2.f * lr : -lr, 1.f, EPI_STORE);
+    HIPCHK(gemm_launch(L_TN, bt, st));
+  }
+  s->steps += 1;
+  return LST_OK;
+}
+
+int lst_sync(lst_state* s) {
+  if (!s) return LST_EINVAL;
+  DeviceGuard dg(s->device);
+  int err = 0;
+  OK_OR_RETURN(read_flag(s, F_ERR, &err));
+  if (err) {
+    const int zero = 0;
+    HIPCHK(hipMemcpy(s->flags + F_ERR, &zero, sizeof(int), hipMemcpyHostToDevice));
+  }
+  return err;
+}
+
+int lst_stats(lst_state* s, lst_stats_t* st) {
+  if (!s || !st) return LST_EINVAL;
+  DeviceGuard dg(s->device);
+  int f[F_COUNT];
+  HIPCHK(hipStreamSynchronize(s->stream));
+  HIPCHK(hipMemcpy(f, s->flags, sizeof(f), hipMemcpyDeviceToHost));
+  st->steps = s->steps;
+  st->restores = f[F_RESTORES];
+  st->last_unique = s->kind == 0 ? f[F_UNIQUE] : 0;
+  st->last_nnz = s->kind == 0 ? f[F_NNZ] : 0;
+  return LST_OK;
+}
+
+int lst_profile_enable(lst_state* s, int32_t enable) {
+  if (!s) return LST_EINVAL;
+  DeviceGuard dg(s->device);
+  HIPCHK(hipStreamSynchronize(s->stream));
+  s->prof = enable ? 1 : 0;
+  s->prof_used = 0;
+  s->prof_steps = 0;
+  return LST_OK;
+}
+
+int lst_profile_read(lst_state* s, double* ms_total, int32_t capacity, int32_t* nphases,
+                     int64_t* nsteps) {
+  if (!s || !nphases || !nsteps || capacity < 0 || (capacity > 0 && !ms_total))
+    return LST_EINVAL;
+  DeviceGuard dg(s->device);
+  HIPCHK(hipStreamSynchronize(s->stream));
+  for (int p = 0; p < capacity && p < PH_COUNT; ++p) ms_total[p] = 0.0;
+  for (int64_t st = 0; st < s->prof_steps; ++st) {
+    for (int p = 0; p < PH_COUNT && p < capacity; ++p) {
+      const size_t b = (size_t)st * (2 * PH_COUNT) + 2 * p;
+      if (b + 1 >= s->prof_used) continue;
+      float ms = 0.f;
+      HIPCHK(hipEventElapsedTime(&ms, s->prof_events[b], s->prof_events[b + 1]));
+      ms_total[p] += ms;
+    }
+  }
+  *nphases = PH_COUNT;
+  *nsteps = s->prof_steps;
+  s->prof_used = 0;
+  s->prof_steps = 0;
+  return LST_OK;
+}
+
+const char* lst_profile_phase_name(int32_t phase) {
+  if (phase < 0 || phase >= PH_COUNT) return nullptr;
+  return kPhaseNames[phase];
+}
+
+void lst_free(lst_state* s) {
+  if (!s) return;
+  DeviceGuard dg(s->device);
+  release(s);
+}
+
+}  // extern "C"

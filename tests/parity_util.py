@@ -1,0 +1,87 @@
+"""Helpers shared by the GPU parity tests: run the HIP library and the fp64
+oracle side by side on the same seeded inputs and measure their distance."""
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Optional
+
+import numpy as np
+
+from oracle import explicit
+from synth import Workload, WorkloadConfig
+
+
+def rel(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    den = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / den) if den > 0 else float(np.linalg.norm(a - b))
+
+
+@dataclasses.dataclass
+class StepReport:
+    step: int
+    loss_rel: float         # |sum L_gpu - sum L_ref| / |sum L_ref|
+    loss_max_rel: float     # max_i |L_i,gpu - L_i,ref| / max(|L_i,ref|, 1e-30)
+    grad_rel: float         # ||dG||_F / ||G_ref||_F
+    rows_equal: bool        # distinct touched rows identical to the oracle's
+    W_rel: Optional[float] = None
+
+
+def run_parity(cfg: WorkloadConfig, steps: int, *, cond_max: float = 0.0, check_rows: bool = True,
+               W_every: int = 0, naive: bool = False, V_check_untouched: bool = False):
+    """Steps the GPU library and the explicit-W oracle from the same initial W.
+
+    Returns (reports, W_rel_final, extra) where extra holds the final layer object."""
+    import torch
+
+    import paper_1412_7091_amd as lst
+
+    wl = Workload(cfg)
+    V0 = wl.init_V()
+    U0 = wl.init_U()
+    dev = torch.device("cuda:0")
+    V0_t = torch.from_numpy(V0).to(dev)
+    U0_t = None if cfg.u_init == "identity" else torch.from_numpy(U0).to(dev)
+    W_ref = V0.astype(np.float64) @ U0.astype(np.float64)
+    if naive:
+        layer = lst.NaiveOutputLayer(torch.from_numpy((V0.astype(np.float64) @ U0.astype(np.float64))
+                                                      .astype(np.float32)).to(dev),
+                                     loss=cfg.loss, sph_eps=cfg.sph_eps, m_max=cfg.m, K_max=cfg.K)
+    else:
+        layer = lst.FactoredOutputLayer(V0_t, U0_t, loss=cfg.loss, sph_eps=cfg.sph_eps,
+                                        m_max=cfg.m, K_max=cfg.K, cond_max=cond_max)
+    reports: List[StepReport] = []
+    V_prev = None
+    for s in range(steps):
+        H, idx, val = wl.batch(s)
+        if V_check_untouched and not naive:
+            V_prev = layer.get_V().cpu().numpy()
+        H_t = torch.from_numpy(H).to(dev)
+        i_t = torch.from_numpy(idx).to(dev)
+        v_t = torch.from_numpy(val).to(dev)
+        loss_t, grad_t = layer.step(H_t, i_t, v_t, cfg.lr)
+        code = layer.sync()
+        assert code == 0, f"step {s}: device status {code}"
+        loss_g = loss_t.cpu().numpy()
+        grad_g = grad_t.cpu().numpy()
+        loss_r, grad_r, W_ref = explicit.step(W_ref, H, idx, val, cfg.lr, cfg.loss, cfg.sph_eps)
+        rows_ok = True
+        if check_rows and not naive:
+            rows_ok = bool(np.array_equal(layer.touched_rows(), explicit.touched_rows(idx)))
+        with np.errstate(divide="ignore", invalid="ignore"):
+            lmax = float(np.max(np.abs(loss_g - loss_r) / np.maximum(np.abs(loss_r), 1e-30)))
+        rep = StepReport(step=s, loss_rel=abs(float(loss_g.astype(np.float64).sum() - loss_r.sum()))
+                         / max(abs(float(loss_r.sum())), 1e-30),
+                         loss_max_rel=lmax, grad_rel=rel(grad_g, grad_r), rows_equal=rows_ok)
+        if W_every and (s + 1) % W_every == 0:
+            rep.W_rel = rel(layer.materialize_W().cpu().numpy(), W_ref)
+        if V_check_untouched and not naive:
+            V_now = layer.get_V().cpu().numpy()
+            touched = explicit.touched_rows(idx)
+            mask = np.ones(V_now.shape[0], dtype=bool)
+            mask[touched] = False
+            assert np.array_equal(V_now[mask], V_prev[mask]), f"step {s}: untouched rows of V changed"
+        reports.append(rep)
+    W_final = layer.materialize_W().cpu().numpy()
+    return reports, rel(W_final, W_ref), {"layer": layer, "W_ref": W_ref}

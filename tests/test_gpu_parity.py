@@ -1,0 +1,236 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 oracle.
+
+Bar (per step, C16 norms): |sum L_gpu - sum L_ref| / |sum L_ref| <= 1e-4 and
+||grad_gpu - grad_ref||_F / ||grad_ref||_F <= 1e-4; after the run
+||V U - W_ref||_F / ||W_ref||_F <= 1e-3; the distinct touched rows equal the
+oracle's np.unique bit for bit; rows of V no target touches stay bitwise equal.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import explicit
+from parity_util import rel, run_parity
+from synth import CONFIGS, Workload, WorkloadConfig
+
+pytestmark = pytest.mark.gpu
+
+TOL_STEP = 1e-4
+TOL_W = 1e-3
+
+
+def _assert(reports, W_rel, tol_step=TOL_STEP, tol_W=TOL_W, rows=True):
+    worst_l = max(r.loss_rel for r in reports)
+    worst_g = max(r.grad_rel for r in reports)
+    print(f"steps={len(reports)} worst loss rel={worst_l:.2e} worst grad rel={worst_g:.2e} "
+          f"W rel={W_rel:.2e}", flush=True)
+    for r in reports:
+        assert r.loss_rel <= tol_step, r
+        assert r.grad_rel <= tol_step, r
+        if rows:
+            assert r.rows_equal, r
+    assert W_rel <= tol_W, W_rel
+
+
+def _cfg(**kw):
+    base = dict(name="t", D=997, d=37, m=13, K=7, loss="squared", lr=1e-2, steps=20,
+                idx_dist="uniform", distinct=False, val_dist="normal", entropy=101)
+    base.update(kw)
+    return WorkloadConfig(**base)
+
+
+def test_c1s_scaled_100_steps(gpu_lib):
+    reports, W_rel, _ = run_parity(CONFIGS["c1s"], 100, V_check_untouched=True)
+    _assert(reports, W_rel)
+
+
+def test_ragged_padding_duplicates(gpu_lib):
+    cfg = _cfg(pad_frac=0.2, dup_frac=0.3)
+    reports, W_rel, _ = run_parity(cfg, 30, V_check_untouched=True)
+    _assert(reports, W_rel)
+
+
+def test_several_tiles_ragged(gpu_lib):
+    cfg = _cfg(D=5003, d=130, m=70, K=9, lr=5e-3, distinct=True, entropy=102)
+    reports, W_rel, _ = run_parity(cfg, 20)
+    _assert(reports, W_rel)
+
+
+def test_single_example(gpu_lib):
+    cfg = _cfg(D=300, d=16, m=1, K=4, lr=2e-2, entropy=103)
+    reports, W_rel, _ = run_parity(cfg, 30)
+    _assert(reports, W_rel)
+
+
+def test_spherical_zipf_small(gpu_lib):
+    cfg = _cfg(D=3001, d=24, m=20, K=1, loss="spherical", lr=1e-2, idx_dist="zipf", zipf_s=1.0,
+               val_dist="one", distinct=True, entropy=104)
+    reports, W_rel, _ = run_parity(cfg, 50, V_check_untouched=True)
+    _assert(reports, W_rel)
+
+
+def test_random_initial_U(gpu_lib):
+    cfg = _cfg(D=800, d=20, m=8, K=5, u_init="random", entropy=105)
+    reports, W_rel, _ = run_parity(cfg, 20)
+    _assert(reports, W_rel)
+
+
+def test_naive_path_small(gpu_lib):
+    for loss in ("squared", "spherical"):
+        kw = dict(K=1, val_dist="one", distinct=True) if loss == "spherical" else {}
+        cfg = _cfg(D=2500, d=40, m=12, loss=loss, entropy=106, **kw)
+        reports, W_rel, _ = run_parity(cfg, 10, naive=True)
+        _assert(reports, W_rel, rows=False)
+
+
+def test_c2_paper_prefix(gpu_lib):
+    """D = 200000, d = 500, m = 128, K = 10 at full size (the benchmarked launch)."""
+    reports, W_rel, _ = run_parity(CONFIGS["c2"], 4)
+    _assert(reports, W_rel)
+
+
+def test_c3_spherical_prefix(gpu_lib):
+    reports, W_rel, _ = run_parity(CONFIGS["c3"], 4)
+    _assert(reports, W_rel)
+
+
+def test_c4_large_vocab_prefix(gpu_lib):
+    reports, W_rel, _ = run_parity(CONFIGS["c4"], 2)
+    _assert(reports, W_rel)
+
+
+def test_c5_wide_prefix(gpu_lib):
+    reports, W_rel, _ = run_parity(CONFIGS["c5"], 2)
+    _assert(reports, W_rel)
+
+
+# ---------------------------------------------------------------- invariants
+def _layer_after(cfg, steps, **kw):
+    import paper_1412_7091_amd as lst
+
+    wl = Workload(cfg)
+    dev = torch.device("cuda:0")
+    layer = lst.FactoredOutputLayer(torch.from_numpy(wl.init_V()).to(dev), loss=cfg.loss,
+                                    sph_eps=cfg.sph_eps, m_max=cfg.m, K_max=cfg.K, **kw)
+    outs = []
+    for s in range(steps):
+        H, idx, val = (torch.from_numpy(x).to(dev) for x in wl.batch(s))
+        loss, grad = layer.step(H, idx, val, cfg.lr)
+        outs.append((loss.clone(), grad.clone()))
+    assert layer.sync() == 0
+    return layer, outs
+
+
+def test_state_invariants(gpu_lib):
+    cfg = _cfg(D=4000, d=70, m=24, K=6, lr=5e-3, distinct=True, entropy=107)
+    layer, _ = _layer_after(cfg, 20)
+    Q, U, Uit = (x.cpu().numpy().astype(np.float64) for x in layer.get_state())
+    W = layer.materialize_W().cpu().numpy().astype(np.float64)
+    assert np.array_equal(Q, Q.T), "Q is not bitwise symmetric"
+    assert rel(Q, W.T @ W) < 1e-4
+    assert np.abs(U @ Uit.T - np.eye(cfg.d)).max() < 1e-4
+
+
+def test_determinism(gpu_lib):
+    cfg = _cfg(D=2000, d=48, m=32, K=8, lr=5e-3, idx_dist="zipf", zipf_s=1.1, entropy=108)
+    a, oa = _layer_after(cfg, 10)
+    b, ob = _layer_after(cfg, 10)
+    for x, y in zip(a.get_state(), b.get_state()):
+        assert torch.equal(x, y)
+    assert torch.equal(a.get_V(), b.get_V())
+    for (la, ga), (lb, gb) in zip(oa, ob):
+        assert torch.equal(la, lb) and torch.equal(ga, gb)
+
+
+def test_restore_keeps_W_and_Q(gpu_lib):
+    cfg = _cfg(D=1500, d=33, m=10, K=5, lr=2e-2, entropy=109)
+    layer, _ = _layer_after(cfg, 8)
+    W1 = layer.materialize_W().cpu().numpy()
+    Q1 = layer.get_state()[0].cpu().numpy()
+    layer.restore()
+    W2 = layer.materialize_W().cpu().numpy()
+    Q2, U2, Uit2 = (x.cpu().numpy() for x in layer.get_state())
+    assert layer.sync() == 0
+    assert rel(W2, W1) < 1e-5
+    assert np.array_equal(Q2, Q1)
+    assert np.array_equal(U2, np.eye(cfg.d, dtype=np.float32))
+    assert np.array_equal(Uit2, np.eye(cfg.d, dtype=np.float32))
+
+
+# ------------------------------------------------------------------ errors
+def _snapshot(layer):
+    return [x.clone() for x in layer.get_state()] + [layer.get_V().clone()]
+
+
+def test_bad_index_leaves_state_unchanged(gpu_lib):
+    import paper_1412_7091_amd as lst
+
+    cfg = _cfg(D=500, d=16, m=4, K=3, entropy=110)
+    layer, _ = _layer_after(cfg, 2)
+    before = _snapshot(layer)
+    wl = Workload(cfg)
+    H, idx, val = wl.batch(5)
+    idx[1, 2] = cfg.D  # out of range
+    dev = torch.device("cuda:0")
+    layer.step(torch.from_numpy(H).to(dev), torch.from_numpy(idx).to(dev),
+               torch.from_numpy(val).to(dev), cfg.lr)
+    assert layer.sync() == lst.LST_EINDEX
+    after = _snapshot(layer)
+    for x, y in zip(before, after):
+        assert torch.equal(x, y)
+    # the error is cleared by sync: the next good step works
+    H, idx, val = (torch.from_numpy(x).to(dev) for x in wl.batch(6))
+    layer.step(H, idx, val, cfg.lr)
+    assert layer.sync() == 0
+
+
+def test_singular_woodbury_matrix(gpu_lib):
+    """lr = 1/8 and h = (2, 0, ...): 2 lr ||h||^2 = 1, so H^T H - I/(2 lr) = 0 exactly."""
+    import paper_1412_7091_amd as lst
+
+    d, D = 8, 100
+    dev = torch.device("cuda:0")
+    V0 = torch.from_numpy(Workload(_cfg(D=D, d=d, m=1, K=1)).init_V()).to(dev)
+    layer = lst.FactoredOutputLayer(V0, m_max=1, K_max=1)
+    before = _snapshot(layer)
+    H = torch.zeros((1, d), dtype=torch.float32, device=dev)
+    H[0, 0] = 2.0
+    idx = torch.tensor([[3]], dtype=torch.int32, device=dev)
+    val = torch.tensor([[1.0]], dtype=torch.float32, device=dev)
+    layer.step(H, idx, val, 0.125)
+    assert layer.sync() == lst.LST_ESINGULAR
+    for x, y in zip(before, _snapshot(layer)):
+        assert torch.equal(x, y)
+
+
+def test_spherical_requires_a_class(gpu_lib):
+    import paper_1412_7091_amd as lst
+
+    dev = torch.device("cuda:0")
+    V0 = torch.from_numpy(Workload(_cfg(D=50, d=8, m=2, K=1)).init_V()).to(dev)
+    layer = lst.FactoredOutputLayer(V0, loss="spherical", m_max=2, K_max=1)
+    H = torch.randn((2, 8), device=dev)
+    idx = torch.tensor([[4], [-1]], dtype=torch.int32, device=dev)
+    layer.step(H, idx, None, 0.01)
+    assert layer.sync() == lst.LST_EINDEX
+
+
+def test_host_argument_errors(gpu_lib):
+    import paper_1412_7091_amd as lst
+
+    dev = torch.device("cuda:0")
+    V0 = torch.from_numpy(Workload(_cfg(D=50, d=8, m=2, K=2)).init_V()).to(dev)
+    layer = lst.FactoredOutputLayer(V0, m_max=2, K_max=2)
+    H = torch.randn((3, 8), device=dev)
+    idx = torch.zeros((3, 2), dtype=torch.int32, device=dev)
+    val = torch.ones((3, 2), device=dev)
+    with pytest.raises(lst.LstError) as e:
+        layer.step(H, idx, val, 0.01)           # m > m_max
+    assert e.value.code == lst.LST_EINVAL
+    with pytest.raises(lst.LstError) as e:
+        layer.step(H[:2], idx[:2], val[:2], 0.0)  # lr must be > 0
+    assert e.value.code == lst.LST_EINVAL
+    with pytest.raises(lst.LstError) as e:
+        layer.step(H[:2], idx[:2], val[:2], float("nan"))
+    assert e.value.code == lst.LST_EINVAL
+    assert layer.sync() == 0
