@@ -1,27 +1,28 @@
 // C ABI of the library: state ownership, argument checks and the order of the
 // kernels of one step.
 //
-// Factored step (Appendix A), with H^T as the m x d row-major input:
-//   side stream : validate + sort each example's targets -> Y^T Y ; global
-//                 (row, slot) sort -> distinct rows and their segments
-//   main stream : gather  G = (V^T Y)^T                                   (step 2, sparse part)
-//                 GEMM 1  [Q; U; U^{-T}; H^T] H -> H^, U H, P = U^{-T} H, H^T H  (steps 1, 7, 8)
-//                 GEMM 2  Y^ = U^T (V^T Y)                                 (step 2)
-//                 GEMM 3  H^T H^, H^T Y^                                   (step 5)
-//                 scalars: loss_i, a_i, b_i, N = (dL/dO)^T dL/dO, S = H^T H - A^{-1}/lr
-//                 S^{-1} (Gauss-Jordan)                                    (step 8, m x m inverse)
-//                 GEMM 4  X = S^{-1} P^T ; grad_H = H^ A + Y^ diag(b),
-//                         T = grad_H - (lr/2) N H^T                        (steps 3-4)
-//                 GEMM 5  U -= lr (U H) A H^T ; U^{-T} -= X^T H^T ;
-//                         Q -= lr (H T^T + T H^T)                          (steps 7, 8, 10)
-//                 scatter V[r] += sum_(i,k): idx=r of c_ik X_i           (step 9)
-//                 [drift control: Appendix C pristine restore]
+// Factored step (Appendix A), with H^T as the m x d row-major input, on two
+// streams (the caller's "main" stream and a library "side" stream):
+//   side : gather G = (V^T Y)^T (step 2, sparse part)
+//          validate + sort each example's targets, Y^T Y; global (row, slot)
+//          sort -> distinct rows and their segments
+//   main : GEMM 1  [Q; U; U^{-T}; H^T] H -> H^ = QH, UH, P = U^{-T}H, H^T H   (steps 1, 7, 8)
+//   side : X = S^{-1} P^T with S = H^T H - diag(1/(lr a_i))                 (step 8, m x m system)
+//   main : GEMM 2  Y^ = U^T G^T ; C1 = H^T H^ ; C2 = H^T Y^ = (UH)^T G^T       (steps 2, 5)
+//          scalars: loss_i, a_i, b_i, N = (dL/dO)^T dL/dO                   (steps 3-6)
+//          GEMM 3  grad_H = H^ A + Y^ diag(b), T = grad_H - (lr/2) N H^T ;
+//                  U -= lr (UH) A H^T ; U^{-T} -= X^T H^T                    (steps 4, 7, 8)
+//          GEMM 4  Q -= lr (H T^T + T H^T)                                 (step 10)
+//   side : V[r] += sum over pairs (i,k) with idx = r of c_ik X_i           (step 9)
+//   main : [drift control: Appendix C pristine restore]
 // Derivation of the shortcuts (exact in real arithmetic):
 //   U_new^{-T} H = -(1/lr) P S^{-1} A^{-1}, so with X = S^{-1} P^T (m x d):
 //   U_new^{-T} = U^{-T} - X^T H^T and V_new = V - lr G (U_new^{-T} H)^T
 //   = V + sum_i (g_i / a_i) X_i, i.e. c = -val (squared) or b_i / a_i (spherical);
 //   Q_new = Q - lr (H grad_H^T + grad_H H^T) + lr^2 H N H^T
 //         = Q - lr (H T^T + T H^T) with T = grad_H - (lr/2) H N.
+// Every update of the state (U, U^{-T}, Q, V) runs after every check that can
+// raise a device error of this step, and skips when the error flag is set.
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
@@ -40,16 +41,16 @@ struct lst_state {
   int device = 0;
   hipStream_t stream = nullptr;
   hipStream_t side = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_yy = nullptr, ev_sort = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_gather = nullptr, ev_yy = nullptr, ev_g1 = nullptr,
+            ev_p2 = nullptr, ev_p3 = nullptr, ev_solve = nullptr, ev_done = nullptr;
   float* V = nullptr;      // V (factored) or W (naive), D x d
   float* state = nullptr;  // [Q; U; U^{-T}], 3d x d
   float* Vtmp = nullptr;   // D x d copy for the pristine restore
   int* flags = nullptr;
   // factored workspace
   float *G = nullptr, *Z0 = nullptr, *Yh = nullptr, *C12 = nullptr, *Nm = nullptr,
-        *Sm = nullptr, *Sinv = nullptr, *a = nullptr, *b = nullptr, *cs = nullptr,
-        *T = nullptr, *X = nullptr;
-  double* gjwork = nullptr;
+        *a = nullptr, *b = nullptr, *cs = nullptr, *T = nullptr, *X = nullptr,
+        *solve_ws = nullptr;
   SparseWs sp{};
   int ld0 = 0, ldc12 = 0;
   // naive workspace
@@ -101,15 +102,16 @@ int dalloc(lst_state* s, T** p, size_t count) {
   } while (0)
 
 enum Phase {
-  PH_GATHER = 0, PH_GEMM_STACK, PH_GEMM_YHAT, PH_GEMM_M, PH_SCALARS, PH_INVERSE, PH_GEMM_XT,
-  PH_GEMM_UPDATE, PH_SCATTER, PH_DRIFT, PH_COUNT
+  PH_GATHER = 0, PH_PREP, PH_GEMM_STACK, PH_SOLVE, PH_GEMM_P2, PH_SCALARS, PH_GEMM_P3,
+  PH_GEMM_Q, PH_SCATTER, PH_DRIFT, PH_COUNT
 };
 const char* const kPhaseNames[PH_COUNT] = {
-    "gather", "gemm_stack", "gemm_yhat", "gemm_m", "scalars", "inverse", "gemm_xt",
-    "gemm_update", "scatter", "drift"};
+    "gather", "prep", "gemm_stack", "solve", "gemm_p2", "scalars", "gemm_p3", "gemm_q",
+    "scatter", "drift"};
 
-// Records the begin (end = 0) or end (end = 1) event of a phase when profiling.
-int prof_mark(lst_state* s, int phase, int end) {
+// Records the begin (end = 0) or end (end = 1) event of a phase on stream st
+// when profiling.
+int prof_mark(lst_state* s, int phase, int end, hipStream_t st) {
   if (!s->prof) return LST_OK;
   const size_t slot = (size_t)(s->prof_steps - 1) * (2 * PH_COUNT) + 2 * phase + end;
   while (s->prof_events.size() <= slot) {
@@ -117,7 +119,7 @@ int prof_mark(lst_state* s, int phase, int end) {
     HIPCHK(hipEventCreate(&e));
     s->prof_events.push_back(e);
   }
-  HIPCHK(hipEventRecord(s->prof_events[slot], s->stream));
+  HIPCHK(hipEventRecord(s->prof_events[slot], st));
   if (slot + 1 > s->prof_used) s->prof_used = slot + 1;
   return LST_OK;
 }
@@ -130,9 +132,9 @@ void release(lst_state* s) {
   }
   for (void* p : s->allocs) (void)hipFree(p);
   s->allocs.clear();
-  if (s->ev_fork) (void)hipEventDestroy(s->ev_fork);
-  if (s->ev_yy) (void)hipEventDestroy(s->ev_yy);
-  if (s->ev_sort) (void)hipEventDestroy(s->ev_sort);
+  for (hipEvent_t e : {s->ev_fork, s->ev_gather, s->ev_yy, s->ev_g1, s->ev_p2, s->ev_p3,
+                       s->ev_solve, s->ev_done})
+    if (e) (void)hipEventDestroy(e);
   if (s->side) (void)hipStreamDestroy(s->side);
   for (hipEvent_t e : s->prof_events) (void)hipEventDestroy(e);
   delete s;
@@ -147,9 +149,10 @@ int check_config(const lst_config* cfg) {
   if (cfg->loss != LST_LOSS_SQUARED && cfg->loss != LST_LOSS_SPHERICAL) return LST_EINVAL;
   if (cfg->loss == LST_LOSS_SPHERICAL && !(cfg->sph_eps > 0.f && isfinite(cfg->sph_eps)))
     return LST_EINVAL;
-  if (cfg->m_max < 1 || cfg->m_max > 4096) return LST_EINVAL;
+  if (cfg->m_max < 1) return LST_EINVAL;
   if (cfg->K_max < 1 || cfg->K_max > 1024) return LST_EINVAL;
   if ((int64_t)cfg->m_max * cfg->K_max > 16384) return LST_EINVAL;
+  if (cfg->m_max > 512) return LST_EINVAL;
   if (!(cfg->cond_max >= 0.f) || !isfinite(cfg->cond_max)) return LST_EINVAL;
   return LST_OK;
 }
@@ -161,9 +164,9 @@ int common_init(lst_state* s, int64_t D, int32_t d, const lst_config* cfg, void*
   HIPCHK(hipGetDevice(&s->device));
   s->stream = static_cast<hipStream_t>(hip_stream);
   HIPCHK(hipStreamCreateWithFlags(&s->side, hipStreamNonBlocking));
-  HIPCHK(hipEventCreateWithFlags(&s->ev_fork, hipEventDisableTiming));
-  HIPCHK(hipEventCreateWithFlags(&s->ev_yy, hipEventDisableTiming));
-  HIPCHK(hipEventCreateWithFlags(&s->ev_sort, hipEventDisableTiming));
+  for (hipEvent_t* e : {&s->ev_fork, &s->ev_gather, &s->ev_yy, &s->ev_g1, &s->ev_p2, &s->ev_p3,
+                        &s->ev_solve, &s->ev_done})
+    HIPCHK(hipEventCreateWithFlags(e, hipEventDisableTiming));
   OK_OR_RETURN(dalloc(s, &s->flags, F_COUNT));
   HIPCHK(hipMemsetAsync(s->flags, 0, F_COUNT * sizeof(int), s->stream));
   OK_OR_RETURN(dalloc(s, &s->V, (size_t)D * d));
@@ -182,11 +185,11 @@ int gram_splitk(lst_state* s, const float* A, int64_t Krows, int n, float* C, fl
   if (hipMalloc((void**)&ws, (size_t)ks * n * n * sizeof(float)) != hipSuccess) return LST_ENOMEM;
   GemmBatch bt{};
   bt.np = 1;
-  bt.p[0] = gemm_problem(n, n, (int)Krows, vmat(A, n, (int)Krows), vmat(A, n, (int)Krows), ws, n,
-                         1.f, 0.f, EPI_PARTIAL);
+  bt.p[0] = gemm_problem(L_TN, n, n, (int)Krows, vmat(A, n, (int)Krows), vmat(A, n, (int)Krows),
+                         ws, n, 1.f, 0.f, EPI_PARTIAL);
   bt.p[0].ksplit = (int)ks;
   int rc = LST_OK;
-  if (gemm_launch(L_TN, bt, s->stream) != hipSuccess) rc = LST_EHIP;
+  if (gemm_launch(bt, s->stream) != hipSuccess) rc = LST_EHIP;
   if (rc == LST_OK &&
       gemm_splitk_reduce(ws, (int)ks, n, n, C, n, alpha, 0.f, 1, nullptr, s->stream) != hipSuccess)
     rc = LST_EHIP;
@@ -200,11 +203,11 @@ int vu_product(lst_state* s, const float* Vsrc, float* Wdst, const int* run_if,
                const int* skip_if) {
   GemmBatch bt{};
   bt.np = 1;
-  bt.p[0] = gemm_problem((int)s->D, s->d, s->d, vmat(Vsrc, s->d, (int)s->D), vmat(Up(s), s->d, s->d),
-                         Wdst, s->d, 1.f, 0.f, EPI_STORE);
+  bt.p[0] = gemm_problem(L_NN, (int)s->D, s->d, s->d, vmat(Vsrc, s->d, (int)s->D),
+                         vmat(Up(s), s->d, s->d), Wdst, s->d, 1.f, 0.f, EPI_STORE);
   bt.run_if = run_if;
   bt.skip_if = skip_if;
-  HIPCHK(gemm_launch(L_NN, bt, s->stream));
+  HIPCHK(gemm_launch(bt, s->stream));
   return LST_OK;
 }
 
@@ -263,17 +266,16 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
     return code;
   };
   if (rc != LST_OK) return fail(rc);
-  s->ld0 = 3 * d + m;
+  s->ld0 = (3 * d + m + 3) / 4 * 4;
   s->ldc12 = 2 * m;
   const size_t md = (size_t)m * d;
   if ((rc = dalloc(s, &s->state, 3 * (size_t)d * d)) ||
       (rc = dalloc(s, &s->G, md)) || (rc = dalloc(s, &s->Z0, (size_t)m * s->ld0)) ||
       (rc = dalloc(s, &s->Yh, md)) || (rc = dalloc(s, &s->C12, (size_t)m * s->ldc12)) ||
-      (rc = dalloc(s, &s->Nm, (size_t)m * m)) || (rc = dalloc(s, &s->Sm, (size_t)m * m)) ||
-      (rc = dalloc(s, &s->Sinv, (size_t)m * m)) || (rc = dalloc(s, &s->a, m)) ||
+      (rc = dalloc(s, &s->Nm, (size_t)m * m)) || (rc = dalloc(s, &s->a, m)) ||
       (rc = dalloc(s, &s->b, m)) || (rc = dalloc(s, &s->cs, m)) || (rc = dalloc(s, &s->T, md)) ||
       (rc = dalloc(s, &s->X, md)) ||
-      (rc = dalloc(s, &s->gjwork, (size_t)(m > 128 ? m : 1) * (m > 128 ? m : 1))) ||
+      (rc = dalloc(s, &s->solve_ws, woodbury_workspace_floats(m, d))) ||
       (rc = dalloc(s, &s->sp.ex_row, (size_t)m * K)) ||
       (rc = dalloc(s, &s->sp.ex_val, (size_t)m * K)) || (rc = dalloc(s, &s->sp.ex_cnt, m)) ||
       (rc = dalloc(s, &s->sp.keys, (size_t)m * K)) ||
@@ -327,67 +329,102 @@ int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* 
   hipStream_t st = s->stream;
   int* fl = s->flags;
   float* U = Up(s);
-
   if (s->prof) s->prof_steps += 1;
-  // side stream: target ordering and Y^T Y
-  HIPCHK(hipEventRecord(s->ev_fork, st));
-  HIPCHK(hipStreamWaitEvent(s->side, s->ev_fork, 0));
-  HIPCHK(prep_examples(Y_idx, Y_val, m, K, D, one_hot, s->sp, fl, s->side));
-  HIPCHK(prep_target_gram(m, K, s->sp, s->side));
-  HIPCHK(hipEventRecord(s->ev_yy, s->side));
-  HIPCHK(prep_global_sort(m, K, s->sp, fl, s->side));
-  HIPCHK(hipEventRecord(s->ev_sort, s->side));
 
-  // step 2, sparse part: G = (V^T Y)^T
-  OK_OR_RETURN(prof_mark(s, PH_GATHER, 0));
-  HIPCHK(gather_rows(s->V, D, d, Y_idx, Y_val, m, K, one_hot, s->G, d, st));
-  OK_OR_RETURN(prof_mark(s, PH_GATHER, 1));
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_STACK, 0));
-  {  // GEMM 1: Z0 = H^T [Q; U; U^{-T}; H^T]^T   (m x (3d + m))
+  hipStream_t sd = s->side;
+  const bool sq = s->cfg.loss == LST_LOSS_SQUARED;
+  HIPCHK(hipEventRecord(s->ev_fork, st));
+  HIPCHK(hipStreamWaitEvent(sd, s->ev_fork, 0));
+
+  // side: G = (V^T Y)^T, then the target ordering and Y^T Y
+  OK_OR_RETURN(prof_mark(s, PH_GATHER, 0, sd));
+  HIPCHK(gather_rows(s->V, D, d, Y_idx, Y_val, m, K, one_hot, s->G, d, sd));
+  OK_OR_RETURN(prof_mark(s, PH_GATHER, 1, sd));
+  HIPCHK(hipEventRecord(s->ev_gather, sd));
+  OK_OR_RETURN(prof_mark(s, PH_PREP, 0, sd));
+  HIPCHK(prep_examples(Y_idx, Y_val, m, K, D, one_hot, s->sp, fl, sd));
+  HIPCHK(prep_target_gram(m, K, s->sp, sd));
+  HIPCHK(hipEventRecord(s->ev_yy, sd));
+  HIPCHK(prep_global_sort(m, K, s->sp, fl, sd));
+  OK_OR_RETURN(prof_mark(s, PH_PREP, 1, sd));
+
+  // main, GEMM 1: Z0 = H^T [Q; U; U^{-T}; H^T]^T   (m x (3d + m))
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_STACK, 0, st));
+  {
     GemmBatch bt{};
     bt.np = 1;
-    bt.p[0] = gemm_problem(m, 3 * d + m, d, vmat(H, d, m), vmat2(s->state, d, 3 * d, H, d, m),
-                           s->Z0, s->ld0, 1.f, 0.f, EPI_STORE);
-    HIPCHK(gemm_launch(L_NT, bt, st));
+    bt.p[0] = gemm_problem(L_NT, m, 3 * d + m, d, vmat(H, d, m),
+                           vmat2(s->state, d, 3 * d, H, d, m), s->Z0, s->ld0, 1.f, 0.f, EPI_STORE);
+    HIPCHK(gemm_launch(bt, st));
   }
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_STACK, 1));
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_YHAT, 0));
-  {  // GEMM 2: Y^ (rows) = G U
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_STACK, 1, st));
+  HIPCHK(hipEventRecord(s->ev_g1, st));
+
+  const float* Hh = s->Z0;           // H^ rows
+  const float* UH = s->Z0 + d;       // (U H)^T rows
+  const float* Pm = s->Z0 + 2 * d;   // P^T rows
+  const float* HH = s->Z0 + 3 * d;   // H^T H
+  // side: the Woodbury system (the spherical weights need C1 from GEMM 2, so
+  // that case is enqueued after GEMM 2 below)
+  if (sq) {
+    HIPCHK(hipStreamWaitEvent(sd, s->ev_g1, 0));
+    OK_OR_RETURN(prof_mark(s, PH_SOLVE, 0, sd));
+    HIPCHK(woodbury_solve(HH, s->ld0, Pm, s->ld0, m, d, s->cfg.loss, s->cfg.sph_eps, D, lr,
+                          s->C12, s->ldc12, s->X, d, s->solve_ws, fl, sd));
+    OK_OR_RETURN(prof_mark(s, PH_SOLVE, 1, sd));
+    HIPCHK(hipEventRecord(s->ev_solve, sd));
+  }
+
+  // main, GEMM 2: Y^ = G U ; C1 = H^T H^ ; C2 = (UH)^T G^T
+  HIPCHK(hipStreamWaitEvent(st, s->ev_gather, 0));
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_P2, 0, st));
+  {
     GemmBatch bt{};
-    bt.np = 1;
-    bt.p[0] = gemm_problem(m, d, d, vmat(s->G, d, m), vmat(U, d, d), s->Yh, d, 1.f, 0.f,
+    bt.np = 3;
+    bt.p[0] = gemm_problem(L_NN, m, d, d, vmat(s->G, d, m), vmat(U, d, d), s->Yh, d, 1.f, 0.f,
                            EPI_STORE);
-    HIPCHK(gemm_launch(L_NN, bt, st));
-  }
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_YHAT, 1));
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_M, 0));
-  {  // GEMM 3: C12 = [H^T H^ | H^T Y^]
-    GemmBatch bt{};
-    bt.np = 1;
-    bt.p[0] = gemm_problem(m, 2 * m, d, vmat(H, d, m), vmat2(s->Z0, s->ld0, m, s->Yh, d, m),
-                           s->C12, s->ldc12, 1.f, 0.f, EPI_STORE);
-    HIPCHK(gemm_launch(L_NT, bt, st));
-  }
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_M, 1));
-  HIPCHK(hipStreamWaitEvent(st, s->ev_yy, 0));
-  OK_OR_RETURN(prof_mark(s, PH_SCALARS, 0));
-  HIPCHK(minibatch_scalars(s->cfg.loss, s->cfg.sph_eps, D, lr, m, s->C12, s->ldc12,
-                           s->Z0 + 3 * d, s->ld0, s->sp.yy, loss, s->a, s->b, s->cs, s->Nm, s->Sm,
-                           fl, st));
-  OK_OR_RETURN(prof_mark(s, PH_SCALARS, 1));
-  OK_OR_RETURN(prof_mark(s, PH_INVERSE, 0));
-  HIPCHK(invert_small(s->Sm, m, s->Sinv, m, m, s->gjwork, fl, 1, st));
-  OK_OR_RETURN(prof_mark(s, PH_INVERSE, 1));
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_XT, 0));
-  {  // GEMM 4: X = S^{-1} P^T ; grad_H and T
-    GemmBatch bt{};
-    bt.np = 2;
-    bt.p[0] = gemm_problem(m, d, m, vmat(s->Sinv, m, m), vmat(s->Z0 + 2 * d, s->ld0, m), s->X, d,
+    bt.p[1] = gemm_problem(L_NT, m, m, d, vmat(H, d, m), vmat(Hh, s->ld0, m), s->C12, s->ldc12,
                            1.f, 0.f, EPI_STORE);
-    GemmProblem& pt = bt.p[1];
-    pt = gemm_problem(m, d, m, vmat(s->Nm, m, m), vmat(H, d, m), s->T, d, -0.5f * lr, 0.f,
+    bt.p[2] = gemm_problem(L_NT, m, m, d, vmat(UH, s->ld0, m), vmat(s->G, d, m), s->C12 + m,
+                           s->ldc12, 1.f, 0.f, EPI_STORE);
+    HIPCHK(gemm_launch(bt, st));
+  }
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_P2, 1, st));
+  HIPCHK(hipEventRecord(s->ev_p2, st));
+  if (!sq) {
+    HIPCHK(hipStreamWaitEvent(sd, s->ev_p2, 0));
+    OK_OR_RETURN(prof_mark(s, PH_SOLVE, 0, sd));
+    HIPCHK(woodbury_solve(HH, s->ld0, Pm, s->ld0, m, d, s->cfg.loss, s->cfg.sph_eps, D, lr,
+                          s->C12, s->ldc12, s->X, d, s->solve_ws, fl, sd));
+    OK_OR_RETURN(prof_mark(s, PH_SOLVE, 1, sd));
+    HIPCHK(hipEventRecord(s->ev_solve, sd));
+  }
+
+  // main: per-example scalars and N
+  HIPCHK(hipStreamWaitEvent(st, s->ev_yy, 0));
+  OK_OR_RETURN(prof_mark(s, PH_SCALARS, 0, st));
+  HIPCHK(minibatch_scalars(s->cfg.loss, s->cfg.sph_eps, D, m, s->C12, s->ldc12, s->sp.yy, loss,
+                           s->a, s->b, s->cs, s->Nm, fl, st));
+  OK_OR_RETURN(prof_mark(s, PH_SCALARS, 1, st));
+  HIPCHK(hipEventRecord(s->ev_p3, st));
+
+  // side: scatter into V once every check of this step has run
+  HIPCHK(hipStreamWaitEvent(sd, s->ev_p3, 0));
+  OK_OR_RETURN(prof_mark(s, PH_SCATTER, 0, sd));
+  HIPCHK(scatter_rows(s->V, d, s->X, d, Y_val, one_hot ? s->cs : nullptr, m, K, s->sp, fl, sd));
+  OK_OR_RETURN(prof_mark(s, PH_SCATTER, 1, sd));
+  HIPCHK(hipEventRecord(s->ev_done, sd));
+
+  // main, GEMM 3: grad_H and T ; rank-m updates of U and U^{-T}
+  HIPCHK(hipStreamWaitEvent(st, s->ev_solve, 0));
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_P3, 0, st));
+  {
+    GemmBatch bt{};
+    bt.np = 3;
+    GemmProblem& pt = bt.p[0];
+    pt = gemm_problem(L_NN, m, d, m, vmat(s->Nm, m, m), vmat(H, d, m), s->T, d, -0.5f * lr, 0.f,
                       EPI_GRADT);
-    pt.e1 = s->Z0;
+    pt.e1 = Hh;
     pt.lde1 = s->ld0;
     pt.e2 = s->Yh;
     pt.lde2 = d;
@@ -395,28 +432,29 @@ int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* 
     pt.s2 = s->b;
     pt.g = grad_H;
     pt.ldg = d;
-    HIPCHK(gemm_launch(L_NN, bt, st));
-  }
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_XT, 1));
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_UPDATE, 0));
-  {  // GEMM 5: rank-m updates of U, U^{-T} and the symmetric rank-2m update of Q
-    GemmBatch bt{};
-    bt.np = 3;
-    bt.skip_if = fl + F_ERR;
-    bt.p[0] = gemm_problem(d, d, m, vmat(s->Z0 + d, s->ld0, m, s->a), vmat(H, d, m), U, d, -lr,
+    // the updates below skip on error; the gradient product above must still run
+    bt.p[1] = gemm_problem(L_TN, d, d, m, vmat(UH, s->ld0, m, s->a), vmat(H, d, m), U, d, -lr,
                            1.f, EPI_STORE);
-    bt.p[1] = gemm_problem(d, d, m, vmat(s->X, d, m), vmat(H, d, m), Uitp(s), d, -1.f, 1.f,
+    bt.p[2] = gemm_problem(L_TN, d, d, m, vmat(s->X, d, m), vmat(H, d, m), Uitp(s), d, -1.f, 1.f,
                            EPI_STORE);
-    bt.p[2] = gemm_problem(d, d, 2 * m, vmat2(H, d, m, s->T, d, m), vmat2(s->T, d, m, H, d, m),
-                           Qp(s), d, -lr, 1.f, EPI_SYM);
-    HIPCHK(gemm_launch(L_TN, bt, st));
+    bt.skip_updates_if = fl + F_ERR;
+    bt.first_update = 1;
+    HIPCHK(gemm_launch(bt, st));
   }
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_UPDATE, 1));
-  HIPCHK(hipStreamWaitEvent(st, s->ev_sort, 0));
-  OK_OR_RETURN(prof_mark(s, PH_SCATTER, 0));
-  HIPCHK(scatter_rows(s->V, d, s->X, d, Y_val, one_hot ? s->cs : nullptr, m, K, s->sp, fl, st));
-  OK_OR_RETURN(prof_mark(s, PH_SCATTER, 1));
-  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 0));
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_P3, 1, st));
+  // main, GEMM 4: Q -= lr (H T^T + T H^T), symmetric
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_Q, 0, st));
+  {
+    GemmBatch bt{};
+    bt.np = 1;
+    bt.skip_if = fl + F_ERR;
+    bt.p[0] = gemm_problem(L_TN, d, d, 2 * m, vmat2(H, d, m, s->T, d, m),
+                           vmat2(s->T, d, m, H, d, m), Qp(s), d, -lr, 1.f, EPI_SYM);
+    HIPCHK(gemm_launch(bt, st));
+  }
+  OK_OR_RETURN(prof_mark(s, PH_GEMM_Q, 1, st));
+  HIPCHK(hipStreamWaitEvent(st, s->ev_done, 0));
+  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 0, st));
   if (s->cfg.cond_max > 0.f) {
     HIPCHK(drift_check(U, Uitp(s), d, s->cfg.cond_max * (float)d, fl, st));
     HIPCHK(copy_if(s->V, s->Vtmp, (size_t)D * d, fl + F_RESTORE, st));
@@ -424,7 +462,7 @@ int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* 
     HIPCHK(set_identity_if(U, d, fl + F_RESTORE, st));
     HIPCHK(set_identity_if(Uitp(s), d, fl + F_RESTORE, st));
   }
-  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 1));
+  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 1, st));
   s->steps += 1;
   return LST_OK;
 }
@@ -531,19 +569,19 @@ int lst_naive_step(lst_state* s, int32_t m, int32_t K, const float* H, const int
   {  // O (m x D) = H^T W^T: every output of every example, O(D d) each
     GemmBatch bt{};
     bt.np = 1;
-    bt.p[0] = gemm_problem(m, (int)D, d, vmat(H, d, m), vmat(s->V, d, (int)D), s->O, (int)D, 1.f,
-                           0.f, EPI_STORE);
-    HIPCHK(gemm_launch(L_NT, bt, st));
+    bt.p[0] = gemm_problem(L_NT, m, (int)D, d, vmat(H, d, m), vmat(s->V, d, (int)D), s->O,
+                           (int)D, 1.f, 0.f, EPI_STORE);
+    HIPCHK(gemm_launch(bt, st));
   }
   HIPCHK(naive_rowstats(s->O, D, D, m, Y_idx, Y_val, K, s->cfg.loss, s->cfg.sph_eps, loss,
                         s->flags, st));
   {  // grad_H = (dL/dO) W  (K = D, split over K)
     GemmBatch bt{};
     bt.np = 1;
-    bt.p[0] = gemm_problem(m, d, (int)D, vmat(s->O, (int)D, m), vmat(s->V, d, (int)D), s->wsplit,
-                           d, 1.f, 0.f, EPI_PARTIAL);
+    bt.p[0] = gemm_problem(L_NN, m, d, (int)D, vmat(s->O, (int)D, m), vmat(s->V, d, (int)D),
+                           s->wsplit, d, 1.f, 0.f, EPI_PARTIAL);
     bt.p[0].ksplit = s->naive_ksplit;
-    HIPCHK(gemm_launch(L_NN, bt, st));
+    HIPCHK(gemm_launch(bt, st));
     HIPCHK(gemm_splitk_reduce(s->wsplit, s->naive_ksplit, m, d, grad_H, d, sq ? 2.f : 1.f, 0.f, 0,
                               nullptr, st));
   }
@@ -551,9 +589,9 @@ int lst_naive_step(lst_state* s, int32_t m, int32_t K, const float* H, const int
     GemmBatch bt{};
     bt.np = 1;
     bt.skip_if = s->flags + F_ERR;
-    bt.p[0] = gemm_problem((int)D, d, m, vmat(s->O, (int)D, m), vmat(H, d, m), s->V, d,
+    bt.p[0] = gemm_problem(L_TN, (int)D, d, m, vmat(s->O, (int)D, m), vmat(H, d, m), s->V, d,
                            sq ? -2.f * lr : -lr, 1.f, EPI_STORE);
-    HIPCHK(gemm_launch(L_TN, bt, st));
+    HIPCHK(gemm_launch(bt, st));
   }
   s->steps += 1;
   return LST_OK;

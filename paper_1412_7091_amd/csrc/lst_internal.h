@@ -49,6 +49,7 @@ enum Layout {
 
 struct GemmProblem {
   int M, N, K;
+  int a_kc, b_kc;   // 1: the operand's rows are the output dimension (K contiguous)
   VMat A, B;
   float* C;
   int ldc;
@@ -72,14 +73,17 @@ struct GemmBatch {
   int total_tiles;
   const int* skip_if;  // nonzero *skip_if: every block returns at once
   const int* run_if;   // zero *run_if: every block returns at once
+  const int* skip_updates_if;  // nonzero: blocks of problems >= first_update return at once
+  int first_update;
 };
 
 VMat vmat(const float* p, int ld, int rows, const float* rscale = nullptr);
 VMat vmat2(const float* p0, int ld0, int rows0, const float* p1, int ld1, int rows1);
-GemmProblem gemm_problem(int M, int N, int K, const VMat& A, const VMat& B, float* C, int ldc,
-                         float alpha, float beta, int epi);
-// Launches every problem of the batch (all of one layout) in one grid.
-hipError_t gemm_launch(int layout, GemmBatch& b, hipStream_t s);
+GemmProblem gemm_problem(int layout, int M, int N, int K, const VMat& A, const VMat& B, float* C,
+                         int ldc, float alpha, float beta, int epi);
+// Launches every problem of the batch in one grid.  tile: 64 or 32 (square
+// output tiles), 0 = choose from the number of tiles.
+hipError_t gemm_launch(GemmBatch& b, hipStream_t s, int tile = 0);
 // Split-K: C = alpha * sum_z ws[z] + beta * C (sym: r <= c mirrored).
 hipError_t gemm_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int ldc,
                               float alpha, float beta, int sym, const int* skip_if,
@@ -111,11 +115,16 @@ hipError_t scatter_rows(float* V, int d, const float* X, int ldx, const float* v
                         hipStream_t s);
 
 // ------------------------------------------------------------ small dense
-// Per-example loss terms and the m x m matrices N and S of the step.
-hipError_t minibatch_scalars(int loss_kind, float eps, int64_t D, float lr, int m,
-                             const float* C12, int ldc12, const float* HH, int ldhh,
-                             const float* yy, float* loss, float* a, float* b, float* cs,
-                             float* N, float* S, int* flags, hipStream_t s);
+// Per-example loss terms (loss, a, b, cs = b/a) and the m x m matrix N of the step.
+hipError_t minibatch_scalars(int loss_kind, float eps, int64_t D, int m, const float* C12,
+                             int ldc12, const float* yy, float* loss, float* a, float* b,
+                             float* cs, float* N, int* flags, hipStream_t s);
+// X = S^{-1} P^T (m x d) with S = H^T H - diag(1 / (lr a_i)), in 16-column blocks.
+hipError_t woodbury_solve(const float* HH, int ldh, const float* P, int ldp, int m, int d,
+                          int loss_kind, float eps, int64_t D, float lr, const float* C12,
+                          int ldc12, float* X, int ldx, float* gj_ws, int* flags, hipStream_t s);
+// Floats of global workspace woodbury_solve needs for its m > 128 fallback.
+size_t woodbury_workspace_floats(int m_max, int d);
 // Sinv = S^{-1} (Gauss-Jordan, partial pivoting); sets F_ERR = LST_ESINGULAR on a zero pivot.
 hipError_t invert_small(const float* S, int lds, float* Sinv, int ldi, int m, double* work,
                         int* flags, int check_err, hipStream_t s);
