@@ -65,10 +65,10 @@ enum {
 typedef struct lst_config {
   int32_t loss;      /* LST_LOSS_SQUARED or LST_LOSS_SPHERICAL                         */
   float sph_eps;     /* eps of the spherical softmax (> 0); unused for squared error   */
-  int32_t m_max;     /* largest minibatch any lst_step call will pass (1..4096)        */
+  int32_t m_max;     /* largest minibatch any lst_step call will pass (1..512)         */
   int32_t K_max;     /* largest K any lst_step call will pass (1..1024); m_max*K_max
-                        must not exceed 16384 (the target pairs of one step are
-                        ordered in one workgroup's LDS)                                */
+                        must not exceed 16384 (lst_touched_rows orders the touched
+                        rows of one step in one workgroup's LDS)                       */
   float cond_max;    /* drift control (Appendix C, pristine restore): after a step, if
                         ||U||_F * ||U^{-T}||_F > cond_max * d, set V <- V U, U <- I,
                         U^{-T} <- I (W and Q unchanged).  0 disables the check.      */
@@ -162,6 +162,18 @@ int lst_naive_init(lst_state** out, int64_t D, int32_t d, const float* W,
  */
 int lst_naive_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* Y_idx,
                    const float* Y_val, float lr, float* loss, float* grad_H);
+
+/*
+ * lst_set_graphs -- enable (the default) or disable HIP-graph replay of lst_step.
+ * When enabled, the first lst_step call with a given argument tuple
+ * (m, K, H, Y_idx, Y_val, lr, loss, grad_H) records its kernels into a graph and
+ * every later call with the same tuple replays that graph with a single launch
+ * on the state's stream (same kernels, same order, same results).  At most 32
+ * graphs are kept; the least recently used is released first.  Profiling
+ * (lst_profile_enable) bypasses the graphs.  Synchronises the stream and
+ * releases the cached graphs.
+ */
+int lst_set_graphs(lst_state* s, int32_t enable);
 
 /*
  * lst_sync -- wait for the state's stream; return and clear the sticky device

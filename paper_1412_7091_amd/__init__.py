@@ -77,6 +77,7 @@ _SIGS = {
     "lst_naive_step": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P, _P, _P,
                                       ctypes.c_float, _P, _P]),
     "lst_sync": (ctypes.c_int, [_P]),
+    "lst_set_graphs": (ctypes.c_int, [_P, ctypes.c_int32]),
     "lst_stats": (ctypes.c_int, [_P, ctypes.POINTER(lst_stats_t)]),
     "lst_profile_enable": (ctypes.c_int, [_P, ctypes.c_int32]),
     "lst_profile_read": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_double), ctypes.c_int32,
@@ -231,6 +232,10 @@ def lst_sync(h) -> int:
     return int(load_library().lst_sync(h))
 
 
+def lst_set_graphs(h, enable: bool = True) -> None:
+    _check(load_library().lst_set_graphs(h, 1 if enable else 0), "lst_set_graphs")
+
+
 def lst_stats(h) -> lst_stats_t:
     st = lst_stats_t()
     _check(load_library().lst_stats(h, ctypes.byref(st)), "lst_stats")
@@ -290,6 +295,9 @@ class _Layer:
 
     def sync(self) -> int:
         return lst_sync(self._h)
+
+    def set_graphs(self, enable: bool = True) -> None:
+        lst_set_graphs(self._h, enable)
 
     def profile(self, enable: bool = True) -> None:
         lst_profile_enable(self._h, enable)

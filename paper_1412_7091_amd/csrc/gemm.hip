@@ -1,196 +1,162 @@
-// fp32 MFMA GEMM family for the dense contractions of the step.
-//
-// The products of the minibatch algorithm (Appendix A steps 1, 2, 5, 7, 8, 10)
-// are small (m = 128 .. 512 on one side, d = 500 .. 1024 on the others), so
-// their time is dominated by memory latency, not by MFMA throughput.  The
-// kernel therefore stages a whole K-chunk of both operands (up to 256 for
-// 64 x 64 tiles, 512 for 32 x 32 tiles) into LDS with every global load of
-// the chunk in flight at once, then runs the MFMAs out of LDS.  Four waves
-// share a tile, each owning a quarter computed with v_mfma_f32_16x16x4f32.
-// Operands are "virtual" row-major matrices (stacked row blocks) and each
-// problem of a grouped launch carries its own layout and epilogue, so the
-// independent products of one phase of the step share a single launch.
-#include "lst_internal.h"
+// fp32 MFMA GEMM for the large products outside the step: the naive
+// explicit-W baseline, W = V U, the initial W^T W.  (The step's own small
+// products run as panel tiles inside the step kernel; see gemm_tile.h.)
+#include "gemm_tile.h"
 
 namespace lst {
 
-typedef float floatx4 __attribute__((ext_vector_type(4)));
+// ---------------------------------------------------------------------------
+// Large products (the naive explicit-W baseline, V U, the initial W^T W): a
+// classic streaming kernel.  128 x 128 output tiles, K in slices of 32 that
+// are double-buffered in LDS (the next slice is loaded while the current one
+// is multiplied), 2 x 2 waves each owning 64 x 64.  74 KB of LDS lets two
+// workgroups share a compute unit.
+// ---------------------------------------------------------------------------
+constexpr int GB_T = 128, GB_BK = 32, GB_LD = GB_BK + 4;
 
-template <int BM, int BN>
-struct Panel {
-  static constexpr int KC = (32768 / (BM + BN)) / 16 * 16;  // k per LDS chunk
-  static constexpr int LD = KC + 4;                          // LDS row stride (floats)
-  static constexpr int WM = BM / 2, WN = BN / 2;             // wave tile (2 x 2 waves)
-  static constexpr int IM = WM / 16, IN = WN / 16;           // 16 x 16 blocks per wave
-  static constexpr int NLA = BM * KC / 4 / 256;              // float4 loads per thread, A
-  static constexpr int NLB = BN * KC / 4 / 256;              // float4 loads per thread, B
-};
-
-__device__ __forceinline__ float4 vm_load4(const VMat& v, int row, int col, int nrows, int ncols) {
-  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (row >= nrows || col >= ncols) return o;
-  int b = 0;
-  while (b + 1 < v.nb && row >= v.r0[b + 1]) ++b;
-  const float* base = v.p[b] + (size_t)(row - v.r0[b]) * (size_t)v.ld[b];
-  if (v.vec && col + 3 < ncols) {
-    o = *reinterpret_cast<const float4*>(base + col);
-  } else {
-    o.x = base[col];
-    if (col + 1 < ncols) o.y = base[col + 1];
-    if (col + 2 < ncols) o.z = base[col + 2];
-    if (col + 3 < ncols) o.w = base[col + 3];
-  }
-  if (v.rscale) {
-    const float s = v.rscale[row];
-    o.x *= s; o.y *= s; o.z *= s; o.w *= s;
-  }
-  return o;
-}
-
-// Loads rows [o0, o0+R) of the output dimension and k in [k0, k0+KC) of one
-// operand into LDS as S[r * LD + k] (k contiguous).  kc: the operand's rows are
-// the output dimension (k contiguous in memory); otherwise its rows are k.
-// Elements outside [0, nout) x [k0, kend) are zero.
-template <int R, int KC, int LD, int NL>
-__device__ __forceinline__ void load_panel(const VMat& v, int kc, int o0, int nout, int k0,
-                                           int kend, float* S) {
-  float4 r[NL];
+template <int KC_FLAG>
+__device__ __forceinline__ void big_load(const VMat& v, int o0, int nout, int k0, int kend,
+                                         float4 r[4]) {
   const int t = threadIdx.x;
-  if (kc) {
 #pragma unroll
-    for (int q = 0; q < NL; ++q) {
-      const int idx = t + 256 * q;
-      const int row = idx / (KC / 4), c4 = idx - row * (KC / 4);
+  for (int q = 0; q < 4; ++q) {
+    const int idx = t + 256 * q;
+    if (KC_FLAG) {
+      const int row = idx >> 3, c4 = idx & 7;  // 8 float4 per 32-wide k row
       r[q] = vm_load4(v, o0 + row, k0 + 4 * c4, nout, kend);
-    }
-#pragma unroll
-    for (int q = 0; q < NL; ++q) {
-      const int idx = t + 256 * q;
-      const int row = idx / (KC / 4), c4 = idx - row * (KC / 4);
-      *reinterpret_cast<float4*>(S + row * LD + 4 * c4) = r[q];
-    }
-  } else {
-#pragma unroll
-    for (int q = 0; q < NL; ++q) {
-      const int idx = t + 256 * q;
-      const int kr = idx / (R / 4), c4 = idx - kr * (R / 4);
+    } else {
+      const int kr = idx >> 5, c4 = idx & 31;  // 32 float4 per 128-wide output row
       r[q] = vm_load4(v, k0 + kr, o0 + 4 * c4, kend, nout);
     }
+  }
+}
+
+template <int KC_FLAG>
+__device__ __forceinline__ void big_store(float* S, const float4 r[4]) {
+  const int t = threadIdx.x;
 #pragma unroll
-    for (int q = 0; q < NL; ++q) {
-      const int idx = t + 256 * q;
-      const int kr = idx / (R / 4), c4 = idx - kr * (R / 4);
-      S[(4 * c4 + 0) * LD + kr] = r[q].x;
-      S[(4 * c4 + 1) * LD + kr] = r[q].y;
-      S[(4 * c4 + 2) * LD + kr] = r[q].z;
-      S[(4 * c4 + 3) * LD + kr] = r[q].w;
+  for (int q = 0; q < 4; ++q) {
+    const int idx = t + 256 * q;
+    if (KC_FLAG) {
+      const int row = idx >> 3, c4 = idx & 7;
+      *reinterpret_cast<float4*>(S + row * GB_LD + 4 * c4) = r[q];
+    } else {
+      const int kr = idx >> 5, c4 = idx & 31;
+      S[(4 * c4 + 0) * GB_LD + kr] = r[q].x;
+      S[(4 * c4 + 1) * GB_LD + kr] = r[q].y;
+      S[(4 * c4 + 2) * GB_LD + kr] = r[q].z;
+      S[(4 * c4 + 3) * GB_LD + kr] = r[q].w;
     }
   }
 }
 
-template <int BM, int BN>
-__global__ __launch_bounds__(256) void gemm_panel_kernel(GemmBatch bt) {
-  using C = Panel<BM, BN>;
-  if (bt.skip_if && *bt.skip_if) return;
-  if (bt.run_if && !*bt.run_if) return;
-  extern __shared__ __attribute__((aligned(16))) float smem[];
-  float* As = smem;
-  float* Bs = smem + BM * C::LD;
-
-  int t = blockIdx.x;
-  int q = 0;
-  while (q + 1 < bt.np && t >= bt.p[q + 1].tile_begin) ++q;
-  if (bt.skip_updates_if && q >= bt.first_update && *bt.skip_updates_if) return;
-  const GemmProblem& P = bt.p[q];
-  int lt = t - P.tile_begin;
-  int tm, tn, kb = 0, ke = P.K, z = 0;
-  if (P.epi == EPI_SYM) {
-    int T = P.tiles_m, r = 0;
-    while (lt >= T - r) { lt -= T - r; ++r; }
-    tm = r; tn = r + lt;
-  } else {
-    const int per = P.tiles_m * P.tiles_n;
-    z = lt / per;
-    lt -= z * per;
-    tm = lt / P.tiles_n;
-    tn = lt - tm * P.tiles_n;
-    if (P.ksplit > 1) {
-      const int kc = ((P.K + P.ksplit - 1) / P.ksplit + 15) / 16 * 16;
-      kb = z * kc;
-      ke = min(P.K, kb + kc);
-    }
+template <int A_KC, int B_KC>
+__global__ __launch_bounds__(256) void gemm_big_kernel(GemmProblem P, const int* skip_if,
+                                                       const int* run_if) {
+  if (skip_if && *skip_if) return;
+  if (run_if && !*run_if) return;
+  __shared__ __attribute__((aligned(16))) float As[2][GB_T * GB_LD];
+  __shared__ __attribute__((aligned(16))) float Bs[2][GB_T * GB_LD];
+  int lt = blockIdx.x;
+  const int per = P.tiles_m * P.tiles_n;
+  const int z = lt / per;
+  lt -= z * per;
+  const int tm = lt / P.tiles_n, tn = lt - tm * P.tiles_n;
+  int kb = 0, ke = P.K;
+  if (P.ksplit > 1) {
+    const int kc = ((P.K + P.ksplit - 1) / P.ksplit + GB_BK - 1) / GB_BK * GB_BK;
+    kb = z * kc;
+    ke = min(P.K, kb + kc);
   }
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int m0 = tm * GB_T, n0 = tn * GB_T;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+  floatx4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  floatx4 acc[C::IM][C::IN];
+  float4 ra[4], rb[4];
+  if (kb < ke) {
+    big_load<A_KC>(P.A, m0, P.M, kb, ke, ra);
+    big_load<B_KC>(P.B, n0, P.N, kb, ke, rb);
+    big_store<A_KC>(As[0], ra);
+    big_store<B_KC>(Bs[0], rb);
+  }
+  __syncthreads();
+  int buf = 0;
+  for (int k0 = kb; k0 < ke; k0 += GB_BK) {
+    const bool more = k0 + GB_BK < ke;
+    if (more) {
+      big_load<A_KC>(P.A, m0, P.M, k0 + GB_BK, ke, ra);
+      big_load<B_KC>(P.B, n0, P.N, k0 + GB_BK, ke, rb);
+    }
+    const float* Aw = As[buf] + (wm * 64 + (lane & 15)) * GB_LD + 4 * (lane >> 4);
+    const float* Bw = Bs[buf] + (wn * 64 + (lane & 15)) * GB_LD + 4 * (lane >> 4);
 #pragma unroll
-  for (int i = 0; i < C::IM; ++i)
+    for (int kk = 0; kk < GB_BK; kk += 16) {
+      float4 fa[4], fb[4];
 #pragma unroll
-    for (int j = 0; j < C::IN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  for (int k0 = kb; k0 < ke; k0 += C::KC) {
-    if (k0 != kb) __syncthreads();
-    load_panel<BM, C::KC, C::LD, C::NLA>(P.A, P.a_kc, m0, P.M, k0, ke, As);
-    load_panel<BN, C::KC, C::LD, C::NLB>(P.B, P.b_kc, n0, P.N, k0, ke, Bs);
-    __syncthreads();
-    const int kcount = min(C::KC, ke - k0);
-    const int kpad = (kcount + 15) & ~15;
-    const float* Aw = As + (wm * C::WM + (lane & 15)) * C::LD + 4 * (lane >> 4);
-    const float* Bw = Bs + (wn * C::WN + (lane & 15)) * C::LD + 4 * (lane >> 4);
-    for (int kk = 0; kk < kpad; kk += 16) {
-      float4 fa[C::IM], fb[C::IN];
+      for (int i = 0; i < 4; ++i) fa[i] = *reinterpret_cast<const float4*>(Aw + i * 16 * GB_LD + kk);
 #pragma unroll
-      for (int i = 0; i < C::IM; ++i)
-        fa[i] = *reinterpret_cast<const float4*>(Aw + i * 16 * C::LD + kk);
+      for (int j = 0; j < 4; ++j) fb[j] = *reinterpret_cast<const float4*>(Bw + j * 16 * GB_LD + kk);
 #pragma unroll
-      for (int j = 0; j < C::IN; ++j)
-        fb[j] = *reinterpret_cast<const float4*>(Bw + j * 16 * C::LD + kk);
-      // MFMA number q of a 16-wide k slice pairs k = 4*(lane/16) + q of A with the same k of B.
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int i = 0; i < C::IM; ++i)
-#pragma unroll
-        for (int j = 0; j < C::IN; ++j) {
+        for (int j = 0; j < 4; ++j) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i].x, fb[j].x, acc[i][j], 0, 0, 0);
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i].y, fb[j].y, acc[i][j], 0, 0, 0);
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i].z, fb[j].z, acc[i][j], 0, 0, 0);
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i].w, fb[j].w, acc[i][j], 0, 0, 0);
         }
     }
+    if (more) {
+      big_store<A_KC>(As[buf ^ 1], ra);
+      big_store<B_KC>(Bs[buf ^ 1], rb);
+    }
+    __syncthreads();
+    buf ^= 1;
   }
-
-  // Element r of acc[i][j]: row 4*(lane/16) + r, column lane % 16 of its 16 x 16 block.
 #pragma unroll
-  for (int i = 0; i < C::IM; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < C::IN; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = m0 + wm * C::WM + i * 16 + 4 * (lane >> 4) + r;
-        const int col = n0 + wn * C::WN + j * 16 + (lane & 15);
+        const int row = m0 + wm * 64 + i * 16 + 4 * (lane >> 4) + r;
+        const int col = n0 + wn * 64 + j * 16 + (lane & 15);
         if (row >= P.M || col >= P.N) continue;
         const float v = acc[i][j][r];
-        if (P.epi == EPI_STORE) {
+        if (P.epi == EPI_PARTIAL) {
+          P.C[(size_t)z * P.M * P.N + (size_t)row * P.N + col] = v;
+        } else {
           float* c = P.C + (size_t)row * P.ldc + col;
           float o = P.alpha * v;
           if (P.beta != 0.f) o += P.beta * *c;
           *c = o;
-        } else if (P.epi == EPI_SYM) {
-          if (row <= col) {
-            const float o = P.C[(size_t)row * P.ldc + col] + P.alpha * v;
-            P.C[(size_t)row * P.ldc + col] = o;
-            P.C[(size_t)col * P.ldc + row] = o;
-          }
-        } else if (P.epi == EPI_GRADT) {
-          const float g = P.s1[row] * P.e1[(size_t)row * P.lde1 + col] +
-                          P.s2[row] * P.e2[(size_t)row * P.lde2 + col];
-          P.g[(size_t)row * P.ldg + col] = g;
-          P.C[(size_t)row * P.ldc + col] = g + P.alpha * v;
-        } else {  // EPI_PARTIAL
-          P.C[(size_t)z * P.M * P.N + (size_t)row * P.N + col] = v;
         }
       }
+}
+
+hipError_t gemm_big_launch(GemmProblem p, hipStream_t s, const int* skip_if, const int* run_if) {
+  if (p.epi != EPI_STORE && p.epi != EPI_PARTIAL) return hipErrorInvalidValue;
+  if (p.ksplit < 1) p.ksplit = 1;
+  p.tiles_m = (p.M + GB_T - 1) / GB_T;
+  p.tiles_n = (p.N + GB_T - 1) / GB_T;
+  p.tile_begin = 0;
+  const int total = p.tiles_m * p.tiles_n * (p.epi == EPI_PARTIAL ? p.ksplit : 1);
+  if (total == 0) return hipSuccess;
+  const dim3 grid(total), block(256);
+  if (p.a_kc && p.b_kc)
+    hipLaunchKernelGGL((gemm_big_kernel<1, 1>), grid, block, 0, s, p, skip_if, run_if);
+  else if (p.a_kc)
+    hipLaunchKernelGGL((gemm_big_kernel<1, 0>), grid, block, 0, s, p, skip_if, run_if);
+  else if (p.b_kc)
+    hipLaunchKernelGGL((gemm_big_kernel<0, 1>), grid, block, 0, s, p, skip_if, run_if);
+  else
+    hipLaunchKernelGGL((gemm_big_kernel<0, 0>), grid, block, 0, s, p, skip_if, run_if);
+  return hipGetLastError();
 }
 
 __global__ void splitk_reduce_kernel(const float* ws, int splits, int M, int N, float* C, int ldc,
@@ -251,60 +217,6 @@ GemmProblem gemm_problem(int layout, int M, int N, int K, const VMat& A, const V
   p.epi = epi;
   p.ksplit = 1;
   return p;
-}
-
-template <int BM, int BN>
-static int assign_tiles(GemmBatch& b) {
-  int total = 0;
-  for (int q = 0; q < b.np; ++q) {
-    GemmProblem& p = b.p[q];
-    p.tiles_m = (p.M + BM - 1) / BM;
-    p.tiles_n = (p.N + BN - 1) / BN;
-    p.tile_begin = total;
-    if (p.ksplit < 1) p.ksplit = 1;
-    if (p.epi == EPI_SYM)
-      total += p.tiles_m * (p.tiles_m + 1) / 2;  // square C: upper-triangle tiles
-    else
-      total += p.tiles_m * p.tiles_n * (p.epi == EPI_PARTIAL ? p.ksplit : 1);
-  }
-  b.total_tiles = total;
-  return total;
-}
-
-template <int BM, int BN>
-static hipError_t launch_tiles(GemmBatch& b, hipStream_t s) {
-  using C = Panel<BM, BN>;
-  const int total = assign_tiles<BM, BN>(b);
-  if (total == 0) return hipSuccess;
-  const size_t lds = (size_t)(BM + BN) * C::LD * sizeof(float);
-  hipLaunchKernelGGL((gemm_panel_kernel<BM, BN>), dim3(total), dim3(256), lds, s, b);
-  return hipGetLastError();
-}
-
-static bool lds_configured = false;
-
-static hipError_t configure_lds() {
-  if (lds_configured) return hipSuccess;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_panel_kernel<64, 64>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)((64 + 64) * Panel<64, 64>::LD * sizeof(float)));
-  if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_panel_kernel<32, 32>),
-                          hipFuncAttributeMaxDynamicSharedMemorySize,
-                          (int)((32 + 32) * Panel<32, 32>::LD * sizeof(float)));
-  if (e != hipSuccess) return e;
-  lds_configured = true;
-  return hipSuccess;
-}
-
-hipError_t gemm_launch(GemmBatch& b, hipStream_t s, int tile) {
-  hipError_t e = configure_lds();
-  if (e != hipSuccess) return e;
-  if (tile == 0) {  // automatic: 64 x 64 unless that leaves most compute units idle
-    GemmBatch probe = b;
-    tile = assign_tiles<64, 64>(probe) >= 160 ? 64 : 32;
-  }
-  return tile == 64 ? launch_tiles<64, 64>(b, s) : launch_tiles<32, 32>(b, s);
 }
 
 hipError_t gemm_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int ldc,

@@ -1,21 +1,8 @@
-// C ABI of the library: state ownership, argument checks and the order of the
-// kernels of one step.
+// C ABI of the library: state ownership, argument checks, and the launches of
+// one step (the kernels themselves are in step.hip, gemm.hip and small.hip).
 //
-// Factored step (Appendix A), with H^T as the m x d row-major input, on two
-// streams (the caller's "main" stream and a library "side" stream):
-//   side : gather G = (V^T Y)^T (step 2, sparse part)
-//          validate + sort each example's targets, Y^T Y; global (row, slot)
-//          sort -> distinct rows and their segments
-//   main : GEMM 1  [Q; U; U^{-T}; H^T] H -> H^ = QH, UH, P = U^{-T}H, H^T H   (steps 1, 7, 8)
-//   side : X = S^{-1} P^T with S = H^T H - diag(1/(lr a_i))                 (step 8, m x m system)
-//   main : GEMM 2  Y^ = U^T G^T ; C1 = H^T H^ ; C2 = H^T Y^ = (UH)^T G^T       (steps 2, 5)
-//          scalars: loss_i, a_i, b_i, N = (dL/dO)^T dL/dO                   (steps 3-6)
-//          GEMM 3  grad_H = H^ A + Y^ diag(b), T = grad_H - (lr/2) N H^T ;
-//                  U -= lr (UH) A H^T ; U^{-T} -= X^T H^T                    (steps 4, 7, 8)
-//          GEMM 4  Q -= lr (H T^T + T H^T)                                 (step 10)
-//   side : V[r] += sum over pairs (i,k) with idx = r of c_ik X_i           (step 9)
-//   main : [drift control: Appendix C pristine restore]
-// Derivation of the shortcuts (exact in real arithmetic):
+// The factored step (Appendix A) is four heterogeneous launches on the
+// state's stream (see step.hip).  Shortcuts used, exact in real arithmetic:
 //   U_new^{-T} H = -(1/lr) P S^{-1} A^{-1}, so with X = S^{-1} P^T (m x d):
 //   U_new^{-T} = U^{-T} - X^T H^T and V_new = V - lr G (U_new^{-T} H)^T
 //   = V + sum_i (g_i / a_i) X_i, i.e. c = -val (squared) or b_i / a_i (spherical);
@@ -40,18 +27,16 @@ struct lst_state {
   lst_config cfg{};
   int device = 0;
   hipStream_t stream = nullptr;
-  hipStream_t side = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_gather = nullptr, ev_yy = nullptr, ev_g1 = nullptr,
-            ev_p2 = nullptr, ev_p3 = nullptr, ev_solve = nullptr, ev_done = nullptr;
   float* V = nullptr;      // V (factored) or W (naive), D x d
   float* state = nullptr;  // [Q; U; U^{-T}], 3d x d
   float* Vtmp = nullptr;   // D x d copy for the pristine restore
   int* flags = nullptr;
   // factored workspace
-  float *G = nullptr, *Z0 = nullptr, *Yh = nullptr, *C12 = nullptr, *Nm = nullptr,
-        *a = nullptr, *b = nullptr, *cs = nullptr, *T = nullptr, *X = nullptr,
-        *solve_ws = nullptr;
-  SparseWs sp{};
+  float *G = nullptr, *Z0 = nullptr, *Yh = nullptr, *C12 = nullptr, *C2t = nullptr,
+        *a = nullptr, *b = nullptr, *cs = nullptr, *T = nullptr, *X = nullptr, *yy = nullptr,
+        *ex_val = nullptr, *solve_ws = nullptr;
+  int *ex_row = nullptr, *ex_cnt = nullptr, *hkey = nullptr, *hmin = nullptr, *touched = nullptr;
+  int hbits = 0;
   int ld0 = 0, ldc12 = 0;
   // naive workspace
   float* O = nullptr;
@@ -59,6 +44,18 @@ struct lst_state {
   int naive_ksplit = 1;
   int64_t steps = 0;
   std::vector<void*> allocs;
+  // captured steps: one instantiated graph per distinct argument tuple (LRU)
+  struct GraphEntry {
+    int m, K;
+    const void *H, *idx, *val, *loss, *grad;
+    uint32_t lr_bits;
+    hipGraphExec_t exec;
+    uint64_t last_use;
+  };
+  std::vector<GraphEntry> graphs;
+  uint64_t graph_clock = 0;
+  int use_graphs = 1;
+  hipStream_t cap = nullptr;  // capture stream
   // profiling: two events per phase per profiled step
   int prof = 0;
   std::vector<hipEvent_t> prof_events;
@@ -85,6 +82,12 @@ struct DeviceGuard {
     if ((x) != hipSuccess) return LST_EHIP;     \
   } while (0)
 
+#define OK_OR_RETURN(x)            \
+  do {                             \
+    int rc_ = (x);                 \
+    if (rc_ != LST_OK) return rc_; \
+  } while (0)
+
 template <class T>
 int dalloc(lst_state* s, T** p, size_t count) {
   if (count == 0) count = 1;
@@ -95,19 +98,8 @@ int dalloc(lst_state* s, T** p, size_t count) {
   return LST_OK;
 }
 
-#define OK_OR_RETURN(x)            \
-  do {                             \
-    int rc_ = (x);                 \
-    if (rc_ != LST_OK) return rc_; \
-  } while (0)
-
-enum Phase {
-  PH_GATHER = 0, PH_PREP, PH_GEMM_STACK, PH_SOLVE, PH_GEMM_P2, PH_SCALARS, PH_GEMM_P3,
-  PH_GEMM_Q, PH_SCATTER, PH_DRIFT, PH_COUNT
-};
-const char* const kPhaseNames[PH_COUNT] = {
-    "gather", "prep", "gemm_stack", "solve", "gemm_p2", "scalars", "gemm_p3", "gemm_q",
-    "scatter", "drift"};
+enum Phase { PH_LAUNCH1 = 0, PH_LAUNCH2, PH_LAUNCH3, PH_LAUNCH4, PH_DRIFT, PH_COUNT };
+const char* const kPhaseNames[PH_COUNT] = {"launch1", "launch2", "launch3", "launch4", "drift"};
 
 // Records the begin (end = 0) or end (end = 1) event of a phase on stream st
 // when profiling.
@@ -126,17 +118,12 @@ int prof_mark(lst_state* s, int phase, int end, hipStream_t st) {
 
 void release(lst_state* s) {
   if (!s) return;
-  if (s->stream || s->side) {
-    (void)hipStreamSynchronize(s->stream);
-    if (s->side) (void)hipStreamSynchronize(s->side);
-  }
+  (void)hipStreamSynchronize(s->stream);
+  for (auto& g : s->graphs) (void)hipGraphExecDestroy(g.exec);
   for (void* p : s->allocs) (void)hipFree(p);
   s->allocs.clear();
-  for (hipEvent_t e : {s->ev_fork, s->ev_gather, s->ev_yy, s->ev_g1, s->ev_p2, s->ev_p3,
-                       s->ev_solve, s->ev_done})
-    if (e) (void)hipEventDestroy(e);
-  if (s->side) (void)hipStreamDestroy(s->side);
   for (hipEvent_t e : s->prof_events) (void)hipEventDestroy(e);
+  if (s->cap) (void)hipStreamDestroy(s->cap);
   delete s;
 }
 
@@ -149,10 +136,9 @@ int check_config(const lst_config* cfg) {
   if (cfg->loss != LST_LOSS_SQUARED && cfg->loss != LST_LOSS_SPHERICAL) return LST_EINVAL;
   if (cfg->loss == LST_LOSS_SPHERICAL && !(cfg->sph_eps > 0.f && isfinite(cfg->sph_eps)))
     return LST_EINVAL;
-  if (cfg->m_max < 1) return LST_EINVAL;
+  if (cfg->m_max < 1 || cfg->m_max > 512) return LST_EINVAL;
   if (cfg->K_max < 1 || cfg->K_max > 1024) return LST_EINVAL;
   if ((int64_t)cfg->m_max * cfg->K_max > 16384) return LST_EINVAL;
-  if (cfg->m_max > 512) return LST_EINVAL;
   if (!(cfg->cond_max >= 0.f) || !isfinite(cfg->cond_max)) return LST_EINVAL;
   return LST_OK;
 }
@@ -163,19 +149,17 @@ int common_init(lst_state* s, int64_t D, int32_t d, const lst_config* cfg, void*
   s->cfg = *cfg;
   HIPCHK(hipGetDevice(&s->device));
   s->stream = static_cast<hipStream_t>(hip_stream);
-  HIPCHK(hipStreamCreateWithFlags(&s->side, hipStreamNonBlocking));
-  for (hipEvent_t* e : {&s->ev_fork, &s->ev_gather, &s->ev_yy, &s->ev_g1, &s->ev_p2, &s->ev_p3,
-                        &s->ev_solve, &s->ev_done})
-    HIPCHK(hipEventCreateWithFlags(e, hipEventDisableTiming));
+  HIPCHK(hipStreamCreateWithFlags(&s->cap, hipStreamNonBlocking));
+  HIPCHK(configure_kernels());
   OK_OR_RETURN(dalloc(s, &s->flags, F_COUNT));
   HIPCHK(hipMemsetAsync(s->flags, 0, F_COUNT * sizeof(int), s->stream));
   OK_OR_RETURN(dalloc(s, &s->V, (size_t)D * d));
   return LST_OK;
 }
 
-// Split-K C = alpha A^T B with A, B: K x n (rows K), C n x n symmetric, K large.
+// Split-K C = alpha A^T A with A: K x n (rows K), C n x n symmetric, K large.
 int gram_splitk(lst_state* s, const float* A, int64_t Krows, int n, float* C, float alpha) {
-  const int tiles = ((n + 63) / 64) * ((n + 63) / 64);
+  const int tiles = ((n + 127) / 128) * ((n + 127) / 128);
   int64_t ks = (2048 + tiles - 1) / tiles;
   const int64_t max_by_k = (Krows + 255) / 256;
   if (ks > max_by_k) ks = max_by_k;
@@ -183,13 +167,11 @@ int gram_splitk(lst_state* s, const float* A, int64_t Krows, int n, float* C, fl
   if (ks > 256) ks = 256;
   float* ws = nullptr;
   if (hipMalloc((void**)&ws, (size_t)ks * n * n * sizeof(float)) != hipSuccess) return LST_ENOMEM;
-  GemmBatch bt{};
-  bt.np = 1;
-  bt.p[0] = gemm_problem(L_TN, n, n, (int)Krows, vmat(A, n, (int)Krows), vmat(A, n, (int)Krows),
-                         ws, n, 1.f, 0.f, EPI_PARTIAL);
-  bt.p[0].ksplit = (int)ks;
+  GemmProblem p = gemm_problem(L_TN, n, n, (int)Krows, vmat(A, n, (int)Krows),
+                               vmat(A, n, (int)Krows), ws, n, 1.f, 0.f, EPI_PARTIAL);
+  p.ksplit = (int)ks;
   int rc = LST_OK;
-  if (gemm_launch(bt, s->stream) != hipSuccess) rc = LST_EHIP;
+  if (gemm_big_launch(p, s->stream) != hipSuccess) rc = LST_EHIP;
   if (rc == LST_OK &&
       gemm_splitk_reduce(ws, (int)ks, n, n, C, n, alpha, 0.f, 1, nullptr, s->stream) != hipSuccess)
     rc = LST_EHIP;
@@ -198,16 +180,12 @@ int gram_splitk(lst_state* s, const float* A, int64_t Krows, int n, float* C, fl
   return rc;
 }
 
-// W = Vsrc U into Wdst (D x d), optionally gated on a device flag.
-int vu_product(lst_state* s, const float* Vsrc, float* Wdst, const int* run_if,
+// W = Vsrc U into Wdst (D x d) on stream st, optionally gated on device flags.
+int vu_product(lst_state* s, hipStream_t st, const float* Vsrc, float* Wdst, const int* run_if,
                const int* skip_if) {
-  GemmBatch bt{};
-  bt.np = 1;
-  bt.p[0] = gemm_problem(L_NN, (int)s->D, s->d, s->d, vmat(Vsrc, s->d, (int)s->D),
-                         vmat(Up(s), s->d, s->d), Wdst, s->d, 1.f, 0.f, EPI_STORE);
-  bt.run_if = run_if;
-  bt.skip_if = skip_if;
-  HIPCHK(gemm_launch(bt, s->stream));
+  GemmProblem p = gemm_problem(L_NN, (int)s->D, s->d, s->d, vmat(Vsrc, s->d, (int)s->D),
+                               vmat(Up(s), s->d, s->d), Wdst, s->d, 1.f, 0.f, EPI_STORE);
+  HIPCHK(gemm_big_launch(p, st, skip_if, run_if));
   return LST_OK;
 }
 
@@ -230,6 +208,126 @@ int check_step_args(lst_state* s, int32_t m, int32_t K, const float* H, const in
   if (s->cfg.loss == LST_LOSS_SQUARED && !Y_val) return LST_EINVAL;
   if (s->cfg.loss == LST_LOSS_SPHERICAL && K != 1) return LST_EINVAL;
   if (!(lr > 0.f) || !isfinite(lr)) return LST_EINVAL;
+  return LST_OK;
+}
+
+// GEMM tile edge for a launch: 64 when that still gives most compute units a
+// tile, else 32.
+int pick_tile(const GemmBatch& b) {
+  int t64 = 0;
+  for (int q = 0; q < b.np; ++q) {
+    const GemmProblem& p = b.p[q];
+    const int tm = (p.M + 63) / 64, tn = (p.N + 63) / 64;
+    t64 += (p.epi == EPI_SYM) ? tm * (tm + 1) / 2 : tm * tn;
+  }
+  return t64 >= 128 ? 64 : 32;
+}
+
+// Enqueues the launches of one factored step on stream st.
+int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float* H,
+                 const int32_t* Y_idx, const float* Y_val, float lr, float* loss, float* grad_H) {
+  const int d = s->d;
+  int* fl = s->flags;
+  StepCtx c{};
+  c.m = m; c.K = K; c.d = d; c.D = s->D;
+  c.loss_kind = s->cfg.loss; c.eps = s->cfg.sph_eps; c.lr = lr;
+  c.H = H; c.idx = Y_idx; c.val = Y_val;
+  c.V = s->V; c.Q = Qp(s); c.U = Up(s); c.Uit = Uitp(s);
+  c.Z0 = s->Z0; c.ld0 = s->ld0;
+  c.G = s->G; c.Yh = s->Yh; c.C12 = s->C12; c.ldc12 = s->ldc12; c.C2t = s->C2t;
+  c.X = s->X; c.T = s->T;
+  c.a = s->a; c.b = s->b; c.cs = s->cs;
+  c.loss = loss; c.grad = grad_H;
+  c.ex_row = s->ex_row; c.ex_val = s->ex_val; c.ex_cnt = s->ex_cnt; c.yy = s->yy;
+  c.hkey = s->hkey; c.hmin = s->hmin; c.hbits = s->hbits;
+  c.touched = s->touched; c.flags = fl; c.solve_ws = s->solve_ws;
+  const float* Hh = s->Z0;          // H^ rows
+  const float* UH = s->Z0 + d;      // (U H)^T rows
+
+  {  // launch 1: GEMM 1, gather, target prep
+    StepLaunch L{};
+    L.ntask = 3;
+    L.kind[0] = TK_GEMM; L.kind[1] = TK_GATHER; L.kind[2] = TK_PREP;
+    L.gemm.np = 1;
+    L.gemm.kcw_max = 256;
+    L.gemm.p[0] = gemm_problem(L_NT, m, 3 * d + m, d, vmat(H, d, m),
+                               vmat2(s->state, d, 3 * d, H, d, m), s->Z0, s->ld0, 1.f, 0.f,
+                               EPI_STORE);
+    L.timing_slot = 0;
+    OK_OR_RETURN(prof_mark(s, PH_LAUNCH1, 0, st));
+    HIPCHK(step_launch(c, L, 32, st));
+    OK_OR_RETURN(prof_mark(s, PH_LAUNCH1, 1, st));
+  }
+  {  // launch 2: Y^, C1, C2, C2^T ; solve ; Y^T Y ; per-example scalars
+    StepLaunch L{};
+    L.ntask = 4;
+    L.kind[0] = TK_GEMM; L.kind[1] = TK_SOLVE; L.kind[2] = TK_YY; L.kind[3] = TK_SCALARS;
+    GemmBatch& g = L.gemm;
+    g.np = 4;
+    g.kcw_max = 256;
+    g.p[0] = gemm_problem(L_NN, m, d, d, vmat(s->G, d, m), vmat(c.U, d, d), s->Yh, d, 1.f, 0.f,
+                          EPI_STORE);
+    g.p[1] = gemm_problem(L_NT, m, m, d, vmat(H, d, m), vmat(Hh, s->ld0, m), s->C12, s->ldc12,
+                          1.f, 0.f, EPI_STORE);
+    g.p[2] = gemm_problem(L_NT, m, m, d, vmat(UH, s->ld0, m), vmat(s->G, d, m), s->C12 + m,
+                          s->ldc12, 1.f, 0.f, EPI_STORE);
+    g.p[3] = gemm_problem(L_NT, m, m, d, vmat(s->G, d, m), vmat(UH, s->ld0, m), s->C2t, m, 1.f,
+                          0.f, EPI_STORE);
+    L.timing_slot = 1;
+    OK_OR_RETURN(prof_mark(s, PH_LAUNCH2, 0, st));
+    HIPCHK(step_launch(c, L, 32, st));
+    OK_OR_RETURN(prof_mark(s, PH_LAUNCH2, 1, st));
+  }
+  {  // launch 3: grad_H and T ; U and U^{-T} updates ; scatter into V
+    StepLaunch L{};
+    L.ntask = 2;
+    L.kind[0] = TK_GEMM; L.kind[1] = TK_SCATTER;
+    GemmBatch& g = L.gemm;
+    g.np = 3;
+    g.kcw_max = 256;
+    GemmProblem& pt = g.p[0];
+    pt = gemm_problem(L_NN, m, d, m, vmat(nullptr, m, m), vmat(H, d, m), s->T, d, -0.5f * lr,
+                      0.f, EPI_GRADT);
+    pt.a_nmat = 1;
+    pt.nC12 = s->C12; pt.nld = s->ldc12; pt.nC2t = s->C2t; pt.nyy = s->yy;
+    pt.na = s->a; pt.nb = s->b; pt.nm = m;
+    pt.e1 = Hh; pt.lde1 = s->ld0; pt.e2 = s->Yh; pt.lde2 = d;
+    pt.s1 = s->a; pt.s2 = s->b; pt.g = grad_H; pt.ldg = d;
+    g.p[1] = gemm_problem(L_TN, d, d, m, vmat(UH, s->ld0, m, s->a), vmat(H, d, m), c.U, d, -lr,
+                          1.f, EPI_STORE);
+    g.p[2] = gemm_problem(L_TN, d, d, m, vmat(s->X, d, m), vmat(H, d, m), c.Uit, d, -1.f, 1.f,
+                          EPI_STORE);
+    g.skip_updates_if = fl + F_ERR;  // the gradient tiles (problem 0) always run
+    g.first_update = 1;
+    L.timing_slot = 2;
+    OK_OR_RETURN(prof_mark(s, PH_LAUNCH3, 0, st));
+    HIPCHK(step_launch(c, L, pick_tile(g), st));
+    OK_OR_RETURN(prof_mark(s, PH_LAUNCH3, 1, st));
+  }
+  {  // launch 4: Q -= lr (H T^T + T H^T) ; clear the hash slots
+    StepLaunch L{};
+    L.ntask = 2;
+    L.kind[0] = TK_GEMM; L.kind[1] = TK_CLEAR;
+    GemmBatch& g = L.gemm;
+    g.np = 1;
+    g.kcw_max = 256;
+    g.skip_if = fl + F_ERR;
+    g.p[0] = gemm_problem(L_TN, d, d, 2 * m, vmat2(H, d, m, s->T, d, m),
+                          vmat2(s->T, d, m, H, d, m), c.Q, d, -lr, 1.f, EPI_SYM);
+    L.timing_slot = 3;
+    OK_OR_RETURN(prof_mark(s, PH_LAUNCH4, 0, st));
+    HIPCHK(step_launch(c, L, 32, st));
+    OK_OR_RETURN(prof_mark(s, PH_LAUNCH4, 1, st));
+  }
+  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 0, st));
+  if (s->cfg.cond_max > 0.f) {
+    HIPCHK(drift_check(c.U, c.Uit, d, s->cfg.cond_max * (float)d, fl, st));
+    HIPCHK(copy_if(s->V, s->Vtmp, (size_t)s->D * d, fl + F_RESTORE, st));
+    OK_OR_RETURN(vu_product(s, st, s->Vtmp, s->V, fl + F_RESTORE, fl + F_ERR));
+    HIPCHK(set_identity_if(c.U, d, fl + F_RESTORE, st));
+    HIPCHK(set_identity_if(c.Uit, d, fl + F_RESTORE, st));
+  }
+  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 1, st));
   return LST_OK;
 }
 
@@ -268,22 +366,24 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
   if (rc != LST_OK) return fail(rc);
   s->ld0 = (3 * d + m + 3) / 4 * 4;
   s->ldc12 = 2 * m;
+  s->hbits = 1;
+  while ((1 << s->hbits) < 2 * m * K) ++s->hbits;
+  const int hsize = 1 << s->hbits;
   const size_t md = (size_t)m * d;
-  if ((rc = dalloc(s, &s->state, 3 * (size_t)d * d)) ||
-      (rc = dalloc(s, &s->G, md)) || (rc = dalloc(s, &s->Z0, (size_t)m * s->ld0)) ||
-      (rc = dalloc(s, &s->Yh, md)) || (rc = dalloc(s, &s->C12, (size_t)m * s->ldc12)) ||
-      (rc = dalloc(s, &s->Nm, (size_t)m * m)) || (rc = dalloc(s, &s->a, m)) ||
-      (rc = dalloc(s, &s->b, m)) || (rc = dalloc(s, &s->cs, m)) || (rc = dalloc(s, &s->T, md)) ||
-      (rc = dalloc(s, &s->X, md)) ||
-      (rc = dalloc(s, &s->solve_ws, woodbury_workspace_floats(m, d))) ||
-      (rc = dalloc(s, &s->sp.ex_row, (size_t)m * K)) ||
-      (rc = dalloc(s, &s->sp.ex_val, (size_t)m * K)) || (rc = dalloc(s, &s->sp.ex_cnt, m)) ||
-      (rc = dalloc(s, &s->sp.keys, (size_t)m * K)) ||
-      (rc = dalloc(s, &s->sp.srt_slot, (size_t)m * K)) ||
-      (rc = dalloc(s, &s->sp.seg_row, (size_t)m * K)) ||
-      (rc = dalloc(s, &s->sp.seg_beg, (size_t)m * K + 1)) ||
-      (rc = dalloc(s, &s->sp.yy, (size_t)m * m)))
+  if ((rc = dalloc(s, &s->state, 3 * (size_t)d * d)) || (rc = dalloc(s, &s->G, md)) ||
+      (rc = dalloc(s, &s->Z0, (size_t)m * s->ld0)) || (rc = dalloc(s, &s->Yh, md)) ||
+      (rc = dalloc(s, &s->C12, (size_t)m * s->ldc12)) || (rc = dalloc(s, &s->C2t, (size_t)m * m)) ||
+      (rc = dalloc(s, &s->a, m)) || (rc = dalloc(s, &s->b, m)) || (rc = dalloc(s, &s->cs, m)) ||
+      (rc = dalloc(s, &s->T, md)) || (rc = dalloc(s, &s->X, md)) ||
+      (rc = dalloc(s, &s->yy, (size_t)m * m)) ||
+      (rc = dalloc(s, &s->solve_ws, solve_workspace_floats(m, d))) ||
+      (rc = dalloc(s, &s->ex_row, (size_t)m * K)) || (rc = dalloc(s, &s->ex_val, (size_t)m * K)) ||
+      (rc = dalloc(s, &s->ex_cnt, m)) || (rc = dalloc(s, &s->hkey, hsize)) ||
+      (rc = dalloc(s, &s->hmin, hsize)) || (rc = dalloc(s, &s->touched, (size_t)m * K)))
     return fail(rc);
+  if (fill_ints(s->hkey, -1, hsize, s->stream) != hipSuccess ||
+      fill_ints(s->hmin, 0x7fffffff, hsize, s->stream) != hipSuccess)
+    return fail(LST_EHIP);
   if (cfg->cond_max > 0.f && (rc = ensure_vtmp(s))) return fail(rc);
   if (hipMemcpyAsync(s->V, V, (size_t)D * d * sizeof(float), hipMemcpyDeviceToDevice, s->stream) !=
       hipSuccess)
@@ -307,7 +407,7 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       return fail(LST_EHIP);
     // Q = (V U)^T (V U); the product goes through the restore buffer
     if ((rc = ensure_vtmp(s))) return fail(rc);
-    if ((rc = vu_product(s, s->V, s->Vtmp, nullptr, nullptr))) return fail(rc);
+    if ((rc = vu_product(s, s->stream, s->V, s->Vtmp, nullptr, nullptr))) return fail(rc);
     if ((rc = gram_splitk(s, s->Vtmp, D, d, Qp(s), 1.f))) return fail(rc);
   }
   int err = 0;
@@ -323,146 +423,48 @@ int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* 
   if (rc != LST_OK) return rc;
   if (s->kind != 0) return LST_ESTATE;
   DeviceGuard dg(s->device);
-  const int d = s->d;
-  const int64_t D = s->D;
-  const int one_hot = s->cfg.loss == LST_LOSS_SPHERICAL;
-  hipStream_t st = s->stream;
-  int* fl = s->flags;
-  float* U = Up(s);
-  if (s->prof) s->prof_steps += 1;
-
-  hipStream_t sd = s->side;
-  const bool sq = s->cfg.loss == LST_LOSS_SQUARED;
-  HIPCHK(hipEventRecord(s->ev_fork, st));
-  HIPCHK(hipStreamWaitEvent(sd, s->ev_fork, 0));
-
-  // side: G = (V^T Y)^T, then the target ordering and Y^T Y
-  OK_OR_RETURN(prof_mark(s, PH_GATHER, 0, sd));
-  HIPCHK(gather_rows(s->V, D, d, Y_idx, Y_val, m, K, one_hot, s->G, d, sd));
-  OK_OR_RETURN(prof_mark(s, PH_GATHER, 1, sd));
-  HIPCHK(hipEventRecord(s->ev_gather, sd));
-  OK_OR_RETURN(prof_mark(s, PH_PREP, 0, sd));
-  HIPCHK(prep_examples(Y_idx, Y_val, m, K, D, one_hot, s->sp, fl, sd));
-  HIPCHK(prep_target_gram(m, K, s->sp, sd));
-  HIPCHK(hipEventRecord(s->ev_yy, sd));
-  HIPCHK(prep_global_sort(m, K, s->sp, fl, sd));
-  OK_OR_RETURN(prof_mark(s, PH_PREP, 1, sd));
-
-  // main, GEMM 1: Z0 = H^T [Q; U; U^{-T}; H^T]^T   (m x (3d + m))
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_STACK, 0, st));
-  {
-    GemmBatch bt{};
-    bt.np = 1;
-    bt.p[0] = gemm_problem(L_NT, m, 3 * d + m, d, vmat(H, d, m),
-                           vmat2(s->state, d, 3 * d, H, d, m), s->Z0, s->ld0, 1.f, 0.f, EPI_STORE);
-    HIPCHK(gemm_launch(bt, st));
+  if (s->prof || !s->use_graphs) {
+    if (s->prof) s->prof_steps += 1;
+    rc = enqueue_step(s, s->stream, m, K, H, Y_idx, Y_val, lr, loss, grad_H);
+    if (rc == LST_OK) s->steps += 1;
+    return rc;
   }
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_STACK, 1, st));
-  HIPCHK(hipEventRecord(s->ev_g1, st));
-
-  const float* Hh = s->Z0;           // H^ rows
-  const float* UH = s->Z0 + d;       // (U H)^T rows
-  const float* Pm = s->Z0 + 2 * d;   // P^T rows
-  const float* HH = s->Z0 + 3 * d;   // H^T H
-  // side: the Woodbury system (the spherical weights need C1 from GEMM 2, so
-  // that case is enqueued after GEMM 2 below)
-  if (sq) {
-    HIPCHK(hipStreamWaitEvent(sd, s->ev_g1, 0));
-    OK_OR_RETURN(prof_mark(s, PH_SOLVE, 0, sd));
-    HIPCHK(woodbury_solve(HH, s->ld0, Pm, s->ld0, m, d, s->cfg.loss, s->cfg.sph_eps, D, lr,
-                          s->C12, s->ldc12, s->X, d, s->solve_ws, fl, sd));
-    OK_OR_RETURN(prof_mark(s, PH_SOLVE, 1, sd));
-    HIPCHK(hipEventRecord(s->ev_solve, sd));
+  uint32_t lr_bits;
+  memcpy(&lr_bits, &lr, sizeof lr_bits);
+  lst_state::GraphEntry* hit = nullptr;
+  for (auto& g : s->graphs)
+    if (g.m == m && g.K == K && g.H == H && g.idx == Y_idx && g.val == Y_val && g.loss == loss &&
+        g.grad == grad_H && g.lr_bits == lr_bits) {
+      hit = &g;
+      break;
+    }
+  if (!hit) {
+    HIPCHK(hipStreamBeginCapture(s->cap, hipStreamCaptureModeRelaxed));
+    rc = enqueue_step(s, s->cap, m, K, H, Y_idx, Y_val, lr, loss, grad_H);
+    hipGraph_t graph = nullptr;
+    const hipError_t ec = hipStreamEndCapture(s->cap, &graph);
+    if (rc != LST_OK || ec != hipSuccess) {
+      if (graph) (void)hipGraphDestroy(graph);
+      return rc != LST_OK ? rc : LST_EHIP;
+    }
+    hipGraphExec_t exec = nullptr;
+    const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (ei != hipSuccess) return LST_EHIP;
+    constexpr size_t kMaxGraphs = 32;
+    if (s->graphs.size() >= kMaxGraphs) {
+      size_t lru = 0;
+      for (size_t i = 1; i < s->graphs.size(); ++i)
+        if (s->graphs[i].last_use < s->graphs[lru].last_use) lru = i;
+      (void)hipStreamSynchronize(s->stream);
+      (void)hipGraphExecDestroy(s->graphs[lru].exec);
+      s->graphs.erase(s->graphs.begin() + lru);
+    }
+    s->graphs.push_back({m, K, H, Y_idx, Y_val, loss, grad_H, lr_bits, exec, 0});
+    hit = &s->graphs.back();
   }
-
-  // main, GEMM 2: Y^ = G U ; C1 = H^T H^ ; C2 = (UH)^T G^T
-  HIPCHK(hipStreamWaitEvent(st, s->ev_gather, 0));
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_P2, 0, st));
-  {
-    GemmBatch bt{};
-    bt.np = 3;
-    bt.p[0] = gemm_problem(L_NN, m, d, d, vmat(s->G, d, m), vmat(U, d, d), s->Yh, d, 1.f, 0.f,
-                           EPI_STORE);
-    bt.p[1] = gemm_problem(L_NT, m, m, d, vmat(H, d, m), vmat(Hh, s->ld0, m), s->C12, s->ldc12,
-                           1.f, 0.f, EPI_STORE);
-    bt.p[2] = gemm_problem(L_NT, m, m, d, vmat(UH, s->ld0, m), vmat(s->G, d, m), s->C12 + m,
-                           s->ldc12, 1.f, 0.f, EPI_STORE);
-    HIPCHK(gemm_launch(bt, st));
-  }
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_P2, 1, st));
-  HIPCHK(hipEventRecord(s->ev_p2, st));
-  if (!sq) {
-    HIPCHK(hipStreamWaitEvent(sd, s->ev_p2, 0));
-    OK_OR_RETURN(prof_mark(s, PH_SOLVE, 0, sd));
-    HIPCHK(woodbury_solve(HH, s->ld0, Pm, s->ld0, m, d, s->cfg.loss, s->cfg.sph_eps, D, lr,
-                          s->C12, s->ldc12, s->X, d, s->solve_ws, fl, sd));
-    OK_OR_RETURN(prof_mark(s, PH_SOLVE, 1, sd));
-    HIPCHK(hipEventRecord(s->ev_solve, sd));
-  }
-
-  // main: per-example scalars and N
-  HIPCHK(hipStreamWaitEvent(st, s->ev_yy, 0));
-  OK_OR_RETURN(prof_mark(s, PH_SCALARS, 0, st));
-  HIPCHK(minibatch_scalars(s->cfg.loss, s->cfg.sph_eps, D, m, s->C12, s->ldc12, s->sp.yy, loss,
-                           s->a, s->b, s->cs, s->Nm, fl, st));
-  OK_OR_RETURN(prof_mark(s, PH_SCALARS, 1, st));
-  HIPCHK(hipEventRecord(s->ev_p3, st));
-
-  // side: scatter into V once every check of this step has run
-  HIPCHK(hipStreamWaitEvent(sd, s->ev_p3, 0));
-  OK_OR_RETURN(prof_mark(s, PH_SCATTER, 0, sd));
-  HIPCHK(scatter_rows(s->V, d, s->X, d, Y_val, one_hot ? s->cs : nullptr, m, K, s->sp, fl, sd));
-  OK_OR_RETURN(prof_mark(s, PH_SCATTER, 1, sd));
-  HIPCHK(hipEventRecord(s->ev_done, sd));
-
-  // main, GEMM 3: grad_H and T ; rank-m updates of U and U^{-T}
-  HIPCHK(hipStreamWaitEvent(st, s->ev_solve, 0));
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_P3, 0, st));
-  {
-    GemmBatch bt{};
-    bt.np = 3;
-    GemmProblem& pt = bt.p[0];
-    pt = gemm_problem(L_NN, m, d, m, vmat(s->Nm, m, m), vmat(H, d, m), s->T, d, -0.5f * lr, 0.f,
-                      EPI_GRADT);
-    pt.e1 = Hh;
-    pt.lde1 = s->ld0;
-    pt.e2 = s->Yh;
-    pt.lde2 = d;
-    pt.s1 = s->a;
-    pt.s2 = s->b;
-    pt.g = grad_H;
-    pt.ldg = d;
-    // the updates below skip on error; the gradient product above must still run
-    bt.p[1] = gemm_problem(L_TN, d, d, m, vmat(UH, s->ld0, m, s->a), vmat(H, d, m), U, d, -lr,
-                           1.f, EPI_STORE);
-    bt.p[2] = gemm_problem(L_TN, d, d, m, vmat(s->X, d, m), vmat(H, d, m), Uitp(s), d, -1.f, 1.f,
-                           EPI_STORE);
-    bt.skip_updates_if = fl + F_ERR;
-    bt.first_update = 1;
-    HIPCHK(gemm_launch(bt, st));
-  }
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_P3, 1, st));
-  // main, GEMM 4: Q -= lr (H T^T + T H^T), symmetric
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_Q, 0, st));
-  {
-    GemmBatch bt{};
-    bt.np = 1;
-    bt.skip_if = fl + F_ERR;
-    bt.p[0] = gemm_problem(L_TN, d, d, 2 * m, vmat2(H, d, m, s->T, d, m),
-                           vmat2(s->T, d, m, H, d, m), Qp(s), d, -lr, 1.f, EPI_SYM);
-    HIPCHK(gemm_launch(bt, st));
-  }
-  OK_OR_RETURN(prof_mark(s, PH_GEMM_Q, 1, st));
-  HIPCHK(hipStreamWaitEvent(st, s->ev_done, 0));
-  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 0, st));
-  if (s->cfg.cond_max > 0.f) {
-    HIPCHK(drift_check(U, Uitp(s), d, s->cfg.cond_max * (float)d, fl, st));
-    HIPCHK(copy_if(s->V, s->Vtmp, (size_t)D * d, fl + F_RESTORE, st));
-    OK_OR_RETURN(vu_product(s, s->Vtmp, s->V, fl + F_RESTORE, fl + F_ERR));
-    HIPCHK(set_identity_if(U, d, fl + F_RESTORE, st));
-    HIPCHK(set_identity_if(Uitp(s), d, fl + F_RESTORE, st));
-  }
-  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 1, st));
+  hit->last_use = ++s->graph_clock;
+  HIPCHK(hipGraphLaunch(hit->exec, s->stream));
   s->steps += 1;
   return LST_OK;
 }
@@ -475,7 +477,7 @@ int lst_materialize_W(lst_state* s, float* W) {
                           s->stream));
     return LST_OK;
   }
-  return vu_product(s, s->V, W, nullptr, nullptr);
+  return vu_product(s, s->stream, s->V, W, nullptr, nullptr);
 }
 
 int lst_get_state(lst_state* s, float* Q, float* U, float* UinvT) {
@@ -506,7 +508,11 @@ int lst_touched_rows(lst_state* s, int32_t* rows, int32_t capacity, int32_t* cou
   OK_OR_RETURN(read_flag(s, F_UNIQUE, &u));
   if (s->steps == 0) u = 0;
   if (u > capacity) return LST_EINVAL;
-  if (u > 0) HIPCHK(hipMemcpy(rows, s->sp.seg_row, (size_t)u * sizeof(int), hipMemcpyDeviceToHost));
+  if (u > 0) {
+    HIPCHK(sort_ints(s->touched, s->flags + F_UNIQUE, s->stream));
+    HIPCHK(hipStreamSynchronize(s->stream));
+    HIPCHK(hipMemcpy(rows, s->touched, (size_t)u * sizeof(int), hipMemcpyDeviceToHost));
+  }
   *count = u;
   return LST_OK;
 }
@@ -518,7 +524,7 @@ int lst_restore(lst_state* s) {
   OK_OR_RETURN(ensure_vtmp(s));
   HIPCHK(hipMemcpyAsync(s->Vtmp, s->V, (size_t)s->D * s->d * sizeof(float),
                         hipMemcpyDeviceToDevice, s->stream));
-  OK_OR_RETURN(vu_product(s, s->Vtmp, s->V, nullptr, nullptr));
+  OK_OR_RETURN(vu_product(s, s->stream, s->Vtmp, s->V, nullptr, nullptr));
   HIPCHK(set_identity_if(Up(s), s->d, nullptr, s->stream));
   HIPCHK(set_identity_if(Uitp(s), s->d, nullptr, s->stream));
   return LST_OK;
@@ -538,8 +544,8 @@ int lst_naive_init(lst_state** out, int64_t D, int32_t d, const float* W, const 
   };
   if (rc != LST_OK) return fail(rc);
   const int m = cfg->m_max;
-  const int tiles = ((m + 63) / 64) * ((d + 63) / 64);
-  int64_t ks = (1024 + tiles - 1) / tiles;
+  const int tiles = ((m + 127) / 128) * ((d + 127) / 128);
+  int64_t ks = (512 + tiles - 1) / tiles;
   const int64_t max_by_k = (D + 255) / 256;
   if (ks > max_by_k) ks = max_by_k;
   if (ks > 256) ks = 256;
@@ -566,33 +572,24 @@ int lst_naive_step(lst_state* s, int32_t m, int32_t K, const float* H, const int
   const int64_t D = s->D;
   hipStream_t st = s->stream;
   const bool sq = s->cfg.loss == LST_LOSS_SQUARED;
-  {  // O (m x D) = H^T W^T: every output of every example, O(D d) each
-    GemmBatch bt{};
-    bt.np = 1;
-    bt.p[0] = gemm_problem(L_NT, m, (int)D, d, vmat(H, d, m), vmat(s->V, d, (int)D), s->O,
-                           (int)D, 1.f, 0.f, EPI_STORE);
-    HIPCHK(gemm_launch(bt, st));
-  }
+  // O (m x D) = H^T W^T: every output of every example, O(D d) each
+  HIPCHK(gemm_big_launch(gemm_problem(L_NT, m, (int)D, d, vmat(H, d, m), vmat(s->V, d, (int)D),
+                                      s->O, (int)D, 1.f, 0.f, EPI_STORE),
+                         st));
   HIPCHK(naive_rowstats(s->O, D, D, m, Y_idx, Y_val, K, s->cfg.loss, s->cfg.sph_eps, loss,
                         s->flags, st));
   {  // grad_H = (dL/dO) W  (K = D, split over K)
-    GemmBatch bt{};
-    bt.np = 1;
-    bt.p[0] = gemm_problem(L_NN, m, d, (int)D, vmat(s->O, (int)D, m), vmat(s->V, d, (int)D),
-                           s->wsplit, d, 1.f, 0.f, EPI_PARTIAL);
-    bt.p[0].ksplit = s->naive_ksplit;
-    HIPCHK(gemm_launch(bt, st));
+    GemmProblem p = gemm_problem(L_NN, m, d, (int)D, vmat(s->O, (int)D, m), vmat(s->V, d, (int)D),
+                                 s->wsplit, d, 1.f, 0.f, EPI_PARTIAL);
+    p.ksplit = s->naive_ksplit;
+    HIPCHK(gemm_big_launch(p, st));
     HIPCHK(gemm_splitk_reduce(s->wsplit, s->naive_ksplit, m, d, grad_H, d, sq ? 2.f : 1.f, 0.f, 0,
                               nullptr, st));
   }
-  {  // W -= lr (dL/dO)^T H^T
-    GemmBatch bt{};
-    bt.np = 1;
-    bt.skip_if = s->flags + F_ERR;
-    bt.p[0] = gemm_problem(L_TN, (int)D, d, m, vmat(s->O, (int)D, m), vmat(H, d, m), s->V, d,
-                           sq ? -2.f * lr : -lr, 1.f, EPI_STORE);
-    HIPCHK(gemm_launch(bt, st));
-  }
+  // W -= lr (dL/dO)^T H^T
+  HIPCHK(gemm_big_launch(gemm_problem(L_TN, (int)D, d, m, vmat(s->O, (int)D, m), vmat(H, d, m),
+                                      s->V, d, sq ? -2.f * lr : -lr, 1.f, EPI_STORE),
+                         st, s->flags + F_ERR));
   s->steps += 1;
   return LST_OK;
 }
@@ -658,6 +655,16 @@ int lst_profile_read(lst_state* s, double* ms_total, int32_t capacity, int32_t* 
 const char* lst_profile_phase_name(int32_t phase) {
   if (phase < 0 || phase >= PH_COUNT) return nullptr;
   return kPhaseNames[phase];
+}
+
+int lst_set_graphs(lst_state* s, int32_t enable) {
+  if (!s) return LST_EINVAL;
+  DeviceGuard dg(s->device);
+  HIPCHK(hipStreamSynchronize(s->stream));
+  s->use_graphs = enable ? 1 : 0;
+  for (auto& g : s->graphs) (void)hipGraphExecDestroy(g.exec);
+  s->graphs.clear();
+  return LST_OK;
 }
 
 void lst_free(lst_state* s) {

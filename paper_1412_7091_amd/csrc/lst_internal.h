@@ -63,9 +63,19 @@ struct GemmProblem {
   const float* s1;
   const float* s2;
   float* g; int ldg;
+  // A operand generated as N (m x m) from its pieces (a_nmat = 1):
+  // N_ij = a_i a_j C1_ij + a_i b_j C2_ij + b_i a_j C2t_ij + b_i b_j yy_ij,
+  // C1 = nC12[:, 0:m], C2 = nC12[:, m:2m] (leading dimension nld).
+  int a_nmat;
+  const float* nC12; int nld;
+  const float* nC2t;
+  const float* nyy;
+  const float* na;
+  const float* nb;
+  int nm;
 };
 
-constexpr int kMaxProblems = 3;
+constexpr int kMaxProblems = 4;
 
 struct GemmBatch {
   GemmProblem p[kMaxProblems];
@@ -75,56 +85,79 @@ struct GemmBatch {
   const int* run_if;   // zero *run_if: every block returns at once
   const int* skip_updates_if;  // nonzero: blocks of problems >= first_update return at once
   int first_update;
+  int kcw_max;                 // K chunk width of the panels (multiple of 16)
 };
+
+// One-time kernel attribute setup (dynamic LDS limits); call before any launch.
+hipError_t configure_kernels();
 
 VMat vmat(const float* p, int ld, int rows, const float* rscale = nullptr);
 VMat vmat2(const float* p0, int ld0, int rows0, const float* p1, int ld1, int rows1);
 GemmProblem gemm_problem(int layout, int M, int N, int K, const VMat& A, const VMat& B, float* C,
                          int ldc, float alpha, float beta, int epi);
-// Launches every problem of the batch in one grid.  tile: 64 or 32 (square
-// output tiles), 0 = choose from the number of tiles.
-hipError_t gemm_launch(GemmBatch& b, hipStream_t s, int tile = 0);
+// One large product (EPI_STORE or EPI_PARTIAL) on 128 x 128 double-buffered tiles.
+hipError_t gemm_big_launch(GemmProblem p, hipStream_t s, const int* skip_if = nullptr,
+                           const int* run_if = nullptr);
 // Split-K: C = alpha * sum_z ws[z] + beta * C (sym: r <= c mirrored).
 hipError_t gemm_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int ldc,
                               float alpha, float beta, int sym, const int* skip_if,
                               hipStream_t s);
 
-// ----------------------------------------------------- sparse target side
-struct SparseWs {
-  int* ex_row;       // m x K: per-example target rows sorted ascending (then by slot)
-  float* ex_val;     // m x K: values in the same order
-  int* ex_cnt;       // m: valid pairs per example
-  unsigned long long* keys;  // m x K: (row << 32 | slot) or ~0 for unused slots
-  int* srt_slot;     // m*K: slots in (row, slot) order
-  int* seg_row;      // m*K: distinct rows, ascending
-  int* seg_beg;      // m*K + 1: first sorted position of each distinct row
-  float* yy;         // m x m: Y^T Y
+// ------------------------------------------------------------ the step
+// Everything the tasks of one factored step read or write (device pointers).
+struct StepCtx {
+  int m, K, d;
+  int64_t D;
+  int loss_kind;
+  float eps, lr;
+  const float* H;
+  const int32_t* idx;
+  const float* val;
+  float *V, *Q, *U, *Uit;
+  float* Z0;   // m x ld0: [H^ | UH | P | H^T H] (rows = examples)
+  int ld0;
+  float *G, *Yh;
+  float* C12;  // m x ldc12: [H^T H^ | H^T Y^]
+  int ldc12;
+  float* C2t;  // m x m: (H^T Y^)^T
+  float *X, *T;
+  float *a, *b, *cs;  // per example
+  float *loss, *grad;
+  int* ex_row;  // m x K: each example's target rows, ascending (-1 after the valid ones)
+  float* ex_val;
+  int* ex_cnt;
+  float* yy;   // m x m: Y^T Y
+  int *hkey, *hmin;  // hash table of the step's target rows: smallest slot of each
+  int hbits;
+  int* touched;  // distinct rows of the step (unordered)
+  int* flags;
+  float* solve_ws;
 };
 
-hipError_t prep_examples(const int32_t* idx, const float* val, int m, int K, int64_t D,
-                         int one_hot, SparseWs ws, int* flags, hipStream_t s);
-hipError_t prep_global_sort(int m, int K, SparseWs ws, int* flags, hipStream_t s);
-hipError_t prep_target_gram(int m, int K, SparseWs ws, hipStream_t s);
-// G[i, :] = sum_k w_ik V[idx_ik, :]  (w = val, or 1 when one_hot)
-hipError_t gather_rows(const float* V, int64_t D, int d, const int32_t* idx, const float* val,
-                       int m, int K, int one_hot, float* G, int ldg, hipStream_t s);
-// V[r, :] += sum over the pairs (i,k) with idx_ik = r, in slot order, of coef * X[i, :]
-// coef = -val[i*K+k] (squared) or cs[i] (per-example coefficient).
-hipError_t scatter_rows(float* V, int d, const float* X, int ldx, const float* val,
-                        const float* cs, int m, int K, SparseWs ws, const int* flags,
-                        hipStream_t s);
+enum TaskKind {
+  TK_GEMM = 0, TK_GATHER, TK_PREP, TK_YY, TK_SCALARS, TK_SOLVE, TK_SCATTER, TK_CLEAR
+};
+constexpr int kMaxTasks = 6;
+
+// One heterogeneous launch: block ranges of its tasks (set by step_launch).
+struct StepLaunch {
+  int ntask;
+  int kind[kMaxTasks];
+  int begin[kMaxTasks + 1];
+  GemmBatch gemm;  // tiles of the TK_GEMM task (at most one per launch)
+  int timing_slot;  // which record of per-block times (builds with LST_TIMING only)
+};
+
+// Launches the tasks of L as one grid of 256-thread blocks; GEMM tiles are
+// tile x tile (32 or 64).
+hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, hipStream_t s);
+// Floats of global workspace the Woodbury solve needs for its m > 128 fallback.
+size_t solve_workspace_floats(int m_max, int d);
+// Sorts *n_ptr (<= 16384) ints ascending in place (one block).
+hipError_t sort_ints(int* v, const int* n_ptr, hipStream_t s);
+hipError_t fill_ints(int* p, int v, int n, hipStream_t s);
 
 // ------------------------------------------------------------ small dense
-// Per-example loss terms (loss, a, b, cs = b/a) and the m x m matrix N of the step.
-hipError_t minibatch_scalars(int loss_kind, float eps, int64_t D, int m, const float* C12,
-                             int ldc12, const float* yy, float* loss, float* a, float* b,
-                             float* cs, float* N, int* flags, hipStream_t s);
-// X = S^{-1} P^T (m x d) with S = H^T H - diag(1 / (lr a_i)), in 16-column blocks.
-hipError_t woodbury_solve(const float* HH, int ldh, const float* P, int ldp, int m, int d,
-                          int loss_kind, float eps, int64_t D, float lr, const float* C12,
-                          int ldc12, float* X, int ldx, float* gj_ws, int* flags, hipStream_t s);
-// Floats of global workspace woodbury_solve needs for its m > 128 fallback.
-size_t woodbury_workspace_floats(int m_max, int d);
 // Sinv = S^{-1} (Gauss-Jordan, partial pivoting); sets F_ERR = LST_ESINGULAR on a zero pivot.
 hipError_t invert_small(const float* S, int lds, float* Sinv, int ldi, int m, double* work,
                         int* flags, int check_err, hipStream_t s);

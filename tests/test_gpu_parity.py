@@ -44,6 +44,18 @@ def test_c1s_scaled_100_steps(gpu_lib):
     _assert(reports, W_rel)
 
 
+def test_c1_literal_with_drift_control(gpu_lib):
+    """D = 2000, d = 32, m = 16, H ~ N(0, 1), lr = 0.01: 2 lr ||H H^T|| exceeds 1, so U
+    turns ill-conditioned within a few steps and the m x m system is indefinite.  With
+    the pristine restore whenever ||U||_F ||U^-T||_F > 3 d, the run stays on the bar."""
+    reports, W_rel, extra = run_parity(CONFIGS["c1"], 100, cond_max=3.0, W_every=10)
+    assert extra["layer"].stats().restores > 0
+    for r in reports:
+        if r.W_rel is not None:
+            assert r.W_rel <= TOL_W, r
+    _assert(reports, W_rel)
+
+
 def test_ragged_padding_duplicates(gpu_lib):
     cfg = _cfg(pad_frac=0.2, dup_frac=0.3)
     reports, W_rel, _ = run_parity(cfg, 30, V_check_untouched=True)
@@ -140,6 +152,39 @@ def test_determinism(gpu_lib):
     assert torch.equal(a.get_V(), b.get_V())
     for (la, ga), (lb, gb) in zip(oa, ob):
         assert torch.equal(la, lb) and torch.equal(ga, gb)
+
+
+def test_graph_replay_matches_eager(gpu_lib):
+    """Captured steps replayed several times (three input buffers cycled, with eager
+    work and synchronisations in between) give bitwise the same results as the
+    eager path."""
+    import paper_1412_7091_amd as lst
+
+    for loss in ("squared", "spherical"):
+        kw = dict(K=1, val_dist="one", distinct=True, idx_dist="zipf") if loss == "spherical" \
+            else dict(K=6)
+        cfg = _cfg(D=3000, d=64, m=32, loss=loss, lr=5e-3, entropy=111, **kw)
+        wl = Workload(cfg)
+        dev = torch.device("cuda:0")
+        V0 = torch.from_numpy(wl.init_V()).to(dev)
+        layers = [lst.FactoredOutputLayer(V0, loss=loss, m_max=cfg.m, K_max=cfg.K) for _ in range(2)]
+        layers[1].set_graphs(False)
+        bufs = [tuple(torch.from_numpy(x).to(dev) for x in wl.batch(s)) for s in range(3)]
+        outs = [[], []]
+        for s in range(12):
+            H, idx, val = bufs[s % 3]
+            for li, layer in enumerate(layers):
+                loss_t, grad_t = layer.step(H, idx, val, cfg.lr)
+                outs[li].append((loss_t.clone(), grad_t.clone()))
+            torch.cuda.synchronize()
+            _ = (H * 2).sum().item()  # eager work between replays
+        for layer in layers:
+            assert layer.sync() == 0
+        for (la, ga), (lb, gb) in zip(*outs):
+            assert torch.equal(la, lb) and torch.equal(ga, gb)
+        for x, y in zip(layers[0].get_state(), layers[1].get_state()):
+            assert torch.equal(x, y)
+        assert torch.equal(layers[0].get_V(), layers[1].get_V())
 
 
 def test_restore_keeps_W_and_Q(gpu_lib):
