@@ -32,12 +32,15 @@ struct lst_state {
   float* Vtmp = nullptr;   // D x d copy for the pristine restore
   int* flags = nullptr;
   // factored workspace
-  float *G = nullptr, *Z0 = nullptr, *Yh = nullptr, *C12 = nullptr, *C2t = nullptr,
-        *a = nullptr, *b = nullptr, *cs = nullptr, *T = nullptr, *X = nullptr, *yy = nullptr,
-        *ex_val = nullptr, *solve_ws = nullptr;
-  int *ex_row = nullptr, *ex_cnt = nullptr, *hkey = nullptr, *hmin = nullptr, *touched = nullptr;
+  float *G = nullptr, *Z0 = nullptr, *Yh = nullptr, *NP = nullptr, *aH = nullptr, *bH = nullptr,
+        *a = nullptr, *b = nullptr, *cs = nullptr, *T = nullptr, *X = nullptr,
+        *ex_val = nullptr, *solve_ws = nullptr, *UHa = nullptr, *c1p = nullptr, *yyd = nullptr;
+  int *ex_row = nullptr, *ex_cnt = nullptr, *hkey = nullptr, *hmin = nullptr, *touched = nullptr,
+      *own = nullptr, *count = nullptr;
+  int last_slots = 0;  // m * K of the last factored step
   int hbits = 0;
-  int ld0 = 0, ldc12 = 0;
+  int ld0 = 0;
+  int n_c1p = 0;  // partial sums of h^T Q h per example (two per 32-column tile of H^)
   // naive workspace
   float* O = nullptr;
   float* wsplit = nullptr;
@@ -64,6 +67,9 @@ struct lst_state {
 };
 
 namespace {
+
+// GEMM tile edge of launch 1 (also fixes the number of h^T Q h partials).
+constexpr int kLaunch1Tile = 32;
 
 struct DeviceGuard {
   int prev = -1;
@@ -223,6 +229,27 @@ int pick_tile(const GemmBatch& b) {
   return t64 >= 128 ? 64 : 32;
 }
 
+// LDS stages of a launch's GEMM tiles: enough to issue every K chunk of the
+// longest problem before the first multiply, at most kMaxStages.
+#ifndef LST_MAX_STAGES
+#define LST_MAX_STAGES 9
+#endif
+constexpr int kMaxStages = LST_MAX_STAGES;
+int stages_for(const GemmBatch& b, int tile, int max_stages = kMaxStages) {
+  const int ck = 2048 / tile;
+  int nch = 1;
+  for (int q = 0; q < b.np; ++q) {
+    const int n = (b.p[q].K + ck - 1) / ck;
+    if (n > nch) nch = n;
+  }
+  return nch + 1 < max_stages ? nch + 1 : max_stages;
+}
+
+// Launch 1 also runs the gather and the target preparation, which need little
+// LDS: with at most 4 stages (64 KB) their blocks share compute units with the
+// GEMM tiles instead of waiting for them.
+constexpr int kLaunch1Stages = 4;
+
 // Enqueues the launches of one factored step on stream st.
 int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float* H,
                  const int32_t* Y_idx, const float* Y_val, float lr, float* loss, float* grad_H) {
@@ -234,13 +261,14 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
   c.H = H; c.idx = Y_idx; c.val = Y_val;
   c.V = s->V; c.Q = Qp(s); c.U = Up(s); c.Uit = Uitp(s);
   c.Z0 = s->Z0; c.ld0 = s->ld0;
-  c.G = s->G; c.Yh = s->Yh; c.C12 = s->C12; c.ldc12 = s->ldc12; c.C2t = s->C2t;
-  c.X = s->X; c.T = s->T;
-  c.a = s->a; c.b = s->b; c.cs = s->cs;
+  c.G = s->G; c.Yh = s->Yh; c.NP = s->NP; c.aH = s->aH; c.bH = s->bH;
+  c.X = s->X; c.T = s->T; c.UHa = s->UHa;
+  c.c1p = s->c1p; c.ld_c1p = s->n_c1p; c.n_c1p = s->n_c1p;
+  c.a = s->a; c.b = s->b; c.cs = s->cs; c.yyd = s->yyd;
   c.loss = loss; c.grad = grad_H;
-  c.ex_row = s->ex_row; c.ex_val = s->ex_val; c.ex_cnt = s->ex_cnt; c.yy = s->yy;
+  c.ex_row = s->ex_row; c.ex_val = s->ex_val; c.ex_cnt = s->ex_cnt;
   c.hkey = s->hkey; c.hmin = s->hmin; c.hbits = s->hbits;
-  c.touched = s->touched; c.flags = fl; c.solve_ws = s->solve_ws;
+  c.own = s->own; c.flags = fl; c.solve_ws = s->solve_ws;
   const float* Hh = s->Z0;          // H^ rows
   const float* UH = s->Z0 + d;      // (U H)^T rows
 
@@ -249,13 +277,15 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     L.ntask = 3;
     L.kind[0] = TK_GEMM; L.kind[1] = TK_GATHER; L.kind[2] = TK_PREP;
     L.gemm.np = 1;
-    L.gemm.kcw_max = 256;
-    L.gemm.p[0] = gemm_problem(L_NT, m, 3 * d + m, d, vmat(H, d, m),
-                               vmat2(s->state, d, 3 * d, H, d, m), s->Z0, s->ld0, 1.f, 0.f,
-                               EPI_STORE);
+    GemmProblem& p1 = L.gemm.p[0];
+    p1 = gemm_problem(L_NT, m, 3 * d + m, d, vmat(H, d, m), vmat2(s->state, d, 3 * d, H, d, m),
+                      s->Z0, s->ld0, 1.f, 0.f, EPI_STORE);
+    p1.dotp = s->c1p; p1.ld_dotp = s->n_c1p; p1.dot_ncols = d;  // h_i^T H^_i partials
+    p1.dot_h = H; p1.ld_doth = d;
+    L.lk = 1;
     L.timing_slot = 0;
     OK_OR_RETURN(prof_mark(s, PH_LAUNCH1, 0, st));
-    HIPCHK(step_launch(c, L, 32, st));
+    HIPCHK(step_launch(c, L, kLaunch1Tile, stages_for(L.gemm, kLaunch1Tile, kLaunch1Stages), st));
     OK_OR_RETURN(prof_mark(s, PH_LAUNCH1, 1, st));
   }
   {  // launch 2: Y^, C1, C2, C2^T ; solve ; Y^T Y ; per-example scalars
@@ -264,18 +294,19 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     L.kind[0] = TK_GEMM; L.kind[1] = TK_SOLVE; L.kind[2] = TK_YY; L.kind[3] = TK_SCALARS;
     GemmBatch& g = L.gemm;
     g.np = 4;
-    g.kcw_max = 256;
     g.p[0] = gemm_problem(L_NN, m, d, d, vmat(s->G, d, m), vmat(c.U, d, d), s->Yh, d, 1.f, 0.f,
                           EPI_STORE);
-    g.p[1] = gemm_problem(L_NT, m, m, d, vmat(H, d, m), vmat(Hh, s->ld0, m), s->C12, s->ldc12,
-                          1.f, 0.f, EPI_STORE);
-    g.p[2] = gemm_problem(L_NT, m, m, d, vmat(UH, s->ld0, m), vmat(s->G, d, m), s->C12 + m,
-                          s->ldc12, 1.f, 0.f, EPI_STORE);
-    g.p[3] = gemm_problem(L_NT, m, m, d, vmat(s->G, d, m), vmat(UH, s->ld0, m), s->C2t, m, 1.f,
+    // C1, C2 and C2^T go into NP = [C1 | C2 | C2^T | Y^T Y] (row stride 4m)
+    g.p[1] = gemm_problem(L_NT, m, m, d, vmat(H, d, m), vmat(Hh, s->ld0, m), s->NP, 4 * m, 1.f,
                           0.f, EPI_STORE);
+    g.p[2] = gemm_problem(L_NT, m, m, d, vmat(UH, s->ld0, m), vmat(s->G, d, m), s->NP + m, 4 * m,
+                          1.f, 0.f, EPI_STORE);
+    g.p[3] = gemm_problem(L_NT, m, m, d, vmat(s->G, d, m), vmat(UH, s->ld0, m), s->NP + 2 * m,
+                          4 * m, 1.f, 0.f, EPI_STORE);
+    L.lk = 2;
     L.timing_slot = 1;
     OK_OR_RETURN(prof_mark(s, PH_LAUNCH2, 0, st));
-    HIPCHK(step_launch(c, L, 32, st));
+    HIPCHK(step_launch(c, L, 32, stages_for(g, 32), st));
     OK_OR_RETURN(prof_mark(s, PH_LAUNCH2, 1, st));
   }
   {  // launch 3: grad_H and T ; U and U^{-T} updates ; scatter into V
@@ -284,24 +315,24 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     L.kind[0] = TK_GEMM; L.kind[1] = TK_SCATTER;
     GemmBatch& g = L.gemm;
     g.np = 3;
-    g.kcw_max = 256;
     GemmProblem& pt = g.p[0];
-    pt = gemm_problem(L_NN, m, d, m, vmat(nullptr, m, m), vmat(H, d, m), s->T, d, -0.5f * lr,
-                      0.f, EPI_GRADT);
-    pt.a_nmat = 1;
-    pt.nC12 = s->C12; pt.nld = s->ldc12; pt.nC2t = s->C2t; pt.nyy = s->yy;
-    pt.na = s->a; pt.nb = s->b; pt.nm = m;
+    // NP viewed as 2m x 2m (row stride 2m): row 2i = [C1 C2]_i, row 2i+1 = [C2^T Y^T Y]_i;
+    // times [a H; b H] it gives both halves of (N H^T)_i, combined in the epilogue.
+    pt = gemm_problem(L_NN, 2 * m, d, 2 * m, vmat(s->NP, 2 * m, 2 * m),
+                      vmat2(s->aH, d, m, s->bH, d, m), s->T, d, -0.5f * lr, 0.f, EPI_GRADT);
     pt.e1 = Hh; pt.lde1 = s->ld0; pt.e2 = s->Yh; pt.lde2 = d;
     pt.s1 = s->a; pt.s2 = s->b; pt.g = grad_H; pt.ldg = d;
-    g.p[1] = gemm_problem(L_TN, d, d, m, vmat(UH, s->ld0, m, s->a), vmat(H, d, m), c.U, d, -lr,
-                          1.f, EPI_STORE);
+    g.p[1] = gemm_problem(L_TN, d, d, m, vmat(s->UHa, d, m), vmat(H, d, m), c.U, d, -lr, 1.f,
+                          EPI_STORE);
     g.p[2] = gemm_problem(L_TN, d, d, m, vmat(s->X, d, m), vmat(H, d, m), c.Uit, d, -1.f, 1.f,
                           EPI_STORE);
     g.skip_updates_if = fl + F_ERR;  // the gradient tiles (problem 0) always run
     g.first_update = 1;
+    L.lk = 3;
     L.timing_slot = 2;
     OK_OR_RETURN(prof_mark(s, PH_LAUNCH3, 0, st));
-    HIPCHK(step_launch(c, L, pick_tile(g), st));
+    const int t3 = pick_tile(g);
+    HIPCHK(step_launch(c, L, t3, stages_for(g, t3), st));
     OK_OR_RETURN(prof_mark(s, PH_LAUNCH3, 1, st));
   }
   {  // launch 4: Q -= lr (H T^T + T H^T) ; clear the hash slots
@@ -310,13 +341,13 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     L.kind[0] = TK_GEMM; L.kind[1] = TK_CLEAR;
     GemmBatch& g = L.gemm;
     g.np = 1;
-    g.kcw_max = 256;
     g.skip_if = fl + F_ERR;
     g.p[0] = gemm_problem(L_TN, d, d, 2 * m, vmat2(H, d, m, s->T, d, m),
                           vmat2(s->T, d, m, H, d, m), c.Q, d, -lr, 1.f, EPI_SYM);
+    L.lk = 4;
     L.timing_slot = 3;
     OK_OR_RETURN(prof_mark(s, PH_LAUNCH4, 0, st));
-    HIPCHK(step_launch(c, L, 32, st));
+    HIPCHK(step_launch(c, L, 32, stages_for(g, 32), st));
     OK_OR_RETURN(prof_mark(s, PH_LAUNCH4, 1, st));
   }
   OK_OR_RETURN(prof_mark(s, PH_DRIFT, 0, st));
@@ -365,21 +396,24 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
   };
   if (rc != LST_OK) return fail(rc);
   s->ld0 = (3 * d + m + 3) / 4 * 4;
-  s->ldc12 = 2 * m;
+  s->n_c1p = 2 * ((d + kLaunch1Tile - 1) / kLaunch1Tile);
   s->hbits = 1;
   while ((1 << s->hbits) < 2 * m * K) ++s->hbits;
   const int hsize = 1 << s->hbits;
   const size_t md = (size_t)m * d;
   if ((rc = dalloc(s, &s->state, 3 * (size_t)d * d)) || (rc = dalloc(s, &s->G, md)) ||
       (rc = dalloc(s, &s->Z0, (size_t)m * s->ld0)) || (rc = dalloc(s, &s->Yh, md)) ||
-      (rc = dalloc(s, &s->C12, (size_t)m * s->ldc12)) || (rc = dalloc(s, &s->C2t, (size_t)m * m)) ||
+      (rc = dalloc(s, &s->NP, (size_t)4 * m * m)) || (rc = dalloc(s, &s->aH, md)) ||
+      (rc = dalloc(s, &s->bH, md)) ||
       (rc = dalloc(s, &s->a, m)) || (rc = dalloc(s, &s->b, m)) || (rc = dalloc(s, &s->cs, m)) ||
       (rc = dalloc(s, &s->T, md)) || (rc = dalloc(s, &s->X, md)) ||
-      (rc = dalloc(s, &s->yy, (size_t)m * m)) ||
       (rc = dalloc(s, &s->solve_ws, solve_workspace_floats(m, d))) ||
       (rc = dalloc(s, &s->ex_row, (size_t)m * K)) || (rc = dalloc(s, &s->ex_val, (size_t)m * K)) ||
       (rc = dalloc(s, &s->ex_cnt, m)) || (rc = dalloc(s, &s->hkey, hsize)) ||
-      (rc = dalloc(s, &s->hmin, hsize)) || (rc = dalloc(s, &s->touched, (size_t)m * K)))
+      (rc = dalloc(s, &s->hmin, hsize)) || (rc = dalloc(s, &s->touched, (size_t)m * K)) ||
+      (rc = dalloc(s, &s->own, (size_t)m * K)) || (rc = dalloc(s, &s->count, 1)) ||
+      (rc = dalloc(s, &s->UHa, md)) || (rc = dalloc(s, &s->yyd, m)) ||
+      (rc = dalloc(s, &s->c1p, (size_t)m * s->n_c1p)))
     return fail(rc);
   if (fill_ints(s->hkey, -1, hsize, s->stream) != hipSuccess ||
       fill_ints(s->hmin, 0x7fffffff, hsize, s->stream) != hipSuccess)
@@ -426,7 +460,10 @@ int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* 
   if (s->prof || !s->use_graphs) {
     if (s->prof) s->prof_steps += 1;
     rc = enqueue_step(s, s->stream, m, K, H, Y_idx, Y_val, lr, loss, grad_H);
-    if (rc == LST_OK) s->steps += 1;
+    if (rc == LST_OK) {
+      s->steps += 1;
+      s->last_slots = m * K;
+    }
     return rc;
   }
   uint32_t lr_bits;
@@ -466,6 +503,7 @@ int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* 
   hit->last_use = ++s->graph_clock;
   HIPCHK(hipGraphLaunch(hit->exec, s->stream));
   s->steps += 1;
+  s->last_slots = m * K;
   return LST_OK;
 }
 
@@ -505,14 +543,14 @@ int lst_touched_rows(lst_state* s, int32_t* rows, int32_t capacity, int32_t* cou
   if (s->kind != 0) return LST_ESTATE;
   DeviceGuard dg(s->device);
   int u = 0;
-  OK_OR_RETURN(read_flag(s, F_UNIQUE, &u));
-  if (s->steps == 0) u = 0;
-  if (u > capacity) return LST_EINVAL;
-  if (u > 0) {
-    HIPCHK(sort_ints(s->touched, s->flags + F_UNIQUE, s->stream));
+  if (s->steps > 0 && s->last_slots > 0) {
+    HIPCHK(compact_owned(s->own, s->last_slots, s->touched, s->count, s->stream));
+    HIPCHK(sort_ints(s->touched, s->count, s->stream));
     HIPCHK(hipStreamSynchronize(s->stream));
-    HIPCHK(hipMemcpy(rows, s->touched, (size_t)u * sizeof(int), hipMemcpyDeviceToHost));
+    HIPCHK(hipMemcpy(&u, s->count, sizeof(int), hipMemcpyDeviceToHost));
   }
+  if (u > capacity) return LST_EINVAL;
+  if (u > 0) HIPCHK(hipMemcpy(rows, s->touched, (size_t)u * sizeof(int), hipMemcpyDeviceToHost));
   *count = u;
   return LST_OK;
 }

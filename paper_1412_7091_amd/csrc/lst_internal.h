@@ -36,7 +36,9 @@ struct VMat {
 enum Epi {
   EPI_STORE = 0,    // C = alpha*acc + beta*C
   EPI_SYM = 1,      // upper-triangle tiles only: C[r][c] = C[c][r] = C[r][c] + alpha*acc (r <= c)
-  EPI_GRADT = 2,    // g = s1[r]*E1[r][c] + s2[r]*E2[r][c]; G[r][c] = g; C[r][c] = g + alpha*acc
+  EPI_GRADT = 2,    // output rows 2i, 2i+1 pair up into row i (M = 2 x rows of C):
+                    //   g = s1[i]*E1[i][c] + s2[i]*E2[i][c]; G[i][c] = g;
+                    //   C[i][c] = g + alpha*(s1[i]*acc[2i][c] + s2[i]*acc[2i+1][c])
   EPI_PARTIAL = 3   // split-K partial: slice z of a M x N workspace, reduced by gemm_splitk_reduce
 };
 
@@ -63,16 +65,12 @@ struct GemmProblem {
   const float* s1;
   const float* s2;
   float* g; int ldg;
-  // A operand generated as N (m x m) from its pieces (a_nmat = 1):
-  // N_ij = a_i a_j C1_ij + a_i b_j C2_ij + b_i a_j C2t_ij + b_i b_j yy_ij,
-  // C1 = nC12[:, 0:m], C2 = nC12[:, m:2m] (leading dimension nld).
-  int a_nmat;
-  const float* nC12; int nld;
-  const float* nC2t;
-  const float* nyy;
-  const float* na;
-  const float* nb;
-  int nm;
+  // EPI_STORE only: per-row partial dot products of the first dot_ncols
+  // output columns with dot_h (same row and column), one per (tile column,
+  // wave column): dotp[row * ld_dotp + 2 * tile_n + wave_n].
+  float* dotp; int ld_dotp;
+  int dot_ncols;
+  const float* dot_h; int ld_doth;
 };
 
 constexpr int kMaxProblems = 4;
@@ -85,7 +83,8 @@ struct GemmBatch {
   const int* run_if;   // zero *run_if: every block returns at once
   const int* skip_updates_if;  // nonzero: blocks of problems >= first_update return at once
   int first_update;
-  int kcw_max;                 // K chunk width of the panels (multiple of 16)
+  int stages;                  // LDS stages of the K pipeline (>= 2)
+  int timing_slot;             // record of per-block phase times (builds with LST_TIMING only)
 };
 
 // One-time kernel attribute setup (dynamic LDS limits); call before any launch.
@@ -117,19 +116,22 @@ struct StepCtx {
   float* Z0;   // m x ld0: [H^ | UH | P | H^T H] (rows = examples)
   int ld0;
   float *G, *Yh;
-  float* C12;  // m x ldc12: [H^T H^ | H^T Y^]
-  int ldc12;
-  float* C2t;  // m x m: (H^T Y^)^T
+  float* NP;   // m x 4m: [C1 | C2 | C2^T | Y^T Y] with C1 = H^T H^, C2 = H^T Y^
   float *X, *T;
+  float* UHa;         // m x d: a_i (U h_i)^T, the left factor of the U update
+  float *aH, *bH;     // m x d: a_i h_i^T and b_i h_i^T
+  float* c1p;         // m x ld_c1p: partial sums of h_i^T Q h_i (from launch 1)
+  int ld_c1p, n_c1p;  // row stride and number of partials per example
   float *a, *b, *cs;  // per example
+  float* yyd;         // per example: (Y^T Y)_ii
   float *loss, *grad;
   int* ex_row;  // m x K: each example's target rows, ascending (-1 after the valid ones)
   float* ex_val;
   int* ex_cnt;
-  float* yy;   // m x m: Y^T Y
   int *hkey, *hmin;  // hash table of the step's target rows: smallest slot of each
   int hbits;
-  int* touched;  // distinct rows of the step (unordered)
+  int* own;      // m x K: the row of slot i*K + k if that slot owns the row's
+                 // scatter in this step (its smallest slot), else -1
   int* flags;
   float* solve_ws;
 };
@@ -140,7 +142,10 @@ enum TaskKind {
 constexpr int kMaxTasks = 6;
 
 // One heterogeneous launch: block ranges of its tasks (set by step_launch).
+// lk (1..4) selects the kernel built for that launch of the step, which
+// contains only the tasks, GEMM layouts and epilogues that launch uses.
 struct StepLaunch {
+  int lk;
   int ntask;
   int kind[kMaxTasks];
   int begin[kMaxTasks + 1];
@@ -149,12 +154,17 @@ struct StepLaunch {
 };
 
 // Launches the tasks of L as one grid of 256-thread blocks; GEMM tiles are
-// tile x tile (32 or 64).
-hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, hipStream_t s);
+// tile x tile (32 or 64) with `stages` LDS stages (>= 2).
+hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, int stages, hipStream_t s);
+// 1 when every operand of the batch allows 16-byte LDS-DMA (aligned rows with
+// ld % 4 == 0, and K % 4 == 0 where k is the contiguous index).
+int gemm_batch_vec16(const GemmBatch& b);
 // Floats of global workspace the Woodbury solve needs for its m > 128 fallback.
 size_t solve_workspace_floats(int m_max, int d);
 // Sorts *n_ptr (<= 16384) ints ascending in place (one block).
 hipError_t sort_ints(int* v, const int* n_ptr, hipStream_t s);
+// out <- the entries of own[0 .. n) that are >= 0 (unordered); *count <- their number.
+hipError_t compact_owned(const int* own, int n, int* out, int* count, hipStream_t s);
 hipError_t fill_ints(int* p, int v, int n, hipStream_t s);
 
 // ------------------------------------------------------------ small dense

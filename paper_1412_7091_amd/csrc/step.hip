@@ -7,11 +7,12 @@
 //             gather G = (V^T Y)^T                                         (step 2, sparse part)
 //             prep  validate and sort each example's targets; record the
 //                   smallest slot of every target row in a hash table
-//   launch 2  GEMM  Y^ = G U, C1 = H^T H^, C2 = H^T Y^, C2t = C2^T          (steps 2, 5)
+//   launch 2  GEMM  Y^ = G U, C1 = H^T H^, C2 = H^T Y^, C2^T               (steps 2, 5)
 //             solve X = S^{-1} P^T, S = H^T H - diag(1/(lr a_i))           (step 8)
 //             yy    Y^T Y                                                  (step 5)
-//             scalars per example: loss, a_i, b_i, c_i                     (steps 3-6)
+//             scalars per example: loss, a_i, b_i, c_i, a h_i, b h_i       (steps 3-6)
 //   launch 3  GEMM  grad_H = H^ A + Y^ diag(b), T = grad_H - (lr/2) N H^T    (step 4)
+//                   with N H^T = A [C1 C2] [AH; BH] + B [C2^T Y^T Y] [AH; BH]
 //                   U -= lr (UH) A H^T, U^{-T} -= X^T H^T                   (steps 7, 8)
 //             scatter V[r] += sum over examples j holding r of c_j X_j     (step 9)
 //   launch 4  GEMM  Q -= lr (H T^T + T H^T), symmetric                      (step 10)
@@ -32,25 +33,32 @@ namespace lst {
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 __device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
 
-// sum_j x[j] y[j] by one full wave in a fixed order (lane-strided partial
-// sums, then a butterfly), so every wave that evaluates it gets the same bits.
-__device__ __forceinline__ float wave_dot(const float* x, const float* y, int n) {
-  float s = 0.f;
-  for (int j = lane_id(); j < n; j += 64) s += x[j] * y[j];
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
-  return s;
-}
-
 __device__ __forceinline__ unsigned row_hash(int r, int bits) {
   return ((unsigned)r * 2654435761u) >> (32 - bits);
 }
 
-// a_i of example i (squared error: 2; spherical: 2 / S_i).  Called by a full wave.
+// c1 = h_i^T Q h_i: the partial sums left by the first product of the step,
+// added in index order (the same bits wherever it is evaluated).
+__device__ __forceinline__ float example_c1(const StepCtx& c, int i) {
+  const float* p = c.c1p + (size_t)i * c.ld_c1p;
+  const int n = c.n_c1p;
+  float s = 0.f;
+  int t = 0;
+  for (; t + 8 <= n; t += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = p[t + u];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  for (; t < n; ++t) s += p[t];
+  return s;
+}
+
+// a_i of example i (squared error: 2; spherical: 2 / S_i, S_i = c1 + D eps).
 __device__ __forceinline__ float example_a(const StepCtx& c, int i) {
   if (c.loss_kind == LST_LOSS_SQUARED) return 2.f;
-  const float c1 = wave_dot(c.H + (size_t)i * c.d, c.Z0 + (size_t)i * c.ld0, c.d);
-  return 2.f / (c1 + (float)c.D * c.eps);
+  return 2.f / (example_c1(c, i) + (float)c.D * c.eps);
 }
 
 // ------------------------------------------------------------------ gather
@@ -110,11 +118,17 @@ __device__ __forceinline__ void task_gather(const StepCtx& c, int local) {
 
 // ------------------------------------------------------------------- prep
 // Example i: validate its K pairs, sort them by (row, slot) into
-// ex_row / ex_val, count them, and record in the hash table the smallest
-// slot (i*K + k) holding each row.  K <= 1024.
+// ex_row / ex_val, count them, record in the hash table the smallest slot
+// (i*K + k) holding each row, and form (Y^T Y)_ii = sum over distinct rows of
+// (sum of the row's values)^2, each row's values added in slot order.
+// K <= 1024.
+constexpr size_t kPrepLds = 1024 * (sizeof(unsigned long long) + sizeof(float)) + 256 * 4 + 16;
+
 __device__ __forceinline__ void task_prep(const StepCtx& c, int i, unsigned char* sraw) {
   unsigned long long* keys = reinterpret_cast<unsigned long long*>(sraw);
-  int* cnt = reinterpret_cast<int*>(sraw + 1024 * sizeof(unsigned long long));
+  float* vals = reinterpret_cast<float*>(sraw + 1024 * sizeof(unsigned long long));
+  float* red = vals + 1024;
+  int* cnt = reinterpret_cast<int*>(red + 256);
   const bool one_hot = c.loss_kind == LST_LOSS_SPHERICAL;
   constexpr unsigned long long kNoKey = ~0ull;
   if (threadIdx.x == 0) *cnt = 0;
@@ -126,6 +140,7 @@ __device__ __forceinline__ void task_prep(const StepCtx& c, int i, unsigned char
     const bool bad = (r < -1) || ((int64_t)r >= c.D) || (one_hot && r == -1);
     if (bad) atomicCAS(c.flags + F_ERR, 0, LST_EINDEX);
     keys[k] = valid ? (((unsigned long long)(unsigned)r << 32) | (unsigned)k) : kNoKey;
+    vals[k] = valid ? (one_hot ? 1.f : c.val[(size_t)i * c.K + k]) : 0.f;
     if (valid) {
       atomicAdd(cnt, 1);
       const int slot = i * c.K + k;
@@ -141,20 +156,36 @@ __device__ __forceinline__ void task_prep(const StepCtx& c, int i, unsigned char
     }
   }
   __syncthreads();
+  float yy_part = 0.f;
   for (int k = threadIdx.x; k < c.K; k += blockDim.x) {
     const unsigned long long key = keys[k];
+    const unsigned row = (unsigned)(key >> 32);
     int rank = 0;
+    bool first = true;
+    float run = 0.f;
     for (int k2 = 0; k2 < c.K; ++k2) {
       const unsigned long long o = keys[k2];
       rank += (o < key) || (o == key && k2 < k);
+      if ((unsigned)(o >> 32) == row && o != kNoKey) {
+        run += vals[k2];
+        first = first && !(k2 < k);
+      }
     }
     const bool valid = key != kNoKey;
-    const int kk = (int)(key & 0xffffffffu);
-    c.ex_row[(size_t)i * c.K + rank] = valid ? (int)(key >> 32) : -1;
-    c.ex_val[(size_t)i * c.K + rank] =
-        valid ? (one_hot ? 1.f : c.val[(size_t)i * c.K + kk]) : 0.f;
+    if (valid && first) yy_part += run * run;
+    c.ex_row[(size_t)i * c.K + rank] = valid ? (int)row : -1;
+    c.ex_val[(size_t)i * c.K + rank] = vals[k];
   }
-  if (threadIdx.x == 0) c.ex_cnt[i] = *cnt;
+  red[threadIdx.x] = yy_part;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    c.ex_cnt[i] = *cnt;
+    c.yyd[i] = red[0];
+  }
 }
 
 // --------------------------------------------------------------------- Y^T Y
@@ -219,46 +250,89 @@ __device__ __forceinline__ void task_yy(const StepCtx& c, int local, unsigned ch
   else
     acc = merge_dot(c.ex_row + (size_t)i * c.K, c.ex_val + (size_t)i * c.K, c.ex_cnt[i],
                     c.ex_row + (size_t)j * c.K, c.ex_val + (size_t)j * c.K, c.ex_cnt[j]);
-  c.yy[(size_t)i * c.m + j] = acc;
-  c.yy[(size_t)j * c.m + i] = acc;
+  float* yy = c.NP + 3 * c.m;  // the Y^T Y block of NP (row stride 4m)
+  yy[(size_t)i * 4 * c.m + j] = acc;
+  yy[(size_t)j * 4 * c.m + i] = acc;
 }
 
 // ----------------------------------------------------------------- scalars
-// One wave per example: c1 = h^T Q h, c2 = h^T W^T y, (Y^T Y)_ii, then
+// One wave per example: c1 = h^T Q h (from the partials of launch 1),
+// c2 = h^T W^T y = (U h)^T (V^T y), (Y^T Y)_ii (from prep), then
 //   squared:   loss = c1 - 2 c2 + (Y^T Y)_ii (= M_ii, Appendix A step 6), a = 2, b = -2
 //   spherical: loss = -log(c2^2 + eps) + log(c1 + D eps), a = 2/(c1 + D eps),
 //              b = -2 c2 / (c2^2 + eps), cs = b / a (the scatter weight)
-// Block 0 also counts the step's target pairs and resets the distinct-row count.
+// and the row a (U h)^T of the U update's left factor.  Block 0 also counts
+// the step's target pairs and resets the distinct-row count.
 __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
-  if (local == 0 && threadIdx.x == 0) {
+  if (local == 0 && wave_id() == 0) {
     int nnz = 0;
-    for (int j = 0; j < c.m; ++j) nnz += c.ex_cnt[j];
-    c.flags[F_NNZ] = nnz;
-    c.flags[F_UNIQUE] = 0;
+    for (int j = lane_id(); j < c.m; j += 64) nnz += c.ex_cnt[j];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) nnz += __shfl_xor(nnz, off);
+    if (lane_id() == 0) {
+      c.flags[F_NNZ] = nnz;
+      c.flags[F_UNIQUE] = 0;
+    }
   }
   const int i = local * 4 + wave_id();
   if (i >= c.m) return;
-  const float c1 = wave_dot(c.H + (size_t)i * c.d, c.Z0 + (size_t)i * c.ld0, c.d);
-  const float c2 = wave_dot(c.Z0 + (size_t)i * c.ld0 + c.d, c.G + (size_t)i * c.d, c.d);
-  if (lane_id() != 0) return;
-  float L, a, b, cs;
+  const int lane = lane_id(), d = c.d;
+  const float c1 = example_c1(c, i);
+  const float Si = c1 + (float)c.D * c.eps;
+  const float a = (c.loss_kind == LST_LOSS_SQUARED) ? 2.f : 2.f / Si;
+  const float* uh = c.Z0 + (size_t)i * c.ld0 + d;
+  const float* gr = c.G + (size_t)i * d;
+  float* uha = c.UHa + (size_t)i * d;
+  float s = 0.f;
+  for (int j0 = 0; j0 < d; j0 += 512) {
+    float xv[8], yv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int j = min(j0 + lane + 64 * u, d - 1);
+      xv[u] = uh[j];
+      yv[u] = gr[j];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int j = j0 + lane + 64 * u;
+      if (j < d) {
+        s += xv[u] * yv[u];
+        uha[j] = a * xv[u];
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+  const float c2 = s;
+  float L, b, cs;
   if (c.loss_kind == LST_LOSS_SQUARED) {
-    const int* ri = c.ex_row + (size_t)i * c.K;
-    const float* vi = c.ex_val + (size_t)i * c.K;
-    const int n = c.ex_cnt[i];
-    const float yy = merge_dot(ri, vi, n, ri, vi, n);
-    L = c1 - 2.f * c2 + yy;
-    a = 2.f;
+    L = c1 - 2.f * c2 + c.yyd[i];
     b = -2.f;
     cs = 0.f;
   } else {
-    const float Si = c1 + (float)c.D * c.eps;
     const float num = c2 * c2 + c.eps;
     L = -logf(num) + logf(Si);
-    a = 2.f / Si;
     b = -2.f * c2 / num;
     cs = b / a;
   }
+  // a h_i and b h_i: the right factor of the product that gives N H^T
+  const float* hr = c.H + (size_t)i * d;
+  float* ah = c.aH + (size_t)i * d;
+  float* bh = c.bH + (size_t)i * d;
+  for (int j0 = 0; j0 < d; j0 += 512) {
+    float hv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) hv[u] = hr[min(j0 + lane + 64 * u, d - 1)];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int j = j0 + lane + 64 * u;
+      if (j < d) {
+        ah[j] = a * hv[u];
+        bh[j] = b * hv[u];
+      }
+    }
+  }
+  if (lane != 0) return;
   c.loss[i] = L;
   c.a[i] = a;
   c.b[i] = b;
@@ -346,8 +420,22 @@ __host__ __device__ inline size_t solve_lds_bytes(int m) {
   return (neumann > gj ? neumann : gj) + extra;
 }
 
+#ifdef LST_TIMING
+// Phase marks of the last solve blocks (latency studies only).
+__device__ unsigned long long g_solve_marks[64][8];
+#define LST_SMARK(k)                                                        \
+  do {                                                                      \
+    if (threadIdx.x == 0 && local < 64) g_solve_marks[local][k] = wall_clock64(); \
+  } while (0)
+#else
+#define LST_SMARK(k) \
+  do {               \
+  } while (0)
+#endif
+
 template <bool SMALL>
 __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned char* sraw) {
+  LST_SMARK(0);
   const int m = c.m, d = c.d;
   const float* HH = c.Z0 + 3 * d;
   const float* P = c.Z0 + 2 * d;
@@ -360,117 +448,106 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   float* red = reinterpret_cast<float*>(sraw + main_bytes);
   double* colk = reinterpret_cast<double*>(red + 256);
   int* s_int = reinterpret_cast<int*>(colk + 512);  // s_p, s_bad
-  float* s_flt = reinterpret_cast<float*>(s_int + 2);  // r, amax
-  float* cinv = reinterpret_cast<float*>(sraw);        // mp
+  float* cinv = reinterpret_cast<float*>(sraw);        // mp: 1 / c_i = lr a_i
   float* Bt = cinv + mp;                               // kSolveCols x LDE: B^T
   float* Y0 = Bt + kSolveCols * LDE;                   // kSolveCols x LDE: Y^T
   float* Y1 = Y0 + kSolveCols * LDE;
-  float* Es = Y1 + kSolveCols * LDE;                   // mp x LDE (SMALL only)
+  float* Hs = Y1 + kSolveCols * LDE;                   // mp x LDE: H^T H (SMALL only)
 
-  for (int i = wave; i < mp; i += 4) {
-    const float a = (i < m) ? example_a(c, i) : 0.f;
-    if (lane == 0) cinv[i] = (i < m) ? c.lr * a : 0.f;  // 1 / c_i
-  }
+  for (int i = tid; i < mp; i += 256) cinv[i] = (i < m) ? c.lr * example_a(c, i) : 0.f;
   if (tid == 0) s_int[1] = 0;
-  __syncthreads();
-  float rowmax = 0.f, amax = 0.f;
+  LST_SMARK(1);
   if (SMALL) {
-    const bool vec4 = (ldh % 4 == 0) && (((uintptr_t)HH & 15) == 0);
+    // H^T H into LDS, zero-padded to mp x mp; addresses are clamped so that
+    // every load is issued before the first store.
+    const bool vec4 = (ldh % 4 == 0) && (((uintptr_t)HH & 15) == 0) && (m % 4 == 0);
     constexpr int NQ = 128 * 128 / 4 / 256;
+    const int q4 = mp / 4;
     float4 r4[NQ];
+    if (vec4) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int e4 = tid + 256 * q;
+        const int i = min(e4 / q4, m - 1), j = min(4 * (e4 % q4), m - 4);
+        r4[q] = *reinterpret_cast<const float4*>(HH + (size_t)i * ldh + j);
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int e4 = tid + 256 * q;
+        const int i = min(e4 / q4, m - 1), j = 4 * (e4 % q4);
+        const float* hr = HH + (size_t)i * ldh;
+        r4[q].x = hr[min(j, m - 1)];
+        r4[q].y = hr[min(j + 1, m - 1)];
+        r4[q].z = hr[min(j + 2, m - 1)];
+        r4[q].w = hr[min(j + 3, m - 1)];
+      }
+    }
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const int e4 = tid + 256 * q;
-      const int i = e4 / (mp / 4), j = 4 * (e4 - i * (mp / 4));
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (e4 < mp * mp / 4 && i < m) {
-        const float* hr = HH + (size_t)i * ldh + j;
-        if (vec4 && j + 3 < m) {
-          v = *reinterpret_cast<const float4*>(hr);
-        } else {
-          if (j < m) v.x = hr[0];
-          if (j + 1 < m) v.y = hr[1];
-          if (j + 2 < m) v.z = hr[2];
-          if (j + 3 < m) v.w = hr[3];
-        }
+      if (e4 < mp * q4) {
+        const int i = e4 / q4, j = 4 * (e4 % q4);
+        const bool ok = i < m;
+        float4 v;
+        v.x = (ok && j < m) ? r4[q].x : 0.f;
+        v.y = (ok && j + 1 < m) ? r4[q].y : 0.f;
+        v.z = (ok && j + 2 < m) ? r4[q].z : 0.f;
+        v.w = (ok && j + 3 < m) ? r4[q].w : 0.f;
+        *reinterpret_cast<float4*>(Hs + i * LDE + j) = v;
       }
-      r4[q] = v;
-    }
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int e4 = tid + 256 * q;
-      if (e4 < mp * mp / 4) {
-        const int i = e4 / (mp / 4), j = 4 * (e4 - i * (mp / 4));
-        const float ci = cinv[i];
-        *reinterpret_cast<float4*>(Es + i * LDE + j) =
-            make_float4(r4[q].x * ci, r4[q].y * ci, r4[q].z * ci, r4[q].w * ci);
-      }
-    }
-    __syncthreads();
-    for (int i = tid; i < m; i += 256) {
-      float sabs = 0.f, hmax = 0.f;
-      const float ci = 1.f / cinv[i];
-      for (int j = 0; j < m; ++j) {
-        const float e = Es[i * LDE + j];
-        sabs += fabsf(e);
-        hmax = fmaxf(hmax, fabsf(e * ci - (i == j ? ci : 0.f)));
-      }
-      rowmax = fmaxf(rowmax, sabs);
-      amax = fmaxf(amax, hmax);
-    }
-  } else {
-    for (int i = tid; i < m; i += 256) {
-      float sabs = 0.f, hmax = 0.f;
-      const float ci = 1.f / cinv[i];
-      const float* hr = HH + (size_t)i * ldh;
-      for (int j0 = 0; j0 < m; j0 += 8) {
-        float hv[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) hv[u] = (j0 + u < m) ? hr[j0 + u] : 0.f;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          sabs += fabsf(hv[u]);
-          hmax = fmaxf(hmax, fabsf(hv[u] - (i == j0 + u ? ci : 0.f)));
-        }
-      }
-      rowmax = fmaxf(rowmax, sabs * cinv[i]);
-      amax = fmaxf(amax, hmax);
     }
   }
-  if (!(rowmax == rowmax)) rowmax = INFINITY;
-  red[tid] = rowmax;
   __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if (tid < off) red[tid] = fmaxf(red[tid], red[tid + off]);
-    __syncthreads();
+  LST_SMARK(2);
+  // r = ||E||_inf with E = diag(1/c) H^T H, and max |S_ij| for the fallback's
+  // pivot threshold.  H^T H is symmetric, so the absolute sum of its row i is
+  // that of column i: thread i walks down column i (consecutive threads read
+  // consecutive addresses), and the block takes the maximum.
+  float rmax = 0.f, amax = 0.f;
+  for (int i = tid; i < m; i += 256) {
+    const float ci = 1.f / cinv[i];
+    float sabs = 0.f, hmax = 0.f;
+#pragma unroll 8
+    for (int j = 0; j < m; ++j) {
+      const float h = SMALL ? Hs[j * LDE + i] : HH[(size_t)j * ldh + i];
+      sabs += fabsf(h);
+      hmax = fmaxf(hmax, fabsf(h - (i == j ? ci : 0.f)));
+    }
+    const float ri = sabs * cinv[i];
+    rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
+    amax = fmaxf(amax, hmax);
   }
-  if (tid == 0) s_flt[0] = red[0];
-  __syncthreads();
-  red[tid] = amax;
-  __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if (tid < off) red[tid] = fmaxf(red[tid], red[tid + off]);
-    __syncthreads();
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    rmax = fmaxf(rmax, __shfl_xor(rmax, off));
+    amax = fmaxf(amax, __shfl_xor(amax, off));
   }
-  if (tid == 0) s_flt[1] = red[0];
+  if (lane == 0) {
+    red[wave] = rmax;
+    red[4 + wave] = amax;
+  }
   __syncthreads();
-  const float r = s_flt[0];
+  const float r = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const float smax = fmaxf(fmaxf(red[4], red[5]), fmaxf(red[6], red[7]));
+  LST_SMARK(3);
 
   if (r < 0.5f) {
+    // B^T = -(P^T_blk) diag(1/c)^T, Y0 = B^T.
     for (int e0 = 0; e0 < kSolveCols * mp; e0 += 256 * 8) {
       float pv[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int e = e0 + tid + 256 * u;
-        const int i = e / kSolveCols, cc = e - i * kSolveCols;
-        pv[u] = (e < kSolveCols * mp && i < m && c0 + cc < d) ? P[(size_t)i * ldp + c0 + cc] : 0.f;
+        const int i = min(e / kSolveCols, m - 1), cc = min(c0 + e % kSolveCols, d - 1);
+        pv[u] = P[(size_t)i * ldp + cc];
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int e = e0 + tid + 256 * u;
         if (e < kSolveCols * mp) {
           const int i = e / kSolveCols, cc = e - i * kSolveCols;
-          const float v = -pv[u] * cinv[i];
+          const float v = (i < m && c0 + cc < d) ? -pv[u] * cinv[i] : 0.f;
           Bt[cc * LDE + i] = v;
           Y0[cc * LDE + i] = v;
         }
@@ -484,57 +561,91 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
       if (iters > 64) iters = 64;
     }
     __syncthreads();
+    LST_SMARK(4);
+#ifdef LST_TIMING
+    if (threadIdx.x == 0 && local < 64) g_solve_marks[local][7] = (unsigned long long)iters;
+#endif
+    // Y_{k+1} = B + diag(1/c) (H^T H) Y_k.  Wave w owns the 16-row blocks
+    // w, w + 4, ...; the B fragment of a k slice is shared by them.
+    constexpr int RBW = SMALL ? 2 : 8;
+    const int nrb = mp / 16;
     float* Yo = Y0;
     float* Yn = Y1;
-    for (int it = 0; it < iters; ++it) {
-      for (int rb = wave; rb < mp / 16; rb += 4) {
-        floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
-        const int arow = rb * 16 + (lane & 15);
-        for (int kk = 0; kk < mp; kk += 16) {
-          const int k = kk + 4 * (lane >> 4);
-          float4 fa;
-          if (SMALL) {
-            fa = *reinterpret_cast<const float4*>(Es + arow * LDE + k);
-          } else {
-            fa = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (arow < m) {
-              const float* hr = HH + (size_t)arow * ldh;
-              if (k < m) fa.x = hr[k];
-              if (k + 1 < m) fa.y = hr[k + 1];
-              if (k + 2 < m) fa.z = hr[k + 2];
-              if (k + 3 < m) fa.w = hr[k + 3];
-            }
-          }
-          const float4 fb = *reinterpret_cast<const float4*>(Yo + (lane & 15) * LDE + k);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.x, fb.x, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.y, fb.y, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.z, fb.z, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.w, fb.w, acc, 0, 0, 0);
+    // One 16-wide k slice: B fragment (shared by the wave's row blocks) and
+    // the A fragments of its row blocks.
+    auto frag = [&](const float* Yk, int kk, float4& fb, float4 (&fa)[RBW]) {
+      const int k = kk + 4 * (lane >> 4);
+      fb = *reinterpret_cast<const float4*>(Yk + (lane & 15) * LDE + k);
+#pragma unroll
+      for (int t = 0; t < RBW; ++t) {
+        const int arow = min((wave + 4 * t) * 16, mp - 16) + (lane & 15);
+        if (SMALL) {
+          fa[t] = *reinterpret_cast<const float4*>(Hs + arow * LDE + k);
+        } else {
+          const float* hr = HH + (size_t)min(arow, m - 1) * ldh;
+          const float x0 = hr[min(k, m - 1)], x1 = hr[min(k + 1, m - 1)];
+          const float x2 = hr[min(k + 2, m - 1)], x3 = hr[min(k + 3, m - 1)];
+          const bool ok = arow < m;
+          fa[t].x = (ok && k < m) ? x0 : 0.f;
+          fa[t].y = (ok && k + 1 < m) ? x1 : 0.f;
+          fa[t].z = (ok && k + 2 < m) ? x2 : 0.f;
+          fa[t].w = (ok && k + 3 < m) ? x3 : 0.f;
         }
-        const int col = lane & 15;
+      }
+    };
+    for (int it = 0; it < iters; ++it) {
+      floatx4 acc[RBW];
+#pragma unroll
+      for (int t = 0; t < RBW; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+      float4 fb0, fb1, fa0[RBW], fa1[RBW];
+      auto mma = [&](const float4& fb, const float4 (&fa)[RBW]) {
+#pragma unroll
+        for (int t = 0; t < RBW; ++t) {
+          if (wave + 4 * t >= nrb) break;
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[t].x, fb.x, acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[t].y, fb.y, acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[t].z, fb.z, acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[t].w, fb.w, acc[t], 0, 0, 0);
+        }
+      };
+      // fragments of slice s + 1 are read while slice s is multiplied
+      frag(Yo, 0, fb0, fa0);
+      for (int kk = 0; kk < mp; kk += 32) {
+        frag(Yo, min(kk + 16, mp - 16), fb1, fa1);
+        mma(fb0, fa0);
+        if (kk + 16 >= mp) break;
+        frag(Yo, min(kk + 32, mp - 16), fb0, fa0);
+        mma(fb1, fa1);
+      }
+      const int col = lane & 15;
+#pragma unroll
+      for (int t = 0; t < RBW; ++t) {
+        const int rb = wave + 4 * t;
+        if (rb >= nrb) break;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int row = rb * 16 + 4 * (lane >> 4) + q;
-          const float ey = SMALL ? acc[q] : acc[q] * cinv[row];
-          Yn[col * LDE + row] = Bt[col * LDE + row] + ey;
+          Yn[col * LDE + row] = Bt[col * LDE + row] + acc[t][q] * cinv[row];
         }
       }
       __syncthreads();
-      float* t = Yo;
+      float* tt = Yo;
       Yo = Yn;
-      Yn = t;
+      Yn = tt;
     }
+    LST_SMARK(5);
     for (int e = tid; e < kSolveCols * m; e += 256) {
       const int i = e / kSolveCols, cc = e - i * kSolveCols;
       if (c0 + cc < d) c.X[(size_t)i * d + c0 + cc] = Yo[cc * LDE + i];
     }
+    LST_SMARK(6);
     return;
   }
 
   // Fallback: Gauss-Jordan on [S | P^T_blk], S = H^T H - diag(c).  c_i moves
   // to colk first: the fp64 matrix overwrites the buffers that hold 1/c_i.
   const int ncol = m + kSolveCols;
-  const double tiny = 1e-13 * (double)s_flt[1];
+  const double tiny = 1e-13 * (double)smax;
   for (int i = tid; i < m; i += 256) colk[i] = 1.0 / (double)cinv[i];
   __syncthreads();
   if (SMALL) {
@@ -591,28 +702,27 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
 // c_j X[j, :], c_j = -(sum of j's values at r) (squared) or cs_j (spherical),
 // in increasing j.  One wave per (example, slot) pair; only the pair with the
 // smallest slot of its row (read from the hash table) does the work, so every
-// row is written once and in a fixed order.  The touched row is appended to
-// the step's row list (the hash slots are cleared from it in launch 4).
+// row is written once and in a fixed order.  Each pair records in own[] the
+// row it owns (or -1); launch 4 clears the hash slots from that record.
 __device__ __forceinline__ void task_scatter(const StepCtx& c, int local) {
   const int e = local * 4 + wave_id();
   if (e >= c.m * c.K) return;
   const int lane = lane_id();
-  const int i = e / c.K, k = e - i * c.K;
+  const int i = e / c.K;
   const int r = c.idx[e];
-  if (r < 0 || (int64_t)r >= c.D) return;
-  const int mask = (1 << c.hbits) - 1;
-  unsigned h = row_hash(r, c.hbits);
-  int probe = 0;
-  while (probe <= mask && c.hkey[h] != r) {
-    h = (h + 1) & mask;
-    ++probe;
+  bool owner = false;
+  if (r >= 0 && (int64_t)r < c.D) {
+    const int mask = (1 << c.hbits) - 1;
+    unsigned h = row_hash(r, c.hbits);
+    int probe = 0;
+    while (probe <= mask && c.hkey[h] != r) {
+      h = (h + 1) & mask;
+      ++probe;
+    }
+    owner = probe <= mask && c.hmin[h] == e;
   }
-  if (probe > mask || c.hmin[h] != e) return;  // not the owner of row r
-  if (lane == 0) {
-    const int pos = atomicAdd(c.flags + F_UNIQUE, 1);
-    c.touched[pos] = r;
-  }
-  if (c.flags[F_ERR]) return;
+  if (lane == 0) c.own[e] = owner ? r : -1;
+  if (!owner || c.flags[F_ERR]) return;
   const bool one_hot = c.loss_kind == LST_LOSS_SPHERICAL;
   const bool vec = (c.d % 4 == 0);
   // columns in groups of 1024 (four 256-column chunks held in registers)
@@ -682,49 +792,93 @@ __device__ __forceinline__ void task_scatter(const StepCtx& c, int local) {
   }
 }
 
-// Launch 4: empty the hash slots of the rows this step touched.
+// Launch 4: empty the hash slots of the rows this step touched (found from
+// own[]) and count the distinct rows (one atomic per block).
 __device__ __forceinline__ void task_clear(const StepCtx& c, int local) {
+  __shared__ int s_cnt[4];
   const int t = local * 256 + threadIdx.x;
-  if (t >= c.flags[F_UNIQUE]) return;
-  const int r = c.touched[t];
-  const int mask = (1 << c.hbits) - 1;
-  unsigned h = row_hash(r, c.hbits);
-  for (int probe = 0; probe <= mask; ++probe) {
-    if (c.hkey[h] == r) {
-      c.hkey[h] = -1;
-      c.hmin[h] = 0x7fffffff;
-      return;
+  const int r = (t < c.m * c.K) ? c.own[t] : -1;
+  if (r >= 0) {
+    const int mask = (1 << c.hbits) - 1;
+    unsigned h = row_hash(r, c.hbits);
+    for (int probe = 0; probe <= mask; ++probe) {
+      if (c.hkey[h] == r) {
+        c.hkey[h] = -1;
+        c.hmin[h] = 0x7fffffff;
+        break;
+      }
+      h = (h + 1) & mask;
     }
-    h = (h + 1) & mask;
+  }
+  const unsigned long long bal = __ballot(r >= 0);
+  if (lane_id() == 0) s_cnt[wave_id()] = __popcll(bal);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int n = s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
+    if (n > 0) atomicAdd(c.flags + F_UNIQUE, n);
   }
 }
 
 // -------------------------------------------------------------- the kernel
+// Dynamic LDS a step launch may use (of the 160 KB of a compute unit).
+constexpr size_t kStepLdsMax = 160 * 1024 - 1024;
+
 #ifdef LST_TIMING
 // Per-block (start, end) wall clock of the last launches, for latency studies.
 __device__ unsigned long long g_step_times[4][8192][3];
 #endif
 
-template <int TILE, bool SMALLM>
+// What each launch kind of the step runs: task kinds, GEMM operand layouts
+// (V_*) and GEMM epilogues.  The kernel of a launch kind compiles only these,
+// which keeps its code small enough for the instruction cache.
+struct LaunchMasks {
+  unsigned tasks, vars, epis;
+};
+constexpr LaunchMasks kLaunchMasks[5] = {
+    {0u, 0u, 0u},
+    {(1u << TK_GEMM) | (1u << TK_GATHER) | (1u << TK_PREP), V_NT, 1u << EPI_STORE},
+    {(1u << TK_GEMM) | (1u << TK_SOLVE) | (1u << TK_YY) | (1u << TK_SCALARS), V_NN | V_NT,
+     1u << EPI_STORE},
+    {(1u << TK_GEMM) | (1u << TK_SCATTER), V_NN | V_TN, (1u << EPI_GRADT) | (1u << EPI_STORE)},
+    {(1u << TK_GEMM) | (1u << TK_CLEAR), V_TN, 1u << EPI_SYM},
+};
+
+template <int TILE, bool SMALLM, int W, int LK>
 __device__ __forceinline__ void run_task(const StepCtx& c, const StepLaunch& L, int t, int local,
                                          unsigned char* sraw) {
-  switch (L.kind[t]) {
-    case TK_GEMM:
+  constexpr LaunchMasks M = kLaunchMasks[LK];
+  const int kind = L.kind[t];
+  if constexpr ((M.tasks >> TK_GEMM) & 1u) {
+    if (kind == TK_GEMM) {
       if (L.gemm.skip_if && *L.gemm.skip_if) return;
-      panel_tile<TILE, TILE>(L.gemm, local, reinterpret_cast<float*>(sraw));
-      break;
-    case TK_GATHER: task_gather(c, local); break;
-    case TK_PREP: task_prep(c, local, sraw); break;
-    case TK_YY: task_yy(c, local, sraw); break;
-    case TK_SCALARS: task_scalars(c, local); break;
-    case TK_SOLVE: task_solve<SMALLM>(c, local, sraw); break;
-    case TK_SCATTER: task_scatter(c, local); break;
-    case TK_CLEAR: task_clear(c, local); break;
-    default: break;
+      panel_tile<TILE, W, M.vars, M.epis>(L.gemm, local, reinterpret_cast<float*>(sraw));
+      return;
+    }
+  }
+  if constexpr ((M.tasks >> TK_GATHER) & 1u) {
+    if (kind == TK_GATHER) { task_gather(c, local); return; }
+  }
+  if constexpr ((M.tasks >> TK_PREP) & 1u) {
+    if (kind == TK_PREP) { task_prep(c, local, sraw); return; }
+  }
+  if constexpr ((M.tasks >> TK_YY) & 1u) {
+    if (kind == TK_YY) { task_yy(c, local, sraw); return; }
+  }
+  if constexpr ((M.tasks >> TK_SCALARS) & 1u) {
+    if (kind == TK_SCALARS) { task_scalars(c, local); return; }
+  }
+  if constexpr ((M.tasks >> TK_SOLVE) & 1u) {
+    if (kind == TK_SOLVE) { task_solve<SMALLM>(c, local, sraw); return; }
+  }
+  if constexpr ((M.tasks >> TK_SCATTER) & 1u) {
+    if (kind == TK_SCATTER) { task_scatter(c, local); return; }
+  }
+  if constexpr ((M.tasks >> TK_CLEAR) & 1u) {
+    if (kind == TK_CLEAR) { task_clear(c, local); return; }
   }
 }
 
-template <int TILE, bool SMALLM>
+template <int TILE, bool SMALLM, int W, int LK>
 __global__ __launch_bounds__(256) void step_kernel(StepCtx c, StepLaunch L) {
   extern __shared__ __attribute__((aligned(16))) unsigned char sraw[];
   const int blk = blockIdx.x;
@@ -734,7 +888,7 @@ __global__ __launch_bounds__(256) void step_kernel(StepCtx c, StepLaunch L) {
 #ifdef LST_TIMING
   const unsigned long long t0 = wall_clock64();
 #endif
-  run_task<TILE, SMALLM>(c, L, t, local, sraw);
+  run_task<TILE, SMALLM, W, LK>(c, L, t, local, sraw);
 #ifdef LST_TIMING
   __syncthreads();
   if (threadIdx.x == 0 && blk < 8192) {
@@ -746,10 +900,10 @@ __global__ __launch_bounds__(256) void step_kernel(StepCtx c, StepLaunch L) {
 }
 
 // ------------------------------------------------------------------- host
-static size_t lds_of(int kind, int tile, int kcw, int m) {
+static size_t lds_of(int kind, int stages, int m) {
   switch (kind) {
-    case TK_GEMM: return (size_t)panel_lds_floats(tile, tile, kcw) * sizeof(float);
-    case TK_PREP: return 1024 * sizeof(unsigned long long) + 16;
+    case TK_GEMM: return (size_t)stages * kPanelStageBytes;
+    case TK_PREP: return kPrepLds;
     case TK_YY: return 2 * 32 * kGramKMax * 4 + 32 * 4;
     case TK_SOLVE: return solve_lds_bytes(m);
     default: return 0;
@@ -786,39 +940,89 @@ int step_task_blocks(int kind, const StepCtx& c) {
   }
 }
 
-hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, hipStream_t s) {
+static int vmat_vec16(const VMat& v) {
+  if (!v.vec) return 0;
+  for (int b = 0; b < v.nb; ++b)
+    if (v.ld[b] % 4 != 0 || ((uintptr_t)v.p[b] & 15) != 0) return 0;
+  return 1;
+}
+
+int gemm_batch_vec16(const GemmBatch& b) {
+  for (int q = 0; q < b.np; ++q) {
+    const GemmProblem& p = b.p[q];
+    if (!vmat_vec16(p.A) || !vmat_vec16(p.B)) return 0;
+    const bool kc = p.a_kc || p.b_kc;
+    if (kc && p.K % 4 != 0) return 0;
+  }
+  return 1;
+}
+
+template <int TILE, bool SMALLM, int W, int LK>
+static const void* kfn() {
+  return reinterpret_cast<const void*>(step_kernel<TILE, SMALLM, W, LK>);
+}
+
+// The kernel built for (launch kind, tile, m <= 128, 16-byte DMA); nullptr for
+// a combination that is not built.
+static const void* step_kernel_for(int lk, int tile, bool small, int w16) {
+  switch (lk) {
+    case 1:
+      if (tile != 32) return nullptr;
+      return w16 ? kfn<32, true, 4, 1>() : kfn<32, true, 1, 1>();
+    case 2:
+      if (tile != 32) return nullptr;
+      if (small) return w16 ? kfn<32, true, 4, 2>() : kfn<32, true, 1, 2>();
+      return w16 ? kfn<32, false, 4, 2>() : kfn<32, false, 1, 2>();
+    case 3:
+      if (tile == 32) return w16 ? kfn<32, true, 4, 3>() : kfn<32, true, 1, 3>();
+      return w16 ? kfn<64, true, 4, 3>() : kfn<64, true, 1, 3>();
+    case 4:
+      if (tile == 32) return w16 ? kfn<32, true, 4, 4>() : kfn<32, true, 1, 4>();
+      return w16 ? kfn<64, true, 4, 4>() : kfn<64, true, 1, 4>();
+    default:
+      return nullptr;
+  }
+}
+
+hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, int stages, hipStream_t s) {
   if (tile != 32 && tile != 64) return hipErrorInvalidValue;
+  if (L.lk < 1 || L.lk > 4) return hipErrorInvalidValue;
+  if (stages < 2 || (size_t)stages * kPanelStageBytes > kStepLdsMax) return hipErrorInvalidValue;
+  const LaunchMasks& M = kLaunchMasks[L.lk];
+  L.gemm.stages = stages;
+  L.gemm.timing_slot = L.timing_slot;
   size_t lds = 0;
   int total = 0;
+  int w16 = 1;
   for (int t = 0; t < L.ntask; ++t) {
+    if (!((M.tasks >> L.kind[t]) & 1u)) return hipErrorInvalidValue;
     L.begin[t] = total;
     int n = 0;
     if (L.kind[t] == TK_GEMM) {
-      if (L.gemm.kcw_max > panel_kcw_max(tile)) L.gemm.kcw_max = panel_kcw_max(tile);
+      for (int q = 0; q < L.gemm.np; ++q) {
+        const GemmProblem& p = L.gemm.p[q];
+        if (!(M.vars & problem_variant(p)) || !((M.epis >> p.epi) & 1u))
+          return hipErrorInvalidValue;
+      }
       n = tiles_of(L.gemm, tile);
+      w16 = gemm_batch_vec16(L.gemm);
     } else {
       n = step_task_blocks(L.kind[t], c);
     }
-    const size_t b = lds_of(L.kind[t], tile, L.gemm.kcw_max, c.m);
+    const size_t b = lds_of(L.kind[t], stages, c.m);
     if (b > lds) lds = b;
     total += n;
   }
   L.begin[L.ntask] = total;
   if (total == 0) return hipSuccess;
-  const bool small = c.m <= 128;
-  const dim3 grid(total), block(256);
-  if (tile == 32) {
-    if (small)
-      hipLaunchKernelGGL((step_kernel<32, true>), grid, block, lds, s, c, L);
-    else
-      hipLaunchKernelGGL((step_kernel<32, false>), grid, block, lds, s, c, L);
-  } else {
-    if (small)
-      hipLaunchKernelGGL((step_kernel<64, true>), grid, block, lds, s, c, L);
-    else
-      hipLaunchKernelGGL((step_kernel<64, false>), grid, block, lds, s, c, L);
-  }
-  return hipGetLastError();
+  if (lds > kStepLdsMax) return hipErrorInvalidValue;
+
+  const void* fn = step_kernel_for(L.lk, tile, c.m <= 128, w16);
+  if (!fn) return hipErrorInvalidValue;
+  StepCtx ca = c;
+  StepLaunch la = L;
+  void* args[] = {&ca, &la};
+  return hipLaunchKernel(fn, dim3(total), dim3(256), args, lds, s);
 }
 
 size_t solve_workspace_floats(int m_max, int d) {
@@ -828,15 +1032,16 @@ size_t solve_workspace_floats(int m_max, int d) {
 }
 
 hipError_t configure_kernels() {
-  const int lds_max = 160 * 1024 - 1024;
-  const void* ks[] = {reinterpret_cast<const void*>(step_kernel<32, true>),
-                      reinterpret_cast<const void*>(step_kernel<32, false>),
-                      reinterpret_cast<const void*>(step_kernel<64, true>),
-                      reinterpret_cast<const void*>(step_kernel<64, false>)};
-  for (const void* k : ks) {
-    const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
-    if (e != hipSuccess) return e;
-  }
+  for (int lk = 1; lk <= 4; ++lk)
+    for (int tile : {32, 64})
+      for (int small = 0; small < 2; ++small)
+        for (int w16 = 0; w16 < 2; ++w16) {
+          const void* k = step_kernel_for(lk, tile, small != 0, w16);
+          if (!k) continue;
+          const hipError_t e = hipFuncSetAttribute(
+              k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kStepLdsMax);
+          if (e != hipSuccess) return e;
+        }
   return hipSuccess;
 }
 
@@ -872,7 +1077,33 @@ extern "C" int lst_debug_step_times(unsigned long long* out) {
   return hipMemcpyFromSymbol(out, HIP_SYMBOL(g_step_times), sizeof(g_step_times)) == hipSuccess
              ? 0 : -5;
 }
+extern "C" int lst_debug_solve_marks(unsigned long long* out) {
+  return hipMemcpyFromSymbol(out, HIP_SYMBOL(g_solve_marks), sizeof(g_solve_marks)) == hipSuccess
+             ? 0 : -5;
+}
+extern "C" int lst_debug_gemm_marks(unsigned long long* out) {
+  return hipMemcpyFromSymbol(out, HIP_SYMBOL(g_gemm_marks), sizeof(g_gemm_marks)) == hipSuccess
+             ? 0 : -5;
+}
 #endif
+
+__global__ __launch_bounds__(1024) void compact_owned_kernel(const int* own, int n, int* out,
+                                                             int* count) {
+  __shared__ int s_n;
+  if (threadIdx.x == 0) s_n = 0;
+  __syncthreads();
+  for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    const int r = own[e];
+    if (r >= 0) out[atomicAdd(&s_n, 1)] = r;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) *count = s_n;
+}
+
+hipError_t compact_owned(const int* own, int n, int* out, int* count, hipStream_t s) {
+  hipLaunchKernelGGL(compact_owned_kernel, dim3(1), dim3(1024), 0, s, own, n, out, count);
+  return hipGetLastError();
+}
 
 hipError_t sort_ints(int* v, const int* n_ptr, hipStream_t s) {
   hipLaunchKernelGGL(sort_ints_kernel, dim3(1), dim3(1024), 0, s, v, n_ptr);
