@@ -70,7 +70,7 @@ def main():
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the step has no "
-              "multi-GPU path in this build", file=sys.stderr)
+              "multi-GPU path (V would be row-sharded across GPUs; not implemented)", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -134,10 +134,17 @@ def main():
     u, nnz = st.last_unique, st.last_nnz
     kernels = {}
     best = None
+    from paper_1412_7091_amd.profiling import measured_traffic
+
+    traffic = measured_traffic(cfg.name) or {}
     for name, tot in phases.items():
         avg_us = 1e3 * tot / max(nsteps, 1)
+        if avg_us <= 0:
+            continue  # phase not run by this configuration (drift control off)
         flops, nbytes = phase_work(name, cfg, u, nnz)
         entry = {"avg_us": round(avg_us, 3)}
+        if name in traffic:
+            entry["hbm_bytes_measured"] = traffic[name]["hbm_bytes"]
         if avg_us > 0 and (flops > 0 or nbytes > 0):
             tf = flops / (avg_us * 1e-6) / 1e12
             gb = nbytes / (avg_us * 1e-6) / 1e9
@@ -149,16 +156,27 @@ def main():
             best = name
     log("per-launch us: " + ", ".join(f"{k}={v['avg_us']:.1f}" for k, v in kernels.items()))
     dom = kernels[best]
+    dom_traffic = dom.get("hbm_bytes_measured")
     if dom["mfma_frac"] >= dom["hbm_frac"]:
         roofline = {"kernel": best, "bound": "mfma", "achieved": dom["tflops"],
                     "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s", "frac": dom["mfma_frac"],
-                    "traffic": None}
+                    "traffic": dom_traffic}
     else:
         roofline = {"kernel": best, "bound": "hbm", "achieved": dom["hbm_gbs"],
                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": dom["hbm_frac"],
-                    "traffic": None}
+                    "traffic": dom_traffic}
     layer.close()
     del layer
+
+    # A plain 64 MiB device copy, outside every timed region: the reference the
+    # FETCH_SIZE / WRITE_SIZE counter runs are scaled by (see profiling.py).  A
+    # 128 MiB fill in between pushes the copy's source out of the L2 caches.
+    calib_src = torch.empty(16 << 20, dtype=torch.float32, device=dev).fill_(1.0)
+    flush = torch.empty(32 << 20, dtype=torch.float32, device=dev).fill_(0.0)
+    calib_dst = torch.empty_like(calib_src)
+    calib_dst.copy_(calib_src)
+    torch.cuda.synchronize()
+    del calib_src, calib_dst, flush
 
     naive = None
     if not args.no_naive:

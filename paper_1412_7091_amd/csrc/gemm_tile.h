@@ -490,11 +490,23 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
   LST_MARK(4);
 }
 
-// Computes tile number t of the batch (problems laid out one after another);
-// smem holds bt.stages stages of kPanelStageBytes.  Only the layouts in VARS
-// and the epilogues in EPIS are compiled (the host checks every problem).
+// Workgroups are dispatched to the 8 XCDs round-robin (block b to XCD b % 8),
+// each XCD with its own L2.  Block b gets tile xcd_tile(b): every XCD takes
+// one contiguous run of the tile sequence, so tiles that read the same
+// operand panels share an L2.  A bijection of [0, total).
+__device__ __forceinline__ int xcd_tile(int b, int total) {
+  const int x = b & 7, li = b >> 3;
+  const int q = total >> 3, r = total & 7;
+  return x * q + min(x, r) + li;
+}
+
+// Computes the tile of block t of the batch (problems laid out one after
+// another, each in column-panel-major order); smem holds bt.stages stages of
+// kPanelStageBytes.  Only the layouts in VARS and the epilogues in EPIS are
+// compiled (the host checks every problem).
 template <int T, int W, unsigned VARS, unsigned EPIS>
 __device__ __forceinline__ void panel_tile(const GemmBatch& bt, int t, float* smem) {
+  t = xcd_tile(t, bt.total_tiles);
   int q = 0;
   while (q + 1 < bt.np && t >= bt.p[q + 1].tile_begin) ++q;
   if (bt.skip_updates_if && q >= bt.first_update && *bt.skip_updates_if) return;
@@ -511,8 +523,8 @@ __device__ __forceinline__ void panel_tile(const GemmBatch& bt, int t, float* sm
     const int per = P.tiles_m * P.tiles_n;
     z = lt / per;
     lt -= z * per;
-    tm = lt / P.tiles_n;
-    tn = lt - tm * P.tiles_n;
+    tn = lt / P.tiles_m;  // the tiles of one B panel are consecutive
+    tm = lt - tn * P.tiles_m;
     if (P.ksplit > 1) {
       const int kc = ((P.K + P.ksplit - 1) / P.ksplit + 15) / 16 * 16;
       kb = z * kc;

@@ -14,6 +14,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "lst_internal.h"
@@ -62,6 +63,7 @@ struct lst_state {
   // profiling: two events per phase per profiled step
   int prof = 0;
   std::vector<hipEvent_t> prof_events;
+  std::vector<char> prof_recorded;  // per event slot: recorded in the current profile
   size_t prof_used = 0;
   int64_t prof_steps = 0;
 };
@@ -116,9 +118,30 @@ int prof_mark(lst_state* s, int phase, int end, hipStream_t st) {
     hipEvent_t e;
     HIPCHK(hipEventCreate(&e));
     s->prof_events.push_back(e);
+    s->prof_recorded.push_back(0);
   }
   HIPCHK(hipEventRecord(s->prof_events[slot], st));
+  s->prof_recorded[slot] = 1;
   if (slot + 1 > s->prof_used) s->prof_used = slot + 1;
+  return LST_OK;
+}
+
+// The start and end events of a launch phase of the current profiled step
+// (both null when not profiling): the launch records them around its kernel.
+int prof_pair(lst_state* s, int phase, hipEvent_t* e0, hipEvent_t* e1) {
+  *e0 = *e1 = nullptr;
+  if (!s->prof) return LST_OK;
+  const size_t slot = (size_t)(s->prof_steps - 1) * (2 * PH_COUNT) + 2 * phase;
+  while (s->prof_events.size() <= slot + 1) {
+    hipEvent_t e;
+    HIPCHK(hipEventCreate(&e));
+    s->prof_events.push_back(e);
+    s->prof_recorded.push_back(0);
+  }
+  *e0 = s->prof_events[slot];
+  *e1 = s->prof_events[slot + 1];
+  s->prof_recorded[slot] = s->prof_recorded[slot + 1] = 1;
+  if (slot + 2 > s->prof_used) s->prof_used = slot + 2;
   return LST_OK;
 }
 
@@ -284,9 +307,10 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     p1.dot_h = H; p1.ld_doth = d;
     L.lk = 1;
     L.timing_slot = 0;
-    OK_OR_RETURN(prof_mark(s, PH_LAUNCH1, 0, st));
-    HIPCHK(step_launch(c, L, kLaunch1Tile, stages_for(L.gemm, kLaunch1Tile, kLaunch1Stages), st));
-    OK_OR_RETURN(prof_mark(s, PH_LAUNCH1, 1, st));
+    hipEvent_t e0, e1;
+    OK_OR_RETURN(prof_pair(s, PH_LAUNCH1, &e0, &e1));
+    HIPCHK(step_launch(c, L, kLaunch1Tile, stages_for(L.gemm, kLaunch1Tile, kLaunch1Stages), st,
+                       e0, e1));
   }
   {  // launch 2: Y^, C1, C2, C2^T ; solve ; Y^T Y ; per-example scalars
     StepLaunch L{};
@@ -305,9 +329,9 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
                           4 * m, 1.f, 0.f, EPI_STORE);
     L.lk = 2;
     L.timing_slot = 1;
-    OK_OR_RETURN(prof_mark(s, PH_LAUNCH2, 0, st));
-    HIPCHK(step_launch(c, L, 32, stages_for(g, 32), st));
-    OK_OR_RETURN(prof_mark(s, PH_LAUNCH2, 1, st));
+    hipEvent_t e0, e1;
+    OK_OR_RETURN(prof_pair(s, PH_LAUNCH2, &e0, &e1));
+    HIPCHK(step_launch(c, L, 32, stages_for(g, 32), st, e0, e1));
   }
   {  // launch 3: grad_H and T ; U and U^{-T} updates ; scatter into V
     StepLaunch L{};
@@ -330,10 +354,10 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     g.first_update = 1;
     L.lk = 3;
     L.timing_slot = 2;
-    OK_OR_RETURN(prof_mark(s, PH_LAUNCH3, 0, st));
+    hipEvent_t e0, e1;
+    OK_OR_RETURN(prof_pair(s, PH_LAUNCH3, &e0, &e1));
     const int t3 = pick_tile(g);
-    HIPCHK(step_launch(c, L, t3, stages_for(g, t3), st));
-    OK_OR_RETURN(prof_mark(s, PH_LAUNCH3, 1, st));
+    HIPCHK(step_launch(c, L, t3, stages_for(g, t3), st, e0, e1));
   }
   {  // launch 4: Q -= lr (H T^T + T H^T) ; clear the hash slots
     StepLaunch L{};
@@ -346,19 +370,19 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
                           vmat2(s->T, d, m, H, d, m), c.Q, d, -lr, 1.f, EPI_SYM);
     L.lk = 4;
     L.timing_slot = 3;
-    OK_OR_RETURN(prof_mark(s, PH_LAUNCH4, 0, st));
-    HIPCHK(step_launch(c, L, 32, stages_for(g, 32), st));
-    OK_OR_RETURN(prof_mark(s, PH_LAUNCH4, 1, st));
+    hipEvent_t e0, e1;
+    OK_OR_RETURN(prof_pair(s, PH_LAUNCH4, &e0, &e1));
+    HIPCHK(step_launch(c, L, 32, stages_for(g, 32), st, e0, e1));
   }
-  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 0, st));
   if (s->cfg.cond_max > 0.f) {
+    OK_OR_RETURN(prof_mark(s, PH_DRIFT, 0, st));
     HIPCHK(drift_check(c.U, c.Uit, d, s->cfg.cond_max * (float)d, fl, st));
     HIPCHK(copy_if(s->V, s->Vtmp, (size_t)s->D * d, fl + F_RESTORE, st));
     OK_OR_RETURN(vu_product(s, st, s->Vtmp, s->V, fl + F_RESTORE, fl + F_ERR));
     HIPCHK(set_identity_if(c.U, d, fl + F_RESTORE, st));
     HIPCHK(set_identity_if(c.Uit, d, fl + F_RESTORE, st));
+    OK_OR_RETURN(prof_mark(s, PH_DRIFT, 1, st));
   }
-  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 1, st));
   return LST_OK;
 }
 
@@ -663,6 +687,7 @@ int lst_profile_enable(lst_state* s, int32_t enable) {
   HIPCHK(hipStreamSynchronize(s->stream));
   s->prof = enable ? 1 : 0;
   s->prof_used = 0;
+  std::fill(s->prof_recorded.begin(), s->prof_recorded.end(), 0);
   s->prof_steps = 0;
   return LST_OK;
 }
@@ -677,7 +702,7 @@ int lst_profile_read(lst_state* s, double* ms_total, int32_t capacity, int32_t* 
   for (int64_t st = 0; st < s->prof_steps; ++st) {
     for (int p = 0; p < PH_COUNT && p < capacity; ++p) {
       const size_t b = (size_t)st * (2 * PH_COUNT) + 2 * p;
-      if (b + 1 >= s->prof_used) continue;
+      if (b + 1 >= s->prof_used || !s->prof_recorded[b] || !s->prof_recorded[b + 1]) continue;
       float ms = 0.f;
       HIPCHK(hipEventElapsedTime(&ms, s->prof_events[b], s->prof_events[b + 1]));
       ms_total[p] += ms;
@@ -686,6 +711,7 @@ int lst_profile_read(lst_state* s, double* ms_total, int32_t capacity, int32_t* 
   *nphases = PH_COUNT;
   *nsteps = s->prof_steps;
   s->prof_used = 0;
+  std::fill(s->prof_recorded.begin(), s->prof_recorded.end(), 0);
   s->prof_steps = 0;
   return LST_OK;
 }

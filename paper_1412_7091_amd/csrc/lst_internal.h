@@ -154,8 +154,10 @@ struct StepLaunch {
 };
 
 // Launches the tasks of L as one grid of 256-thread blocks; GEMM tiles are
-// tile x tile (32 or 64) with `stages` LDS stages (>= 2).
-hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, int stages, hipStream_t s);
+// tile x tile (32 or 64) with `stages` LDS stages (>= 2).  With ev0 / ev1 the
+// launch records them at the start and the end of the kernel's execution.
+hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, int stages, hipStream_t s,
+                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // 1 when every operand of the batch allows 16-byte LDS-DMA (aligned rows with
 // ld % 4 == 0, and K % 4 == 0 where k is the contiguous index).
 int gemm_batch_vec16(const GemmBatch& b);

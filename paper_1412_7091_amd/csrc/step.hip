@@ -23,6 +23,7 @@
 // b_i = -2 o_c / (o_c^2 + eps), o_c = h_i^T W^T y_i.  N = (dL/dO)^T dL/dO.
 // Every update of the state (launches 3 and 4) skips when the step's error
 // flag is set; all checks that can set it run in launches 1 and 2.
+#include <hip/hip_ext.h>
 #include <math.h>
 
 #include "gemm_tile.h"
@@ -984,7 +985,8 @@ static const void* step_kernel_for(int lk, int tile, bool small, int w16) {
   }
 }
 
-hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, int stages, hipStream_t s) {
+hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, int stages, hipStream_t s,
+                       hipEvent_t ev0, hipEvent_t ev1) {
   if (tile != 32 && tile != 64) return hipErrorInvalidValue;
   if (L.lk < 1 || L.lk > 4) return hipErrorInvalidValue;
   if (stages < 2 || (size_t)stages * kPanelStageBytes > kStepLdsMax) return hipErrorInvalidValue;
@@ -1022,6 +1024,7 @@ hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, int stages, hi
   StepCtx ca = c;
   StepLaunch la = L;
   void* args[] = {&ca, &la};
+  if (ev0 && ev1) return hipExtLaunchKernel(fn, dim3(total), dim3(256), args, lds, s, ev0, ev1, 0);
   return hipLaunchKernel(fn, dim3(total), dim3(256), args, lds, s);
 }
 
