@@ -401,12 +401,14 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
     else
       fill_nk<T, W>(P.B, n0, P.N, k0, ke, st + G::OPF);
   };
-  const int ahead = nch < S - 1 ? nch : S - 1;
+  // Every chunk fits (chunk c in stage c): all are issued at once.  Otherwise
+  // a ring keeps S - 1 chunks ahead of the one being multiplied.
+  const bool resident = nch <= S;
+  const int ahead = resident ? nch : S - 1;
   for (int c = 0; c < ahead; ++c) fill(c);
   LST_MARK(1);
-  if (nch <= S - 1) {
-    // Every chunk is in flight already (chunk c in stage c): one wait, then
-    // one uninterrupted MFMA loop over all of K.
+  if (resident) {
+    // one wait, then one uninterrupted MFMA loop over all of K
     wait_vm_le(0);
     lds_barrier();
     LST_MARK(2);
@@ -500,11 +502,26 @@ __device__ __forceinline__ int xcd_tile(int b, int total) {
   return x * q + min(x, r) + li;
 }
 
+// The operand layouts of problem P (one of VARS) for tile edge T.
+template <int T, int W, unsigned VARS, unsigned EPIS>
+__device__ __forceinline__ void panel_layout(const GemmBatch& bt, const GemmProblem& P, int tm,
+                                             int tn, int z, int kb, int ke, float* smem) {
+  if ((VARS & V_NT) && P.a_kc && P.b_kc)
+    panel_run<T, W, 1, 1, EPIS>(bt, P, tm, tn, z, kb, ke, smem);
+  else if ((VARS & V_NN) && P.a_kc && !P.b_kc)
+    panel_run<T, W, 1, 0, EPIS>(bt, P, tm, tn, z, kb, ke, smem);
+  else if ((VARS & V_TN) && !P.a_kc)
+    panel_run<T, W, 0, 0, EPIS>(bt, P, tm, tn, z, kb, ke, smem);
+}
+
+// Tile-edge masks of a kernel instantiation.
+enum : unsigned { TILE32 = 1, TILE64 = 2 };
+
 // Computes the tile of block t of the batch (problems laid out one after
 // another, each in column-panel-major order); smem holds bt.stages stages of
-// kPanelStageBytes.  Only the layouts in VARS and the epilogues in EPIS are
-// compiled (the host checks every problem).
-template <int T, int W, unsigned VARS, unsigned EPIS>
+// kPanelStageBytes.  Only the tile edges in TILES, the layouts in VARS and the
+// epilogues in EPIS are compiled (the host checks every problem).
+template <unsigned TILES, int W, unsigned VARS, unsigned EPIS>
 __device__ __forceinline__ void panel_tile(const GemmBatch& bt, int t, float* smem) {
   t = xcd_tile(t, bt.total_tiles);
   int q = 0;
@@ -531,12 +548,10 @@ __device__ __forceinline__ void panel_tile(const GemmBatch& bt, int t, float* sm
       ke = min(P.K, kb + kc);
     }
   }
-  if ((VARS & V_NT) && P.a_kc && P.b_kc)
-    panel_run<T, W, 1, 1, EPIS>(bt, P, tm, tn, z, kb, ke, smem);
-  else if ((VARS & V_NN) && P.a_kc && !P.b_kc)
-    panel_run<T, W, 1, 0, EPIS>(bt, P, tm, tn, z, kb, ke, smem);
-  else if ((VARS & V_TN) && !P.a_kc)
-    panel_run<T, W, 0, 0, EPIS>(bt, P, tm, tn, z, kb, ke, smem);
+  if ((TILES & TILE64) && P.tile == 64)
+    panel_layout<64, W, VARS, EPIS>(bt, P, tm, tn, z, kb, ke, smem);
+  else if (TILES & TILE32)
+    panel_layout<32, W, VARS, EPIS>(bt, P, tm, tn, z, kb, ke, smem);
 }
 
 // Layout bit of a problem (matches the dispatch above).

@@ -240,38 +240,27 @@ int check_step_args(lst_state* s, int32_t m, int32_t K, const float* H, const in
   return LST_OK;
 }
 
-// GEMM tile edge for a launch: 64 when that still gives most compute units a
-// tile, else 32.
-int pick_tile(const GemmBatch& b) {
-  int t64 = 0;
-  for (int q = 0; q < b.np; ++q) {
-    const GemmProblem& p = b.p[q];
-    const int tm = (p.M + 63) / 64, tn = (p.N + 63) / 64;
-    t64 += (p.epi == EPI_SYM) ? tm * (tm + 1) / 2 : tm * tn;
-  }
-  return t64 >= 128 ? 64 : 32;
-}
-
-// LDS stages of a launch's GEMM tiles: enough to issue every K chunk of the
-// longest problem before the first multiply, at most kMaxStages.
-#ifndef LST_MAX_STAGES
-#define LST_MAX_STAGES 9
-#endif
-constexpr int kMaxStages = LST_MAX_STAGES;
-int stages_for(const GemmBatch& b, int tile, int max_stages = kMaxStages) {
-  const int ck = 2048 / tile;
+// LDS stages of a launch's GEMM tiles: one per K chunk of the longest problem
+// (every chunk issued before the first multiply), at most max_stages.
+constexpr int kMaxStages = 9;
+int stages_for(const GemmBatch& b, int max_stages = kMaxStages) {
   int nch = 1;
   for (int q = 0; q < b.np; ++q) {
+    const int ck = 2048 / (b.p[q].tile == 64 ? 64 : 32);  // k per 16 KB stage
     const int n = (b.p[q].K + ck - 1) / ck;
     if (n > nch) nch = n;
   }
-  return nch + 1 < max_stages ? nch + 1 : max_stages;
+  const int st = nch < max_stages ? nch : max_stages;
+  return st < 2 ? 2 : st;
 }
 
 // Launch 1 also runs the gather and the target preparation, which need little
 // LDS: with at most 4 stages (64 KB) their blocks share compute units with the
-// GEMM tiles instead of waiting for them.
+// GEMM tiles instead of waiting for them (K = d > 256 then takes the ring).
 constexpr int kLaunch1Stages = 4;
+// Launches 3 and 4 keep at most 4 stages (64 KB): two blocks share a compute
+// unit, so the short tasks run beside the GEMM tiles.
+constexpr int kLaunch34Stages = 4;
 
 // Enqueues the launches of one factored step on stream st.
 int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float* H,
@@ -309,8 +298,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     L.timing_slot = 0;
     hipEvent_t e0, e1;
     OK_OR_RETURN(prof_pair(s, PH_LAUNCH1, &e0, &e1));
-    HIPCHK(step_launch(c, L, kLaunch1Tile, stages_for(L.gemm, kLaunch1Tile, kLaunch1Stages), st,
-                       e0, e1));
+    HIPCHK(step_launch(c, L, stages_for(L.gemm, kLaunch1Stages), st, e0, e1));
   }
   {  // launch 2: Y^, C1, C2, C2^T ; solve ; Y^T Y ; per-example scalars
     StepLaunch L{};
@@ -331,14 +319,16 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     L.timing_slot = 1;
     hipEvent_t e0, e1;
     OK_OR_RETURN(prof_pair(s, PH_LAUNCH2, &e0, &e1));
-    HIPCHK(step_launch(c, L, 32, stages_for(g, 32), st, e0, e1));
+    HIPCHK(step_launch(c, L, stages_for(g), st, e0, e1));
   }
-  {  // launch 3: grad_H and T ; U and U^{-T} updates ; scatter into V
+  {  // launch 3: grad_H and T ; scatter into V
     StepLaunch L{};
     L.ntask = 2;
-    L.kind[0] = TK_GEMM; L.kind[1] = TK_SCATTER;
+    // the scatter's blocks are dispatched first: they are short and must not
+    // wait behind the GEMM tiles for a compute unit
+    L.kind[0] = TK_SCATTER; L.kind[1] = TK_GEMM;
     GemmBatch& g = L.gemm;
-    g.np = 3;
+    g.np = 1;
     GemmProblem& pt = g.p[0];
     // NP viewed as 2m x 2m (row stride 2m): row 2i = [C1 C2]_i, row 2i+1 = [C2^T Y^T Y]_i;
     // times [a H; b H] it gives both halves of (N H^T)_i, combined in the epilogue.
@@ -346,33 +336,34 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
                       vmat2(s->aH, d, m, s->bH, d, m), s->T, d, -0.5f * lr, 0.f, EPI_GRADT);
     pt.e1 = Hh; pt.lde1 = s->ld0; pt.e2 = s->Yh; pt.lde2 = d;
     pt.s1 = s->a; pt.s2 = s->b; pt.g = grad_H; pt.ldg = d;
-    g.p[1] = gemm_problem(L_TN, d, d, m, vmat(s->UHa, d, m), vmat(H, d, m), c.U, d, -lr, 1.f,
-                          EPI_STORE);
-    g.p[2] = gemm_problem(L_TN, d, d, m, vmat(s->X, d, m), vmat(H, d, m), c.Uit, d, -1.f, 1.f,
-                          EPI_STORE);
-    g.skip_updates_if = fl + F_ERR;  // the gradient tiles (problem 0) always run
-    g.first_update = 1;
+    pt.tile = 32;
     L.lk = 3;
     L.timing_slot = 2;
     hipEvent_t e0, e1;
     OK_OR_RETURN(prof_pair(s, PH_LAUNCH3, &e0, &e1));
-    const int t3 = pick_tile(g);
-    HIPCHK(step_launch(c, L, t3, stages_for(g, t3), st, e0, e1));
+    HIPCHK(step_launch(c, L, stages_for(g, kLaunch34Stages), st, e0, e1));
   }
-  {  // launch 4: Q -= lr (H T^T + T H^T) ; clear the hash slots
+  {  // launch 4: Q -= lr (H T^T + T H^T) ; U and U^{-T} updates ; clear the hash slots
     StepLaunch L{};
     L.ntask = 2;
     L.kind[0] = TK_GEMM; L.kind[1] = TK_CLEAR;
     GemmBatch& g = L.gemm;
-    g.np = 1;
-    g.skip_if = fl + F_ERR;
+    g.np = 3;
+    g.skip_if = fl + F_ERR;  // every product of this launch updates the state
     g.p[0] = gemm_problem(L_TN, d, d, 2 * m, vmat2(H, d, m, s->T, d, m),
                           vmat2(s->T, d, m, H, d, m), c.Q, d, -lr, 1.f, EPI_SYM);
+    g.p[0].tile = 32;
+    g.p[1] = gemm_problem(L_TN, d, d, m, vmat(s->UHa, d, m), vmat(H, d, m), c.U, d, -lr, 1.f,
+                          EPI_STORE);
+    g.p[1].tile = 64;
+    g.p[2] = gemm_problem(L_TN, d, d, m, vmat(s->X, d, m), vmat(H, d, m), c.Uit, d, -1.f, 1.f,
+                          EPI_STORE);
+    g.p[2].tile = 64;
     L.lk = 4;
     L.timing_slot = 3;
     hipEvent_t e0, e1;
     OK_OR_RETURN(prof_pair(s, PH_LAUNCH4, &e0, &e1));
-    HIPCHK(step_launch(c, L, 32, stages_for(g, 32), st, e0, e1));
+    HIPCHK(step_launch(c, L, stages_for(g, kLaunch34Stages), st, e0, e1));
   }
   if (s->cfg.cond_max > 0.f) {
     OK_OR_RETURN(prof_mark(s, PH_DRIFT, 0, st));

@@ -58,6 +58,7 @@ struct GemmProblem {
   float alpha, beta;
   int epi;
   int ksplit;       // EPI_PARTIAL: number of K slices (>= 1)
+  int tile;         // step GEMMs: output tile edge, 32 or 64 (0: 32)
   int tiles_m, tiles_n, tile_begin;
   // EPI_GRADT operands
   const float* e1; int lde1;
@@ -153,10 +154,11 @@ struct StepLaunch {
   int timing_slot;  // which record of per-block times (builds with LST_TIMING only)
 };
 
-// Launches the tasks of L as one grid of 256-thread blocks; GEMM tiles are
-// tile x tile (32 or 64) with `stages` LDS stages (>= 2).  With ev0 / ev1 the
-// launch records them at the start and the end of the kernel's execution.
-hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, int stages, hipStream_t s,
+// Launches the tasks of L as one grid of 256-thread blocks; each GEMM problem
+// has its own tile edge (GemmProblem::tile), all share `stages` LDS stages
+// (>= 2).  With ev0 / ev1 the launch records them at the start and the end of
+// the kernel's execution.
+hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t s,
                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // 1 when every operand of the batch allows 16-byte LDS-DMA (aligned rows with
 // ld % 4 == 0, and K % 4 == 0 where k is the contiguous index).

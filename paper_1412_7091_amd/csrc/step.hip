@@ -412,10 +412,14 @@ __device__ void gj_augmented(TT* A, int lda, int m, int ncol, double* colk, doub
 }
 
 // LDS bytes of the solve for m (both branches share the buffer).
+// Row stride (floats) of the solve's column blocks B^T, Y^T (padded).
+__host__ __device__ inline int solve_lde(int mp) { return mp + 4; }
+
 __host__ __device__ inline size_t solve_lds_bytes(int m) {
   const int mp = (m + 15) & ~15;
+  const int lde = solve_lde(mp);
   const size_t neumann =
-      (size_t)(mp + 3 * kSolveCols * (mp + 4) + (m <= 128 ? mp * (mp + 4) : 0)) * sizeof(float);
+      (size_t)(mp + 3 * kSolveCols * lde + (m <= 128 ? mp * mp : 0)) * sizeof(float);
   const size_t gj = m <= 128 ? (size_t)m * (m + kSolveCols) * sizeof(double) : 0;
   const size_t extra = 256 * sizeof(float) + 512 * sizeof(double) + 64;  // red, colk, scalars
   return (neumann > gj ? neumann : gj) + extra;
@@ -443,7 +447,7 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   const int ldh = c.ld0, ldp = c.ld0;
   const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
   const int mp = (m + 15) & ~15;
-  const int LDE = mp + 4;
+  const int LDE = solve_lde(mp);
   const int c0 = local * kSolveCols;
   const size_t main_bytes = solve_lds_bytes(m) - (256 * sizeof(float) + 512 * sizeof(double) + 64);
   float* red = reinterpret_cast<float*>(sraw + main_bytes);
@@ -453,71 +457,114 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   float* Bt = cinv + mp;                               // kSolveCols x LDE: B^T
   float* Y0 = Bt + kSolveCols * LDE;                   // kSolveCols x LDE: Y^T
   float* Y1 = Y0 + kSolveCols * LDE;
-  float* Hs = Y1 + kSolveCols * LDE;                   // mp x LDE: H^T H (SMALL only)
+  float* Hs = Y1 + kSolveCols * LDE;                   // mp x mp: H^T H (SMALL only)
 
   for (int i = tid; i < mp; i += 256) cinv[i] = (i < m) ? c.lr * example_a(c, i) : 0.f;
   if (tid == 0) s_int[1] = 0;
   LST_SMARK(1);
+  // This block's columns of P^T (registers; for m <= 128 they are fetched now,
+  // together with H^T H, and used once the branch below is known).
+  float pv[8];
+  // H^T H in LDS (m <= 128): mp rows of mp floats, the 16-byte slot s of row j
+  // stored at slot s ^ (j & hsw) (bank-conflict-free reads down a column and
+  // across 16 rows); rows and columns beyond m are zero.
+  const int hsw = (mp % 32 == 0) ? 7 : 3;  // the XOR must stay inside a row's mp/4 slots
   if (SMALL) {
-    // H^T H into LDS, zero-padded to mp x mp; addresses are clamped so that
-    // every load is issued before the first store.
+    const int q4 = mp / 4;  // slots per row
     const bool vec4 = (ldh % 4 == 0) && (((uintptr_t)HH & 15) == 0) && (m % 4 == 0);
-    constexpr int NQ = 128 * 128 / 4 / 256;
-    const int q4 = mp / 4;
-    float4 r4[NQ];
     if (vec4) {
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const int e4 = tid + 256 * q;
-        const int i = min(e4 / q4, m - 1), j = min(4 * (e4 % q4), m - 4);
-        r4[q] = *reinterpret_cast<const float4*>(HH + (size_t)i * ldh + j);
+      // 16-byte DMA: instruction q fills slots [64 q, 64 q + 64) of the matrix
+      const unsigned hb = lds_u32(Hs);
+      const float* zero = g_dma_zero;
+      for (int q = wave; q < mp * q4 / 64; q += 4) {
+        const int e = 64 * q + lane;
+        const int j = e / q4, col = 4 * ((e % q4) ^ (j & hsw));
+        dma16((j < m && col < m) ? HH + (size_t)j * ldh + col : zero, hb + 1024u * q);
       }
     } else {
+      for (int e0 = 0; e0 < mp * q4; e0 += 256 * 4) {
+        float4 r4[4];
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const int e4 = tid + 256 * q;
-        const int i = min(e4 / q4, m - 1), j = 4 * (e4 % q4);
-        const float* hr = HH + (size_t)i * ldh;
-        r4[q].x = hr[min(j, m - 1)];
-        r4[q].y = hr[min(j + 1, m - 1)];
-        r4[q].z = hr[min(j + 2, m - 1)];
-        r4[q].w = hr[min(j + 3, m - 1)];
+        for (int u = 0; u < 4; ++u) {
+          const int e = e0 + tid + 256 * u;
+          const int j = min(e / q4, m - 1), col = 4 * ((e % q4) ^ ((e / q4) & hsw));
+          const float* hr = HH + (size_t)j * ldh;
+          r4[u].x = hr[min(col, m - 1)];
+          r4[u].y = hr[min(col + 1, m - 1)];
+          r4[u].z = hr[min(col + 2, m - 1)];
+          r4[u].w = hr[min(col + 3, m - 1)];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int e = e0 + tid + 256 * u;
+          if (e < mp * q4) {
+            const int j = e / q4, col = 4 * ((e % q4) ^ (j & hsw));
+            const bool ok = j < m;
+            float4 v;
+            v.x = (ok && col < m) ? r4[u].x : 0.f;
+            v.y = (ok && col + 1 < m) ? r4[u].y : 0.f;
+            v.z = (ok && col + 2 < m) ? r4[u].z : 0.f;
+            v.w = (ok && col + 3 < m) ? r4[u].w : 0.f;
+            *reinterpret_cast<float4*>(Hs + 4 * e) = v;
+          }
+        }
       }
     }
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int e4 = tid + 256 * q;
-      if (e4 < mp * q4) {
-        const int i = e4 / q4, j = 4 * (e4 % q4);
-        const bool ok = i < m;
-        float4 v;
-        v.x = (ok && j < m) ? r4[q].x : 0.f;
-        v.y = (ok && j + 1 < m) ? r4[q].y : 0.f;
-        v.z = (ok && j + 2 < m) ? r4[q].z : 0.f;
-        v.w = (ok && j + 3 < m) ? r4[q].w : 0.f;
-        *reinterpret_cast<float4*>(Hs + i * LDE + j) = v;
-      }
+    for (int u = 0; u < 8; ++u) {
+      const int e = tid + 256 * u;
+      const int i = min(e / kSolveCols, m - 1), cc = min(c0 + e % kSolveCols, d - 1);
+      pv[u] = P[(size_t)i * ldp + cc];
     }
+    wait_vm_le(0);
   }
-  __syncthreads();
+  lds_barrier();
   LST_SMARK(2);
   // r = ||E||_inf with E = diag(1/c) H^T H, and max |S_ij| for the fallback's
   // pivot threshold.  H^T H is symmetric, so the absolute sum of its row i is
-  // that of column i: thread i walks down column i (consecutive threads read
-  // consecutive addresses), and the block takes the maximum.
+  // that of column i: consecutive threads walk down consecutive columns (two
+  // halves of the rows per column when m <= 128, added in a fixed order).
   float rmax = 0.f, amax = 0.f;
-  for (int i = tid; i < m; i += 256) {
-    const float ci = 1.f / cinv[i];
-    float sabs = 0.f, hmax = 0.f;
+  if (SMALL) {
+    float* psum = Y1;            // 2 x mp partial sums (Y1 is free until the iterations)
+    float* pmax = Y1 + 2 * mp;   // 2 x mp partial maxima
+    const int half = (m + 1) / 2;
+    for (int p = tid; p < 2 * mp; p += 256) {
+      const int i = p % mp, hf = p / mp;
+      float sabs = 0.f, hmax = 0.f;
+      if (i < m) {
+        const float ci = 1.f / cinv[i];
+        const int j1 = hf ? m : half;
 #pragma unroll 8
-    for (int j = 0; j < m; ++j) {
-      const float h = SMALL ? Hs[j * LDE + i] : HH[(size_t)j * ldh + i];
-      sabs += fabsf(h);
-      hmax = fmaxf(hmax, fabsf(h - (i == j ? ci : 0.f)));
+        for (int j = hf * half; j < j1; ++j) {
+          const float h = Hs[j * mp + 4 * ((i >> 2) ^ (j & hsw)) + (i & 3)];
+          sabs += fabsf(h);
+          hmax = fmaxf(hmax, fabsf(h - (i == j ? ci : 0.f)));
+        }
+      }
+      psum[hf * mp + i] = sabs;
+      pmax[hf * mp + i] = hmax;
     }
-    const float ri = sabs * cinv[i];
-    rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
-    amax = fmaxf(amax, hmax);
+    __syncthreads();
+    for (int i = tid; i < m; i += 256) {
+      const float ri = (psum[i] + psum[mp + i]) * cinv[i];
+      rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
+      amax = fmaxf(amax, fmaxf(pmax[i], pmax[mp + i]));
+    }
+  } else {
+    for (int i = tid; i < m; i += 256) {
+      const float ci = 1.f / cinv[i];
+      float sabs = 0.f, hmax = 0.f;
+#pragma unroll 8
+      for (int j = 0; j < m; ++j) {
+        const float h = HH[(size_t)j * ldh + i];
+        sabs += fabsf(h);
+        hmax = fmaxf(hmax, fabsf(h - (i == j ? ci : 0.f)));
+      }
+      const float ri = sabs * cinv[i];
+      rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
+      amax = fmaxf(amax, hmax);
+    }
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -536,12 +583,13 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   if (r < 0.5f) {
     // B^T = -(P^T_blk) diag(1/c)^T, Y0 = B^T.
     for (int e0 = 0; e0 < kSolveCols * mp; e0 += 256 * 8) {
-      float pv[8];
+      if (!SMALL) {  // (m <= 128: fetched above, and one pass covers all)
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int e = e0 + tid + 256 * u;
-        const int i = min(e / kSolveCols, m - 1), cc = min(c0 + e % kSolveCols, d - 1);
-        pv[u] = P[(size_t)i * ldp + cc];
+        for (int u = 0; u < 8; ++u) {
+          const int e = e0 + tid + 256 * u;
+          const int i = min(e / kSolveCols, m - 1), cc = min(c0 + e % kSolveCols, d - 1);
+          pv[u] = P[(size_t)i * ldp + cc];
+        }
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -581,7 +629,7 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
       for (int t = 0; t < RBW; ++t) {
         const int arow = min((wave + 4 * t) * 16, mp - 16) + (lane & 15);
         if (SMALL) {
-          fa[t] = *reinterpret_cast<const float4*>(Hs + arow * LDE + k);
+          fa[t] = *reinterpret_cast<const float4*>(Hs + arow * mp + 4 * ((k >> 2) ^ (arow & hsw)));
         } else {
           const float* hr = HH + (size_t)min(arow, m - 1) * ldh;
           const float x0 = hr[min(k, m - 1)], x1 = hr[min(k + 1, m - 1)];
@@ -705,9 +753,19 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
 // smallest slot of its row (read from the hash table) does the work, so every
 // row is written once and in a fixed order.  Each pair records in own[] the
 // row it owns (or -1); launch 4 clears the hash slots from that record.
+constexpr int kScatterSlotsPerWave = 1;
+
+__device__ __forceinline__ void scatter_slot(const StepCtx& c, int e);
+
+// A wave handles kScatterSlotsPerWave consecutive slots in turn (few blocks,
+// so that they share the launch's compute units with the GEMM tiles).
 __device__ __forceinline__ void task_scatter(const StepCtx& c, int local) {
-  const int e = local * 4 + wave_id();
-  if (e >= c.m * c.K) return;
+  const int e0 = (local * 4 + wave_id()) * kScatterSlotsPerWave;
+  for (int u = 0; u < kScatterSlotsPerWave; ++u)
+    if (e0 + u < c.m * c.K) scatter_slot(c, e0 + u);
+}
+
+__device__ __forceinline__ void scatter_slot(const StepCtx& c, int e) {
   const int lane = lane_id();
   const int i = e / c.K;
   const int r = c.idx[e];
@@ -833,18 +891,19 @@ __device__ unsigned long long g_step_times[4][8192][3];
 // (V_*) and GEMM epilogues.  The kernel of a launch kind compiles only these,
 // which keeps its code small enough for the instruction cache.
 struct LaunchMasks {
-  unsigned tasks, vars, epis;
+  unsigned tasks, vars, epis, tiles;
 };
 constexpr LaunchMasks kLaunchMasks[5] = {
-    {0u, 0u, 0u},
-    {(1u << TK_GEMM) | (1u << TK_GATHER) | (1u << TK_PREP), V_NT, 1u << EPI_STORE},
+    {0u, 0u, 0u, 0u},
+    {(1u << TK_GEMM) | (1u << TK_GATHER) | (1u << TK_PREP), V_NT, 1u << EPI_STORE, TILE32},
     {(1u << TK_GEMM) | (1u << TK_SOLVE) | (1u << TK_YY) | (1u << TK_SCALARS), V_NN | V_NT,
-     1u << EPI_STORE},
-    {(1u << TK_GEMM) | (1u << TK_SCATTER), V_NN | V_TN, (1u << EPI_GRADT) | (1u << EPI_STORE)},
-    {(1u << TK_GEMM) | (1u << TK_CLEAR), V_TN, 1u << EPI_SYM},
+     1u << EPI_STORE, TILE32},
+    {(1u << TK_GEMM) | (1u << TK_SCATTER), V_NN, 1u << EPI_GRADT, TILE32},
+    {(1u << TK_GEMM) | (1u << TK_CLEAR), V_TN, (1u << EPI_SYM) | (1u << EPI_STORE),
+     TILE32 | TILE64},
 };
 
-template <int TILE, bool SMALLM, int W, int LK>
+template <bool SMALLM, int W, int LK>
 __device__ __forceinline__ void run_task(const StepCtx& c, const StepLaunch& L, int t, int local,
                                          unsigned char* sraw) {
   constexpr LaunchMasks M = kLaunchMasks[LK];
@@ -852,7 +911,7 @@ __device__ __forceinline__ void run_task(const StepCtx& c, const StepLaunch& L, 
   if constexpr ((M.tasks >> TK_GEMM) & 1u) {
     if (kind == TK_GEMM) {
       if (L.gemm.skip_if && *L.gemm.skip_if) return;
-      panel_tile<TILE, W, M.vars, M.epis>(L.gemm, local, reinterpret_cast<float*>(sraw));
+      panel_tile<M.tiles, W, M.vars, M.epis>(L.gemm, local, reinterpret_cast<float*>(sraw));
       return;
     }
   }
@@ -879,7 +938,7 @@ __device__ __forceinline__ void run_task(const StepCtx& c, const StepLaunch& L, 
   }
 }
 
-template <int TILE, bool SMALLM, int W, int LK>
+template <bool SMALLM, int W, int LK>
 __global__ __launch_bounds__(256) void step_kernel(StepCtx c, StepLaunch L) {
   extern __shared__ __attribute__((aligned(16))) unsigned char sraw[];
   const int blk = blockIdx.x;
@@ -889,7 +948,7 @@ __global__ __launch_bounds__(256) void step_kernel(StepCtx c, StepLaunch L) {
 #ifdef LST_TIMING
   const unsigned long long t0 = wall_clock64();
 #endif
-  run_task<TILE, SMALLM, W, LK>(c, L, t, local, sraw);
+  run_task<SMALLM, W, LK>(c, L, t, local, sraw);
 #ifdef LST_TIMING
   __syncthreads();
   if (threadIdx.x == 0 && blk < 8192) {
@@ -911,12 +970,13 @@ static size_t lds_of(int kind, int stages, int m) {
   }
 }
 
-static int tiles_of(GemmBatch& b, int tile) {
+static int tiles_of(GemmBatch& b) {
   int total = 0;
   for (int q = 0; q < b.np; ++q) {
     GemmProblem& p = b.p[q];
-    p.tiles_m = (p.M + tile - 1) / tile;
-    p.tiles_n = (p.N + tile - 1) / tile;
+    if (p.tile == 0) p.tile = 32;
+    p.tiles_m = (p.M + p.tile - 1) / p.tile;
+    p.tiles_n = (p.N + p.tile - 1) / p.tile;
     p.tile_begin = total;
     if (p.ksplit < 1) p.ksplit = 1;
     if (p.epi == EPI_SYM)
@@ -935,7 +995,7 @@ int step_task_blocks(int kind, const StepCtx& c) {
     case TK_YY: { const int nb = (c.m + 15) / 16; return nb * (nb + 1) / 2; }
     case TK_SCALARS: return (c.m + 3) / 4;
     case TK_SOLVE: return (c.d + kSolveCols - 1) / kSolveCols;
-    case TK_SCATTER: return (c.m * c.K + 3) / 4;
+    case TK_SCATTER: return (c.m * c.K + 4 * kScatterSlotsPerWave - 1) / (4 * kScatterSlotsPerWave);
     case TK_CLEAR: return (c.m * c.K + 255) / 256;
     default: return 0;
   }
@@ -958,36 +1018,27 @@ int gemm_batch_vec16(const GemmBatch& b) {
   return 1;
 }
 
-template <int TILE, bool SMALLM, int W, int LK>
+template <bool SMALLM, int W, int LK>
 static const void* kfn() {
-  return reinterpret_cast<const void*>(step_kernel<TILE, SMALLM, W, LK>);
+  return reinterpret_cast<const void*>(step_kernel<SMALLM, W, LK>);
 }
 
-// The kernel built for (launch kind, tile, m <= 128, 16-byte DMA); nullptr for
-// a combination that is not built.
-static const void* step_kernel_for(int lk, int tile, bool small, int w16) {
+// The kernel built for (launch kind, m <= 128, 16-byte DMA); nullptr for a
+// combination that is not built.
+static const void* step_kernel_for(int lk, bool small, int w16) {
   switch (lk) {
-    case 1:
-      if (tile != 32) return nullptr;
-      return w16 ? kfn<32, true, 4, 1>() : kfn<32, true, 1, 1>();
+    case 1: return w16 ? kfn<true, 4, 1>() : kfn<true, 1, 1>();
     case 2:
-      if (tile != 32) return nullptr;
-      if (small) return w16 ? kfn<32, true, 4, 2>() : kfn<32, true, 1, 2>();
-      return w16 ? kfn<32, false, 4, 2>() : kfn<32, false, 1, 2>();
-    case 3:
-      if (tile == 32) return w16 ? kfn<32, true, 4, 3>() : kfn<32, true, 1, 3>();
-      return w16 ? kfn<64, true, 4, 3>() : kfn<64, true, 1, 3>();
-    case 4:
-      if (tile == 32) return w16 ? kfn<32, true, 4, 4>() : kfn<32, true, 1, 4>();
-      return w16 ? kfn<64, true, 4, 4>() : kfn<64, true, 1, 4>();
-    default:
-      return nullptr;
+      if (small) return w16 ? kfn<true, 4, 2>() : kfn<true, 1, 2>();
+      return w16 ? kfn<false, 4, 2>() : kfn<false, 1, 2>();
+    case 3: return w16 ? kfn<true, 4, 3>() : kfn<true, 1, 3>();
+    case 4: return w16 ? kfn<true, 4, 4>() : kfn<true, 1, 4>();
+    default: return nullptr;
   }
 }
 
-hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, int stages, hipStream_t s,
+hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t s,
                        hipEvent_t ev0, hipEvent_t ev1) {
-  if (tile != 32 && tile != 64) return hipErrorInvalidValue;
   if (L.lk < 1 || L.lk > 4) return hipErrorInvalidValue;
   if (stages < 2 || (size_t)stages * kPanelStageBytes > kStepLdsMax) return hipErrorInvalidValue;
   const LaunchMasks& M = kLaunchMasks[L.lk];
@@ -1003,10 +1054,11 @@ hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, int stages, hi
     if (L.kind[t] == TK_GEMM) {
       for (int q = 0; q < L.gemm.np; ++q) {
         const GemmProblem& p = L.gemm.p[q];
-        if (!(M.vars & problem_variant(p)) || !((M.epis >> p.epi) & 1u))
+        const unsigned tbit = (p.tile == 64) ? TILE64 : (p.tile == 32 || p.tile == 0) ? TILE32 : 0u;
+        if (!(M.vars & problem_variant(p)) || !((M.epis >> p.epi) & 1u) || !(M.tiles & tbit))
           return hipErrorInvalidValue;
       }
-      n = tiles_of(L.gemm, tile);
+      n = tiles_of(L.gemm);
       w16 = gemm_batch_vec16(L.gemm);
     } else {
       n = step_task_blocks(L.kind[t], c);
@@ -1019,7 +1071,7 @@ hipError_t step_launch(const StepCtx& c, StepLaunch& L, int tile, int stages, hi
   if (total == 0) return hipSuccess;
   if (lds > kStepLdsMax) return hipErrorInvalidValue;
 
-  const void* fn = step_kernel_for(L.lk, tile, c.m <= 128, w16);
+  const void* fn = step_kernel_for(L.lk, c.m <= 128, w16);
   if (!fn) return hipErrorInvalidValue;
   StepCtx ca = c;
   StepLaunch la = L;
@@ -1036,15 +1088,14 @@ size_t solve_workspace_floats(int m_max, int d) {
 
 hipError_t configure_kernels() {
   for (int lk = 1; lk <= 4; ++lk)
-    for (int tile : {32, 64})
-      for (int small = 0; small < 2; ++small)
-        for (int w16 = 0; w16 < 2; ++w16) {
-          const void* k = step_kernel_for(lk, tile, small != 0, w16);
-          if (!k) continue;
-          const hipError_t e = hipFuncSetAttribute(
-              k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kStepLdsMax);
-          if (e != hipSuccess) return e;
-        }
+    for (int small = 0; small < 2; ++small)
+      for (int w16 = 0; w16 < 2; ++w16) {
+        const void* k = step_kernel_for(lk, small != 0, w16);
+        if (!k) continue;
+        const hipError_t e =
+            hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kStepLdsMax);
+        if (e != hipSuccess) return e;
+      }
   return hipSuccess;
 }
 
