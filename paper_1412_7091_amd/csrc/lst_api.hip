@@ -254,10 +254,6 @@ int stages_for(const GemmBatch& b, int max_stages = kMaxStages) {
   return st < 2 ? 2 : st;
 }
 
-// Launch 1 also runs the gather and the target preparation, which need little
-// LDS: with at most 4 stages (64 KB) their blocks share compute units with the
-// GEMM tiles instead of waiting for them (K = d > 256 then takes the ring).
-constexpr int kLaunch1Stages = 4;
 // Launches 3 and 4 keep at most 4 stages (64 KB): two blocks share a compute
 // unit, so the short tasks run beside the GEMM tiles.
 constexpr int kLaunch34Stages = 4;
@@ -286,8 +282,8 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
 
   {  // launch 1: GEMM 1, gather, target prep
     StepLaunch L{};
-    L.ntask = 3;
-    L.kind[0] = TK_GEMM; L.kind[1] = TK_GATHER; L.kind[2] = TK_PREP;
+    L.ntask = 2;
+    L.kind[0] = TK_GEMM; L.kind[1] = TK_TARGETS;
     L.gemm.np = 1;
     GemmProblem& p1 = L.gemm.p[0];
     p1 = gemm_problem(L_NT, m, 3 * d + m, d, vmat(H, d, m), vmat2(s->state, d, 3 * d, H, d, m),
@@ -298,7 +294,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     L.timing_slot = 0;
     hipEvent_t e0, e1;
     OK_OR_RETURN(prof_pair(s, PH_LAUNCH1, &e0, &e1));
-    HIPCHK(step_launch(c, L, stages_for(L.gemm, kLaunch1Stages), st, e0, e1));
+    HIPCHK(step_launch(c, L, stages_for(L.gemm), st, e0, e1));
   }
   {  // launch 2: Y^, C1, C2, C2^T ; solve ; Y^T Y ; per-example scalars
     StepLaunch L{};

@@ -138,7 +138,7 @@ struct StepCtx {
 };
 
 enum TaskKind {
-  TK_GEMM = 0, TK_GATHER, TK_PREP, TK_YY, TK_SCALARS, TK_SOLVE, TK_SCATTER, TK_CLEAR
+  TK_GEMM = 0, TK_TARGETS, TK_YY, TK_SCALARS, TK_SOLVE, TK_SCATTER, TK_CLEAR
 };
 constexpr int kMaxTasks = 6;
 

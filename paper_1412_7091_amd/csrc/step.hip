@@ -1,28 +1,28 @@
 // The factored minibatch step (Appendix A) as four launches on one stream.
 //
 // Each launch is one grid whose blocks run tiles of several independent tasks
-// (a "heterogeneous" launch), so the step pays four launch latencies instead
-// of one per task:
-//   launch 1  GEMM  Z0 = H^T [Q; U; U^{-T}; H^T]^T -> H^, UH, P, H^T H        (steps 1, 7, 8)
-//             gather G = (V^T Y)^T                                         (step 2, sparse part)
-//             prep  validate and sort each example's targets; record the
-//                   smallest slot of every target row in a hash table
-//   launch 2  GEMM  Y^ = G U, C1 = H^T H^, C2 = H^T Y^, C2^T               (steps 2, 5)
-//             solve X = S^{-1} P^T, S = H^T H - diag(1/(lr a_i))           (step 8)
-//             yy    Y^T Y                                                  (step 5)
-//             scalars per example: loss, a_i, b_i, c_i, a h_i, b h_i       (steps 3-6)
-//   launch 3  GEMM  grad_H = H^ A + Y^ diag(b), T = grad_H - (lr/2) N H^T    (step 4)
-//                   with N H^T = A [C1 C2] [AH; BH] + B [C2^T Y^T Y] [AH; BH]
-//                   U -= lr (UH) A H^T, U^{-T} -= X^T H^T                   (steps 7, 8)
+// (a "heterogeneous" launch), and each launch has its own kernel holding only
+// its tasks:
+//   launch 1  GEMM    Z0 = H [Q; U; U^{-T}; H^T]^T -> H^, UH, P, H^T H      (steps 1, 7, 8)
+//             targets per example: validate and order the targets, (Y^T Y)_ii,
+//                     gather G = (V^T Y)^T                                  (step 2, sparse part)
+//   launch 2  GEMM    Y^ = G U, C1 = H^T H^, C2 = H^T Y^, C2^T                (steps 2, 5)
+//             solve   X = S^{-1} P^T, S = H^T H - diag(1/(lr a_i))         (step 8)
+//             yy      Y^T Y                                                (step 5)
+//             scalars per example: loss, a_i, b_i, c_i, a h_i, b h_i, and the
+//                     hash table of each target row's smallest slot         (steps 3-6)
+//   launch 3  GEMM    grad_H = H^ A + Y^ diag(b), T = grad_H - (lr/2) N H^T  (step 4)
+//                     with N H^T = A [C1 C2] [AH; BH] + B [C2^T Y^T Y] [AH; BH]
 //             scatter V[r] += sum over examples j holding r of c_j X_j     (step 9)
-//   launch 4  GEMM  Q -= lr (H T^T + T H^T), symmetric                      (step 10)
-//             clear the hash slots used by this step
+//   launch 4  GEMM    Q -= lr (H T^T + T H^T), symmetric; U -= lr (UH) A H^T;
+//                     U^{-T} -= X^T H^T                                     (steps 7, 8, 10)
+//             clear   the hash slots used by this step
 // With A = diag(a_i) and G the part of dL/dO sparse on the targets,
 // dL/dO = W H A + G: squared error a_i = 2, G = -2 Y; spherical softmax
 // a_i = 2 / S_i, G = Y diag(b_i), S_i = h_i^T Q h_i + D eps,
 // b_i = -2 o_c / (o_c^2 + eps), o_c = h_i^T W^T y_i.  N = (dL/dO)^T dL/dO.
-// Every update of the state (launches 3 and 4) skips when the step's error
-// flag is set; all checks that can set it run in launches 1 and 2.
+// Every update of the state (the scatter, launch 4) skips when the step's
+// error flag is set; all checks that can set it run in launches 1 and 2.
 #include <hip/hip_ext.h>
 #include <math.h>
 
@@ -62,131 +62,171 @@ __device__ __forceinline__ float example_a(const StepCtx& c, int i) {
   return 2.f / (example_c1(c, i) + (float)c.D * c.eps);
 }
 
-// ------------------------------------------------------------------ gather
-// G[i, :] = sum_k w_ik V[idx_ik, :]: one wave per (example, 256-column chunk),
-// four consecutive columns per lane, eight rows of V in flight at once.
-__device__ __forceinline__ void task_gather(const StepCtx& c, int local) {
-  const int nchunk = (c.d + 255) / 256;
-  const int item = local * 4 + wave_id();
-  if (item >= c.m * nchunk) return;
-  const int i = item / nchunk, ch = item - i * nchunk;
-  const int col = ch * 256 + lane_id() * 4;
-  if (col >= c.d) return;
-  const bool vec = (c.d % 4 == 0);
-  const bool one_hot = c.loss_kind == LST_LOSS_SPHERICAL;
-  const int32_t* ix = c.idx + (size_t)i * c.K;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int k0 = 0; k0 < c.K; k0 += 8) {
-    float4 rv[8];
-    float w[8];
+// ----------------------------------------------------------------- targets
+// Launch 1, one wave per example i (four per block, no block barrier):
+//  - load and validate its K (index, value) pairs (LST_EINDEX on a bad index);
+//  - order the pairs by (row, slot) into ex_row / ex_val (rank sort in this
+//    wave's part of LDS) and count them;
+//  - (Y^T Y)_ii = sum over distinct rows of (sum of the row's values)^2, each
+//    row's values added in slot order;
+//  - G_i = sum_k y_ik V[r_ik, :] (Appendix A step 2, the sparse product),
+//    slots in order, up to 16 rows of V in flight.
+constexpr unsigned long long kNoKey = ~0ull;
+
+__host__ __device__ inline size_t targets_lds_bytes(int K) {
+  return (size_t)4 * K * (sizeof(unsigned long long) + sizeof(float));
+}
+
+// One batch of the gather: rows of slots k0 .. k0+7 (weights wv, 0 for slots
+// past K or without a valid target), columns cb + 256 h + 4 lane, h < 2.
+__device__ __forceinline__ void gather_load(const StepCtx& c, const unsigned long long* keys,
+                                            const float* vals, int k0, int cb, float4 (&rv)[8][2],
+                                            float (&wv)[8]) {
+  const int K = c.K, d = c.d, lane = lane_id();
+  const bool vec = (d % 4 == 0);
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      rv[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-      w[u] = 0.f;
-      const int k = k0 + u;
-      if (k >= c.K) continue;
-      const int r = ix[k];
-      if (r < 0 || (int64_t)r >= c.D) continue;
-      w[u] = one_hot ? 1.f : c.val[(size_t)i * c.K + k];
-      const float* row = c.V + (size_t)r * c.d + col;
+  for (int u = 0; u < 8; ++u) {
+    const int k = min(k0 + u, K - 1);
+    const unsigned long long key = keys[k];
+    const bool use = (k0 + u < K) && key != kNoKey;
+    wv[u] = use ? vals[k] : 0.f;
+    const float* row = c.V + (size_t)(use ? (unsigned)(key >> 32) : 0u) * d;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int col = min(cb + 256 * h + 4 * lane, vec ? d - 4 : d - 1);
       if (vec) {
-        rv[u] = *reinterpret_cast<const float4*>(row);
+        rv[u][h] = *reinterpret_cast<const float4*>(row + col);
       } else {
-        rv[u].x = row[0];
-        if (col + 1 < c.d) rv[u].y = row[1];
-        if (col + 2 < c.d) rv[u].z = row[2];
-        if (col + 3 < c.d) rv[u].w = row[3];
+        rv[u][h].x = row[col];
+        rv[u][h].y = row[min(col + 1, d - 1)];
+        rv[u][h].z = row[min(col + 2, d - 1)];
+        rv[u][h].w = row[min(col + 3, d - 1)];
       }
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      acc.x += w[u] * rv[u].x;
-      acc.y += w[u] * rv[u].y;
-      acc.z += w[u] * rv[u].z;
-      acc.w += w[u] * rv[u].w;
-    }
-  }
-  float* out = c.G + (size_t)i * c.d + col;
-  if (vec) {
-    *reinterpret_cast<float4*>(out) = acc;
-  } else {
-    out[0] = acc.x;
-    if (col + 1 < c.d) out[1] = acc.y;
-    if (col + 2 < c.d) out[2] = acc.z;
-    if (col + 3 < c.d) out[3] = acc.w;
   }
 }
 
-// ------------------------------------------------------------------- prep
-// Example i: validate its K pairs, sort them by (row, slot) into
-// ex_row / ex_val, count them, record in the hash table the smallest slot
-// (i*K + k) holding each row, and form (Y^T Y)_ii = sum over distinct rows of
-// (sum of the row's values)^2, each row's values added in slot order.
-// K <= 1024.
-constexpr size_t kPrepLds = 1024 * (sizeof(unsigned long long) + sizeof(float)) + 256 * 4 + 16;
+__device__ __forceinline__ void gather_add(const float4 (&rv)[8][2], const float (&wv)[8],
+                                           float4 (&acc)[2]) {
+#pragma unroll
+  for (int u = 0; u < 8; ++u)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      // unused slots add nothing (not even a non-finite value of row 0)
+      const bool use = wv[u] != 0.f;
+      acc[h].x += use ? wv[u] * rv[u][h].x : 0.f;
+      acc[h].y += use ? wv[u] * rv[u][h].y : 0.f;
+      acc[h].z += use ? wv[u] * rv[u][h].z : 0.f;
+      acc[h].w += use ? wv[u] * rv[u][h].w : 0.f;
+    }
+}
 
-__device__ __forceinline__ void task_prep(const StepCtx& c, int i, unsigned char* sraw) {
-  unsigned long long* keys = reinterpret_cast<unsigned long long*>(sraw);
-  float* vals = reinterpret_cast<float*>(sraw + 1024 * sizeof(unsigned long long));
-  float* red = vals + 1024;
-  int* cnt = reinterpret_cast<int*>(red + 256);
+#ifdef LST_TIMING
+__device__ unsigned long long g_target_marks[64][6];
+#define LST_TMARK(k)                                                            \
+  do {                                                                          \
+    if (lane == 0 && w == 0 && local < 64) g_target_marks[local][k] = wall_clock64(); \
+  } while (0)
+#else
+#define LST_TMARK(k) \
+  do {               \
+  } while (0)
+#endif
+
+__device__ __forceinline__ void task_targets(const StepCtx& c, int local, unsigned char* sraw) {
+  const int w = wave_id(), lane = lane_id();
+  const int i = local * 4 + w;
+  if (i >= c.m) return;
+  LST_TMARK(0);
+  const int K = c.K, d = c.d;
+  unsigned long long* keys = reinterpret_cast<unsigned long long*>(sraw) + (size_t)w * K;
+  float* vals = reinterpret_cast<float*>(sraw + (size_t)4 * K * sizeof(unsigned long long)) +
+                (size_t)w * K;
   const bool one_hot = c.loss_kind == LST_LOSS_SPHERICAL;
-  constexpr unsigned long long kNoKey = ~0ull;
-  if (threadIdx.x == 0) *cnt = 0;
-  __syncthreads();
-  const int mask = (1 << c.hbits) - 1;
-  for (int k = threadIdx.x; k < c.K; k += blockDim.x) {
-    const int r = c.idx[(size_t)i * c.K + k];
-    const bool valid = (r >= 0) && ((int64_t)r < c.D);
-    const bool bad = (r < -1) || ((int64_t)r >= c.D) || (one_hot && r == -1);
+  const int32_t* ix = c.idx + (size_t)i * K;
+  int nvalid = 0;
+  for (int k0 = 0; k0 < K; k0 += 64) {
+    const int k = k0 + lane;
+    const bool in = k < K;
+    const int r = in ? ix[k] : -1;
+    const float v = (in && !one_hot) ? c.val[(size_t)i * K + k] : 1.f;
+    const bool valid = in && r >= 0 && (int64_t)r < c.D;
+    const bool bad = in && ((r < -1) || ((int64_t)r >= c.D) || (one_hot && r == -1));
     if (bad) atomicCAS(c.flags + F_ERR, 0, LST_EINDEX);
-    keys[k] = valid ? (((unsigned long long)(unsigned)r << 32) | (unsigned)k) : kNoKey;
-    vals[k] = valid ? (one_hot ? 1.f : c.val[(size_t)i * c.K + k]) : 0.f;
-    if (valid) {
-      atomicAdd(cnt, 1);
-      const int slot = i * c.K + k;
-      unsigned h = row_hash(r, c.hbits);
-      for (int probe = 0; probe <= mask; ++probe) {  // the table is at most half full
-        const int prev = atomicCAS(c.hkey + h, -1, r);
-        if (prev == -1 || prev == r) {
-          atomicMin(c.hmin + h, slot);
-          break;
+    if (in) {
+      keys[k] = valid ? (((unsigned long long)(unsigned)r << 32) | (unsigned)k) : kNoKey;
+      vals[k] = valid ? v : 0.f;
+    }
+    nvalid += __popcll(__ballot(valid));
+  }
+  // LDS is read back by other lanes of this wave: the wave's LDS accesses
+  // complete in order, so only the compiler must not move them.
+  asm volatile("" ::: "memory");
+
+  LST_TMARK(1);
+  // The first rows of V are requested now and used after the ordering below,
+  // whose latency they overlap.
+  float4 rv[8][2];
+  float wv[8];
+  gather_load(c, keys, vals, 0, 0, rv, wv);
+
+  LST_TMARK(2);
+  float yy = 0.f;
+  for (int k0 = 0; k0 < K; k0 += 64) {
+    const int k = k0 + lane;
+    if (k < K) {
+      const unsigned long long key = keys[k];
+      const unsigned row = (unsigned)(key >> 32);
+      int rank = 0;
+      bool first = true;
+      float run = 0.f;
+      for (int k2 = 0; k2 < K; ++k2) {
+        const unsigned long long o = keys[k2];
+        rank += (o < key) || (o == key && k2 < k);
+        if ((unsigned)(o >> 32) == row && o != kNoKey) {
+          run += vals[k2];
+          first = first && !(k2 < k);
         }
-        h = (h + 1) & mask;
+      }
+      const bool valid = key != kNoKey;
+      if (valid && first) yy += run * run;
+      c.ex_row[(size_t)i * K + rank] = valid ? (int)row : -1;
+      c.ex_val[(size_t)i * K + rank] = vals[k];
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) yy += __shfl_xor(yy, off);
+  if (lane == 0) {
+    c.ex_cnt[i] = nvalid;
+    c.yyd[i] = yy;
+  }
+
+  LST_TMARK(3);
+  // G_i = sum_k y_ik V[r_ik, :]: lane l owns columns cb + 256 h + 4 l, slots
+  // in order, 8 rows (16 loads) in flight.
+  const bool vec = (d % 4 == 0);
+  float* gout = c.G + (size_t)i * d;
+  for (int cb = 0; cb < d; cb += 512) {
+    float4 acc[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
+    for (int k0 = 0; k0 < K; k0 += 8) {
+      if (cb > 0 || k0 > 0) gather_load(c, keys, vals, k0, cb, rv, wv);
+      gather_add(rv, wv, acc);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int col = cb + 256 * h + 4 * lane;
+      if (col >= d) continue;
+      if (vec) {
+        *reinterpret_cast<float4*>(gout + col) = acc[h];
+      } else {
+        gout[col] = acc[h].x;
+        if (col + 1 < d) gout[col + 1] = acc[h].y;
+        if (col + 2 < d) gout[col + 2] = acc[h].z;
+        if (col + 3 < d) gout[col + 3] = acc[h].w;
       }
     }
   }
-  __syncthreads();
-  float yy_part = 0.f;
-  for (int k = threadIdx.x; k < c.K; k += blockDim.x) {
-    const unsigned long long key = keys[k];
-    const unsigned row = (unsigned)(key >> 32);
-    int rank = 0;
-    bool first = true;
-    float run = 0.f;
-    for (int k2 = 0; k2 < c.K; ++k2) {
-      const unsigned long long o = keys[k2];
-      rank += (o < key) || (o == key && k2 < k);
-      if ((unsigned)(o >> 32) == row && o != kNoKey) {
-        run += vals[k2];
-        first = first && !(k2 < k);
-      }
-    }
-    const bool valid = key != kNoKey;
-    if (valid && first) yy_part += run * run;
-    c.ex_row[(size_t)i * c.K + rank] = valid ? (int)row : -1;
-    c.ex_val[(size_t)i * c.K + rank] = vals[k];
-  }
-  red[threadIdx.x] = yy_part;
-  __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if ((int)threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) {
-    c.ex_cnt[i] = *cnt;
-    c.yyd[i] = red[0];
-  }
+  LST_TMARK(4);
 }
 
 // --------------------------------------------------------------------- Y^T Y
@@ -262,8 +302,10 @@ __device__ __forceinline__ void task_yy(const StepCtx& c, int local, unsigned ch
 //   squared:   loss = c1 - 2 c2 + (Y^T Y)_ii (= M_ii, Appendix A step 6), a = 2, b = -2
 //   spherical: loss = -log(c2^2 + eps) + log(c1 + D eps), a = 2/(c1 + D eps),
 //              b = -2 c2 / (c2^2 + eps), cs = b / a (the scatter weight)
-// and the row a (U h)^T of the U update's left factor.  Block 0 also counts
-// the step's target pairs and resets the distinct-row count.
+// and the row a (U h)^T of the U update's left factor; also inserts the
+// example's target rows into the hash table that decides the scatter's
+// owners.  Block 0 also counts the step's target pairs and resets the
+// distinct-row count.
 __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
   if (local == 0 && wave_id() == 0) {
     int nnz = 0;
@@ -278,6 +320,25 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
   const int i = local * 4 + wave_id();
   if (i >= c.m) return;
   const int lane = lane_id(), d = c.d;
+  // Record, for every target row, the smallest slot i*K + k holding it (the
+  // owner of the row's scatter in launch 3): open addressing, at most half full.
+  {
+    const int mask = (1 << c.hbits) - 1;
+    for (int k = lane; k < c.K; k += 64) {
+      const int r = c.idx[(size_t)i * c.K + k];
+      if (r < 0 || (int64_t)r >= c.D) continue;
+      const int slot = i * c.K + k;
+      unsigned h = row_hash(r, c.hbits);
+      for (int probe = 0; probe <= mask; ++probe) {
+        const int prev = atomicCAS(c.hkey + h, -1, r);
+        if (prev == -1 || prev == r) {
+          atomicMin(c.hmin + h, slot);
+          break;
+        }
+        h = (h + 1) & mask;
+      }
+    }
+  }
   const float c1 = example_c1(c, i);
   const float Si = c1 + (float)c.D * c.eps;
   const float a = (c.loss_kind == LST_LOSS_SQUARED) ? 2.f : 2.f / Si;
@@ -895,7 +956,7 @@ struct LaunchMasks {
 };
 constexpr LaunchMasks kLaunchMasks[5] = {
     {0u, 0u, 0u, 0u},
-    {(1u << TK_GEMM) | (1u << TK_GATHER) | (1u << TK_PREP), V_NT, 1u << EPI_STORE, TILE32},
+    {(1u << TK_GEMM) | (1u << TK_TARGETS), V_NT, 1u << EPI_STORE, TILE32},
     {(1u << TK_GEMM) | (1u << TK_SOLVE) | (1u << TK_YY) | (1u << TK_SCALARS), V_NN | V_NT,
      1u << EPI_STORE, TILE32},
     {(1u << TK_GEMM) | (1u << TK_SCATTER), V_NN, 1u << EPI_GRADT, TILE32},
@@ -915,11 +976,8 @@ __device__ __forceinline__ void run_task(const StepCtx& c, const StepLaunch& L, 
       return;
     }
   }
-  if constexpr ((M.tasks >> TK_GATHER) & 1u) {
-    if (kind == TK_GATHER) { task_gather(c, local); return; }
-  }
-  if constexpr ((M.tasks >> TK_PREP) & 1u) {
-    if (kind == TK_PREP) { task_prep(c, local, sraw); return; }
+  if constexpr ((M.tasks >> TK_TARGETS) & 1u) {
+    if (kind == TK_TARGETS) { task_targets(c, local, sraw); return; }
   }
   if constexpr ((M.tasks >> TK_YY) & 1u) {
     if (kind == TK_YY) { task_yy(c, local, sraw); return; }
@@ -960,10 +1018,10 @@ __global__ __launch_bounds__(256) void step_kernel(StepCtx c, StepLaunch L) {
 }
 
 // ------------------------------------------------------------------- host
-static size_t lds_of(int kind, int stages, int m) {
+static size_t lds_of(int kind, int stages, int m, int K) {
   switch (kind) {
     case TK_GEMM: return (size_t)stages * kPanelStageBytes;
-    case TK_PREP: return kPrepLds;
+    case TK_TARGETS: return targets_lds_bytes(K);
     case TK_YY: return 2 * 32 * kGramKMax * 4 + 32 * 4;
     case TK_SOLVE: return solve_lds_bytes(m);
     default: return 0;
@@ -990,8 +1048,7 @@ static int tiles_of(GemmBatch& b) {
 
 int step_task_blocks(int kind, const StepCtx& c) {
   switch (kind) {
-    case TK_GATHER: return (c.m * ((c.d + 255) / 256) + 3) / 4;
-    case TK_PREP: return c.m;
+    case TK_TARGETS: return (c.m + 3) / 4;
     case TK_YY: { const int nb = (c.m + 15) / 16; return nb * (nb + 1) / 2; }
     case TK_SCALARS: return (c.m + 3) / 4;
     case TK_SOLVE: return (c.d + kSolveCols - 1) / kSolveCols;
@@ -1063,7 +1120,7 @@ hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t 
     } else {
       n = step_task_blocks(L.kind[t], c);
     }
-    const size_t b = lds_of(L.kind[t], stages, c.m);
+    const size_t b = lds_of(L.kind[t], stages, c.m, c.K);
     if (b > lds) lds = b;
     total += n;
   }
@@ -1129,6 +1186,10 @@ __global__ __launch_bounds__(1024) void sort_ints_kernel(int* v, const int* n_pt
 #ifdef LST_TIMING
 extern "C" int lst_debug_step_times(unsigned long long* out) {
   return hipMemcpyFromSymbol(out, HIP_SYMBOL(g_step_times), sizeof(g_step_times)) == hipSuccess
+             ? 0 : -5;
+}
+extern "C" int lst_debug_target_marks(unsigned long long* out) {
+  return hipMemcpyFromSymbol(out, HIP_SYMBOL(g_target_marks), sizeof(g_target_marks)) == hipSuccess
              ? 0 : -5;
 }
 extern "C" int lst_debug_solve_marks(unsigned long long* out) {
