@@ -164,8 +164,10 @@ int lst_naive_step(lst_state* s, int32_t m, int32_t K, const float* H, const int
                    const float* Y_val, float lr, float* loss, float* grad_H);
 
 /*
- * lst_set_graphs -- enable (the default) or disable HIP-graph replay of lst_step.
- * When enabled, the first lst_step call with a given argument tuple
+ * lst_set_graphs -- enable or disable (the default) HIP-graph replay of lst_step.
+ * Replay lowers the host cost of a call; on MI355X it lengthens the step on
+ * the device (the GPU idles between replays), so direct launches are the
+ * default.  When enabled, the first lst_step call with a given argument tuple
  * (m, K, H, Y_idx, Y_val, lr, loss, grad_H) records its kernels into a graph and
  * every later call with the same tuple replays that graph with a single launch
  * on the state's stream (same kernels, same order, same results).  At most 32

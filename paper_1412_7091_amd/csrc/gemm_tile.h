@@ -83,15 +83,17 @@ __device__ __forceinline__ unsigned lds_u32(const void* p) {
 // own global address gp to LDS byte address lds + 16 l (4 l); lds must be the
 // same for the whole wave.  The compiler does not see these as memory
 // operations on LDS, so waits for them are explicit (wait_vm_le) and the
-// barrier that publishes them is lds_barrier.
+// barrier that publishes them is lds_barrier.  The LDS address travels in m0
+// (the compiler itself puts nothing in m0 in these kernels); an SALU write of
+// m0 needs one wait state before an LDS-DMA instruction reads it.
 __device__ __forceinline__ void dma16(const float* gp, unsigned lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
                :
                : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(gp)
                : "memory", "m0");
 }
 __device__ __forceinline__ void dma4(const float* gp, unsigned lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off"
                :
                : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(gp)
                : "memory", "m0");
@@ -326,6 +328,11 @@ __device__ __forceinline__ void mma_slices(const float* smem, int nsl, Accum<T>&
 // Operand layouts a kernel instantiation supports (bit masks).
 enum : unsigned { V_NT = 2, V_NN = 4, V_TN = 8 };
 
+// Epilogue-mask bit (beyond the Epi values) of the per-row partial sums that
+// EPI_STORE can produce (GemmProblem::dotp, GemmProblem::absp); kernels
+// without it compile neither.
+constexpr unsigned EPX_ROWSUMS = 8;
+
 // P.epi == e, folded away when the instantiation does not support e.
 template <unsigned EPIS>
 __device__ __forceinline__ bool epi_is(const GemmProblem& P, int e) {
@@ -343,7 +350,9 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
   const int m0 = tm * T, n0 = tn * T;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const bool dot = P.dotp != nullptr && n0 < P.dot_ncols;
+  constexpr bool kRowSums = (EPIS >> EPX_ROWSUMS) & 1u;
+  const bool dot = kRowSums && P.dotp != nullptr && n0 < P.dot_ncols;
+  const bool absr = kRowSums && P.absp != nullptr && n0 + T > P.abs_col0;
   LST_MARK(0);
 
   // Operands of the epilogue, fetched before the first chunk.
@@ -437,11 +446,11 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
 
   LST_MARK(3);
   // Element r of acc[i][j]: row 4*(lane/16) + r, column lane % 16 of its 16 x 16 block.
-  float dsum[IB][4];
+  float dsum[IB][4], asum[IB][4];
 #pragma unroll
   for (int i = 0; i < IB; ++i)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) dsum[i][r] = 0.f;
+    for (int r = 0; r < 4; ++r) dsum[i][r] = asum[i][r] = 0.f;
 #pragma unroll
   for (int i = 0; i < IB; ++i)
 #pragma unroll
@@ -455,6 +464,7 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
         if (epi_is<EPIS>(P, EPI_STORE)) {
           P.C[(size_t)row * P.ldc + col] = P.alpha * v + P.beta * pre1[i][j][r];
           if (dot && col < P.dot_ncols) dsum[i][r] += pre2[i][j][r] * v;
+          if (absr && col >= P.abs_col0) asum[i][r] += fabsf(v);
         } else if (epi_is<EPIS>(P, EPI_SYM)) {
           if (row <= col) {
             const float o = pre1[i][j][r] + P.alpha * v;
@@ -487,6 +497,21 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
         v += __shfl_xor(v, 8);
         const int row = m0 + wm * G::WT + i * 16 + 4 * (lane >> 4) + r;
         if ((lane & 15) == 0 && row < P.M) P.dotp[(size_t)row * P.ld_dotp + 2 * tn + wn] = v;
+      }
+  }
+  if (absr) {  // the same for the sums of |C| (a wave left of abs_col0 writes 0)
+    const int pc = 2 * (tn - P.abs_col0 / T) + wn;
+#pragma unroll
+    for (int i = 0; i < IB; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float v = asum[i][r];
+        v += __shfl_xor(v, 1);
+        v += __shfl_xor(v, 2);
+        v += __shfl_xor(v, 4);
+        v += __shfl_xor(v, 8);
+        const int row = m0 + wm * G::WT + i * 16 + 4 * (lane >> 4) + r;
+        if ((lane & 15) == 0 && row < P.M) P.absp[(size_t)row * P.ld_absp + pc] = v;
       }
   }
   LST_MARK(4);

@@ -35,13 +35,15 @@ struct lst_state {
   // factored workspace
   float *G = nullptr, *Z0 = nullptr, *Yh = nullptr, *NP = nullptr, *aH = nullptr, *bH = nullptr,
         *a = nullptr, *b = nullptr, *cs = nullptr, *T = nullptr, *X = nullptr,
-        *ex_val = nullptr, *solve_ws = nullptr, *UHa = nullptr, *c1p = nullptr, *yyd = nullptr;
+        *ex_val = nullptr, *solve_ws = nullptr, *UHa = nullptr, *c1p = nullptr, *yyd = nullptr,
+        *hap = nullptr;
   int *ex_row = nullptr, *ex_cnt = nullptr, *hkey = nullptr, *hmin = nullptr, *touched = nullptr,
       *own = nullptr, *count = nullptr;
   int last_slots = 0;  // m * K of the last factored step
   int hbits = 0;
   int ld0 = 0;
   int n_c1p = 0;  // partial sums of h^T Q h per example (two per 32-column tile of H^)
+  int n_hap_max = 0;  // partial sums of |H^T H| per row for m = m_max
   // naive workspace
   float* O = nullptr;
   float* wsplit = nullptr;
@@ -58,7 +60,7 @@ struct lst_state {
   };
   std::vector<GraphEntry> graphs;
   uint64_t graph_clock = 0;
-  int use_graphs = 1;
+  int use_graphs = 0;  // direct launches: graph replay adds device-side gaps between steps
   hipStream_t cap = nullptr;  // capture stream
   // profiling: two events per phase per profiled step
   int prof = 0;
@@ -240,6 +242,13 @@ int check_step_args(lst_state* s, int32_t m, int32_t K, const float* H, const in
   return LST_OK;
 }
 
+// Partial sums of |H^T H| per row written by the first GEMM: two per tile
+// column that holds columns of H^T H (Z0 columns [3d, 3d + m)).
+int hap_count(int d, int m) {
+  const int first = 3 * d / kLaunch1Tile, end = (3 * d + m + kLaunch1Tile - 1) / kLaunch1Tile;
+  return 2 * (end - first);
+}
+
 // LDS stages of a launch's GEMM tiles: one per K chunk of the longest problem
 // (every chunk issued before the first multiply), at most max_stages.
 constexpr int kMaxStages = 9;
@@ -272,6 +281,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
   c.G = s->G; c.Yh = s->Yh; c.NP = s->NP; c.aH = s->aH; c.bH = s->bH;
   c.X = s->X; c.T = s->T; c.UHa = s->UHa;
   c.c1p = s->c1p; c.ld_c1p = s->n_c1p; c.n_c1p = s->n_c1p;
+  c.hap = s->hap; c.n_hap = hap_count(d, m);
   c.a = s->a; c.b = s->b; c.cs = s->cs; c.yyd = s->yyd;
   c.loss = loss; c.grad = grad_H;
   c.ex_row = s->ex_row; c.ex_val = s->ex_val; c.ex_cnt = s->ex_cnt;
@@ -289,6 +299,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     p1 = gemm_problem(L_NT, m, 3 * d + m, d, vmat(H, d, m), vmat2(s->state, d, 3 * d, H, d, m),
                       s->Z0, s->ld0, 1.f, 0.f, EPI_STORE);
     p1.dotp = s->c1p; p1.ld_dotp = s->n_c1p; p1.dot_ncols = d;  // h_i^T H^_i partials
+    p1.absp = s->hap; p1.ld_absp = c.n_hap; p1.abs_col0 = 3 * d;  // |H^T H| row partials
     p1.dot_h = H; p1.ld_doth = d;
     L.lk = 1;
     L.timing_slot = 0;
@@ -408,6 +419,7 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
   if (rc != LST_OK) return fail(rc);
   s->ld0 = (3 * d + m + 3) / 4 * 4;
   s->n_c1p = 2 * ((d + kLaunch1Tile - 1) / kLaunch1Tile);
+  s->n_hap_max = hap_count(d, m);
   s->hbits = 1;
   while ((1 << s->hbits) < 2 * m * K) ++s->hbits;
   const int hsize = 1 << s->hbits;
@@ -424,7 +436,8 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       (rc = dalloc(s, &s->hmin, hsize)) || (rc = dalloc(s, &s->touched, (size_t)m * K)) ||
       (rc = dalloc(s, &s->own, (size_t)m * K)) || (rc = dalloc(s, &s->count, 1)) ||
       (rc = dalloc(s, &s->UHa, md)) || (rc = dalloc(s, &s->yyd, m)) ||
-      (rc = dalloc(s, &s->c1p, (size_t)m * s->n_c1p)))
+      (rc = dalloc(s, &s->c1p, (size_t)m * s->n_c1p)) ||
+      (rc = dalloc(s, &s->hap, (size_t)m * s->n_hap_max)))
     return fail(rc);
   if (fill_ints(s->hkey, -1, hsize, s->stream) != hipSuccess ||
       fill_ints(s->hmin, 0x7fffffff, hsize, s->stream) != hipSuccess)

@@ -72,6 +72,11 @@ struct GemmProblem {
   float* dotp; int ld_dotp;
   int dot_ncols;
   const float* dot_h; int ld_doth;
+  // EPI_STORE only: per-row partial sums of |C| over the output columns
+  // >= abs_col0, one per (tile column, wave column) from the tile column
+  // abs_col0 / tile on: absp[row * ld_absp + 2 * (tile_n - abs_col0 / tile) + wave_n].
+  float* absp; int ld_absp;
+  int abs_col0;
 };
 
 constexpr int kMaxProblems = 4;
@@ -123,6 +128,8 @@ struct StepCtx {
   float *aH, *bH;     // m x d: a_i h_i^T and b_i h_i^T
   float* c1p;         // m x ld_c1p: partial sums of h_i^T Q h_i (from launch 1)
   int ld_c1p, n_c1p;  // row stride and number of partials per example
+  float* hap;         // m x n_hap: partial sums of |H^T H| along row i (from launch 1)
+  int n_hap;
   float *a, *b, *cs;  // per example
   float* yyd;         // per example: (Y^T Y)_ii
   float *loss, *grad;

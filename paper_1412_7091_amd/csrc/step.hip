@@ -476,11 +476,18 @@ __device__ void gj_augmented(TT* A, int lda, int m, int ncol, double* colk, doub
 // Row stride (floats) of the solve's column blocks B^T, Y^T (padded).
 __host__ __device__ inline int solve_lde(int mp) { return mp + 4; }
 
+// Floats of the LDS copy of the |H^T H| row partials (m <= 128): at most
+// 2 (ceil(m / 32) + 1) per row, rounded up to whole 64-float transfers.
+__host__ __device__ inline int solve_ha_floats(int m) {
+  return (m * (2 * ((m + 31) / 32) + 2) + 63) / 64 * 64;
+}
+
 __host__ __device__ inline size_t solve_lds_bytes(int m) {
   const int mp = (m + 15) & ~15;
   const int lde = solve_lde(mp);
   const size_t neumann =
-      (size_t)(mp + 3 * kSolveCols * lde + (m <= 128 ? mp * mp : 0)) * sizeof(float);
+      (size_t)(mp + 3 * kSolveCols * lde + (m <= 128 ? mp * mp + solve_ha_floats(m) : 0)) *
+      sizeof(float);
   const size_t gj = m <= 128 ? (size_t)m * (m + kSolveCols) * sizeof(double) : 0;
   const size_t extra = 256 * sizeof(float) + 512 * sizeof(double) + 64;  // red, colk, scalars
   return (neumann > gj ? neumann : gj) + extra;
@@ -519,28 +526,43 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   float* Y0 = Bt + kSolveCols * LDE;                   // kSolveCols x LDE: Y^T
   float* Y1 = Y0 + kSolveCols * LDE;
   float* Hs = Y1 + kSolveCols * LDE;                   // mp x mp: H^T H (SMALL only)
+  float* Ha = Hs + mp * mp;                            // m x n_hap: |H^T H| row partials (SMALL)
 
   for (int i = tid; i < mp; i += 256) cinv[i] = (i < m) ? c.lr * example_a(c, i) : 0.f;
   if (tid == 0) s_int[1] = 0;
   LST_SMARK(1);
-  // This block's columns of P^T (registers; for m <= 128 they are fetched now,
-  // together with H^T H, and used once the branch below is known).
-  float pv[8];
-  // H^T H in LDS (m <= 128): mp rows of mp floats, the 16-byte slot s of row j
-  // stored at slot s ^ (j & hsw) (bank-conflict-free reads down a column and
-  // across 16 rows); rows and columns beyond m are zero.
+  // r = ||E||_inf with E = diag(1/c) H^T H; the absolute row sums of H^T H
+  // come as partials from the first GEMM.  For m <= 128 this block's columns
+  // of P and the partials are fetched first, H^T H (into LDS) after them, and
+  // r and the right-hand side are formed while H^T H is still arriving.
+  // H^T H in LDS: mp rows of mp floats, the 16-byte slot s of row j stored at
+  // slot s ^ (j & hsw) (bank-conflict-free reads down a column and across 16
+  // rows); rows and columns beyond m are zero.
   const int hsw = (mp % 32 == 0) ? 7 : 3;  // the XOR must stay inside a row's mp/4 slots
+  float* Pb = Y1;  // m <= 128: P block as Pb[i * kSolveCols + cc] (Y1 is free until the iterations)
+  float rmax = 0.f;
   if (SMALL) {
+    const float* zero = g_dma_zero;
+    const unsigned pb = lds_u32(Pb), hb = lds_u32(Ha);
+    for (int q = wave; q < mp * kSolveCols / 64; q += 4) {
+      const int e = 64 * q + lane, i = e / kSolveCols, cc = e % kSolveCols;
+      dma4((i < m && c0 + cc < d) ? P + (size_t)i * ldp + c0 + cc : zero, pb + 256u * q);
+    }
+    const int nha = m * c.n_hap;
+    for (int q = wave; 64 * q < nha; q += 4) {
+      const int e = 64 * q + lane;
+      dma4(e < nha ? c.hap + e : zero, hb + 256u * q);
+    }
+    int nbig = 0;  // this wave's H^T H transfers still in flight below
     const int q4 = mp / 4;  // slots per row
     const bool vec4 = (ldh % 4 == 0) && (((uintptr_t)HH & 15) == 0) && (m % 4 == 0);
     if (vec4) {
       // 16-byte DMA: instruction q fills slots [64 q, 64 q + 64) of the matrix
-      const unsigned hb = lds_u32(Hs);
-      const float* zero = g_dma_zero;
-      for (int q = wave; q < mp * q4 / 64; q += 4) {
+      const unsigned hh = lds_u32(Hs);
+      for (int q = wave; q < mp * q4 / 64; q += 4, ++nbig) {
         const int e = 64 * q + lane;
         const int j = e / q4, col = 4 * ((e % q4) ^ (j & hsw));
-        dma16((j < m && col < m) ? HH + (size_t)j * ldh + col : zero, hb + 1024u * q);
+        dma16((j < m && col < m) ? HH + (size_t)j * ldh + col : zero, hh + 1024u * q);
       }
     } else {
       for (int e0 = 0; e0 < mp * q4; e0 += 256 * 4) {
@@ -571,95 +593,58 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
         }
       }
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int e = tid + 256 * u;
-      const int i = min(e / kSolveCols, m - 1), cc = min(c0 + e % kSolveCols, d - 1);
-      pv[u] = P[(size_t)i * ldp + cc];
-    }
-    wait_vm_le(0);
-  }
-  lds_barrier();
-  LST_SMARK(2);
-  // r = ||E||_inf with E = diag(1/c) H^T H, and max |S_ij| for the fallback's
-  // pivot threshold.  H^T H is symmetric, so the absolute sum of its row i is
-  // that of column i: consecutive threads walk down consecutive columns (two
-  // halves of the rows per column when m <= 128, added in a fixed order).
-  float rmax = 0.f, amax = 0.f;
-  if (SMALL) {
-    float* psum = Y1;            // 2 x mp partial sums (Y1 is free until the iterations)
-    float* pmax = Y1 + 2 * mp;   // 2 x mp partial maxima
-    const int half = (m + 1) / 2;
-    for (int p = tid; p < 2 * mp; p += 256) {
-      const int i = p % mp, hf = p / mp;
-      float sabs = 0.f, hmax = 0.f;
-      if (i < m) {
-        const float ci = 1.f / cinv[i];
-        const int j1 = hf ? m : half;
-#pragma unroll 8
-        for (int j = hf * half; j < j1; ++j) {
-          const float h = Hs[j * mp + 4 * ((i >> 2) ^ (j & hsw)) + (i & 3)];
-          sabs += fabsf(h);
-          hmax = fmaxf(hmax, fabsf(h - (i == j ? ci : 0.f)));
-        }
-      }
-      psum[hf * mp + i] = sabs;
-      pmax[hf * mp + i] = hmax;
-    }
-    __syncthreads();
+    wait_vm_le(nbig);  // the P block and the partials (issued first) have landed
+    lds_barrier();
+    LST_SMARK(2);
     for (int i = tid; i < m; i += 256) {
-      const float ri = (psum[i] + psum[mp + i]) * cinv[i];
-      rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
-      amax = fmaxf(amax, fmaxf(pmax[i], pmax[mp + i]));
-    }
-  } else {
-    for (int i = tid; i < m; i += 256) {
-      const float ci = 1.f / cinv[i];
-      float sabs = 0.f, hmax = 0.f;
-#pragma unroll 8
-      for (int j = 0; j < m; ++j) {
-        const float h = HH[(size_t)j * ldh + i];
-        sabs += fabsf(h);
-        hmax = fmaxf(hmax, fabsf(h - (i == j ? ci : 0.f)));
-      }
+      float sabs = 0.f;
+      for (int p = 0; p < c.n_hap; ++p) sabs += Ha[i * c.n_hap + p];
       const float ri = sabs * cinv[i];
       rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
-      amax = fmaxf(amax, hmax);
+    }
+  } else {
+    LST_SMARK(2);
+    for (int i = tid; i < m; i += 256) {
+      float sabs = 0.f;
+      for (int p = 0; p < c.n_hap; ++p) sabs += c.hap[(size_t)i * c.n_hap + p];
+      const float ri = sabs * cinv[i];
+      rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
     }
   }
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    rmax = fmaxf(rmax, __shfl_xor(rmax, off));
-    amax = fmaxf(amax, __shfl_xor(amax, off));
-  }
-  if (lane == 0) {
-    red[wave] = rmax;
-    red[4 + wave] = amax;
-  }
+  for (int off = 32; off > 0; off >>= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, off));
+  if (lane == 0) red[wave] = rmax;
   __syncthreads();
   const float r = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  const float smax = fmaxf(fmaxf(red[4], red[5]), fmaxf(red[6], red[7]));
   LST_SMARK(3);
 
   if (r < 0.5f) {
     // B^T = -(P^T_blk) diag(1/c)^T, Y0 = B^T.
-    for (int e0 = 0; e0 < kSolveCols * mp; e0 += 256 * 8) {
-      if (!SMALL) {  // (m <= 128: fetched above, and one pass covers all)
+    if (SMALL) {
+      for (int e = tid; e < kSolveCols * mp; e += 256) {
+        const int i = e / kSolveCols, cc = e - i * kSolveCols;
+        const float v = (i < m) ? -Pb[e] * cinv[i] : 0.f;  // Pb is zero past column d
+        Bt[cc * LDE + i] = v;
+        Y0[cc * LDE + i] = v;
+      }
+    } else {
+      for (int e0 = 0; e0 < kSolveCols * mp; e0 += 256 * 8) {
+        float pv[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
           const int e = e0 + tid + 256 * u;
           const int i = min(e / kSolveCols, m - 1), cc = min(c0 + e % kSolveCols, d - 1);
           pv[u] = P[(size_t)i * ldp + cc];
         }
-      }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int e = e0 + tid + 256 * u;
-        if (e < kSolveCols * mp) {
-          const int i = e / kSolveCols, cc = e - i * kSolveCols;
-          const float v = (i < m && c0 + cc < d) ? -pv[u] * cinv[i] : 0.f;
-          Bt[cc * LDE + i] = v;
-          Y0[cc * LDE + i] = v;
+        for (int u = 0; u < 8; ++u) {
+          const int e = e0 + tid + 256 * u;
+          if (e < kSolveCols * mp) {
+            const int i = e / kSolveCols, cc = e - i * kSolveCols;
+            const float v = (i < m && c0 + cc < d) ? -pv[u] * cinv[i] : 0.f;
+            Bt[cc * LDE + i] = v;
+            Y0[cc * LDE + i] = v;
+          }
         }
       }
     }
@@ -670,7 +655,8 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
       if (iters < 0) iters = 0;
       if (iters > 64) iters = 64;
     }
-    __syncthreads();
+    if (SMALL) wait_vm_le(0);  // H^T H has landed
+    lds_barrier();
     LST_SMARK(4);
 #ifdef LST_TIMING
     if (threadIdx.x == 0 && local < 64) g_solve_marks[local][7] = (unsigned long long)iters;
@@ -707,25 +693,31 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
       floatx4 acc[RBW];
 #pragma unroll
       for (int t = 0; t < RBW; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-      float4 fb0, fb1, fa0[RBW], fa1[RBW];
-      auto mma = [&](const float4& fb, const float4 (&fa)[RBW]) {
+      constexpr int NB = 3;
+      float4 fb[NB], fa[NB][RBW];
+      // Every wave multiplies all RBW of its row blocks (a block past the last
+      // reads a clamped one and is never stored): the waves run side by side,
+      // so the extra MFMAs cost no time and the loop carries no branches.
+      auto mma = [&](const float4& b, const float4 (&a)[RBW]) {
 #pragma unroll
         for (int t = 0; t < RBW; ++t) {
-          if (wave + 4 * t >= nrb) break;
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[t].x, fb.x, acc[t], 0, 0, 0);
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[t].y, fb.y, acc[t], 0, 0, 0);
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[t].z, fb.z, acc[t], 0, 0, 0);
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[t].w, fb.w, acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].x, b.x, acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].y, b.y, acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].z, b.z, acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].w, b.w, acc[t], 0, 0, 0);
         }
       };
-      // fragments of slice s + 1 are read while slice s is multiplied
-      frag(Yo, 0, fb0, fa0);
-      for (int kk = 0; kk < mp; kk += 32) {
-        frag(Yo, min(kk + 16, mp - 16), fb1, fa1);
-        mma(fb0, fa0);
-        if (kk + 16 >= mp) break;
-        frag(Yo, min(kk + 32, mp - 16), fb0, fa0);
-        mma(fb1, fa1);
+      // Three fragment buffers rotate: slice s + 1 is read while slice s is
+      // multiplied, into the buffer of slice s - 2 (whose MFMAs are done).
+      const int nsl = mp / 16;
+      frag(Yo, 0, fb[0], fa[0]);
+      for (int sl = 0; sl < nsl; sl += NB) {
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          if (sl + j >= nsl) break;
+          frag(Yo, min(sl + j + 1, nsl - 1) * 16, fb[(j + 1) % NB], fa[(j + 1) % NB]);
+          mma(fb[j], fa[j]);
+        }
       }
       const int col = lane & 15;
 #pragma unroll
@@ -753,11 +745,25 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   }
 
   // Fallback: Gauss-Jordan on [S | P^T_blk], S = H^T H - diag(c).  c_i moves
-  // to colk first: the fp64 matrix overwrites the buffers that hold 1/c_i.
+  // to colk first: the fp64 matrix overwrites the buffers that hold 1/c_i
+  // (and the LDS copy of H^T H, whose transfer must have landed first).  The
+  // pivot threshold scales with max |S_ij|.
   const int ncol = m + kSolveCols;
-  const double tiny = 1e-13 * (double)smax;
+  if (SMALL) wait_vm_le(0);
+  float amax = 0.f;
+  for (int e = tid; e < m * m; e += 256) {
+    const int i = e / m, j = e - i * m;
+    const float ci = 1.f / cinv[i];
+    amax = fmaxf(amax, fabsf(HH[(size_t)i * ldh + j] - (i == j ? ci : 0.f)));
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
+  __syncthreads();  // every wave has read red[0..3] (r) above
+  if (lane == 0) red[4 + wave] = amax;
   for (int i = tid; i < m; i += 256) colk[i] = 1.0 / (double)cinv[i];
   __syncthreads();
+  const float smax = fmaxf(fmaxf(red[4], red[5]), fmaxf(red[6], red[7]));
+  const double tiny = 1e-13 * (double)smax;
   if (SMALL) {
     double* A = reinterpret_cast<double*>(sraw);  // aliases the Neumann buffers
     for (int e = tid; e < m * ncol; e += 256) {
@@ -956,7 +962,7 @@ struct LaunchMasks {
 };
 constexpr LaunchMasks kLaunchMasks[5] = {
     {0u, 0u, 0u, 0u},
-    {(1u << TK_GEMM) | (1u << TK_TARGETS), V_NT, 1u << EPI_STORE, TILE32},
+    {(1u << TK_GEMM) | (1u << TK_TARGETS), V_NT, (1u << EPI_STORE) | (1u << EPX_ROWSUMS), TILE32},
     {(1u << TK_GEMM) | (1u << TK_SOLVE) | (1u << TK_YY) | (1u << TK_SCALARS), V_NN | V_NT,
      1u << EPI_STORE, TILE32},
     {(1u << TK_GEMM) | (1u << TK_SCATTER), V_NN, 1u << EPI_GRADT, TILE32},
@@ -1010,9 +1016,19 @@ __global__ __launch_bounds__(256) void step_kernel(StepCtx c, StepLaunch L) {
 #ifdef LST_TIMING
   __syncthreads();
   if (threadIdx.x == 0 && blk < 8192) {
+    // kind | GEMM problem + 1 << 4 | HW_ID << 8 | XCC_ID << 40
+    unsigned long long tag = (unsigned long long)L.kind[t];
+    if (L.kind[t] == TK_GEMM) {
+      const int tt = xcd_tile(local, L.gemm.total_tiles);
+      int q = 0;
+      while (q + 1 < L.gemm.np && tt >= L.gemm.p[q + 1].tile_begin) ++q;
+      tag |= (unsigned long long)(q + 1) << 4;
+    }
+    tag |= (unsigned long long)(unsigned)__builtin_amdgcn_s_getreg((31 << 11) | 4) << 8;
+    tag |= (unsigned long long)((unsigned)__builtin_amdgcn_s_getreg((3 << 11) | 20) & 15u) << 40;
     g_step_times[L.timing_slot & 3][blk][0] = t0;
     g_step_times[L.timing_slot & 3][blk][1] = wall_clock64();
-    g_step_times[L.timing_slot & 3][blk][2] = (unsigned long long)L.kind[t];
+    g_step_times[L.timing_slot & 3][blk][2] = tag;
   }
 #endif
 }
@@ -1112,7 +1128,9 @@ hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t 
       for (int q = 0; q < L.gemm.np; ++q) {
         const GemmProblem& p = L.gemm.p[q];
         const unsigned tbit = (p.tile == 64) ? TILE64 : (p.tile == 32 || p.tile == 0) ? TILE32 : 0u;
-        if (!(M.vars & problem_variant(p)) || !((M.epis >> p.epi) & 1u) || !(M.tiles & tbit))
+        const bool rowsums = (p.dotp != nullptr || p.absp != nullptr);
+        if (!(M.vars & problem_variant(p)) || !((M.epis >> p.epi) & 1u) || !(M.tiles & tbit) ||
+            (rowsums && (p.epi != EPI_STORE || !((M.epis >> EPX_ROWSUMS) & 1u))))
           return hipErrorInvalidValue;
       }
       n = tiles_of(L.gemm);

@@ -168,6 +168,7 @@ def test_graph_replay_matches_eager(gpu_lib):
         dev = torch.device("cuda:0")
         V0 = torch.from_numpy(wl.init_V()).to(dev)
         layers = [lst.FactoredOutputLayer(V0, loss=loss, m_max=cfg.m, K_max=cfg.K) for _ in range(2)]
+        layers[0].set_graphs(True)
         layers[1].set_graphs(False)
         bufs = [tuple(torch.from_numpy(x).to(dev) for x in wl.batch(s)) for s in range(3)]
         outs = [[], []]
