@@ -444,6 +444,17 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
       if (Accum<T>::NS == 2) acc[i][j] += acs.v[Accum<T>::NS - 1][i][j];
     }
 
+  // The epilogue's operands were fetched before the K loop.  Waiting for them
+  // here, once, keeps the waits out of the stores below: the compiler would
+  // otherwise wait at each element's first use, and on this chip those waits
+  // also wait for every store issued before them.
+#pragma unroll
+  for (int i = 0; i < IB; ++i)
+#pragma unroll
+    for (int j = 0; j < IB; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) asm volatile("" ::"v"(pre1[i][j][r]), "v"(pre2[i][j][r]));
+
   LST_MARK(3);
   // Element r of acc[i][j]: row 4*(lane/16) + r, column lane % 16 of its 16 x 16 block.
   float dsum[IB][4], asum[IB][4];
@@ -550,7 +561,7 @@ template <unsigned TILES, int W, unsigned VARS, unsigned EPIS>
 __device__ __forceinline__ void panel_tile(const GemmBatch& bt, int t, float* smem) {
   t = xcd_tile(t, bt.total_tiles);
   int q = 0;
-  while (q + 1 < bt.np && t >= bt.p[q + 1].tile_begin) ++q;
+  while (q + 1 < bt.np && t >= bt.tile_begins[q + 1]) ++q;
   if (bt.skip_updates_if && q >= bt.first_update && *bt.skip_updates_if) return;
   // A private copy: the inline-asm memory clobbers of the pipeline would
   // otherwise make every use re-read the descriptor from kernel arguments.

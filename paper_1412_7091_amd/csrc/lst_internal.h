@@ -82,15 +82,19 @@ struct GemmProblem {
 constexpr int kMaxProblems = 4;
 
 struct GemmBatch {
-  GemmProblem p[kMaxProblems];
+  // Header first: a block finds its problem and its options from these
+  // without touching the (large) problem descriptors, whose kernel-argument
+  // lines it would otherwise fetch one after another.
   int np;
   int total_tiles;
-  const int* skip_if;  // nonzero *skip_if: every block returns at once
-  const int* run_if;   // zero *run_if: every block returns at once
-  const int* skip_updates_if;  // nonzero: blocks of problems >= first_update return at once
-  int first_update;
+  int tile_begins[kMaxProblems + 1];  // first tile of each problem; [np] = total_tiles
   int stages;                  // LDS stages of the K pipeline (>= 2)
   int timing_slot;             // record of per-block phase times (builds with LST_TIMING only)
+  int first_update;
+  const int* skip_if;          // nonzero *skip_if: every block returns at once
+  const int* run_if;           // zero *run_if: every block returns at once
+  const int* skip_updates_if;  // nonzero: blocks of problems >= first_update return at once
+  GemmProblem p[kMaxProblems];
 };
 
 // One-time kernel attribute setup (dynamic LDS limits); call before any launch.

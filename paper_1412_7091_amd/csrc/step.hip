@@ -77,24 +77,31 @@ __host__ __device__ inline size_t targets_lds_bytes(int K) {
   return (size_t)4 * K * (sizeof(unsigned long long) + sizeof(float));
 }
 
-// One batch of the gather: rows of slots k0 .. k0+7 (weights wv, 0 for slots
-// past K or without a valid target), columns cb + 256 h + 4 lane, h < 2.
+// Slots per batch of the gather: one batch covers K <= 16.
+constexpr int kGatherRows = 16;
+
+// One batch of the gather: rows of slots k0 .. k0 + kGatherRows - 1 (weights
+// wv, 0 for slots past K or without a valid target), columns cb + 256 h +
+// 4 lane, h < 2.  VEC: d % 4 == 0 (16-byte loads).  Every key is read from
+// LDS before the first row is requested, and slots past K request nothing.
+template <bool VEC>
 __device__ __forceinline__ void gather_load(const StepCtx& c, const unsigned long long* keys,
-                                            const float* vals, int k0, int cb, float4 (&rv)[8][2],
-                                            float (&wv)[8]) {
+                                            const float* vals, int k0, int cb,
+                                            float4 (&rv)[kGatherRows][2], float (&wv)[kGatherRows]) {
   const int K = c.K, d = c.d, lane = lane_id();
-  const bool vec = (d % 4 == 0);
+  unsigned long long key[kGatherRows];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int k = min(k0 + u, K - 1);
-    const unsigned long long key = keys[k];
-    const bool use = (k0 + u < K) && key != kNoKey;
-    wv[u] = use ? vals[k] : 0.f;
-    const float* row = c.V + (size_t)(use ? (unsigned)(key >> 32) : 0u) * d;
+  for (int u = 0; u < kGatherRows; ++u) key[u] = keys[min(k0 + u, K - 1)];
+#pragma unroll
+  for (int u = 0; u < kGatherRows; ++u) {
+    const bool use = (k0 + u < K) && key[u] != kNoKey;
+    wv[u] = use ? vals[min(k0 + u, K - 1)] : 0.f;
+    if (k0 + u >= K) continue;  // uniform: K is the same for every lane
+    const float* row = c.V + (size_t)(use ? (unsigned)(key[u] >> 32) : 0u) * d;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int col = min(cb + 256 * h + 4 * lane, vec ? d - 4 : d - 1);
-      if (vec) {
+      const int col = min(cb + 256 * h + 4 * lane, VEC ? d - 4 : d - 1);
+      if (VEC) {
         rv[u][h] = *reinterpret_cast<const float4*>(row + col);
       } else {
         rv[u][h].x = row[col];
@@ -106,10 +113,10 @@ __device__ __forceinline__ void gather_load(const StepCtx& c, const unsigned lon
   }
 }
 
-__device__ __forceinline__ void gather_add(const float4 (&rv)[8][2], const float (&wv)[8],
-                                           float4 (&acc)[2]) {
+__device__ __forceinline__ void gather_add(const float4 (&rv)[kGatherRows][2],
+                                           const float (&wv)[kGatherRows], float4 (&acc)[2]) {
 #pragma unroll
-  for (int u = 0; u < 8; ++u)
+  for (int u = 0; u < kGatherRows; ++u)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       // unused slots add nothing (not even a non-finite value of row 0)
@@ -133,6 +140,7 @@ __device__ unsigned long long g_target_marks[64][6];
   } while (0)
 #endif
 
+template <bool VEC>
 __device__ __forceinline__ void task_targets(const StepCtx& c, int local, unsigned char* sraw) {
   const int w = wave_id(), lane = lane_id();
   const int i = local * 4 + w;
@@ -166,9 +174,9 @@ __device__ __forceinline__ void task_targets(const StepCtx& c, int local, unsign
   LST_TMARK(1);
   // The first rows of V are requested now and used after the ordering below,
   // whose latency they overlap.
-  float4 rv[8][2];
-  float wv[8];
-  gather_load(c, keys, vals, 0, 0, rv, wv);
+  float4 rv[kGatherRows][2];
+  float wv[kGatherRows];
+  gather_load<VEC>(c, keys, vals, 0, 0, rv, wv);
 
   LST_TMARK(2);
   float yy = 0.f;
@@ -203,20 +211,19 @@ __device__ __forceinline__ void task_targets(const StepCtx& c, int local, unsign
 
   LST_TMARK(3);
   // G_i = sum_k y_ik V[r_ik, :]: lane l owns columns cb + 256 h + 4 l, slots
-  // in order, 8 rows (16 loads) in flight.
-  const bool vec = (d % 4 == 0);
+  // in order, kGatherRows rows (2 kGatherRows loads) in flight.
   float* gout = c.G + (size_t)i * d;
   for (int cb = 0; cb < d; cb += 512) {
     float4 acc[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
-    for (int k0 = 0; k0 < K; k0 += 8) {
-      if (cb > 0 || k0 > 0) gather_load(c, keys, vals, k0, cb, rv, wv);
+    for (int k0 = 0; k0 < K; k0 += kGatherRows) {
+      if (cb > 0 || k0 > 0) gather_load<VEC>(c, keys, vals, k0, cb, rv, wv);
       gather_add(rv, wv, acc);
     }
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int col = cb + 256 * h + 4 * lane;
       if (col >= d) continue;
-      if (vec) {
+      if (VEC) {
         *reinterpret_cast<float4*>(gout + col) = acc[h];
       } else {
         gout[col] = acc[h].x;
@@ -983,7 +990,13 @@ __device__ __forceinline__ void run_task(const StepCtx& c, const StepLaunch& L, 
     }
   }
   if constexpr ((M.tasks >> TK_TARGETS) & 1u) {
-    if (kind == TK_TARGETS) { task_targets(c, local, sraw); return; }
+    if (kind == TK_TARGETS) {
+      if (c.d % 4 == 0)
+        task_targets<true>(c, local, sraw);
+      else
+        task_targets<false>(c, local, sraw);
+      return;
+    }
   }
   if constexpr ((M.tasks >> TK_YY) & 1u) {
     if (kind == TK_YY) { task_yy(c, local, sraw); return; }
@@ -1021,7 +1034,7 @@ __global__ __launch_bounds__(256) void step_kernel(StepCtx c, StepLaunch L) {
     if (L.kind[t] == TK_GEMM) {
       const int tt = xcd_tile(local, L.gemm.total_tiles);
       int q = 0;
-      while (q + 1 < L.gemm.np && tt >= L.gemm.p[q + 1].tile_begin) ++q;
+      while (q + 1 < L.gemm.np && tt >= L.gemm.tile_begins[q + 1]) ++q;
       tag |= (unsigned long long)(q + 1) << 4;
     }
     tag |= (unsigned long long)(unsigned)__builtin_amdgcn_s_getreg((31 << 11) | 4) << 8;
@@ -1052,6 +1065,7 @@ static int tiles_of(GemmBatch& b) {
     p.tiles_m = (p.M + p.tile - 1) / p.tile;
     p.tiles_n = (p.N + p.tile - 1) / p.tile;
     p.tile_begin = total;
+    b.tile_begins[q] = total;
     if (p.ksplit < 1) p.ksplit = 1;
     if (p.epi == EPI_SYM)
       total += p.tiles_m * (p.tiles_m + 1) / 2;
@@ -1059,6 +1073,7 @@ static int tiles_of(GemmBatch& b) {
       total += p.tiles_m * p.tiles_n * (p.epi == EPI_PARTIAL ? p.ksplit : 1);
   }
   b.total_tiles = total;
+  b.tile_begins[b.np] = total;
   return total;
 }
 
