@@ -483,18 +483,11 @@ __device__ void gj_augmented(TT* A, int lda, int m, int ncol, double* colk, doub
 // Row stride (floats) of the solve's column blocks B^T, Y^T (padded).
 __host__ __device__ inline int solve_lde(int mp) { return mp + 4; }
 
-// Floats of the LDS copy of the |H^T H| row partials (m <= 128): at most
-// 2 (ceil(m / 32) + 1) per row, rounded up to whole 64-float transfers.
-__host__ __device__ inline int solve_ha_floats(int m) {
-  return (m * (2 * ((m + 31) / 32) + 2) + 63) / 64 * 64;
-}
-
 __host__ __device__ inline size_t solve_lds_bytes(int m) {
   const int mp = (m + 15) & ~15;
   const int lde = solve_lde(mp);
   const size_t neumann =
-      (size_t)(mp + 3 * kSolveCols * lde + (m <= 128 ? mp * mp + solve_ha_floats(m) : 0)) *
-      sizeof(float);
+      (size_t)(mp + 3 * kSolveCols * lde + (m <= 128 ? mp * mp : 0)) * sizeof(float);
   const size_t gj = m <= 128 ? (size_t)m * (m + kSolveCols) * sizeof(double) : 0;
   const size_t extra = 256 * sizeof(float) + 512 * sizeof(double) + 64;  // red, colk, scalars
   return (neumann > gj ? neumann : gj) + extra;
@@ -533,7 +526,6 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   float* Y0 = Bt + kSolveCols * LDE;                   // kSolveCols x LDE: Y^T
   float* Y1 = Y0 + kSolveCols * LDE;
   float* Hs = Y1 + kSolveCols * LDE;                   // mp x mp: H^T H (SMALL only)
-  float* Ha = Hs + mp * mp;                            // m x n_hap: |H^T H| row partials (SMALL)
 
   for (int i = tid; i < mp; i += 256) cinv[i] = (i < m) ? c.lr * example_a(c, i) : 0.f;
   if (tid == 0) s_int[1] = 0;
@@ -546,32 +538,15 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   // slot s ^ (j & hsw) (bank-conflict-free reads down a column and across 16
   // rows); rows and columns beyond m are zero.
   const int hsw = (mp % 32 == 0) ? 7 : 3;  // the XOR must stay inside a row's mp/4 slots
-  float* Pb = Y1;  // m <= 128: P block as Pb[i * kSolveCols + cc] (Y1 is free until the iterations)
-  float rmax = 0.f;
+  float r;
   if (SMALL) {
+    // Waves 2 and 3 fetch this block's columns of P and the partial sums
+    // first (plain loads, waited for by them alone), then form r and the
+    // right-hand side; waves 0 and 1 move H^T H meanwhile.
     const float* zero = g_dma_zero;
-    const unsigned pb = lds_u32(Pb), hb = lds_u32(Ha);
-    for (int q = wave; q < mp * kSolveCols / 64; q += 4) {
-      const int e = 64 * q + lane, i = e / kSolveCols, cc = e % kSolveCols;
-      dma4((i < m && c0 + cc < d) ? P + (size_t)i * ldp + c0 + cc : zero, pb + 256u * q);
-    }
-    const int nha = m * c.n_hap;
-    for (int q = wave; 64 * q < nha; q += 4) {
-      const int e = 64 * q + lane;
-      dma4(e < nha ? c.hap + e : zero, hb + 256u * q);
-    }
-    int nbig = 0;  // this wave's H^T H transfers still in flight below
     const int q4 = mp / 4;  // slots per row
     const bool vec4 = (ldh % 4 == 0) && (((uintptr_t)HH & 15) == 0) && (m % 4 == 0);
-    if (vec4) {
-      // 16-byte DMA: instruction q fills slots [64 q, 64 q + 64) of the matrix
-      const unsigned hh = lds_u32(Hs);
-      for (int q = wave; q < mp * q4 / 64; q += 4, ++nbig) {
-        const int e = 64 * q + lane;
-        const int j = e / q4, col = 4 * ((e % q4) ^ (j & hsw));
-        dma16((j < m && col < m) ? HH + (size_t)j * ldh + col : zero, hh + 1024u * q);
-      }
-    } else {
+    if (!vec4) {
       for (int e0 = 0; e0 < mp * q4; e0 += 256 * 4) {
         float4 r4[4];
 #pragma unroll
@@ -600,41 +575,90 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
         }
       }
     }
-    wait_vm_le(nbig);  // the P block and the partials (issued first) have landed
-    lds_barrier();
-    LST_SMARK(2);
-    for (int i = tid; i < m; i += 256) {
-      float sabs = 0.f;
-      for (int p = 0; p < c.n_hap; ++p) sabs += Ha[i * c.n_hap + p];
-      const float ri = sabs * cinv[i];
-      rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
+    __syncthreads();  // 1 / c_i (and H^T H without DMA) visible to every wave
+    if (wave == 3) {
+      // Every load below is unconditional at a clamped (valid) address, so
+      // all of them are in flight before the first is needed; the values are
+      // masked afterwards.
+      constexpr int NPV = 128 * kSolveCols / 64;   // P elements per lane for mp = 128
+      constexpr int kMaxHap = 2 * (128 / 32 + 1);  // partials per row for m <= 128
+      float pv[NPV], hv[2][kMaxHap];
+#pragma unroll
+      for (int u = 0; u < NPV; ++u) {
+        const int e = lane + 64 * u;
+        const int i = min(e / kSolveCols, m - 1), cc = min(c0 + e % kSolveCols, d - 1);
+        pv[u] = P[(size_t)i * ldp + cc];
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int hrow = min(lane + 64 * h, m - 1);
+#pragma unroll
+        for (int p = 0; p < kMaxHap; ++p)
+          hv[h][p] = c.hap[(size_t)hrow * c.n_hap + min(p, c.n_hap - 1)];
+      }
+      __builtin_amdgcn_s_barrier();  // the H^T H transfers start after these loads
+      float rw = 0.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        float sabs = 0.f;
+#pragma unroll
+        for (int p = 0; p < kMaxHap; ++p) sabs += p < c.n_hap ? hv[h][p] : 0.f;
+        const int row = lane + 64 * h;
+        if (row < m) {
+          const float ri = sabs * cinv[row];
+          rw = (ri == ri) ? fmaxf(rw, ri) : INFINITY;
+        }
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) rw = fmaxf(rw, __shfl_xor(rw, off));
+      if (lane == 0) red[3] = rw;
+      // B^T = -(P^T_blk) diag(1/c)^T and Y0 = B^T (used when the series converges)
+#pragma unroll
+      for (int u = 0; u < NPV; ++u) {
+        const int e = lane + 64 * u, i = e / kSolveCols, cc = e % kSolveCols;
+        if (i < mp) {
+          const float v = (i < m && c0 + cc < d) ? -pv[u] * cinv[i] : 0.f;
+          Bt[cc * LDE + i] = v;
+          Y0[cc * LDE + i] = v;
+        }
+      }
+    } else {
+      __builtin_amdgcn_s_barrier();
+      if (vec4) {
+        // 16-byte DMA by waves 0-2: instruction q fills slots [64 q, 64 q + 64)
+        const unsigned hh = lds_u32(Hs);
+        for (int q = wave; q < mp * q4 / 64; q += 3) {
+          const int e = 64 * q + lane;
+          const int j = e / q4, col = 4 * ((e % q4) ^ (j & hsw));
+          dma16((j < m && col < m) ? HH + (size_t)j * ldh + col : zero, hh + 1024u * q);
+        }
+      }
+      if (lane == 0) red[wave] = 0.f;
     }
+    LST_SMARK(2);
+    wait_vm_le(0);  // H^T H has landed
+    lds_barrier();
+    r = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   } else {
     LST_SMARK(2);
+    float rmax = 0.f;
     for (int i = tid; i < m; i += 256) {
       float sabs = 0.f;
       for (int p = 0; p < c.n_hap; ++p) sabs += c.hap[(size_t)i * c.n_hap + p];
       const float ri = sabs * cinv[i];
       rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
     }
-  }
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, off));
-  if (lane == 0) red[wave] = rmax;
-  __syncthreads();
-  const float r = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    for (int off = 32; off > 0; off >>= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, off));
+    if (lane == 0) red[wave] = rmax;
+    __syncthreads();
+    r = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  }
   LST_SMARK(3);
 
   if (r < 0.5f) {
-    // B^T = -(P^T_blk) diag(1/c)^T, Y0 = B^T.
-    if (SMALL) {
-      for (int e = tid; e < kSolveCols * mp; e += 256) {
-        const int i = e / kSolveCols, cc = e - i * kSolveCols;
-        const float v = (i < m) ? -Pb[e] * cinv[i] : 0.f;  // Pb is zero past column d
-        Bt[cc * LDE + i] = v;
-        Y0[cc * LDE + i] = v;
-      }
-    } else {
+    if (!SMALL) {
+      // B^T = -(P^T_blk) diag(1/c)^T, Y0 = B^T.
       for (int e0 = 0; e0 < kSolveCols * mp; e0 += 256 * 8) {
         float pv[8];
 #pragma unroll
@@ -662,8 +686,7 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
       if (iters < 0) iters = 0;
       if (iters > 64) iters = 64;
     }
-    if (SMALL) wait_vm_le(0);  // H^T H has landed
-    lds_barrier();
+    if (!SMALL) __syncthreads();
     LST_SMARK(4);
 #ifdef LST_TIMING
     if (threadIdx.x == 0 && local < 64) g_solve_marks[local][7] = (unsigned long long)iters;
