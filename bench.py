@@ -39,20 +39,23 @@ def log(*a):
 def phase_work(name, cfg, u, nnz):
     """(algorithmic fp32 flops, algorithmic HBM bytes of V) of one launch of the step.
 
-    Flops are those of the method's dense contractions that run in the launch
-    (the symmetric Q update counted once per upper-triangle entry); bytes are
-    the rows of V the launch must touch: u distinct target rows of d floats,
-    read by the gather (launch 1) and read + written by the scatter (launch 3).
+    Flops are those of the method's products that run in the launch, 2 per
+    multiply-add, each product counted once at its algorithmic size: the
+    m x m Woodbury solve as m^3 + m^2 d (one factorisation, d right-hand
+    sides), N H^T as the m x m times m x d product it is, the symmetric Q
+    update once per upper-triangle entry.  Bytes are the rows of V the launch
+    must touch: u distinct target rows of d floats, read by the gather
+    (launch 1) and read + written by the scatter (launch 3).
     """
     D, d, m, K = cfg.D, cfg.d, cfg.m, cfg.K
     if name == "launch1":   # [Q; U; U^-T; H^T] H  +  gather of V^T Y
         return 2.0 * m * d * (3 * d + m), float(u * d * 4)
-    if name == "launch2":   # U^T G, H^T H^, H^T Y^, (H^T Y^)^T, X = S^-1 P^T
-        return 2.0 * m * d * d + 3 * 2.0 * m * m * d + 2.0 * m * m * d, 0.0
-    if name == "launch3":   # N H^T, U and U^-T rank-m updates  +  scatter into V
-        return 2.0 * m * m * d + 2 * 2.0 * d * d * m, float(2 * u * d * 4)
-    if name == "launch4":   # symmetric rank-2m update of Q
-        return 2.0 * (d * (d + 1) / 2) * 2 * m, 0.0
+    if name == "launch2":   # U^T G; H^T H^, H^T Y^ (C1, C2); X = S^-1 P^T
+        return 2.0 * (m * d * d + 2 * m * m * d + m ** 3 + m * m * d), 0.0
+    if name == "launch3":   # grad_H and T = grad_H - (lr/2) N H^T  +  scatter into V
+        return 2.0 * m * m * d, float(2 * u * d * 4)
+    if name == "launch4":   # symmetric rank-2m update of Q; rank-m updates of U and U^-T
+        return 2.0 * (d * (d + 1) / 2) * 2 * m + 2 * 2.0 * m * d * d, 0.0
     return 0.0, 0.0
 
 

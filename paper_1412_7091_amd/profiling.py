@@ -40,7 +40,7 @@ def source_digest() -> str:
 
 def launch_of(kernel_name: str) -> str | None:
     """'launch1'..'launch4' for the step kernels (last template argument), else None."""
-    m = re.search(r"step_kernel<\s*\d+\s*,\s*\w+\s*,\s*\d+\s*,\s*(\d)\s*>", kernel_name)
+    m = re.search(r"step_kernel<[^<>]*?,\s*(\d)\s*>", kernel_name)
     return f"launch{m.group(1)}" if m else None
 
 
