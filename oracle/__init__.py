@@ -14,10 +14,13 @@ Modules
             algorithm of Appendix A, the pristine restore of Appendix C), used
             only to check the paper's identities against the explicit
             definition: W = VU, Q = W^T W, U (U^{-T})^T = I.
+  stabilize Appendix C's correction of out-of-range singular values of U
+            (fix-singular-value, with a full SVD or with power iterations),
+            and the recomputation of U^{-T}.
 
 Pin status (what fixes each function other than itself) is listed in each
 function's docstring; the only function without a pin by the paper is the
 minibatch form of the spherical-softmax factored step, which is pinned by the
 explicit definition and by finite differences instead.
 """
-from . import explicit, factored  # noqa: F401
+from . import explicit, factored, stabilize  # noqa: F401

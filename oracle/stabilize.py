@@ -1,0 +1,130 @@
+"""Appendix C numerical stabilisation, plainly, in fp64 (test infrastructure only).
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+The factored state (V, U, U^{-T}, Q) of `oracle.factored` represents W = V U.
+Appendix C keeps U well conditioned without the O(D d^2) pristine restore:
+it corrects only the singular values of U that leave a safe range
+[sigma_low, sigma_high], each with a rank-one change of U, U^{-T} and V that
+leaves W = V U (hence Q = W^T W) unchanged.
+
+Functions (Appendix C, in the order the appendix introduces them)
+  fix_singular_value       the procedure that moves one singular value sigma of U,
+                           with left singular vector u, to sigma_star.
+  stabilize_svd            the appendix's procedure with a full SVD of U: every
+                           singular value outside the range is moved to 1.
+  top_left_singular_pair   the power iteration the appendix proposes instead of the
+                           SVD: the largest singular value of a d x d matrix A and
+                           its left singular vector, by x <- A A^T x / ||A A^T x||.
+  reinvert                 U^{-T} recomputed from U (the appendix does this before
+                           every check).
+  stabilize_power          the appendix's loop: find the smallest singular value of
+                           U (power iteration on U^{-T}, whose largest singular
+                           value is 1 / sigma_min(U) with the same left singular
+                           vector), correct it while it is below the range, then
+                           the same for the largest (power iteration on U).
+
+Pins: every function here is checked against numpy's SVD / inverse and the
+invariants the appendix states (W, Q unchanged; U^{-T} stays the inverse; only
+the chosen singular value moves) in tests/test_stabilize_pins.py.
+"""
+from __future__ import annotations
+
+from typing import List, Tuple
+
+import numpy as np
+
+from .factored import FactoredState
+
+
+def fix_singular_value(st: FactoredState, sigma: float, u: np.ndarray, sigma_star: float = 1.0):
+    """Move the singular value sigma of U (left singular vector u, unit norm) to sigma_star.
+
+    alpha = (sigma_star - sigma) / sigma and beta = -alpha / (1 + alpha), then
+        U      <- U + alpha u (U^T u)^T
+        V      <- V + beta (V u) u^T
+        U^{-T} <- U^{-T} + beta u (U^{-1} u)^T,  U^{-1} = (U^{-T})^T before this update.
+    With U = sum_k s_k u_k v_k^T, U^T u_k = s_k v_k, so the new U has s_k (1 + alpha)
+    = sigma_star in place of s_k and the same singular vectors; V is multiplied on
+    the right by (I + alpha u u^T)^{-1} = I + beta u u^T, so V U is unchanged.
+    Applied in place; returns (alpha, beta).
+    """
+    u = np.asarray(u, dtype=np.float64)
+    alpha = (sigma_star - sigma) / sigma
+    beta = -alpha / (1.0 + alpha)
+    Uinv = st.UinvT.T
+    w_u = st.U.T @ u
+    w_i = Uinv @ u
+    st.U = st.U + alpha * np.outer(u, w_u)
+    st.V = st.V + beta * np.outer(st.V @ u, u)
+    st.UinvT = st.UinvT + beta * np.outer(u, w_i)
+    return alpha, beta
+
+
+def stabilize_svd(st: FactoredState, sigma_low: float, sigma_high: float) -> List[int]:
+    """The appendix's procedure with a full SVD: fix every out-of-range singular value.
+
+    One SVD serves all corrections: a correction changes only its own singular
+    value, so the other singular values and vectors stay valid.  Returns the
+    indices (in decreasing-sigma order) that were corrected.
+    """
+    Ub, s, _ = np.linalg.svd(st.U)
+    fixed = []
+    for k in range(len(s)):
+        if s[k] < sigma_low or s[k] > sigma_high:
+            fix_singular_value(st, float(s[k]), Ub[:, k], 1.0)
+            fixed.append(k)
+    return fixed
+
+
+def top_left_singular_pair(A: np.ndarray, iterations: int, x0: np.ndarray
+                           ) -> Tuple[float, np.ndarray]:
+    """Power iteration for the largest singular value of A and its left singular vector.
+
+    x <- A (A^T x), normalised, `iterations` times from x0; then u = x and the
+    estimate sigma = ||A^T u|| (for an exact singular vector, A^T u = sigma v).
+    """
+    x = np.asarray(x0, dtype=np.float64)
+    x = x / np.linalg.norm(x)
+    for _ in range(iterations):
+        x = A @ (A.T @ x)
+        x = x / np.linalg.norm(x)
+    return float(np.linalg.norm(A.T @ x)), x
+
+
+def reinvert(st: FactoredState) -> None:
+    """U^{-T} <- (U^{-1})^T, computed from U itself."""
+    st.UinvT = np.linalg.inv(st.U).T
+
+
+def stabilize_power(st: FactoredState, sigma_low: float, sigma_high: float, iterations: int,
+                    max_fixes: int, x0: np.ndarray, do_reinvert: bool = True):
+    """The appendix's loop with power iterations instead of the SVD.
+
+    Optionally recompute U^{-T} first.  Then, at most max_fixes times: estimate
+    sigma_min(U) as 1 / sigma_max(U^{-T}) with u the top left singular vector of
+    U^{-T} (the left singular vector of U for sigma_min); stop when it is not
+    below sigma_low, else move it to 1.  Then the same for sigma_max(U) against
+    sigma_high.  Returns a list of (end, sigma estimate, corrected) per round,
+    end being "low" or "high".
+    """
+    rounds = []
+    if do_reinvert:
+        reinvert(st)
+    for _ in range(max_fixes):
+        s_inv, u = top_left_singular_pair(st.UinvT, iterations, x0)
+        # sigma_min(U) from the same vector: 1 / ||U^{-1} u||
+        sigma = 1.0 / float(np.linalg.norm(st.UinvT.T @ u))
+        go = sigma < sigma_low
+        rounds.append(("low", sigma, go))
+        if not go:
+            break
+        fix_singular_value(st, sigma, u, 1.0)
+    for _ in range(max_fixes):
+        sigma, u = top_left_singular_pair(st.U, iterations, x0)
+        go = sigma > sigma_high
+        rounds.append(("high", sigma, go))
+        if not go:
+            break
+        fix_singular_value(st, sigma, u, 1.0)
+    return rounds
