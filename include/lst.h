@@ -148,6 +148,66 @@ int lst_touched_rows(lst_state* s, int32_t* rows, int32_t capacity, int32_t* cou
 int lst_restore(lst_state* s);
 
 /*
+ * Appendix C, "stabilizing only problematic singular values": keep the
+ * singular values of U inside a safe range [sigma_low, sigma_high] with
+ * rank-one corrections that leave W = V U and Q unchanged, instead of the
+ * O(D d^2) pristine restore.
+ */
+typedef struct lst_stab_config {
+  float sigma_low;     /* safe range of the singular values of U; the appendix's   */
+  float sigma_high;    /* example is [0.001, 100].  0 < sigma_low <= 1 <= sigma_high */
+  int32_t squarings;   /* each estimate is 2^squarings power iterations (0..16; 7
+                          gives 128, the appendix uses 100)                        */
+  int32_t max_fixes;   /* at most this many corrections at each end of the spectrum
+                          in one call (1..16)                                      */
+  int32_t reinvert;    /* recompute U^{-T} from U: 0 never; 1 after each correction
+                          (its rank-one update of U^{-T} cancels a term of size
+                          1/sigma, costing about log10(1/sigma) digits in fp32);
+                          2 also before the search, as the appendix does before
+                          every check                                              */
+} lst_stab_config;
+
+typedef struct lst_stab_report {
+  int32_t fixes_low;   /* singular values raised to 1 (they were below sigma_low)    */
+  int32_t fixes_high;  /* singular values lowered to 1 (they were above sigma_high)  */
+  float sigma_min;     /* estimate of sigma_min(U) made by the last round at the low
+                          end (NaN if none ran); a value in range ended the rounds */
+  float sigma_max;     /* the same at the high end                                  */
+} lst_stab_report;
+
+/*
+ * lst_stabilize -- one run of the appendix's procedure on a factored state:
+ *   1. if cfg->reinvert == 2, recompute U^{-T} from U (two Newton-Schulz steps
+ *      Z <- 2Z - Z U^T Z from the current U^{-T}; they converge to the inverse
+ *      whenever ||I - Z U^T|| < 1; in fp32 the result is accurate to about
+ *      1e-7 cond(U), so with an ill-conditioned U prefer 1);
+ *   2. estimate the smallest singular value of U and its left singular vector
+ *      u by power iteration on U^{-T}; while it is below sigma_low (at most
+ *      max_fixes times) apply fix-singular-value with target 1:
+ *        alpha = (1 - sigma)/sigma, beta = -alpha/(1 + alpha),
+ *        U <- U + alpha u (U^T u)^T,  V <- V + beta (V u) u^T,
+ *        U^{-T} <- U^{-T} + beta u (U^{-1} u)^T;
+ *   3. the same for the largest singular value (power iteration on U) against
+ *      sigma_high.
+ *   With cfg->reinvert >= 1, three Newton-Schulz steps follow every correction.
+ * The power iteration starts from the vector of ones.  Every decision is taken
+ * on the device; the call enqueues its kernels on the state's stream and, with
+ * report == NULL, returns at once.  With report (host) it synchronises and
+ * fills it.  Skipped (no change) when a step error is pending.  Allocates a
+ * workspace of (2 + k) d^2 floats at its first call (k = split of the d^3 products).
+ * Errors: LST_EINVAL for a null state or config or a config outside its ranges,
+ * LST_ESTATE for a naive state, LST_ENOMEM, LST_EHIP.
+ */
+int lst_stabilize(lst_state* s, const lst_stab_config* cfg, lst_stab_report* report);
+
+/*
+ * lst_set_stabilize -- run lst_stabilize(cfg, NULL) after every `every`-th
+ * lst_step (the appendix's n_check; 0 turns it off, the default).  With
+ * HIP-graph replay the stabilisation runs outside the step's graph.
+ */
+int lst_set_stabilize(lst_state* s, int32_t every, const lst_stab_config* cfg);
+
+/*
  * lst_naive_init -- explicit-W baseline state (sections 2.3 and 3.1: the
  * O(D d) per example computation the method avoids), same library, same GEMM
  * kernels.  W (device, D x d) is copied.  Synchronous.

@@ -98,18 +98,22 @@ def reinvert(st: FactoredState) -> None:
 
 
 def stabilize_power(st: FactoredState, sigma_low: float, sigma_high: float, iterations: int,
-                    max_fixes: int, x0: np.ndarray, do_reinvert: bool = True):
+                    max_fixes: int, x0: np.ndarray, reinvert_mode: int = 1):
     """The appendix's loop with power iterations instead of the SVD.
 
-    Optionally recompute U^{-T} first.  Then, at most max_fixes times: estimate
-    sigma_min(U) as 1 / sigma_max(U^{-T}) with u the top left singular vector of
-    U^{-T} (the left singular vector of U for sigma_min); stop when it is not
-    below sigma_low, else move it to 1.  Then the same for sigma_max(U) against
-    sigma_high.  Returns a list of (end, sigma estimate, corrected) per round,
-    end being "low" or "high".
+    With reinvert_mode 2, recompute U^{-T} first (the appendix's practice).
+    Then, at most max_fixes times: estimate sigma_min(U) as 1 / sigma_max(U^{-T})
+    with u the top left singular vector of U^{-T} (the left singular vector of U
+    for sigma_min); stop when it is not below sigma_low, else move it to 1.  Then
+    the same for sigma_max(U) against sigma_high.  With reinvert_mode >= 1,
+    U^{-T} is recomputed after every correction (in exact arithmetic the
+    correction's own update of U^{-T} is already exact, so this changes nothing
+    here; it mirrors what a finite-precision implementation must do).
+    Returns a list of (end, sigma estimate, corrected) per round, end being
+    "low" or "high".
     """
     rounds = []
-    if do_reinvert:
+    if reinvert_mode >= 2:
         reinvert(st)
     for _ in range(max_fixes):
         s_inv, u = top_left_singular_pair(st.UinvT, iterations, x0)
@@ -120,6 +124,8 @@ def stabilize_power(st: FactoredState, sigma_low: float, sigma_high: float, iter
         if not go:
             break
         fix_singular_value(st, sigma, u, 1.0)
+        if reinvert_mode >= 1:
+            reinvert(st)
     for _ in range(max_fixes):
         sigma, u = top_left_singular_pair(st.U, iterations, x0)
         go = sigma > sigma_high
@@ -127,4 +133,6 @@ def stabilize_power(st: FactoredState, sigma_low: float, sigma_high: float, iter
         if not go:
             break
         fix_singular_value(st, sigma, u, 1.0)
+        if reinvert_mode >= 1:
+            reinvert(st)
     return rounds

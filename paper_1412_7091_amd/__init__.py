@@ -52,6 +52,25 @@ class lst_stats_t(ctypes.Structure):
     ]
 
 
+class lst_stab_config(ctypes.Structure):
+    _fields_ = [
+        ("sigma_low", ctypes.c_float),
+        ("sigma_high", ctypes.c_float),
+        ("squarings", ctypes.c_int32),
+        ("max_fixes", ctypes.c_int32),
+        ("reinvert", ctypes.c_int32),
+    ]
+
+
+class lst_stab_report(ctypes.Structure):
+    _fields_ = [
+        ("fixes_low", ctypes.c_int32),
+        ("fixes_high", ctypes.c_int32),
+        ("sigma_min", ctypes.c_float),
+        ("sigma_max", ctypes.c_float),
+    ]
+
+
 class LstError(RuntimeError):
     def __init__(self, code: int, what: str = ""):
         self.code = code
@@ -72,6 +91,9 @@ _SIGS = {
     "lst_get_V": (ctypes.c_int, [_P, _P]),
     "lst_touched_rows": (ctypes.c_int, [_P, _P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
     "lst_restore": (ctypes.c_int, [_P]),
+    "lst_stabilize": (ctypes.c_int, [_P, ctypes.POINTER(lst_stab_config),
+                                     ctypes.POINTER(lst_stab_report)]),
+    "lst_set_stabilize": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(lst_stab_config)]),
     "lst_naive_init": (ctypes.c_int, [ctypes.POINTER(_P), ctypes.c_int64, ctypes.c_int32, _P,
                                       ctypes.POINTER(lst_config), _P]),
     "lst_naive_step": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P, _P, _P,
@@ -227,6 +249,30 @@ def lst_restore(h):
     _check(load_library().lst_restore(h), "lst_restore")
 
 
+def _stab_config(sigma_low, sigma_high, squarings, max_fixes, reinvert) -> lst_stab_config:
+    return lst_stab_config(float(sigma_low), float(sigma_high), int(squarings), int(max_fixes),
+                           int(reinvert))
+
+
+def lst_stabilize(h, sigma_low=1e-3, sigma_high=100.0, squarings=7, max_fixes=2, reinvert=1,
+                  report=True):
+    """Appendix C correction of out-of-range singular values of U.  With report, synchronises
+    and returns the lst_stab_report; else enqueues and returns None."""
+    cfg = _stab_config(sigma_low, sigma_high, squarings, max_fixes, reinvert)
+    rep = lst_stab_report() if report else None
+    _check(load_library().lst_stabilize(h, ctypes.byref(cfg),
+                                        ctypes.byref(rep) if rep is not None else None),
+           "lst_stabilize")
+    return rep
+
+
+def lst_set_stabilize(h, every, sigma_low=1e-3, sigma_high=100.0, squarings=7, max_fixes=2,
+                      reinvert=1):
+    cfg = _stab_config(sigma_low, sigma_high, squarings, max_fixes, reinvert)
+    _check(load_library().lst_set_stabilize(h, int(every), ctypes.byref(cfg)),
+           "lst_set_stabilize")
+
+
 def lst_sync(h) -> int:
     """Wait for the state's stream; returns (and clears) the sticky device status code."""
     return int(load_library().lst_sync(h))
@@ -354,6 +400,12 @@ class FactoredOutputLayer(_Layer):
 
     def restore(self):
         lst_restore(self._h)
+
+    def stabilize(self, **kw):
+        return lst_stabilize(self._h, **kw)
+
+    def set_stabilize(self, every: int, **kw) -> None:
+        lst_set_stabilize(self._h, every, **kw)
 
 
 class NaiveOutputLayer(_Layer):

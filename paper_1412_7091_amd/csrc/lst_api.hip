@@ -62,6 +62,13 @@ struct lst_state {
   uint64_t graph_clock = 0;
   int use_graphs = 0;  // direct launches: graph replay adds device-side gaps between steps
   hipStream_t cap = nullptr;  // capture stream
+  // Appendix C stabilisation: workspace (allocated at first use) and the
+  // periodic setting
+  float* stab_f = nullptr;
+  int* stab_i = nullptr;
+  int stab_ksplit = 0, stab_rounds = 0;
+  int stab_every = 0;
+  lst_stab_config stab_cfg{};
   // profiling: two events per phase per profiled step
   int prof = 0;
   std::vector<hipEvent_t> prof_events;
@@ -153,6 +160,8 @@ void release(lst_state* s) {
   for (auto& g : s->graphs) (void)hipGraphExecDestroy(g.exec);
   for (void* p : s->allocs) (void)hipFree(p);
   s->allocs.clear();
+  if (s->stab_f) (void)hipFree(s->stab_f);
+  if (s->stab_i) (void)hipFree(s->stab_i);
   for (hipEvent_t e : s->prof_events) (void)hipEventDestroy(e);
   if (s->cap) (void)hipStreamDestroy(s->cap);
   delete s;
@@ -384,6 +393,62 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
   return LST_OK;
 }
 
+int check_stab_config(const lst_stab_config* c) {
+  if (!c) return LST_EINVAL;
+  if (!(c->sigma_low > 0.f) || !(c->sigma_low <= 1.f) || !(c->sigma_high >= 1.f) ||
+      !isfinite(c->sigma_high))
+    return LST_EINVAL;
+  if (c->squarings < 0 || c->squarings > 16 || c->max_fixes < 1 || c->max_fixes > 16)
+    return LST_EINVAL;
+  if (c->reinvert < 0 || c->reinvert > 2) return LST_EINVAL;
+  return LST_OK;
+}
+
+// Enqueues one stabilisation on stream st (the workspace is sized for the
+// largest max_fixes seen so far; a larger one reallocates it).
+int enqueue_stabilize(lst_state* s, const lst_stab_config& cfg, hipStream_t st) {
+  const int d = s->d;
+  if (!s->stab_f || cfg.max_fixes > s->stab_rounds) {
+    if (s->stab_f) {
+      HIPCHK(hipStreamSynchronize(st));
+      (void)hipFree(s->stab_f);
+      (void)hipFree(s->stab_i);
+      s->stab_f = nullptr;
+      s->stab_i = nullptr;
+    }
+    const int ks = stab_ksplit(d);
+    const StabLayout l = stab_layout(d, ks, cfg.max_fixes);
+    if (hipMalloc((void**)&s->stab_f, l.floats * sizeof(float)) != hipSuccess) return LST_ENOMEM;
+    if (hipMalloc((void**)&s->stab_i, l.ints * sizeof(int)) != hipSuccess) {
+      (void)hipFree(s->stab_f);
+      s->stab_f = nullptr;
+      return LST_ENOMEM;
+    }
+    s->stab_ksplit = ks;
+    s->stab_rounds = cfg.max_fixes;
+  }
+  const StabLayout l = stab_layout(d, s->stab_ksplit, cfg.max_fixes);
+  StabArgs a{};
+  a.D = s->D;
+  a.d = d;
+  a.V = s->V;
+  a.U = Up(s);
+  a.Uit = Uitp(s);
+  a.flags = s->flags;
+  a.sigma_low = cfg.sigma_low;
+  a.sigma_high = cfg.sigma_high;
+  a.squarings = cfg.squarings;
+  a.max_fixes = cfg.max_fixes;
+  a.reinvert = cfg.reinvert;
+  a.ksplit = s->stab_ksplit;
+  float* f = s->stab_f;
+  a.G = f + l.G; a.G2 = f + l.G2; a.ws = f + l.ws; a.x = f + l.x; a.u = f + l.u; a.w = f + l.w;
+  a.wpart = f + l.wpart; a.scal = f + l.scal; a.sig = f + l.sig;
+  a.chain = s->stab_i;
+  HIPCHK(stabilize_enqueue(a, st));
+  return LST_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -487,6 +552,8 @@ int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* 
     if (rc == LST_OK) {
       s->steps += 1;
       s->last_slots = m * K;
+      if (s->stab_every > 0 && s->steps % s->stab_every == 0)
+        rc = enqueue_stabilize(s, s->stab_cfg, s->stream);
     }
     return rc;
   }
@@ -528,6 +595,48 @@ int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* 
   HIPCHK(hipGraphLaunch(hit->exec, s->stream));
   s->steps += 1;
   s->last_slots = m * K;
+  if (s->stab_every > 0 && s->steps % s->stab_every == 0)
+    return enqueue_stabilize(s, s->stab_cfg, s->stream);
+  return LST_OK;
+}
+
+int lst_stabilize(lst_state* s, const lst_stab_config* cfg, lst_stab_report* report) {
+  if (!s) return LST_EINVAL;
+  OK_OR_RETURN(check_stab_config(cfg));
+  if (s->kind != 0) return LST_ESTATE;
+  DeviceGuard dg(s->device);
+  OK_OR_RETURN(enqueue_stabilize(s, *cfg, s->stream));
+  if (!report) return LST_OK;
+  const int R = cfg->max_fixes;
+  const StabLayout l = stab_layout(s->d, s->stab_ksplit, R);
+  std::vector<int> chain(2 * (R + 1));
+  std::vector<float> sig(2 * R);
+  HIPCHK(hipStreamSynchronize(s->stream));
+  HIPCHK(hipMemcpy(chain.data(), s->stab_i, chain.size() * sizeof(int), hipMemcpyDeviceToHost));
+  HIPCHK(hipMemcpy(sig.data(), s->stab_f + l.sig, sig.size() * sizeof(float),
+                   hipMemcpyDeviceToHost));
+  int fixes[2] = {0, 0};
+  float last[2] = {NAN, NAN};
+  for (int e = 0; e < 2; ++e)
+    for (int r = 0; r < R; ++r) {
+      fixes[e] += chain[e * (R + 1) + r + 1];
+      if (chain[e * (R + 1) + r]) last[e] = sig[e * R + r];
+    }
+  report->fixes_low = fixes[0];
+  report->fixes_high = fixes[1];
+  report->sigma_min = last[0];
+  report->sigma_max = last[1];
+  return LST_OK;
+}
+
+int lst_set_stabilize(lst_state* s, int32_t every, const lst_stab_config* cfg) {
+  if (!s || every < 0) return LST_EINVAL;
+  if (s->kind != 0) return LST_ESTATE;
+  if (every > 0) {
+    OK_OR_RETURN(check_stab_config(cfg));
+    s->stab_cfg = *cfg;
+  }
+  s->stab_every = every;
   return LST_OK;
 }
 

@@ -194,6 +194,27 @@ hipError_t set_identity_if(float* A, int d, const int* run_if, hipStream_t s);
 hipError_t set_flag(int* p, int v, hipStream_t s);
 hipError_t transpose_square(const float* A, float* At, int d, hipStream_t s);
 
+// ---------------------------------------------------- Appendix C stabilisation
+// Everything one stabilisation call reads or writes (device pointers).
+struct StabArgs {
+  int64_t D;
+  int d;
+  float *V, *U, *Uit;
+  const int* flags;
+  float sigma_low, sigma_high;
+  int squarings, max_fixes, reinvert, ksplit;
+  // workspace (StabLayout offsets into one float buffer, chain in an int buffer)
+  float *G, *G2, *ws, *x, *u, *w, *wpart, *scal, *sig;
+  int* chain;  // 2 x (max_fixes + 1) round flags: [end][0] = no pending error,
+               // [end][r + 1] = round r of that end corrected a singular value
+};
+struct StabLayout {
+  size_t G, G2, ws, x, u, w, wpart, scal, sig, floats, ints;
+};
+StabLayout stab_layout(int d, int ksplit, int max_fixes);
+int stab_ksplit(int d);
+hipError_t stabilize_enqueue(const StabArgs& a, hipStream_t s);
+
 // ----------------------------------------------------------------- naive
 hipError_t naive_rowstats(float* O, int64_t ldo, int64_t D, int m, const int32_t* idx,
                           const float* val, int K, int loss_kind, float eps, float* loss,

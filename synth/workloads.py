@@ -40,7 +40,9 @@ class WorkloadConfig:
     val_dist   'normal' (N(0,1)), 'one' (all 1.0) or 'poisson2p1' (Poisson(2)+1).
     h_scale    standard deviation of the N(0, h_scale^2) entries of H.
     v_bound    V0 entries are U(-v_bound, v_bound).
-    u_init     'identity' or 'random' (I + N(0, (0.3/sqrt(d))^2) entries; tests only).
+    u_init     'identity', 'random' (I + N(0, (0.3/sqrt(d))^2) entries; tests only) or
+               'spectrum' (Q1 diag(s) Q2^T with Haar-random orthogonal Q1, Q2 and
+               s = 1 except s[:len(u_sigma)] = u_sigma; tests only).
     pad_frac   fraction of target slots replaced by the padding index -1 (tests only).
     dup_frac   fraction of target slots that copy another slot's index of the same
                example, so that an index repeats inside one example (tests only).
@@ -61,6 +63,7 @@ class WorkloadConfig:
     h_scale: Optional[float] = None  # None means 1/sqrt(d)
     v_bound: Optional[float] = None  # None means 1/sqrt(d)
     u_init: str = "identity"
+    u_sigma: Tuple[float, ...] = ()
     sph_eps: float = 1e-3
     pad_frac: float = 0.0
     dup_frac: float = 0.0
@@ -172,6 +175,15 @@ class Workload:
             rng = _rng(c, _STREAM_INIT, 1)
             U = np.eye(c.d) + rng.standard_normal((c.d, c.d)) * (0.3 / math.sqrt(c.d))
             return np.ascontiguousarray(U, dtype=np.float32)
+        if c.u_init == "spectrum":
+            rng = _rng(c, _STREAM_INIT, 2)
+            s = np.ones(c.d)
+            s[: len(c.u_sigma)] = c.u_sigma
+            q = []
+            for _ in range(2):
+                a, r = np.linalg.qr(rng.standard_normal((c.d, c.d)))
+                q.append(a * np.sign(np.diag(r)))
+            return np.ascontiguousarray((q[0] * s) @ q[1].T, dtype=np.float32)
         raise ValueError(f"unknown u_init {c.u_init!r}")
 
     # ------------------------------------------------------------- batches

@@ -60,3 +60,9 @@ def test_null_state_and_bad_config_rejected_on_host(lib):
     assert lib.lst_init(ctypes.byref(h), 10, 0, fake_dev, None, ctypes.byref(cfg), None) == lst.LST_EINVAL
     assert lib.lst_init(ctypes.byref(h), 10, 4, None, None, ctypes.byref(cfg), None) == lst.LST_EINVAL
     assert h.value is None
+
+
+def test_stabilize_arguments_rejected_on_host(lib):
+    good = lst.lst_stab_config(1e-3, 100.0, 7, 2, 1)
+    assert lib.lst_stabilize(None, ctypes.byref(good), None) == lst.LST_EINVAL
+    assert lib.lst_set_stabilize(None, 1, ctypes.byref(good)) == lst.LST_EINVAL

@@ -126,7 +126,7 @@ def test_stabilize_svd_and_power_agree():
 def test_in_range_changes_nothing():
     st0 = _state([2.0, 1.0, 0.5])
     st1 = _copy(st0)
-    rounds = stabilize.stabilize_power(st1, 1e-3, 100.0, 64, 2, np.ones(3), do_reinvert=False)
+    rounds = stabilize.stabilize_power(st1, 1e-3, 100.0, 64, 2, np.ones(3), reinvert_mode=0)
     assert [r[2] for r in rounds] == [False, False]
     np.testing.assert_array_equal(st1.U, st0.U)
     np.testing.assert_array_equal(st1.V, st0.V)
