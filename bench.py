@@ -69,6 +69,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-naive", action="store_true")
+    ap.add_argument("--no-stabilize", action="store_true")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -171,6 +172,12 @@ def main():
     layer.close()
     del layer
 
+    stab = None
+    if not args.no_stabilize:
+        stab = stabilize_cost(lst, torch, cfg, V0_t, dev)
+        log(f"stabilize: {stab['ms_in_range']:.3f} ms when nothing is out of range, "
+            f"{stab['ms_one_fix']:.3f} ms with one correction (one pass over V)")
+
     # A plain 64 MiB device copy, outside every timed region: the reference the
     # FETCH_SIZE / WRITE_SIZE counter runs are scaled by (see profiling.py).  A
     # 128 MiB fill in between pushes the copy's source out of the L2 caches.
@@ -228,10 +235,57 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "naive": naive,
+        "stabilize": stab,
         "kernels": kernels,
         "last_step": {"distinct_rows": u, "pairs": nnz},
     }
     print(json.dumps(out), flush=True)
+
+
+def stabilize_cost(lst, torch, cfg, V0_t, dev):
+    """Cost of one Appendix C stabilisation call on a state of the workload's size.
+
+    Two states: U = I (every singular value in range: one power-iteration
+    round at each end, no correction) and U with one singular value of 1e-4
+    (one correction: rank-one updates of U and U^{-T}, a pass over V, and the
+    refinement of U^{-T}).  Each call is timed alone, with a report (which
+    synchronises).  Not part of the step's throughput.
+    """
+    from synth import Workload
+
+    def timed(layer):
+        layer.stabilize(sigma_low=1e-3, sigma_high=100.0, squarings=7, max_fixes=1, reinvert=1)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        rep = layer.stabilize(sigma_low=1e-3, sigma_high=100.0, squarings=7, max_fixes=1,
+                              reinvert=1)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1), rep
+
+    layer = lst.FactoredOutputLayer(V0_t, loss=cfg.loss, sph_eps=cfg.sph_eps, m_max=cfg.m,
+                                    K_max=cfg.K)
+    ms_in, rep_in = timed(layer)
+    layer.close()
+    U0 = Workload(cfg.replace(u_init="spectrum", u_sigma=(1e-4,))).init_U()
+    U0_t = torch.from_numpy(U0).to(dev)
+    fix_ms = []
+    for _ in range(2):  # the first call warms up; a fresh state each time (one fix each)
+        layer = lst.FactoredOutputLayer(V0_t, U0_t, loss=cfg.loss, sph_eps=cfg.sph_eps,
+                                        m_max=cfg.m, K_max=cfg.K)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        rep = layer.stabilize(sigma_low=1e-3, sigma_high=100.0, squarings=7, max_fixes=1,
+                              reinvert=1)
+        e1.record()
+        torch.cuda.synchronize()
+        fix_ms.append(e0.elapsed_time(e1))
+        layer.close()
+    return {"ms_in_range": round(ms_in, 4), "ms_one_fix": round(fix_ms[-1], 4),
+            "fixes": [rep_in.fixes_low + rep_in.fixes_high, rep.fixes_low + rep.fixes_high],
+            "V_pass_bytes": 2 * cfg.D * cfg.d * 4, "squarings": 7}
 
 
 def cpu_baseline(cfg, wl, V0, seconds):

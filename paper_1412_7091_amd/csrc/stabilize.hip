@@ -210,33 +210,44 @@ __global__ __launch_bounds__(256) void stab_fix_v_kernel(float* __restrict__ V, 
   const int64_t wave0 = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int64_t nwaves = (int64_t)gridDim.x * 4;
   if (VEC) {
-    // lane owns the 16-byte pieces lane, lane + 64, lane + 128, lane + 192 of a row
+    // lane owns the 16-byte pieces lane, lane + 64, ... of a row; a wave takes
+    // two rows at a time, both rows' loads in flight before either reduction.
+    constexpr int NQ = 4, NR = 2;
     const int nq = d / 4;
-    f32x4 uq[4];
+    f32x4 uq[NQ];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < NQ; ++t) {
       const int q = lane + 64 * t;
       uq[t] = q < nq ? reinterpret_cast<const f32x4*>(u)[q] : f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    for (int64_t r = wave0; r < D; r += nwaves) {
-      f32x4* row = reinterpret_cast<f32x4*>(V + r * d);
-      f32x4 v[4];
+    for (int64_t r0 = wave0 * NR; r0 < D; r0 += nwaves * NR) {
+      f32x4 v[NR][NQ];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int q = lane + 64 * t;
-        v[t] = q < nq ? __builtin_nontemporal_load(row + q) : f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int k = 0; k < NR; ++k) {
+        const f32x4* row = reinterpret_cast<const f32x4*>(V + (r0 + k) * d);
+#pragma unroll
+        for (int t = 0; t < NQ; ++t) {
+          const int q = lane + 64 * t;
+          v[k][t] = (q < nq && r0 + k < D) ? __builtin_nontemporal_load(row + q)
+                                           : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
       }
-      float s = 0.f;
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-        s += v[t].x * uq[t].x + v[t].y * uq[t].y + v[t].z * uq[t].z + v[t].w * uq[t].w;
+      for (int k = 0; k < NR; ++k) {
+        float s = 0.f;
 #pragma unroll
-      for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
-      const float c = beta * s;
+        for (int t = 0; t < NQ; ++t)
+          s += v[k][t].x * uq[t].x + v[k][t].y * uq[t].y + v[k][t].z * uq[t].z +
+               v[k][t].w * uq[t].w;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int q = lane + 64 * t;
-        if (q < nq) __builtin_nontemporal_store(v[t] + c * uq[t], row + q);
+        for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+        const float c = beta * s;
+        f32x4* row = reinterpret_cast<f32x4*>(V + (r0 + k) * d);
+#pragma unroll
+        for (int t = 0; t < NQ; ++t) {
+          const int q = lane + 64 * t;
+          if (q < nq && r0 + k < D) __builtin_nontemporal_store(v[k][t] + c * uq[t], row + q);
+        }
       }
     }
   } else {

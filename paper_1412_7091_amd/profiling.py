@@ -26,7 +26,8 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 REPO = os.path.dirname(PKG)
 PROFILES = os.path.join(REPO, "profiles")
-SOURCES = ["gemm_tile.h", "lst_internal.h", "step.hip", "lst_api.hip", "gemm.hip", "small.hip"]
+SOURCES = ["gemm_tile.h", "lst_internal.h", "step.hip", "lst_api.hip", "gemm.hip", "small.hip",
+           "stabilize.hip"]
 CALIBRATION_BYTES = 64 << 20  # the benchmark's plain device-to-device copy
 
 
@@ -39,9 +40,12 @@ def source_digest() -> str:
 
 
 def launch_of(kernel_name: str) -> str | None:
-    """'launch1'..'launch4' for the step kernels (last template argument), else None."""
+    """'launch1'..'launch4' for the step kernels (last template argument),
+    'stab_fix_v' for the stabilisation's pass over V, else None."""
     m = re.search(r"step_kernel<[^<>]*?,\s*(\d)\s*>", kernel_name)
-    return f"launch{m.group(1)}" if m else None
+    if m:
+        return f"launch{m.group(1)}"
+    return "stab_fix_v" if "stab_fix_v_kernel" in kernel_name else None
 
 
 def _db(directory: str) -> sqlite3.Connection:
