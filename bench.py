@@ -70,7 +70,13 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-naive", action="store_true")
     ap.add_argument("--no-stabilize", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the benchmark line: factored vs naive step time over the "
+                         "vocabulary size D at d = 300, m = 128 (the paper's timing figure and "
+                         "speedup table)")
     args = ap.parse_args()
+    if args.sweep:
+        return sweep(args)
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the step has no "
@@ -286,6 +292,93 @@ def stabilize_cost(lst, torch, cfg, V0_t, dev):
     return {"ms_in_range": round(ms_in, 4), "ms_one_fix": round(fix_ms[-1], 4),
             "fixes": [rep_in.fixes_low + rep_in.fixes_high, rep.fixes_low + rep.fixes_high],
             "V_pass_bytes": 2 * cfg.D * cfg.d * 4, "squarings": 7}
+
+
+SWEEP_D = (10_000, 50_000, 100_000, 200_000, 400_000, 793_471)
+
+
+def sweep(args):
+    """Step time of the factored and the naive (explicit W) output layer over D.
+
+    d = 300, m = 128, one target word per example (K = 1, value 1, uniform),
+    squared error, lr = 1e-3: the setting of the paper's timing figure and of
+    its speedup table (D = 793 471).  At the largest D the fp64 CPU oracle
+    (explicit W) is timed too, as the table's CPU-naive reference, and the
+    factored step is also timed at m = 1 (one example per step).  Prints one
+    JSON object.
+    """
+    import torch
+
+    import paper_1412_7091_amd as lst
+    from synth import Workload, WorkloadConfig
+
+    lst.load_library()
+    dev = torch.device("cuda:0")
+    rows = []
+    for D in SWEEP_D:
+        cfg = WorkloadConfig(name=f"sweep_D{D}", D=D, d=300, m=128, K=1, loss="squared",
+                             lr=1e-3, idx_dist="uniform", val_dist="one",
+                             entropy=14127091 + 100 + SWEEP_D.index(D))
+        wl = Workload(cfg)
+        V0 = wl.init_V()
+        V0_t = torch.from_numpy(V0).to(dev)
+        pool = [tuple(torch.from_numpy(x).to(dev) for x in wl.batch(s)) for s in range(8)]
+        loss_t = torch.empty(cfg.m, device=dev)
+        grad_t = torch.empty((cfg.m, cfg.d), device=dev)
+
+        def timed(layer, n, warm, m=None):
+            def one(s):
+                H, idx, val = pool[s % len(pool)]
+                if m is not None:
+                    H, idx, val = H[:m].contiguous(), idx[:m].contiguous(), val[:m].contiguous()
+                    layer.step(H, idx, val, cfg.lr, out=(loss_t[:m], grad_t[:m]))
+                else:
+                    layer.step(H, idx, val, cfg.lr, out=(loss_t, grad_t))
+            for s in range(warm):
+                one(s)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for s in range(n):
+                one(warm + s)
+            e1.record()
+            torch.cuda.synchronize()
+            assert layer.sync() == 0
+            return e0.elapsed_time(e1) / n
+
+        fl = lst.FactoredOutputLayer(V0_t, m_max=cfg.m, K_max=cfg.K)
+        f_ms = timed(fl, 200, 20)
+        row = {"D": D, "factored_us": round(1e3 * f_ms, 2)}
+        if D == SWEEP_D[-1]:
+            row["factored_m1_us"] = round(1e3 * timed(fl, 200, 20, m=1), 2)
+        fl.close()
+        nl = lst.NaiveOutputLayer(V0_t, m_max=cfg.m, K_max=cfg.K)
+        n_ms = timed(nl, 10, 2)
+        nl.close()
+        row.update(naive_us=round(1e3 * n_ms, 2), speedup=round(n_ms / f_ms, 2),
+                   D_over_4d=round(D / (4 * cfg.d), 2))
+        if D == SWEEP_D[-1] and not args.no_cpu_baseline:
+            from oracle import explicit
+
+            W = V0.astype(np.float64)
+            t0 = time.perf_counter()
+            n = 0
+            while n < 2 or (time.perf_counter() - t0 < args.cpu_seconds and n < 10):
+                H, idx, val = wl.batch(n)
+                _, _, W = explicit.step(W, H, idx, val, cfg.lr, cfg.loss, cfg.sph_eps)
+                n += 1
+            cpu_ms = 1e3 * (time.perf_counter() - t0) / n
+            row.update(cpu_naive_oracle_ms=round(cpu_ms, 1),
+                       speedup_vs_cpu_naive=round(cpu_ms / f_ms, 1),
+                       naive_gpu_vs_cpu_naive=round(cpu_ms / n_ms, 1))
+        log(json.dumps(row))
+        rows.append(row)
+        del V0_t, pool
+        torch.cuda.empty_cache()
+    print(json.dumps({"sweep": "factored vs naive output-layer step over D", "d": 300, "m": 128,
+                      "K": 1, "loss": "squared", "dtype": "f32", "data": "synthetic",
+                      "rows": rows}), flush=True)
+    return 0
 
 
 def cpu_baseline(cfg, wl, V0, seconds):
