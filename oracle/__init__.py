@@ -17,10 +17,12 @@ Modules
   stabilize Appendix C's correction of out-of-range singular values of U
             (fix-singular-value, with a full SVD or with power iterations),
             and the recomputation of U^{-T}.
+  input_layer  the sparse input layer of section 2.2 (forward A = X W_in and
+            the update of the rows of W_in the inputs refer to).
 
 Pin status (what fixes each function other than itself) is listed in each
 function's docstring; the only function without a pin by the paper is the
 minibatch form of the spherical-softmax factored step, which is pinned by the
 explicit definition and by finite differences instead.
 """
-from . import explicit, factored, stabilize  # noqa: F401
+from . import explicit, factored, input_layer, stabilize  # noqa: F401
