@@ -184,6 +184,12 @@ def main():
         log(f"stabilize: {stab['ms_in_range']:.3f} ms when nothing is out of range, "
             f"{stab['ms_one_fix']:.3f} ms with one correction (one pass over V)")
 
+    inp = None
+    if not args.no_stabilize:
+        inp = input_layer_cost(lst, torch, cfg, wl, V0_t, pool)
+        log(f"input layer: forward {inp['forward_us']:.2f} us, update {inp['update_us']:.2f} us "
+            f"per minibatch")
+
     # A plain 64 MiB device copy, outside every timed region: the reference the
     # FETCH_SIZE / WRITE_SIZE counter runs are scaled by (see profiling.py).  A
     # 128 MiB fill in between pushes the copy's source out of the L2 caches.
@@ -242,6 +248,7 @@ def main():
         "cpu_baseline": cpu,
         "naive": naive,
         "stabilize": stab,
+        "input_layer": inp,
         "kernels": kernels,
         "last_step": {"distinct_rows": u, "pairs": nnz},
     }
@@ -379,6 +386,35 @@ def sweep(args):
                       "K": 1, "loss": "squared", "dtype": "f32", "data": "synthetic",
                       "rows": rows}), flush=True)
     return 0
+
+
+def input_layer_cost(lst, torch, cfg, wl, V0_t, pool):
+    """Section 2.2 input layer at the workload's sizes (D_in = D, d, m, K = the
+    targets' K as input pairs): mean time of a forward and of an update over
+    the pool of minibatches (the batch's H stands in for dL/dA)."""
+    layer = lst.SparseInputLayer(V0_t)
+    A = torch.empty((cfg.m, cfg.d), dtype=torch.float32, device=V0_t.device)
+    res = {}
+    for what in ("forward", "update"):
+        def run(n):
+            for s in range(n):
+                H, idx, val = pool[s % len(pool)]
+                if what == "forward":
+                    layer.forward(idx, val, out=A)
+                else:
+                    layer.update(idx, val, H, 1e-6)
+        run(10)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run(200)
+        e1.record()
+        torch.cuda.synchronize()
+        res[f"{what}_us"] = round(1e3 * e0.elapsed_time(e1) / 200, 3)
+    assert layer.sync() == 0
+    layer.close()
+    res["rows_per_minibatch"] = cfg.m * cfg.K
+    return res
 
 
 def cpu_baseline(cfg, wl, V0, seconds):

@@ -265,6 +265,52 @@ int lst_profile_read(lst_state* s, double* ms_total, int32_t capacity, int32_t* 
 /* Name of phase i of lst_step (NULL when out of range). */
 const char* lst_profile_phase_name(int32_t phase);
 
+/*
+ * The sparse input layer (section 2.2, "the easy part"): a D_in x d matrix
+ * W_in whose input is K-sparse, given like the targets as K (index, value)
+ * pairs per example (index -1 unused; a repeated index adds its values).
+ * Only the rows the inputs refer to are read (forward) or written (update):
+ * O(m K d) per minibatch instead of O(m D_in d).
+ */
+typedef struct lst_input lst_input;
+
+/*
+ * lst_input_init -- create an input layer; W_in (device, D_in x d) is copied.
+ * D_in >= 1, 1 <= d <= 4096.  Synchronous.
+ */
+int lst_input_init(lst_input** out, int64_t D_in, int32_t d, const float* W_in,
+                   void* hip_stream);
+
+/*
+ * lst_input_forward -- A = X W_in: row i of A (device, m x d) is
+ * sum_k val[i][k] W_in[idx[i][k], :], the pairs added in k order.
+ *   idx, val (device) m x K.  m, K >= 1, m * K <= 65536.
+ * An index outside [-1, D_in) sets the sticky status LST_EINDEX (reported by
+ * lst_input_sync) and its pair is left out of A.
+ */
+int lst_input_forward(lst_input* s, int32_t m, int32_t K, const int32_t* idx, const float* val,
+                      float* A);
+
+/*
+ * lst_input_update -- W_in <- W_in - lr X^T grad_A (section 2.2: W_in[u_k] -=
+ * lr v_k grad_a for every pair of every example; pairs that share a row add
+ * up, in (example, pair) order, and each row is written once).  grad_A
+ * (device, m x d) is dL/dA.  lr > 0 and finite.  Rows no pair refers to are
+ * not touched.  Skipped entirely (W_in unchanged) while the sticky status is
+ * set, e.g. by an index outside [-1, D_in) in this call.
+ */
+int lst_input_update(lst_input* s, int32_t m, int32_t K, const int32_t* idx, const float* val,
+                     const float* grad_A, float lr);
+
+/* lst_input_get_W -- copy W_in into W (device, D_in x d). */
+int lst_input_get_W(lst_input* s, float* W);
+
+/* lst_input_sync -- wait for the stream; return and clear the sticky status. */
+int lst_input_sync(lst_input* s);
+
+/* lst_input_free -- synchronise and release the layer (NULL ok). */
+void lst_input_free(lst_input* s);
+
 /* lst_strerror -- static description of a status code. */
 const char* lst_strerror(int status);
 

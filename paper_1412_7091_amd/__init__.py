@@ -106,6 +106,13 @@ _SIGS = {
                                         ctypes.POINTER(ctypes.c_int32),
                                         ctypes.POINTER(ctypes.c_int64)]),
     "lst_profile_phase_name": (ctypes.c_char_p, [ctypes.c_int32]),
+    "lst_input_init": (ctypes.c_int, [ctypes.POINTER(_P), ctypes.c_int64, ctypes.c_int32, _P, _P]),
+    "lst_input_forward": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P, _P, _P]),
+    "lst_input_update": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P, _P, _P,
+                                        ctypes.c_float]),
+    "lst_input_get_W": (ctypes.c_int, [_P, _P]),
+    "lst_input_sync": (ctypes.c_int, [_P]),
+    "lst_input_free": (None, [_P]),
     "lst_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "lst_free": (None, [_P]),
 }
@@ -406,6 +413,66 @@ class FactoredOutputLayer(_Layer):
 
     def set_stabilize(self, every: int, **kw) -> None:
         lst_set_stabilize(self._h, every, **kw)
+
+
+class SparseInputLayer:
+    """Section 2.2 input layer: W_in (D_in x d) with K-sparse inputs."""
+
+    def __init__(self, W_in, stream=None):
+        import torch
+
+        lib = load_library()
+        self.D, self.d = W_in.shape
+        self.device = W_in.device
+        h = _P()
+        _check(lib.lst_input_init(ctypes.byref(h), self.D, self.d,
+                                  _ptr(W_in, torch.float32, "W_in"), _stream_handle(stream)),
+               "lst_input_init")
+        self._h = h
+
+    def forward(self, idx, val, out=None):
+        import torch
+
+        m, K = idx.shape
+        if out is None:
+            out = torch.empty((m, self.d), dtype=torch.float32, device=self.device)
+        _check(load_library().lst_input_forward(self._h, m, K, _ptr(idx, torch.int32, "idx"),
+                                                _ptr(val, torch.float32, "val"),
+                                                _ptr(out, torch.float32, "A")), "lst_input_forward")
+        return out
+
+    def update(self, idx, val, grad_A, lr):
+        import torch
+
+        m, K = idx.shape
+        if tuple(grad_A.shape) != (m, self.d):
+            raise ValueError("grad_A must be (m, d)")
+        _check(load_library().lst_input_update(self._h, m, K, _ptr(idx, torch.int32, "idx"),
+                                               _ptr(val, torch.float32, "val"),
+                                               _ptr(grad_A, torch.float32, "grad_A"), float(lr)),
+               "lst_input_update")
+
+    def get_W(self):
+        import torch
+
+        W = torch.empty((self.D, self.d), dtype=torch.float32, device=self.device)
+        _check(load_library().lst_input_get_W(self._h, _ptr(W, torch.float32, "W")),
+               "lst_input_get_W")
+        return W
+
+    def sync(self) -> int:
+        return int(load_library().lst_input_sync(self._h))
+
+    def close(self) -> None:
+        if self._h is not None:
+            load_library().lst_input_free(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 class NaiveOutputLayer(_Layer):

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(REPO, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liblst.so")
 
-SOURCES = ["gemm.hip", "step.hip", "small.hip", "stabilize.hip", "lst_api.hip"]
+SOURCES = ["gemm.hip", "step.hip", "small.hip", "stabilize.hip", "input_layer.hip", "lst_api.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",
@@ -50,7 +50,7 @@ def _compile(src: str) -> str:
 
 def build(verbose: bool = True) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(5, len(SOURCES))) as ex:
+    with cf.ThreadPoolExecutor(max_workers=min(6, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]

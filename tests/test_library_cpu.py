@@ -66,3 +66,15 @@ def test_stabilize_arguments_rejected_on_host(lib):
     good = lst.lst_stab_config(1e-3, 100.0, 7, 2, 1)
     assert lib.lst_stabilize(None, ctypes.byref(good), None) == lst.LST_EINVAL
     assert lib.lst_set_stabilize(None, 1, ctypes.byref(good)) == lst.LST_EINVAL
+
+
+def test_input_layer_arguments_rejected_on_host(lib):
+    h = ctypes.c_void_p()
+    fake_dev = ctypes.c_void_p(16)  # never dereferenced
+    assert lib.lst_input_init(ctypes.byref(h), 0, 4, fake_dev, None) == lst.LST_EINVAL
+    assert lib.lst_input_init(ctypes.byref(h), 10, 0, fake_dev, None) == lst.LST_EINVAL
+    assert lib.lst_input_init(ctypes.byref(h), 10, 4, None, None) == lst.LST_EINVAL
+    assert lib.lst_input_forward(None, 1, 1, fake_dev, fake_dev, fake_dev) == lst.LST_EINVAL
+    assert lib.lst_input_update(None, 1, 1, fake_dev, fake_dev, fake_dev, 0.1) == lst.LST_EINVAL
+    assert lib.lst_input_sync(None) == lst.LST_EINVAL
+    lib.lst_input_free(None)
