@@ -303,8 +303,72 @@ __device__ __forceinline__ void mma_frags(const float (&a)[PanelGeom<T>::IB][4],
 // acc += the first nsl 16-wide k slices held in consecutive stages from
 // smem (slice s lives in stage s / (CK / 16)).  The fragments of slice s + 1
 // are read from LDS while the MFMAs of slice s run.
+// 32-tiles with both operands k-contiguous (the stacked product of the first
+// launch, the m x m products): the fragment reads go through inline asm, one
+// slice ahead of the MFMAs they feed, and each slice waits only for the pair
+// of reads issued a slice earlier.  Left to the compiler, the wait for a
+// slice's fragments lands right after the reads of the next slice were issued
+// (it counts outstanding LDS reads conservatively across the loop), so every
+// slice pays the LDS latency.  The per-lane offsets of the four slices of a
+// stage are computed once.  Slices past nsl inside the last stage are read
+// (inside the stage) but not multiplied.
+__device__ __forceinline__ void lds_read_pair(floatx4& a, floatx4& b, unsigned pa, unsigned pb) {
+  asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %3" : "=&v"(a), "=&v"(b) : "v"(pa), "v"(pb));
+}
+// Waits until at most the pair issued after (a, b) is outstanding.
+__device__ __forceinline__ void lds_wait_pair(floatx4& a, floatx4& b) {
+  asm volatile("s_waitcnt lgkmcnt(2)" : "+v"(a), "+v"(b));
+}
+
+__device__ __forceinline__ void mma_pair32(const floatx4& a, const floatx4& b, Accum<32>& acc) {
+  acc.v[0][0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, acc.v[0][0][0], 0, 0, 0);
+  acc.v[1][0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, acc.v[1][0][0], 0, 0, 0);
+  acc.v[0][0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, acc.v[0][0][0], 0, 0, 0);
+  acc.v[1][0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, acc.v[1][0][0], 0, 0, 0);
+}
+
+__device__ __forceinline__ void mma_slices_kc32(const float* smem, int nsl, Accum<32>& acc) {
+  using G = PanelGeom<32>;
+  constexpr unsigned SB = G::STAGE * 4;  // bytes per stage
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, l16 = lane & 15;
+  const int ra = (wave >> 1) * G::WT + l16, rb = (wave & 1) * G::WT + l16;
+  const unsigned base = lds_u32(smem);
+  unsigned oa[4], ob[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    oa[j] = base + 4u * (unsigned)(ra * G::CK + 4 * ((4 * j + g) ^ (ra & 7)));
+    ob[j] = base + 4u * (unsigned)(G::OPF + rb * G::CK + 4 * ((4 * j + g) ^ (rb & 7)));
+  }
+  if (nsl <= 0) return;
+  const int nst = (nsl + 3) >> 2;
+  floatx4 a0, b0, a1, b1;
+  lds_read_pair(a0, b0, oa[0], ob[0]);
+  for (int st = 0; st < nst; ++st) {
+    const unsigned sb = (unsigned)st * SB, nb = (st + 1 < nst) ? sb + SB : sb;
+    const int s0 = 4 * st;
+    lds_read_pair(a1, b1, oa[1] + sb, ob[1] + sb);
+    lds_wait_pair(a0, b0);
+    mma_pair32(a0, b0, acc);  // slice s0 < nsl always
+    lds_read_pair(a0, b0, oa[2] + sb, ob[2] + sb);
+    lds_wait_pair(a1, b1);
+    if (s0 + 1 < nsl) mma_pair32(a1, b1, acc);
+    lds_read_pair(a1, b1, oa[3] + sb, ob[3] + sb);
+    lds_wait_pair(a0, b0);
+    if (s0 + 2 < nsl) mma_pair32(a0, b0, acc);
+    lds_read_pair(a0, b0, oa[0] + nb, ob[0] + nb);
+    lds_wait_pair(a1, b1);
+    if (s0 + 3 < nsl) mma_pair32(a1, b1, acc);
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a0), "+v"(b0));
+}
+
 template <int T, int AKC, int BKC>
 __device__ __forceinline__ void mma_slices(const float* smem, int nsl, Accum<T>& acc) {
+  if constexpr (T == 32 && AKC && BKC) {
+    mma_slices_kc32(smem, nsl, acc);
+    return;
+  }
   using G = PanelGeom<T>;
   constexpr int IB = G::IB, NKK = G::CK / 16;
   auto frags = [&](int sl, float (&a)[IB][4], float (&b)[IB][4]) {
