@@ -719,6 +719,77 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
         }
       }
     };
+    if constexpr (SMALL) {
+      // m <= 128: at most 8 slices.  The fragment reads go through inline asm
+      // one slice ahead of the MFMAs they feed, each slice waiting only for
+      // the reads issued a slice earlier (left to the compiler, that wait
+      // lands after the next slice's reads and every slice pays the LDS
+      // latency); per-lane offsets of every slice are computed once, slices
+      // past the last re-read it.
+      const int nsl = mp / 16;
+      unsigned oa[RBW][8];
+#pragma unroll
+      for (int t = 0; t < RBW; ++t) {
+        const int arow = min((wave + 4 * t) * 16, mp - 16) + (lane & 15);
+#pragma unroll
+        for (int sl = 0; sl < 8; ++sl) {
+          const int k = min(sl, nsl - 1) * 16 + 4 * (lane >> 4);
+          oa[t][sl] = lds_u32(Hs + arow * mp + 4 * ((k >> 2) ^ (arow & hsw)));
+        }
+      }
+      const unsigned yl = 4u * (unsigned)((lane & 15) * LDE + 4 * (lane >> 4));
+      for (int it = 0; it < iters; ++it) {
+        floatx4 acc[RBW];
+#pragma unroll
+        for (int t = 0; t < RBW; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+        const unsigned yb = lds_u32(Yo) + yl;
+        floatx4 fb[2], fa[2][RBW];
+        auto rd = [&](int b, int sl) {
+          static_assert(RBW == 2, "three reads per slice");
+          asm volatile("ds_read_b128 %0, %3\n\tds_read_b128 %1, %4\n\tds_read_b128 %2, %5"
+                       : "=&v"(fb[b]), "=&v"(fa[b][0]), "=&v"(fa[b][1])
+                       : "v"(yb + 64u * (unsigned)min(sl, nsl - 1)), "v"(oa[0][sl]), "v"(oa[1][sl]));
+        };
+        auto mm = [&](int b) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int t = 0; t < RBW; ++t)
+              acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[b][t][q], fb[b][q], acc[t], 0, 0, 0);
+        };
+        rd(0, 0);
+#pragma unroll
+        for (int sl = 0; sl < 8; ++sl) {
+          if (sl < nsl) {
+            const int b = sl & 1;
+            if (sl + 1 < 8) {
+              rd(b ^ 1, sl + 1);
+              asm volatile("s_waitcnt lgkmcnt(3)" : "+v"(fb[b]), "+v"(fa[b][0]), "+v"(fa[b][1]));
+            } else {
+              asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fb[b]), "+v"(fa[b][0]), "+v"(fa[b][1]));
+            }
+            mm(b);
+          }
+        }
+        // the reads of slice nsl (a re-read of the last one) may be outstanding
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        const int col = lane & 15;
+#pragma unroll
+        for (int t = 0; t < RBW; ++t) {
+          const int rb = wave + 4 * t;
+          if (rb >= nrb) break;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int row = rb * 16 + 4 * (lane >> 4) + q;
+            Yn[col * LDE + row] = Bt[col * LDE + row] + acc[t][q] * cinv[row];
+          }
+        }
+        __syncthreads();
+        float* tt = Yo;
+        Yo = Yn;
+        Yn = tt;
+      }
+    } else {
     for (int it = 0; it < iters; ++it) {
       floatx4 acc[RBW];
 #pragma unroll
@@ -764,6 +835,7 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
       float* tt = Yo;
       Yo = Yn;
       Yn = tt;
+    }
     }
     LST_SMARK(5);
     for (int e = tid; e < kSolveCols * m; e += 256) {
