@@ -320,6 +320,11 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     StepLaunch L{};
     L.ntask = 4;
     L.kind[0] = TK_GEMM; L.kind[1] = TK_SOLVE; L.kind[2] = TK_YY; L.kind[3] = TK_SCALARS;
+    if (m > 128) {
+      // the solve (H^T H read from memory, many iterations' MFMAs per block)
+      // outlasts the GEMM tiles: its blocks go first
+      L.kind[0] = TK_SOLVE; L.kind[1] = TK_GEMM;
+    }
     GemmBatch& g = L.gemm;
     g.np = 4;
     g.p[0] = gemm_problem(L_NN, m, d, d, vmat(s->G, d, m), vmat(c.U, d, d), s->Yh, d, 1.f, 0.f,

@@ -506,6 +506,89 @@ __device__ unsigned long long g_solve_marks[64][8];
   } while (0)
 #endif
 
+// The Neumann iterations for m > 128 (m % 4 == 0, 16-byte aligned rows of
+// H^T H): H^T H (up to 1 MB) does not fit in LDS and is read from memory each
+// iteration by every solve block, where it stays L2-resident.  Wave w owns the
+// 16-row blocks w, w + 4, ... (RBW of them; a block past the last runs on a
+// clamped row, branch-free, and is never stored).  The A fragments are loaded
+// NB - 1 k slices ahead of the MFMAs that use them and the stream runs on
+// across iteration boundaries (H^T H does not change), so its latency is paid
+// once; only the B fragment, read from Y_k in LDS, waits for the barrier that
+// ends an iteration.  Columns k >= m of H^T H are read at a clamped position:
+// they meet rows of Y_k that are zero.  Returns the buffer holding the result.
+template <int RBW>
+__device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int ldh, int m, int mp,
+                                              int iters, int LDE, const float* cinv,
+                                              const float* Bt, float* Yo, float* Yn) {
+  constexpr int NB = 3;
+  const int lane = lane_id(), wave = __builtin_amdgcn_readfirstlane(wave_id());
+  const int nsl = mp / 16, nrb = mp / 16;
+  const int kl = 4 * (lane >> 4);
+  unsigned rofs[RBW];
+#pragma unroll
+  for (int t = 0; t < RBW; ++t)
+    rofs[t] = (unsigned)min((wave + 4 * t) * 16 + (lane & 15), m - 1) * (unsigned)ldh;
+  floatx4 fa[NB][RBW];
+  auto load = [&](floatx4(&f)[RBW], int sl) {
+    const unsigned ko = (unsigned)min(sl * 16 + kl, m - 4);
+#pragma unroll
+    for (int t = 0; t < RBW; ++t) f[t] = *reinterpret_cast<const floatx4*>(HH + (rofs[t] + ko));
+  };
+  int lsl = 0;  // slice of the next load
+#pragma unroll
+  for (int j = 0; j + 1 < NB; ++j) {
+    load(fa[j], lsl);
+    lsl = (lsl + 1 == nsl) ? 0 : lsl + 1;
+  }
+  floatx4 acc[RBW];
+#pragma unroll
+  for (int t = 0; t < RBW; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int yl = (lane & 15) * LDE + kl;
+  const int total = iters * nsl;
+  int sl = 0;  // slice of the next MFMAs
+  for (int g0 = 0; g0 < total; g0 += NB) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      // the loads run unconditionally (past the end they re-read H^T H), so
+      // the buffers need no copies between unrolled steps
+      load(fa[(j + NB - 1) % NB], lsl);
+      lsl = (lsl + 1 == nsl) ? 0 : lsl + 1;
+      if (g0 + j < total) {
+        const floatx4 fb = *reinterpret_cast<const floatx4*>(Yo + yl + sl * 16);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int t = 0; t < RBW; ++t)
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[j][t][q], fb[q], acc[t], 0, 0, 0);
+        if (++sl == nsl) {
+          // Y_{k+1} rows of the wave's blocks: every read first, then the writes
+          sl = 0;
+          floatx4 bv[RBW], cv[RBW];
+#pragma unroll
+          for (int t = 0; t < RBW; ++t) {
+            const int row = min(wave + 4 * t, nrb - 1) * 16 + kl;
+            bv[t] = *reinterpret_cast<const floatx4*>(Bt + (lane & 15) * LDE + row);
+            cv[t] = *reinterpret_cast<const floatx4*>(cinv + row);
+          }
+#pragma unroll
+          for (int t = 0; t < RBW; ++t) {
+            const int rb = wave + 4 * t;
+            if (rb < nrb)
+              *reinterpret_cast<floatx4*>(Yn + (lane & 15) * LDE + rb * 16 + kl) =
+                  bv[t] + acc[t] * cv[t];
+            acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+          }
+          lds_barrier();
+          float* tt = Yo;
+          Yo = Yn;
+          Yn = tt;
+        }
+      }
+    }
+  }
+  return Yo;
+}
+
 template <bool SMALL>
 __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned char* sraw) {
   LST_SMARK(0);
@@ -641,10 +724,35 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
     r = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   } else {
     LST_SMARK(2);
+    // At most two rows per thread (m <= 512) with at most 34 partials each:
+    // every load is issued, at a clamped valid address, before the first is
+    // used (partials past the 34th, never present for m <= 512, are summed
+    // one by one).
+    constexpr int kMaxHapBig = 2 * (512 / 32 + 1);
+    const int nh = c.n_hap;
+    float hv[2][kMaxHapBig];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const float* hp = c.hap + (size_t)min(tid + 256 * h, m - 1) * nh;
+#pragma unroll
+      for (int p = 0; p < kMaxHapBig; ++p) hv[h][p] = hp[min(p, nh - 1)];
+    }
     float rmax = 0.f;
-    for (int i = tid; i < m; i += 256) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int i = tid + 256 * h;
       float sabs = 0.f;
-      for (int p = 0; p < c.n_hap; ++p) sabs += c.hap[(size_t)i * c.n_hap + p];
+#pragma unroll
+      for (int p = 0; p < kMaxHapBig; ++p) sabs += p < nh ? hv[h][p] : 0.f;
+      if (i < m) {
+        for (int p = kMaxHapBig; p < nh; ++p) sabs += c.hap[(size_t)i * nh + p];
+        const float ri = sabs * cinv[i];
+        rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
+      }
+    }
+    for (int i = tid + 512; i < m; i += 256) {  // m > 512: not reached (m_max <= 512)
+      float sabs = 0.f;
+      for (int p = 0; p < nh; ++p) sabs += c.hap[(size_t)i * nh + p];
       const float ri = sabs * cinv[i];
       rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
     }
@@ -656,8 +764,39 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   }
   LST_SMARK(3);
 
+  // m > 128 with m % 4 == 0 and 16-byte aligned rows of H^T H and P: vector
+  // loads (the right-hand side and the iterations)
+  const bool gvec = !SMALL && m % 4 == 0 && d % 4 == 0 && ldh % 4 == 0 &&
+                    ((uintptr_t)HH & 15) == 0 && ((uintptr_t)P & 15) == 0;
   if (r < 0.5f) {
-    if (!SMALL) {
+    if (gvec) {
+      // B^T = -(P^T_blk) diag(1/c)^T, Y0 = B^T: 16-byte loads, slot e = row
+      // e / 4, columns c0 + 4 (e % 4) ... + 3 (all in or all out of range)
+      const int nq = 4 * mp;
+      for (int e0 = 0; e0 < nq; e0 += 256 * 8) {
+        floatx4 pv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int e = e0 + tid + 256 * u;
+          const int i = min(e >> 2, m - 1), col = min(c0 + 4 * (e & 3), d - 4);
+          pv[u] = *reinterpret_cast<const floatx4*>(P + (size_t)i * ldp + col);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int e = e0 + tid + 256 * u;
+          if (e < nq) {
+            const int i = e >> 2, cq = 4 * (e & 3);
+            const bool ok = i < m && c0 + cq < d;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const float val = ok ? -pv[u][v] * cinv[i] : 0.f;
+              Bt[(cq + v) * LDE + i] = val;
+              Y0[(cq + v) * LDE + i] = val;
+            }
+          }
+        }
+      }
+    } else if (!SMALL) {
       // B^T = -(P^T_blk) diag(1/c)^T, Y0 = B^T.
       for (int e0 = 0; e0 < kSolveCols * mp; e0 += 256 * 8) {
         float pv[8];
@@ -789,6 +928,9 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
         Yo = Yn;
         Yn = tt;
       }
+    } else if (gvec) {
+      Yo = (nrb <= 16) ? neumann_mem<4>(HH, ldh, m, mp, iters, LDE, cinv, Bt, Yo, Yn)
+                       : neumann_mem<8>(HH, ldh, m, mp, iters, LDE, cinv, Bt, Yo, Yn);
     } else {
     for (int it = 0; it < iters; ++it) {
       floatx4 acc[RBW];

@@ -68,6 +68,22 @@ def test_several_tiles_ragged(gpu_lib):
     _assert(reports, W_rel)
 
 
+def test_wide_minibatch_ragged(gpu_lib):
+    """m = 260 > 128: the Woodbury solve reads H^T H from memory with 16-byte loads;
+    260 is not a multiple of 16 (clamped row blocks and k slices), r is about 0.3,
+    so a dozen Neumann iterations run."""
+    cfg = _cfg(D=3000, d=64, m=260, K=3, lr=5e-3, pad_frac=0.1, entropy=112)
+    reports, W_rel, _ = run_parity(cfg, 4)
+    _assert(reports, W_rel)
+
+
+def test_wide_minibatch_unaligned(gpu_lib):
+    """m = 150 and d = 70 (rows not 16-byte aligned): the scalar-load solve path."""
+    cfg = _cfg(D=2000, d=70, m=150, K=2, lr=5e-3, entropy=113)
+    reports, W_rel, _ = run_parity(cfg, 4)
+    _assert(reports, W_rel)
+
+
 def test_single_example(gpu_lib):
     cfg = _cfg(D=300, d=16, m=1, K=4, lr=2e-2, entropy=103)
     reports, W_rel, _ = run_parity(cfg, 30)
