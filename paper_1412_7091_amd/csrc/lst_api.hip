@@ -322,8 +322,9 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     L.kind[0] = TK_GEMM; L.kind[1] = TK_SOLVE; L.kind[2] = TK_YY; L.kind[3] = TK_SCALARS;
     if (m > 128) {
       // the solve (H^T H read from memory, many iterations' MFMAs per block)
-      // outlasts the GEMM tiles: its blocks go first
-      L.kind[0] = TK_SOLVE; L.kind[1] = TK_GEMM;
+      // outlasts the GEMM tiles, and the merges of Y^T Y take long for long
+      // target lists: their blocks go first
+      L.kind[0] = TK_SOLVE; L.kind[1] = TK_YY; L.kind[2] = TK_GEMM;
     }
     GemmBatch& g = L.gemm;
     g.np = 4;

@@ -240,8 +240,11 @@ __device__ __forceinline__ void task_targets(const StepCtx& c, int local, unsign
 // One thread per (i, j), i <= j, merging the two sorted target lists; a row
 // that repeats inside an example contributes the sum of its values.  A block
 // owns a 16 x 16 block of pairs on or above the diagonal and stages the 32
-// lists it needs in LDS (K <= 64; longer lists are merged from memory).
+// lists it needs in LDS (K <= 64, every load in flight at once; longer lists
+// are merged from memory), with a row stride of 65 words so that lanes at the
+// same position of different lists fall in different LDS banks.
 constexpr int kGramKMax = 64;
+constexpr int kGramLd = kGramKMax + 1;
 
 __device__ __forceinline__ float merge_dot(const int* ri, const float* vi, int ni, const int* rj,
                                            const float* vj, int nj) {
@@ -264,9 +267,9 @@ __device__ __forceinline__ float merge_dot(const int* ri, const float* vi, int n
 }
 
 __device__ __forceinline__ void task_yy(const StepCtx& c, int local, unsigned char* sraw) {
-  int(*srow)[kGramKMax] = reinterpret_cast<int(*)[kGramKMax]>(sraw);
-  float(*sval)[kGramKMax] = reinterpret_cast<float(*)[kGramKMax]>(sraw + 32 * kGramKMax * 4);
-  int* scnt = reinterpret_cast<int*>(sraw + 2 * 32 * kGramKMax * 4);
+  int(*srow)[kGramLd] = reinterpret_cast<int(*)[kGramLd]>(sraw);
+  float(*sval)[kGramLd] = reinterpret_cast<float(*)[kGramLd]>(sraw + 32 * kGramLd * 4);
+  int* scnt = reinterpret_cast<int*>(sraw + 2 * 32 * kGramLd * 4);
   const int nb = (c.m + 15) / 16;
   int bi = 0, rem = local;
   while (rem >= nb - bi) { rem -= nb - bi; ++bi; }
@@ -274,19 +277,34 @@ __device__ __forceinline__ void task_yy(const StepCtx& c, int local, unsigned ch
   const int I0 = bi * 16, J0 = bj * 16;
   const bool staged = c.K <= kGramKMax;
   if (staged) {
-    for (int e = threadIdx.x; e < 32 * c.K; e += blockDim.x) {
-      const int l = e / c.K, k = e - l * c.K;
-      const int ex = (l < 16) ? I0 + l : J0 + l - 16;
-      if (ex < c.m) {
-        srow[l][k] = c.ex_row[(size_t)ex * c.K + k];
-        sval[l][k] = c.ex_val[(size_t)ex * c.K + k];
-      }
-    }
+    constexpr int kPer = 32 * kGramKMax / 256;  // list entries per thread
+    int rv[kPer];
+    float vv[kPer];
+    int cnt = 0;
     if (threadIdx.x < 32) {
       const int l = threadIdx.x;
       const int ex = (l < 16) ? I0 + l : J0 + l - 16;
-      scnt[l] = ex < c.m ? c.ex_cnt[ex] : 0;
+      cnt = ex < c.m ? c.ex_cnt[ex] : 0;
     }
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = threadIdx.x + 256 * u;
+      const int l = e / c.K, k = e - l * c.K;
+      const int ex = (l < 16) ? I0 + l : J0 + l - 16;
+      const size_t at = (e < 32 * c.K && ex < c.m) ? (size_t)ex * c.K + k : 0;
+      rv[u] = c.ex_row[at];
+      vv[u] = c.ex_val[at];
+    }
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = threadIdx.x + 256 * u;
+      const int l = e / c.K, k = e - l * c.K;
+      if (e < 32 * c.K) {
+        srow[l][k] = rv[u];
+        sval[l][k] = vv[u];
+      }
+    }
+    if (threadIdx.x < 32) scnt[threadIdx.x] = cnt;
     __syncthreads();
   }
   const int li = threadIdx.x >> 4, lj = threadIdx.x & 15;
@@ -1065,6 +1083,7 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
 // row is written once and in a fixed order.  Each pair records in own[] the
 // row it owns (or -1); launch 4 clears the hash slots from that record.
 constexpr int kScatterSlotsPerWave = 1;
+constexpr int kScatterBatch = 4;
 
 __device__ __forceinline__ void scatter_slot(const StepCtx& c, int e);
 
@@ -1122,6 +1141,41 @@ __device__ __forceinline__ void scatter_slot(const StepCtx& c, int e) {
         cj = one_hot ? c.cs[j] : -sum;
       }
       unsigned long long bal = __ballot(found);
+      if (vec) {
+        // kScatterBatch examples at a time: their rows of X are all in flight
+        // before the first is added (a row of a common target, in nearly every
+        // example, would otherwise pay the memory latency once per example);
+        // the additions keep increasing example order.
+        while (bal) {
+          float w[kScatterBatch];
+          float4 x[kScatterBatch][4];
+          bool on[kScatterBatch];
+#pragma unroll
+          for (int u = 0; u < kScatterBatch; ++u) {
+            on[u] = bal != 0;
+            const int src = on[u] ? __ffsll((long long)bal) - 1 : 0;
+            bal &= bal - 1;
+            w[u] = __shfl(cj, src);
+            const float* xr = c.X + (size_t)(j0 + src) * c.d;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int col = cg + q * 256 + lane * 4;
+              if (col < c.d) x[u][q] = *reinterpret_cast<const float4*>(xr + col);
+            }
+          }
+#pragma unroll
+          for (int u = 0; u < kScatterBatch; ++u) {
+            if (!on[u]) break;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int col = cg + q * 256 + lane * 4;
+              if (col >= c.d) continue;
+              acc[q].x += w[u] * x[u][q].x; acc[q].y += w[u] * x[u][q].y;
+              acc[q].z += w[u] * x[u][q].z; acc[q].w += w[u] * x[u][q].w;
+            }
+          }
+        }
+      }
       while (bal) {
         const int src = __ffsll((long long)bal) - 1;
         bal &= bal - 1;
@@ -1131,15 +1185,10 @@ __device__ __forceinline__ void scatter_slot(const StepCtx& c, int e) {
         for (int q = 0; q < 4; ++q) {
           const int col = cg + q * 256 + lane * 4;
           if (col >= c.d) continue;
-          if (vec) {
-            const float4 x = *reinterpret_cast<const float4*>(xr + col);
-            acc[q].x += w * x.x; acc[q].y += w * x.y; acc[q].z += w * x.z; acc[q].w += w * x.w;
-          } else {
-            acc[q].x += w * xr[col];
-            if (col + 1 < c.d) acc[q].y += w * xr[col + 1];
-            if (col + 2 < c.d) acc[q].z += w * xr[col + 2];
-            if (col + 3 < c.d) acc[q].w += w * xr[col + 3];
-          }
+          acc[q].x += w * xr[col];
+          if (col + 1 < c.d) acc[q].y += w * xr[col + 1];
+          if (col + 2 < c.d) acc[q].z += w * xr[col + 2];
+          if (col + 3 < c.d) acc[q].w += w * xr[col + 3];
         }
       }
     }
@@ -1288,7 +1337,7 @@ static size_t lds_of(int kind, int stages, int m, int K) {
   switch (kind) {
     case TK_GEMM: return (size_t)stages * kPanelStageBytes;
     case TK_TARGETS: return targets_lds_bytes(K);
-    case TK_YY: return 2 * 32 * kGramKMax * 4 + 32 * 4;
+    case TK_YY: return 2 * 32 * kGramLd * 4 + 32 * 4;
     case TK_SOLVE: return solve_lds_bytes(m);
     default: return 0;
   }
