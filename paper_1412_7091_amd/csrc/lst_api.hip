@@ -79,8 +79,15 @@ struct lst_state {
 
 namespace {
 
-// GEMM tile edge of launch 1 (also fixes the number of h^T Q h partials).
-constexpr int kLaunch1Tile = 32;
+// GEMM tile edge of launch 1: 64 when m > 128 and 64 x 64 tiles alone fill
+// the 256 compute units (half the bytes per output of 32 x 32 tiles), else 32.
+// The edge also fixes the number of h^T Q h and |H^T H| partials.
+int launch1_tile(int d, int m) {
+  return (m > 128 && (size_t)((m + 63) / 64) * ((3 * d + m + 63) / 64) >= 256) ? 64 : 32;
+}
+// Stages of launch 1's 64 x 64 tiles: four (64 KB), so that two tiles share a
+// compute unit and the tiles run in one round.
+constexpr int kLaunch1Stages64 = 4;
 
 struct DeviceGuard {
   int prev = -1;
@@ -252,9 +259,9 @@ int check_step_args(lst_state* s, int32_t m, int32_t K, const float* H, const in
 }
 
 // Partial sums of |H^T H| per row written by the first GEMM: two per tile
-// column that holds columns of H^T H (Z0 columns [3d, 3d + m)).
-int hap_count(int d, int m) {
-  const int first = 3 * d / kLaunch1Tile, end = (3 * d + m + kLaunch1Tile - 1) / kLaunch1Tile;
+// column (edge t) that holds columns of H^T H (Z0 columns [3d, 3d + m)).
+int hap_count(int d, int m, int t) {
+  const int first = 3 * d / t, end = (3 * d + m + t - 1) / t;
   return 2 * (end - first);
 }
 
@@ -289,8 +296,9 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
   c.Z0 = s->Z0; c.ld0 = s->ld0;
   c.G = s->G; c.Yh = s->Yh; c.NP = s->NP; c.aH = s->aH; c.bH = s->bH;
   c.X = s->X; c.T = s->T; c.UHa = s->UHa;
-  c.c1p = s->c1p; c.ld_c1p = s->n_c1p; c.n_c1p = s->n_c1p;
-  c.hap = s->hap; c.n_hap = hap_count(d, m);
+  const int t1 = launch1_tile(d, m);
+  c.c1p = s->c1p; c.ld_c1p = s->n_c1p; c.n_c1p = 2 * ((d + t1 - 1) / t1);
+  c.hap = s->hap; c.n_hap = hap_count(d, m, t1);
   c.a = s->a; c.b = s->b; c.cs = s->cs; c.yyd = s->yyd;
   c.loss = loss; c.grad = grad_H;
   c.ex_row = s->ex_row; c.ex_val = s->ex_val; c.ex_cnt = s->ex_cnt;
@@ -309,12 +317,14 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
                       s->Z0, s->ld0, 1.f, 0.f, EPI_STORE);
     p1.dotp = s->c1p; p1.ld_dotp = s->n_c1p; p1.dot_ncols = d;  // h_i^T H^_i partials
     p1.absp = s->hap; p1.ld_absp = c.n_hap; p1.abs_col0 = 3 * d;  // |H^T H| row partials
+    p1.tile = t1;
     p1.dot_h = H; p1.ld_doth = d;
     L.lk = 1;
     L.timing_slot = 0;
     hipEvent_t e0, e1;
     OK_OR_RETURN(prof_pair(s, PH_LAUNCH1, &e0, &e1));
-    HIPCHK(step_launch(c, L, stages_for(L.gemm), st, e0, e1));
+    HIPCHK(step_launch(c, L, stages_for(L.gemm, t1 == 64 ? kLaunch1Stages64 : kMaxStages), st,
+                       e0, e1));
   }
   {  // launch 2: Y^, C1, C2, C2^T ; solve ; Y^T Y ; per-example scalars
     StepLaunch L{};
@@ -489,8 +499,9 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
   };
   if (rc != LST_OK) return fail(rc);
   s->ld0 = (3 * d + m + 3) / 4 * 4;
-  s->n_c1p = 2 * ((d + kLaunch1Tile - 1) / kLaunch1Tile);
-  s->n_hap_max = hap_count(d, m);
+  s->n_c1p = 2 * ((d + 31) / 32);  // the most partials (32-column tiles)
+  s->n_hap_max = hap_count(d, m, 32) > hap_count(d, m, 64) ? hap_count(d, m, 32)
+                                                           : hap_count(d, m, 64);
   s->hbits = 1;
   while ((1 << s->hbits) < 2 * m * K) ++s->hbits;
   const int hsize = 1 << s->hbits;

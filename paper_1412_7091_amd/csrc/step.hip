@@ -1263,10 +1263,19 @@ constexpr LaunchMasks kLaunchMasks[5] = {
      TILE32 | TILE64},
 };
 
+// The launch-1 kernel built for m > 128 also compiles 64 x 64 tiles: a large
+// stacked product fills the chip with them and fetches half the bytes per
+// output of 32 x 32 tiles.
+constexpr LaunchMasks launch_masks(int lk, bool small) {
+  LaunchMasks M = kLaunchMasks[lk];
+  if (!small && lk == 1) M.tiles |= TILE64;
+  return M;
+}
+
 template <bool SMALLM, int W, int LK>
 __device__ __forceinline__ void run_task(const StepCtx& c, const StepLaunch& L, int t, int local,
                                          unsigned char* sraw) {
-  constexpr LaunchMasks M = kLaunchMasks[LK];
+  constexpr LaunchMasks M = launch_masks(LK, SMALLM);
   const int kind = L.kind[t];
   if constexpr ((M.tasks >> TK_GEMM) & 1u) {
     if (kind == TK_GEMM) {
@@ -1401,7 +1410,9 @@ static const void* kfn() {
 // combination that is not built.
 static const void* step_kernel_for(int lk, bool small, int w16) {
   switch (lk) {
-    case 1: return w16 ? kfn<true, 4, 1>() : kfn<true, 1, 1>();
+    case 1:
+      if (small) return w16 ? kfn<true, 4, 1>() : kfn<true, 1, 1>();
+      return w16 ? kfn<false, 4, 1>() : kfn<false, 1, 1>();
     case 2:
       if (small) return w16 ? kfn<true, 4, 2>() : kfn<true, 1, 2>();
       return w16 ? kfn<false, 4, 2>() : kfn<false, 1, 2>();
@@ -1415,7 +1426,7 @@ hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t 
                        hipEvent_t ev0, hipEvent_t ev1) {
   if (L.lk < 1 || L.lk > 4) return hipErrorInvalidValue;
   if (stages < 2 || (size_t)stages * kPanelStageBytes > kStepLdsMax) return hipErrorInvalidValue;
-  const LaunchMasks& M = kLaunchMasks[L.lk];
+  const LaunchMasks M = launch_masks(L.lk, c.m <= 128);
   L.gemm.stages = stages;
   L.gemm.timing_slot = L.timing_slot;
   size_t lds = 0;

@@ -84,6 +84,14 @@ def test_wide_minibatch_unaligned(gpu_lib):
     _assert(reports, W_rel)
 
 
+def test_wide_tiles64_ragged(gpu_lib):
+    """m = 510, d = 1000: launch 1 runs 64 x 64 tiles (its row-sum partials counted per
+    64-column tile), ragged in both m and d."""
+    cfg = _cfg(D=4001, d=1000, m=510, K=5, lr=1e-3, entropy=114)
+    reports, W_rel, _ = run_parity(cfg, 2)
+    _assert(reports, W_rel)
+
+
 def test_single_example(gpu_lib):
     cfg = _cfg(D=300, d=16, m=1, K=4, lr=2e-2, entropy=103)
     reports, W_rel, _ = run_parity(cfg, 30)
