@@ -276,7 +276,8 @@ typedef struct lst_input lst_input;
 
 /*
  * lst_input_init -- create an input layer; W_in (device, D_in x d) is copied.
- * D_in >= 1, 1 <= d <= 4096.  Synchronous.
+ * D_in >= 1, 1 <= d <= 4096.  Besides W_in the layer holds a 1.8 MB table of
+ * the rows of one update.  Synchronous.
  */
 int lst_input_init(lst_input** out, int64_t D_in, int32_t d, const float* W_in,
                    void* hip_stream);

@@ -66,6 +66,14 @@ def test_input_layer_full_size(gpu_lib):
     _check_steps(cfg, 2, 1e-3)
 
 
+def test_input_layer_max_slots_zipf(gpu_lib):
+    """m K = 65 536 slots (the largest call), Zipf 1.1 inputs: rows held by thousands of
+    slots next to rows held by one; two calls, so the row table must be left empty."""
+    cfg = WorkloadConfig(name="inpmax", D=20000, d=40, m=512, K=128, idx_dist="zipf",
+                         zipf_s=1.1, distinct=False, val_dist="normal", entropy=4300)
+    _check_steps(cfg, 2, 1e-3)
+
+
 def test_input_layer_bad_index_leaves_W(gpu_lib):
     import torch
 
@@ -81,4 +89,11 @@ def test_input_layer_bad_index_leaves_W(gpu_lib):
                  torch.from_numpy(G).cuda(), 0.1)
     assert layer.sync() == lst.LST_EINDEX
     assert np.array_equal(layer.get_W().cpu().numpy(), W)
+    # the rejected call still emptied its row table: the next call is exact
+    G1, idx1, val1 = wl.batch(1)
+    layer.update(torch.from_numpy(idx1).cuda(), torch.from_numpy(val1).cuda(),
+                 torch.from_numpy(G1).cuda(), 0.1)
+    assert layer.sync() == 0
+    W_ref = input_layer.update(W.astype(np.float64), idx1, val1, G1, 0.1)
+    assert rel(layer.get_W().cpu().numpy(), W_ref) < 1e-6
     layer.close()
