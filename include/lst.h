@@ -284,7 +284,8 @@ int lst_input_init(lst_input** out, int64_t D_in, int32_t d, const float* W_in,
 
 /*
  * lst_input_forward -- A = X W_in: row i of A (device, m x d) is
- * sum_k val[i][k] W_in[idx[i][k], :], the pairs added in k order.
+ * sum_k val[i][k] W_in[idx[i][k], :], the pairs added in k order (for K > 16:
+ * in k order within each quarter of the list, the quarters then added in order).
  *   idx, val (device) m x K.  m, K >= 1, m * K <= 65536.
  * An index outside [-1, D_in) sets the sticky status LST_EINDEX (reported by
  * lst_input_sync) and its pair is left out of A.

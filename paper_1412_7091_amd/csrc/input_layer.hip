@@ -165,6 +165,72 @@ __global__ __launch_bounds__(256) void input_forward_kernel(const float* __restr
   }
 }
 
+// Long inputs (K > kInputSplitK): one block per (example, 256-column chunk);
+// wave w sums the pairs of the w-th quarter of the example's list in order,
+// and the four partial sums are added in wave order, so the result does not
+// depend on timing.
+constexpr int kInputSplitK = 16;
+
+template <bool VEC>
+__global__ __launch_bounds__(256) void input_forward_split_kernel(
+    const float* __restrict__ W, int64_t D, int d, const int32_t* __restrict__ idx,
+    const float* __restrict__ val, int m, int K, float* __restrict__ A) {
+  __shared__ float4 part[3][64];
+  const int nch = (d + 255) / 256;
+  const int i = blockIdx.x / nch, c0 = (blockIdx.x % nch) * 256;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = c0 + 4 * lane;
+  const int q = (K + 3) / 4, kb = wave * q, ke = min(K, kb + q);
+  const int32_t* ip = idx + (size_t)i * K;
+  const float* vp = val + (size_t)i * K;
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+  for (int k0 = kb; k0 < ke; k0 += kInputBatch) {
+    float4 w[kInputBatch];
+    float v[kInputBatch];
+#pragma unroll
+    for (int u = 0; u < kInputBatch; ++u) {
+      const int k = k0 + u;
+      const int r = k < ke ? ip[k] : -1;
+      const bool on = r >= 0 && (int64_t)r < D;
+      v[u] = on ? vp[k] : 0.f;
+      const float* row = W + (size_t)(on ? r : 0) * d;
+      w[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (on && col < d) {
+        if (VEC) {
+          w[u] = *reinterpret_cast<const float4*>(row + col);
+        } else {
+          w[u].x = row[col];
+          if (col + 1 < d) w[u].y = row[col + 1];
+          if (col + 2 < d) w[u].z = row[col + 2];
+          if (col + 3 < d) w[u].w = row[col + 3];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kInputBatch; ++u) {
+      if (k0 + u >= ke) break;
+      a0 += v[u] * w[u].x; a1 += v[u] * w[u].y; a2 += v[u] * w[u].z; a3 += v[u] * w[u].w;
+    }
+  }
+  if (wave > 0) part[wave - 1][lane] = make_float4(a0, a1, a2, a3);
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int p = 0; p < 3; ++p) {
+    const float4 o = part[p][lane];
+    a0 += o.x; a1 += o.y; a2 += o.z; a3 += o.w;
+  }
+  float* out = A + (size_t)i * d;
+  if (VEC) {
+    if (col < d) *reinterpret_cast<float4*>(out + col) = make_float4(a0, a1, a2, a3);
+  } else {
+    if (col < d) out[col] = a0;
+    if (col + 1 < d) out[col + 1] = a1;
+    if (col + 2 < d) out[col + 2] = a2;
+    if (col + 3 < d) out[col + 3] = a3;
+  }
+}
+
 // One wave per slot e = i*K + k.  The wave of the first slot holding row r
 // (from the table) records the entry it owns, then sums v dA over every slot
 // holding r, in slot order, and updates the row: at once when the row has one
@@ -348,12 +414,21 @@ int lst_input_forward(lst_input* s, int32_t m, int32_t K, const int32_t* idx, co
   hipLaunchKernelGGL(input_validate_kernel, dim3((n + 255) / 256), dim3(256), 0, s->stream, idx,
                      n, s->D, s->flags);
   const bool vec = (s->d % 4 == 0) && (((uintptr_t)A & 15) == 0);
-  if (vec)
+  if (K > kInputSplitK) {
+    const dim3 grid((unsigned)(m * ((s->d + 255) / 256)));
+    if (vec)
+      hipLaunchKernelGGL(input_forward_split_kernel<true>, grid, dim3(256), 0, s->stream, s->W,
+                         s->D, s->d, idx, val, m, K, A);
+    else
+      hipLaunchKernelGGL(input_forward_split_kernel<false>, grid, dim3(256), 0, s->stream, s->W,
+                         s->D, s->d, idx, val, m, K, A);
+  } else if (vec) {
     hipLaunchKernelGGL(input_forward_kernel<true>, dim3((m + 3) / 4), dim3(256), 0, s->stream,
                        s->W, s->D, s->d, idx, val, m, K, A);
-  else
+  } else {
     hipLaunchKernelGGL(input_forward_kernel<false>, dim3((m + 3) / 4), dim3(256), 0, s->stream,
                        s->W, s->D, s->d, idx, val, m, K, A);
+  }
   return hipGetLastError() == hipSuccess ? LST_OK : LST_EHIP;
 }
 

@@ -54,6 +54,15 @@ def test_input_layer_small_with_repeats(gpu_lib, d):
     _check_steps(cfg, 4, 0.05)
 
 
+@pytest.mark.parametrize("d", [300, 37])
+def test_input_layer_long_lists(gpu_lib, d):
+    """K = 300 > 16: the forward pass splits each list into quarters over four waves."""
+    cfg = WorkloadConfig(name="inpl", D=3000, d=d, m=12, K=300, idx_dist="uniform",
+                         distinct=False, val_dist="normal", pad_frac=0.1, dup_frac=0.2,
+                         entropy=4400 + d)
+    _check_steps(cfg, 2, 0.01)
+
+
 def test_input_layer_zipf_shared_rows(gpu_lib):
     cfg = WorkloadConfig(name="inpz", D=5000, d=64, m=128, K=8, idx_dist="zipf", zipf_s=1.1,
                          distinct=True, val_dist="one", entropy=4100)
