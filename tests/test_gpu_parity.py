@@ -92,6 +92,15 @@ def test_wide_tiles64_ragged(gpu_lib):
     _assert(reports, W_rel)
 
 
+def test_long_target_lists(gpu_lib):
+    """K = 1024 (the largest list): Y^T Y merges its lists from memory (K > 64), the
+    targets and the scatter walk long ordered lists; duplicates and padding included."""
+    cfg = _cfg(D=20011, d=48, m=16, K=1024, lr=5e-3, pad_frac=0.1, dup_frac=0.1,
+               entropy=115)
+    reports, W_rel, _ = run_parity(cfg, 3, V_check_untouched=True)
+    _assert(reports, W_rel)
+
+
 def test_single_example(gpu_lib):
     cfg = _cfg(D=300, d=16, m=1, K=4, lr=2e-2, entropy=103)
     reports, W_rel, _ = run_parity(cfg, 30)
