@@ -37,7 +37,8 @@ struct lst_state {
         *a = nullptr, *b = nullptr, *cs = nullptr, *T = nullptr, *X = nullptr,
         *ex_val = nullptr, *solve_ws = nullptr, *UHa = nullptr, *c1p = nullptr, *yyd = nullptr,
         *hap = nullptr;
-  int *ex_row = nullptr, *ex_cnt = nullptr, *hkey = nullptr, *hmin = nullptr, *touched = nullptr,
+  int *ex_row = nullptr, *ex_cnt = nullptr, *hkey = nullptr, *hmin = nullptr, *hcnt = nullptr,
+      *touched = nullptr,
       *own = nullptr, *count = nullptr;
   int last_slots = 0;  // m * K of the last factored step
   int hbits = 0;
@@ -302,7 +303,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
   c.a = s->a; c.b = s->b; c.cs = s->cs; c.yyd = s->yyd;
   c.loss = loss; c.grad = grad_H;
   c.ex_row = s->ex_row; c.ex_val = s->ex_val; c.ex_cnt = s->ex_cnt;
-  c.hkey = s->hkey; c.hmin = s->hmin; c.hbits = s->hbits;
+  c.hkey = s->hkey; c.hmin = s->hmin; c.hcnt = s->hcnt; c.hbits = s->hbits;
   c.own = s->own; c.flags = fl; c.solve_ws = s->solve_ws;
   const float* Hh = s->Z0;          // H^ rows
   const float* UH = s->Z0 + d;      // (U H)^T rows
@@ -515,14 +516,16 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       (rc = dalloc(s, &s->solve_ws, solve_workspace_floats(m, d))) ||
       (rc = dalloc(s, &s->ex_row, (size_t)m * K)) || (rc = dalloc(s, &s->ex_val, (size_t)m * K)) ||
       (rc = dalloc(s, &s->ex_cnt, m)) || (rc = dalloc(s, &s->hkey, hsize)) ||
-      (rc = dalloc(s, &s->hmin, hsize)) || (rc = dalloc(s, &s->touched, (size_t)m * K)) ||
+      (rc = dalloc(s, &s->hmin, hsize)) || (rc = dalloc(s, &s->hcnt, hsize)) ||
+      (rc = dalloc(s, &s->touched, (size_t)m * K)) ||
       (rc = dalloc(s, &s->own, (size_t)m * K)) || (rc = dalloc(s, &s->count, 1)) ||
       (rc = dalloc(s, &s->UHa, md)) || (rc = dalloc(s, &s->yyd, m)) ||
       (rc = dalloc(s, &s->c1p, (size_t)m * s->n_c1p)) ||
       (rc = dalloc(s, &s->hap, (size_t)m * s->n_hap_max)))
     return fail(rc);
   if (fill_ints(s->hkey, -1, hsize, s->stream) != hipSuccess ||
-      fill_ints(s->hmin, 0x7fffffff, hsize, s->stream) != hipSuccess)
+      fill_ints(s->hmin, 0x7fffffff, hsize, s->stream) != hipSuccess ||
+      fill_ints(s->hcnt, 0, hsize, s->stream) != hipSuccess)
     return fail(LST_EHIP);
   if (cfg->cond_max > 0.f && (rc = ensure_vtmp(s))) return fail(rc);
   if (hipMemcpyAsync(s->V, V, (size_t)D * d * sizeof(float), hipMemcpyDeviceToDevice, s->stream) !=

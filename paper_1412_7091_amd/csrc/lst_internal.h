@@ -140,7 +140,8 @@ struct StepCtx {
   int* ex_row;  // m x K: each example's target rows, ascending (-1 after the valid ones)
   float* ex_val;
   int* ex_cnt;
-  int *hkey, *hmin;  // hash table of the step's target rows: smallest slot of each
+  int *hkey, *hmin, *hcnt;  // hash table of the step's target rows: smallest slot
+                            // and number of slots of each
   int hbits;
   int* own;      // m x K: the row of slot i*K + k if that slot owns the row's
                  // scatter in this step (its smallest slot), else -1

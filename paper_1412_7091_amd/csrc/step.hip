@@ -346,7 +346,8 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
   if (i >= c.m) return;
   const int lane = lane_id(), d = c.d;
   // Record, for every target row, the smallest slot i*K + k holding it (the
-  // owner of the row's scatter in launch 3): open addressing, at most half full.
+  // owner of the row's scatter in launch 3) and the number of slots holding it:
+  // open addressing, at most half full.
   {
     const int mask = (1 << c.hbits) - 1;
     for (int k = lane; k < c.K; k += 64) {
@@ -358,6 +359,7 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
         const int prev = atomicCAS(c.hkey + h, -1, r);
         if (prev == -1 || prev == r) {
           atomicMin(c.hmin + h, slot);
+          atomicAdd(c.hcnt + h, 1);
           break;
         }
         h = (h + 1) & mask;
@@ -1100,9 +1102,10 @@ __device__ __forceinline__ void scatter_slot(const StepCtx& c, int e) {
   const int i = e / c.K;
   const int r = c.idx[e];
   bool owner = false;
+  unsigned h = 0;
   if (r >= 0 && (int64_t)r < c.D) {
     const int mask = (1 << c.hbits) - 1;
-    unsigned h = row_hash(r, c.hbits);
+    h = row_hash(r, c.hbits);
     int probe = 0;
     while (probe <= mask && c.hkey[h] != r) {
       h = (h + 1) & mask;
@@ -1114,15 +1117,33 @@ __device__ __forceinline__ void scatter_slot(const StepCtx& c, int e) {
   if (!owner || c.flags[F_ERR]) return;
   const bool one_hot = c.loss_kind == LST_LOSS_SPHERICAL;
   const bool vec = (c.d % 4 == 0);
+  // slots holding r in this step: the examples are searched only until all
+  // have been met, and a row held by this slot alone takes its example's row
+  // of X directly (the same sum as the search would form: one term)
+  const int cnt = c.hcnt[h];
+  if (cnt == 1 && vec) {
+    const float w = one_hot ? c.cs[i] : -c.val[e];
+    const float* xr = c.X + (size_t)i * c.d;
+    float* vr = c.V + (size_t)r * c.d;
+    for (int col = 4 * lane; col < c.d; col += 256) {
+      const float4 x = *reinterpret_cast<const float4*>(xr + col);
+      float4 v = *reinterpret_cast<float4*>(vr + col);
+      v.x += 0.f + w * x.x; v.y += 0.f + w * x.y; v.z += 0.f + w * x.z; v.w += 0.f + w * x.w;
+      *reinterpret_cast<float4*>(vr + col) = v;
+    }
+    return;
+  }
   // columns in groups of 1024 (four 256-column chunks held in registers)
   for (int cg = 0; cg < c.d; cg += 1024) {
     float4 acc[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) acc[q] = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int j0 = i; j0 < c.m; j0 += 64) {
+    int met = 0;
+    for (int j0 = i; j0 < c.m && met < cnt; j0 += 64) {
       const int j = j0 + lane;
       float cj = 0.f;
       bool found = false;
+      int nrun = 0;
       if (j < c.m) {
         const int* rows = c.ex_row + (size_t)j * c.K;
         const float* vals = c.ex_val + (size_t)j * c.K;
@@ -1136,10 +1157,14 @@ __device__ __forceinline__ void scatter_slot(const StepCtx& c, int e) {
         while (lo < n && rows[lo] == r) {
           sum += vals[lo];
           ++lo;
+          ++nrun;
           found = true;
         }
         cj = one_hot ? c.cs[j] : -sum;
       }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) nrun += __shfl_xor(nrun, off);
+      met += nrun;
       unsigned long long bal = __ballot(found);
       if (vec) {
         // kScatterBatch examples at a time: their rows of X are all in flight
@@ -1224,6 +1249,7 @@ __device__ __forceinline__ void task_clear(const StepCtx& c, int local) {
       if (c.hkey[h] == r) {
         c.hkey[h] = -1;
         c.hmin[h] = 0x7fffffff;
+        c.hcnt[h] = 0;
         break;
       }
       h = (h + 1) & mask;
