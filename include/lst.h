@@ -296,7 +296,9 @@ int lst_input_forward(lst_input* s, int32_t m, int32_t K, const int32_t* idx, co
 /*
  * lst_input_update -- W_in <- W_in - lr X^T grad_A (section 2.2: W_in[u_k] -=
  * lr v_k grad_a for every pair of every example; pairs that share a row add
- * up, in (example, pair) order, and each row is written once).  grad_A
+ * up, in (example, pair) order, and each row is written once; a row named by
+ * 64 or more pairs is summed in that order over each sixteenth of the m K
+ * pairs, the sixteen sums then added in order).  grad_A
  * (device, m x d) is dL/dA.  lr > 0 and finite.  Rows no pair refers to are
  * not touched.  Skipped entirely (W_in unchanged) while the sticky status is
  * set, e.g. by an index outside [-1, D_in) in this call.

@@ -9,7 +9,9 @@
 // with no atomics on W_in.  A hash table (row -> first slot, number of slots)
 // built by a pass over the slots finds the owner of a row in O(1); a row held
 // by one slot is updated at once, a repeated row's owner scans the later slots
-// until it has met them all.
+// until it has met them all, and a row held by kInputHotSlots slots or more is
+// summed by a block of sixteen waves (fixed sixteenths of the slots, their sums
+// added in order).
 #include <math.h>
 #include <stdlib.h>
 
@@ -31,6 +33,9 @@ struct lst_input {
   int* hmin = nullptr;
   int* hcnt = nullptr;
   int* own = nullptr;
+  // rows held by at least kInputHotSlots slots, summed by input_hot_kernel
+  // ([0]: count, then the rows)
+  int* hot = nullptr;
 };
 
 namespace lst {
@@ -51,6 +56,10 @@ constexpr int kInputMaxSlots = 65536;
 constexpr int kInputHashBits = 17;
 constexpr int kInputHashSize = 1 << kInputHashBits;
 static_assert(kInputHashSize >= 2 * kInputMaxSlots, "the row table must stay half empty");
+// A row held by this many slots or more is summed by a block of 16 waves, each
+// over a fixed sixteenth of the slots (the partial sums then added in order).
+constexpr int kInputHotSlots = 64;
+constexpr int kInputMaxHot = kInputMaxSlots / kInputHotSlots;
 
 __device__ __forceinline__ unsigned input_hash(int r) {
   return ((unsigned)r * 2654435761u) >> (32 - kInputHashBits);
@@ -80,9 +89,11 @@ __global__ void input_insert_kernel(const int32_t* __restrict__ idx, int n, int6
   }
 }
 
-// Empties the entries recorded in own[] (one per distinct row).
-__global__ void input_clear_kernel(int* own, int n, int* hkey, int* hmin, int* hcnt) {
+// Empties the entries recorded in own[] (one per distinct row) and the list
+// of hot rows.
+__global__ void input_clear_kernel(int* own, int n, int* hkey, int* hmin, int* hcnt, int* hot) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e == 0) hot[0] = 0;
   if (e >= n) return;
   const int h = own[e];
   if (h < 0) return;
@@ -93,8 +104,9 @@ __global__ void input_clear_kernel(int* own, int n, int* hkey, int* hmin, int* h
 }
 
 // The empty table (init): every key -1, every smallest slot INT_MAX, counts 0.
-__global__ void input_table_init_kernel(int* hkey, int* hmin, int* hcnt, int* own) {
+__global__ void input_table_init_kernel(int* hkey, int* hmin, int* hcnt, int* own, int* hot) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e == 0) hot[0] = 0;
   if (e < kInputHashSize) {
     hkey[e] = -1;
     hmin[e] = 0x7fffffff;
@@ -107,7 +119,7 @@ __global__ void input_table_init_kernel(int* hkey, int* hmin, int* hcnt, int* ow
 // first result is used, so a long list pays the memory latency once per round.
 constexpr int kInputBatch = 8;
 // Slots whose rows of dA an owner wave has in flight at once.
-constexpr int kInputRows = 8;
+constexpr int kInputRows = 4;
 
 // A[i, :] = sum_k v_ik W[u_ik, :], one wave per example, pairs in order.
 // Columns in chunks of 256 (four per lane; 16-byte loads when VEC).
@@ -244,7 +256,7 @@ __global__ __launch_bounds__(256) void input_update_kernel(float* __restrict__ W
                                                            const float* __restrict__ gA, int n,
                                                            int K, float lr, const int* hkey,
                                                            const int* hmin, const int* hcnt,
-                                                           int* own, const int* flags) {
+                                                           int* own, int* hot, const int* flags) {
   const int e = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (e >= n) return;
   const int r = idx[e];
@@ -259,6 +271,10 @@ __global__ __launch_bounds__(256) void input_update_kernel(float* __restrict__ W
   if (lane == 0) own[e] = (int)h;
   if (*flags) return;
   const int cnt = hcnt[h];
+  if (cnt >= kInputHotSlots) {
+    if (lane == 0) hot[1 + atomicAdd(hot, 1)] = r;
+    return;
+  }
   const bool vec = (d % 4 == 0);
   // columns in groups of 1024 (four 256-column chunks per lane); one scan per group
   for (int cg = 0; cg < d; cg += 1024) {
@@ -343,6 +359,94 @@ __global__ __launch_bounds__(256) void input_update_kernel(float* __restrict__ W
   }
 }
 
+// Block b (1024 threads) sums the hot row hot[1 + b / nch] over columns
+// [256 (b % nch), +256): wave w adds v dA over the slots of the w-th sixteenth
+// of [0, n) that hold the row, in slot order; the sixteen partial sums are then
+// added in wave order and the row is updated once.  Blocks past the number of
+// hot rows exit.
+__global__ __launch_bounds__(1024) void input_hot_kernel(float* __restrict__ W, int d,
+                                                         const int32_t* __restrict__ idx,
+                                                         const float* __restrict__ val,
+                                                         const float* __restrict__ gA, int n,
+                                                         int K, float lr, const int* hot,
+                                                         const int* flags) {
+  __shared__ float4 part[16][64];
+  const int nch = (d + 255) / 256;
+  const int hid = blockIdx.x / nch;
+  if (hid >= hot[0] || *flags) return;
+  const int r = hot[1 + hid];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = (blockIdx.x % nch) * 256 + 4 * lane;
+  const bool vec = (d % 4 == 0);
+  const int span = (n + 15) / 16, sb = wave * span, se = min(n, sb + span);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s0 = sb; s0 < se; s0 += 64 * kInputBatch) {
+    unsigned long long hits[kInputBatch];
+    {
+      int x[kInputBatch];
+#pragma unroll
+      for (int u = 0; u < kInputBatch; ++u) {
+        const int s = s0 + 64 * u + lane;
+        x[u] = s < se ? idx[s] : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < kInputBatch; ++u) hits[u] = __ballot(x[u] == r);
+    }
+#pragma unroll
+    for (int u = 0; u < kInputBatch; ++u) {
+      unsigned long long hb = hits[u];
+      while (hb) {
+        int t[kInputRows];
+        bool on[kInputRows];
+#pragma unroll
+        for (int q = 0; q < kInputRows; ++q) {
+          on[q] = hb != 0;
+          t[q] = s0 + 64 * u + (on[q] ? __ffsll((long long)hb) - 1 : 0);
+          hb &= hb - 1;
+        }
+        float v[kInputRows];
+        float4 g[kInputRows];
+#pragma unroll
+        for (int q = 0; q < kInputRows; ++q) {
+          const int tq = on[q] ? t[q] : sb;
+          v[q] = val[tq];
+          const float* gr = gA + (size_t)(tq / K) * d;
+          g[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (on[q] && col < d) {
+            if (vec) {
+              g[q] = *reinterpret_cast<const float4*>(gr + col);
+            } else {
+              g[q].x = gr[col];
+              if (col + 1 < d) g[q].y = gr[col + 1];
+              if (col + 2 < d) g[q].z = gr[col + 2];
+              if (col + 3 < d) g[q].w = gr[col + 3];
+            }
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < kInputRows; ++q) {
+          if (!on[q]) break;
+          acc.x += v[q] * g[q].x; acc.y += v[q] * g[q].y;
+          acc.z += v[q] * g[q].z; acc.w += v[q] * g[q].w;
+        }
+      }
+    }
+  }
+  part[wave][lane] = acc;
+  __syncthreads();
+  if (wave != 0) return;
+  float4 sum = part[0][lane];
+  for (int w = 1; w < 16; ++w) {
+    const float4 o = part[w][lane];
+    sum.x += o.x; sum.y += o.y; sum.z += o.z; sum.w += o.w;
+  }
+  float* row = W + (size_t)r * d;
+  if (col < d) row[col] -= lr * sum.x;
+  if (col + 1 < d) row[col + 1] -= lr * sum.y;
+  if (col + 2 < d) row[col + 2] -= lr * sum.z;
+  if (col + 3 < d) row[col + 3] -= lr * sum.w;
+}
+
 int check_batch(lst_input* s, int32_t m, int32_t K, const int32_t* idx, const float* val) {
   if (!s || m < 1 || K < 1 || !idx || !val) return LST_EINVAL;
   if ((int64_t)m * K > kInputMaxSlots) return LST_EINVAL;
@@ -380,7 +484,7 @@ int lst_input_init(lst_input** out, int64_t D_in, int32_t d, const float* W_in,
   auto fail = [&](int code) {
     (void)hipStreamSynchronize(s->stream);
     for (void* p : {(void*)s->W, (void*)s->flags, (void*)s->hkey, (void*)s->hmin, (void*)s->hcnt,
-                    (void*)s->own})
+                    (void*)s->own, (void*)s->hot})
       if (p) (void)hipFree(p);
     delete s;
     return code;
@@ -391,10 +495,11 @@ int lst_input_init(lst_input** out, int64_t D_in, int32_t d, const float* W_in,
       hipMalloc((void**)&s->hkey, kInputHashSize * sizeof(int)) != hipSuccess ||
       hipMalloc((void**)&s->hmin, kInputHashSize * sizeof(int)) != hipSuccess ||
       hipMalloc((void**)&s->hcnt, kInputHashSize * sizeof(int)) != hipSuccess ||
-      hipMalloc((void**)&s->own, kInputMaxSlots * sizeof(int)) != hipSuccess)
+      hipMalloc((void**)&s->own, kInputMaxSlots * sizeof(int)) != hipSuccess ||
+      hipMalloc((void**)&s->hot, (1 + kInputMaxHot) * sizeof(int)) != hipSuccess)
     return fail(LST_ENOMEM);
   hipLaunchKernelGGL(input_table_init_kernel, dim3(kInputHashSize / 256), dim3(256), 0, s->stream,
-                     s->hkey, s->hmin, s->hcnt, s->own);
+                     s->hkey, s->hmin, s->hcnt, s->own, s->hot);
   if (hipMemsetAsync(s->flags, 0, sizeof(int), s->stream) != hipSuccess ||
       hipMemcpyAsync(s->W, W_in, (size_t)D_in * d * sizeof(float), hipMemcpyDeviceToDevice,
                      s->stream) != hipSuccess ||
@@ -443,9 +548,15 @@ int lst_input_update(lst_input* s, int32_t m, int32_t K, const int32_t* idx, con
                      s->D, s->hkey, s->hmin, s->hcnt, s->flags);
   hipLaunchKernelGGL(input_update_kernel, dim3((n + 3) / 4), dim3(256), 0, s->stream, s->W, s->D,
                      s->d,
-                     idx, val, grad_A, n, K, lr, s->hkey, s->hmin, s->hcnt, s->own, s->flags);
+                     idx, val, grad_A, n, K, lr, s->hkey, s->hmin, s->hcnt, s->own, s->hot,
+                     s->flags);
+  if (n >= kInputHotSlots) {
+    const int nch = (s->d + 255) / 256;
+    hipLaunchKernelGGL(input_hot_kernel, dim3((unsigned)((n / kInputHotSlots) * nch)), dim3(1024),
+                       0, s->stream, s->W, s->d, idx, val, grad_A, n, K, lr, s->hot, s->flags);
+  }
   hipLaunchKernelGGL(input_clear_kernel, dim3((n + 255) / 256), dim3(256), 0, s->stream, s->own, n,
-                     s->hkey, s->hmin, s->hcnt);
+                     s->hkey, s->hmin, s->hcnt, s->hot);
   return hipGetLastError() == hipSuccess ? LST_OK : LST_EHIP;
 }
 
@@ -478,7 +589,7 @@ void lst_input_free(lst_input* s) {
   DeviceScope g(s->device);
   (void)hipStreamSynchronize(s->stream);
   for (void* p : {(void*)s->W, (void*)s->flags, (void*)s->hkey, (void*)s->hmin, (void*)s->hcnt,
-                  (void*)s->own})
+                  (void*)s->own, (void*)s->hot})
     (void)hipFree(p);
   delete s;
 }
