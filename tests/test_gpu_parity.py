@@ -101,6 +101,16 @@ def test_long_target_lists(gpu_lib):
     _assert(reports, W_rel)
 
 
+@pytest.mark.parametrize("d", [40, 37])
+def test_hot_rows_zipf(gpu_lib, d):
+    """m K = 4096 Zipf 1.1 targets with repeats: rows held by hundreds of slots, whose
+    scatter owners search every later example (d = 37: the unaligned path)."""
+    cfg = _cfg(D=3000, d=d, m=64, K=64, lr=5e-3, idx_dist="zipf", zipf_s=1.1, distinct=False,
+               entropy=116 + d)
+    reports, W_rel, _ = run_parity(cfg, 3, V_check_untouched=True)
+    _assert(reports, W_rel)
+
+
 def test_single_example(gpu_lib):
     cfg = _cfg(D=300, d=16, m=1, K=4, lr=2e-2, entropy=103)
     reports, W_rel, _ = run_parity(cfg, 30)
