@@ -432,7 +432,8 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
         pre1[i][j][r] = 0.f;
         pre2[i][j][r] = 0.f;
         if (row >= P.M || col >= P.N) continue;
-        if ((epi_is<EPIS>(P, EPI_STORE) && P.beta != 0.f) || (epi_is<EPIS>(P, EPI_SYM) && row <= col)) {
+        if (((epi_is<EPIS>(P, EPI_STORE) || epi_is<EPIS>(P, EPI_SCALED)) && P.beta != 0.f) ||
+            (epi_is<EPIS>(P, EPI_SYM) && row <= col)) {
           pre1[i][j][r] = P.C[(size_t)row * P.ldc + col];
         } else if (epi_is<EPIS>(P, EPI_GRADT)) {
           // accumulator rows 2o and 2o + 1 (r even / odd) both feed output row o
@@ -520,6 +521,13 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
       for (int r = 0; r < 4; ++r) asm volatile("" ::"v"(pre1[i][j][r]), "v"(pre2[i][j][r]));
 
   LST_MARK(3);
+  // EPI_SCALED: the power-of-two scale from the trace of the previous product
+  // (exact, so the vector the products converge to does not depend on it).
+  float pscale = 1.f, tsum = 0.f;
+  if (epi_is<EPIS>(P, EPI_SCALED) && P.s1 != nullptr) {
+    const float t = *P.s1;
+    if (t > 0.f && isfinite(t)) pscale = ldexpf(1.f, max(-126, min(126, -2 * ilogbf(t))));
+  }
   // Element r of acc[i][j]: row 4*(lane/16) + r, column lane % 16 of its 16 x 16 block.
   float dsum[IB][4], asum[IB][4];
 #pragma unroll
@@ -556,8 +564,18 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
           }
         } else if (epi_is<EPIS>(P, EPI_PARTIAL)) {
           P.C[(size_t)z * P.M * P.N + (size_t)row * P.N + col] = v;
+        } else if (epi_is<EPIS>(P, EPI_SCALED)) {
+          const float o = P.alpha * pscale * v + P.beta * pre1[i][j][r];
+          P.C[(size_t)row * P.ldc + col] = o;
+          if (row == col) tsum += o;
         }
       }
+  if (epi_is<EPIS>(P, EPI_SCALED) && P.g != nullptr && tm == tn) {
+    // the diagonal of a tile on the diagonal: one atomic per wave
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) tsum += __shfl_xor(tsum, off);
+    if (lane == 0) atomicAdd(P.g, tsum);
+  }
   if (dot) {
     // Row sums over this wave's columns, reduced across the 16 lanes of a row
     // in a fixed butterfly; one partial per (row, tile column, wave column).

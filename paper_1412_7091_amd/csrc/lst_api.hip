@@ -460,8 +460,9 @@ int enqueue_stabilize(lst_state* s, const lst_stab_config& cfg, hipStream_t st) 
   a.ksplit = s->stab_ksplit;
   float* f = s->stab_f;
   a.G = f + l.G; a.G2 = f + l.G2; a.ws = f + l.ws; a.x = f + l.x; a.u = f + l.u; a.w = f + l.w;
-  a.wpart = f + l.wpart; a.scal = f + l.scal; a.sig = f + l.sig;
+  a.wpart = f + l.wpart; a.scal = f + l.scal; a.sig = f + l.sig; a.trace = f + l.trace;
   a.chain = s->stab_i;
+  a.stop = s->stab_i + 2 * (cfg.max_fixes + 1);
   HIPCHK(stabilize_enqueue(a, st));
   return LST_OK;
 }

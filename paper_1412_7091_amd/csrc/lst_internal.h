@@ -39,7 +39,10 @@ enum Epi {
   EPI_GRADT = 2,    // output rows 2i, 2i+1 pair up into row i (M = 2 x rows of C):
                     //   g = s1[i]*E1[i][c] + s2[i]*E2[i][c]; G[i][c] = g;
                     //   C[i][c] = g + alpha*(s1[i]*acc[2i][c] + s2[i]*acc[2i+1][c])
-  EPI_PARTIAL = 3   // split-K partial: slice z of a M x N workspace, reduced by gemm_splitk_reduce
+  EPI_PARTIAL = 3,  // split-K partial: slice z of a M x N workspace, reduced by gemm_splitk_reduce
+  EPI_SCALED = 4    // C = alpha * p * acc + beta * C with p = 2^(-2 ilogb(*s1)) (p = 1 when s1
+                    // is null or *s1 is not positive and finite); with g non-null the diagonal
+                    // of C is also added into *g (atomically: only its exponent is used)
 };
 
 // Layouts of C = op(A) op(B):  M x K times K x N.
@@ -206,11 +209,14 @@ struct StabArgs {
   int squarings, max_fixes, reinvert, ksplit;
   // workspace (StabLayout offsets into one float buffer, chain in an int buffer)
   float *G, *G2, *ws, *x, *u, *w, *wpart, *scal, *sig;
+  float* trace;  // 2 x max_fixes x (kStabMaxSquarings + 1) traces of the round's products
   int* chain;  // 2 x (max_fixes + 1) round flags: [end][0] = no pending error,
                // [end][r + 1] = round r of that end corrected a singular value
+  int* stop;   // the same flags negated (the tile products skip while set)
 };
+constexpr int kStabMaxSquarings = 16;
 struct StabLayout {
-  size_t G, G2, ws, x, u, w, wpart, scal, sig, floats, ints;
+  size_t G, G2, ws, x, u, w, wpart, scal, sig, trace, floats, ints;
 };
 StabLayout stab_layout(int d, int ksplit, int max_fixes);
 int stab_ksplit(int d);

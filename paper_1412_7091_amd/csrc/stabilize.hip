@@ -8,8 +8,13 @@
 //      moves it to 1; at most max_fixes rounds;
 //   2. the same for the largest singular value of U against sigma_high.
 // A round's power iteration applies A A^T 2^s times to the start vector of
-// ones, as s squarings of G = A A^T (each scaled by 1 / trace^2, so the top
-// eigenvalue never underflows), which is the same vector in exact arithmetic.
+// ones, as s squarings of G = A A^T, which is the same vector in exact
+// arithmetic.  Each squaring is scaled by the power of two nearest below
+// 1 / trace^2 of the matrix it squares (the trace summed in its epilogue), so
+// the top eigenvalue neither overflows nor underflows and the scaling itself
+// rounds nothing.  The products run on the step's 32 x 32 MFMA tiles, one
+// launch each; only the in-place product of the refinement goes through
+// split-K partials.
 // fix-singular-value with target 1 and alpha = (1 - sigma) / sigma,
 // beta = -alpha / (1 + alpha):
 //   U <- U + alpha u (U^T u)^T,  U^{-T} <- U^{-T} + beta u (U^{-1} u)^T,
@@ -31,11 +36,16 @@ namespace lst {
 namespace {
 
 // ------------------------------------------------------------------ kernels
-__global__ void stab_begin_kernel(const int* flags, int* chain, int rounds, float* sig,
-                                  int nsig) {
+__global__ void stab_begin_kernel(const int* flags, int* chain, int* stop, int rounds, float* sig,
+                                  int nsig, float* trace, int ntrace) {
   const int ok = flags[F_ERR] == 0;
-  for (int i = threadIdx.x; i < 2 * (rounds + 1); i += blockDim.x) chain[i] = (i % (rounds + 1) == 0) ? ok : 0;
+  for (int i = threadIdx.x; i < 2 * (rounds + 1); i += blockDim.x) {
+    const int v = (i % (rounds + 1) == 0) ? ok : 0;
+    chain[i] = v;
+    stop[i] = !v;
+  }
   for (int i = threadIdx.x; i < nsig; i += blockDim.x) sig[i] = __uint_as_float(0x7fc00000u);
+  for (int i = threadIdx.x; i < ntrace; i += blockDim.x) trace[i] = 0.f;
 }
 
 // C = alpha * (scale ? *scale : 1) * sum_z ws[z] + beta * C (z ascending).
@@ -52,28 +62,6 @@ __global__ void stab_reduce_kernel(const float* __restrict__ ws, int splits, siz
   }
 }
 
-// *out = 1 / trace(G)^2 (fp64 sum in a fixed tree order); 1 when the trace is
-// not positive and finite.
-__global__ __launch_bounds__(256) void stab_trace_kernel(const float* __restrict__ G, int d,
-                                                         float* out, const int* run_if) {
-  if (run_if && !*run_if) return;
-  __shared__ double red[256];
-  double t = 0.0;
-  for (int i = threadIdx.x; i < d; i += 256) t += (double)G[(size_t)i * d + i];
-  red[threadIdx.x] = t;
-  __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if (threadIdx.x < (unsigned)off) red[threadIdx.x] += red[threadIdx.x + off];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) {
-    const double tr = red[0];
-    *out = (tr > 0.0 && isfinite(tr)) ? (float)(1.0 / (tr * tr)) : 1.f;
-  }
-}
-
-// x = G 1 (row sums), one wave per row (coalesced), then in a second kernel
-// u = x / ||x||.
 __global__ __launch_bounds__(256) void stab_rowsum_kernel(const float* __restrict__ G, int d,
                                                           float* __restrict__ x,
                                                           const int* run_if) {
@@ -137,9 +125,12 @@ __global__ __launch_bounds__(256) void stab_decide_kernel(const float* __restric
                                                           float* __restrict__ w, int high,
                                                           float sigma_low, float sigma_high,
                                                           const int* run_if, int* go,
-                                                          float* sig, float* scal) {
+                                                          int* go_stop, float* sig, float* scal) {
   if (!*run_if) {
-    if (threadIdx.x == 0) *go = 0;
+    if (threadIdx.x == 0) {
+      *go = 0;
+      *go_stop = 1;
+    }
     return;
   }
   __shared__ double red[2][256];
@@ -171,6 +162,7 @@ __global__ __launch_bounds__(256) void stab_decide_kernel(const float* __restric
     const bool ok = out && sigma > 0.0 && isfinite(sigma);
     *sig = (float)sigma;
     *go = ok ? 1 : 0;
+    *go_stop = ok ? 0 : 1;
     if (ok) {
       const double alpha = (1.0 - sigma) / sigma;
       scal[0] = (float)alpha;
@@ -277,7 +269,35 @@ unsigned grid_for(size_t n, unsigned cap) {
   return (unsigned)b;
 }
 
-// C (d x d) = alpha * (scale) * op(A) op(B) + beta * C through split-K partials.
+// C (d x d) = alpha * p * A B^T (NT) or A B (NN) + beta * C on the 32 x 32 MFMA tiles of
+// the step, one launch: p = 2^(-2 ilogb(*scale_in)) (1 without scale_in), and the
+// trace of C added into *trace_out when given.  Skipped while *stop is set.  C must
+// not alias A or B.
+hipError_t tile_product(const StabArgs& a, int layout, const float* A, const float* B, float* C,
+                        float alpha, float beta, const float* scale_in, float* trace_out,
+                        const int* stop, hipStream_t s) {
+  const int d = a.d;
+  StepCtx c{};
+  c.m = 1;
+  StepLaunch L{};
+  L.ntask = 1;
+  L.kind[0] = TK_GEMM;
+  L.lk = 5;
+  L.gemm.np = 1;
+  L.gemm.skip_if = stop;
+  GemmProblem& p = L.gemm.p[0];
+  p = gemm_problem(layout, d, d, d, vmat(A, d, d), vmat(B, d, d), C, d, alpha, beta, EPI_SCALED);
+  p.s1 = scale_in;
+  p.g = trace_out;
+  p.tile = 32;
+  int stages = (d + 63) / 64;  // every K chunk resident when it fits
+  if (stages > 9) stages = 9;
+  if (stages < 2) stages = 2;
+  return step_launch(c, L, stages, s);
+}
+
+// C (d x d) = alpha * (scale) * op(A) op(B) + beta * C through split-K partials
+// (safe when C is also an operand).
 hipError_t dd_product(const StabArgs& a, int layout, const float* A, const float* B, float* C,
                       float alpha, float beta, const float* scale, const int* run_if,
                       hipStream_t s) {
@@ -309,8 +329,9 @@ StabLayout stab_layout(int d, int ksplit, int max_fixes) {
   l.wpart = o; o += nchunk * 2 * d;
   l.scal = o; o += 8;
   l.sig = o; o += 2 * (size_t)max_fixes;
+  l.trace = o; o += 2 * (size_t)max_fixes * (kStabMaxSquarings + 1);
   l.floats = o;
-  l.ints = 2 * ((size_t)max_fixes + 1);
+  l.ints = 4 * ((size_t)max_fixes + 1);  // the round flags, then the same negated
   return l;
 }
 
@@ -327,15 +348,18 @@ hipError_t stabilize_enqueue(const StabArgs& a, hipStream_t s) {
   const size_t dd = (size_t)d * d;
   const int R = a.max_fixes;
   const int nchunk = (d + kStabRowChunk - 1) / kStabRowChunk;
-  hipLaunchKernelGGL(stab_begin_kernel, dim3(1), dim3(64), 0, s, a.flags, a.chain, R, a.sig, 2 * R);
+  const int per_round = kStabMaxSquarings + 1;
+  hipLaunchKernelGGL(stab_begin_kernel, dim3(1), dim3(256), 0, s, a.flags, a.chain, a.stop, R,
+                     a.sig, 2 * R, a.trace, 2 * R * per_round);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int* ok = a.chain;  // chain[0]: no pending step error
+  auto stop_of = [&](const int* run) { return a.stop + (run - a.chain); };
   // Z <- 2 Z - (Z U^T) Z on Z = U^{-T}, n times, gated by run; T = Z U^T lives in G2.
   auto refine = [&](int n, const int* run) -> hipError_t {
     hipError_t r = hipSuccess;
     for (int it = 0; it < n && r == hipSuccess; ++it) {
-      r = dd_product(a, L_NT, a.Uit, a.U, a.G2, 1.f, 0.f, nullptr, run, s);
+      r = tile_product(a, L_NT, a.Uit, a.U, a.G2, 1.f, 0.f, nullptr, nullptr, stop_of(run), s);
       if (r == hipSuccess) r = dd_product(a, L_NN, a.G2, a.Uit, a.Uit, -1.f, 2.f, nullptr, run, s);
     }
     return r;
@@ -347,12 +371,16 @@ hipError_t stabilize_enqueue(const StabArgs& a, hipStream_t s) {
     for (int r = 0; r < R; ++r) {
       const int* run = chain + r;
       int* go = chain + r + 1;
-      if ((e = dd_product(a, L_NT, A, A, a.G, 1.f, 0.f, nullptr, run, s))) return e;
+      float* tr = a.trace + (size_t)(end * R + r) * per_round;
+      // G = A A^T, then squarings G <- p G G (G is symmetric, so G G^T), each
+      // scaled by a power of two from the trace of the one before
+      if ((e = tile_product(a, L_NT, A, A, a.G, 1.f, 0.f, nullptr, tr, stop_of(run), s)))
+        return e;
       float* G = a.G;
       float* G2 = a.G2;
       for (int q = 0; q < a.squarings; ++q) {
-        hipLaunchKernelGGL(stab_trace_kernel, dim3(1), dim3(256), 0, s, G, d, a.scal + 2, run);
-        if ((e = dd_product(a, L_NT, G, G, G2, 1.f, 0.f, a.scal + 2, run, s))) return e;
+        if ((e = tile_product(a, L_NT, G, G, G2, 1.f, 0.f, tr + q, tr + q + 1, stop_of(run), s)))
+          return e;
         float* t = G;
         G = G2;
         G2 = t;
@@ -362,7 +390,8 @@ hipError_t stabilize_enqueue(const StabArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(stab_matvec_t_kernel, dim3((d + 255) / 256, nchunk), dim3(256), 0, s,
                          a.U, a.Uit, d, a.u, a.wpart, run);
       hipLaunchKernelGGL(stab_decide_kernel, dim3(1), dim3(256), 0, s, a.wpart, nchunk, d, a.w,
-                         end, a.sigma_low, a.sigma_high, run, go, a.sig + end * R + r, a.scal);
+                         end, a.sigma_low, a.sigma_high, run, go, a.stop + (go - a.chain),
+                         a.sig + end * R + r, a.scal);
       hipLaunchKernelGGL(stab_rank1_kernel, dim3(grid_for(dd, 1024)), dim3(256), 0, s, a.U, a.Uit,
                          d, a.u, a.w, a.scal, go);
       if (d % 4 == 0 && d <= 1024)

@@ -1279,7 +1279,7 @@ __device__ unsigned long long g_step_times[4][8192][3];
 struct LaunchMasks {
   unsigned tasks, vars, epis, tiles;
 };
-constexpr LaunchMasks kLaunchMasks[5] = {
+constexpr LaunchMasks kLaunchMasks[6] = {
     {0u, 0u, 0u, 0u},
     {(1u << TK_GEMM) | (1u << TK_TARGETS), V_NT, (1u << EPI_STORE) | (1u << EPX_ROWSUMS), TILE32},
     {(1u << TK_GEMM) | (1u << TK_SOLVE) | (1u << TK_YY) | (1u << TK_SCALARS), V_NN | V_NT,
@@ -1287,6 +1287,8 @@ constexpr LaunchMasks kLaunchMasks[5] = {
     {(1u << TK_GEMM) | (1u << TK_SCATTER), V_NN, 1u << EPI_GRADT, TILE32},
     {(1u << TK_GEMM) | (1u << TK_CLEAR), V_TN, (1u << EPI_SYM) | (1u << EPI_STORE),
      TILE32 | TILE64},
+    // the d x d products of the Appendix C stabilisation
+    {1u << TK_GEMM, V_NT | V_NN, 1u << EPI_SCALED, TILE32},
 };
 
 // The launch-1 kernel built for m > 128 also compiles 64 x 64 tiles: a large
@@ -1444,13 +1446,14 @@ static const void* step_kernel_for(int lk, bool small, int w16) {
       return w16 ? kfn<false, 4, 2>() : kfn<false, 1, 2>();
     case 3: return w16 ? kfn<true, 4, 3>() : kfn<true, 1, 3>();
     case 4: return w16 ? kfn<true, 4, 4>() : kfn<true, 1, 4>();
+    case 5: return w16 ? kfn<true, 4, 5>() : kfn<true, 1, 5>();
     default: return nullptr;
   }
 }
 
 hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t s,
                        hipEvent_t ev0, hipEvent_t ev1) {
-  if (L.lk < 1 || L.lk > 4) return hipErrorInvalidValue;
+  if (L.lk < 1 || L.lk > 5) return hipErrorInvalidValue;
   if (stages < 2 || (size_t)stages * kPanelStageBytes > kStepLdsMax) return hipErrorInvalidValue;
   const LaunchMasks M = launch_masks(L.lk, c.m <= 128);
   L.gemm.stages = stages;
@@ -1500,7 +1503,7 @@ size_t solve_workspace_floats(int m_max, int d) {
 }
 
 hipError_t configure_kernels() {
-  for (int lk = 1; lk <= 4; ++lk)
+  for (int lk = 1; lk <= 5; ++lk)
     for (int small = 0; small < 2; ++small)
       for (int w16 = 0; w16 < 2; ++w16) {
         const void* k = step_kernel_for(lk, small != 0, w16);
