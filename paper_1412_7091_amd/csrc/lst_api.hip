@@ -283,6 +283,10 @@ int stages_for(const GemmBatch& b, int max_stages = kMaxStages) {
 // Launches 3 and 4 keep at most 4 stages (64 KB): two blocks share a compute
 // unit, so the short tasks run beside the GEMM tiles.
 constexpr int kLaunch34Stages = 4;
+// Slots a row needs to be scattered by the launch-4 clear blocks instead of its
+// owner in launch 3; at most m K / kHotMinSlots rows qualify, which sizes
+// their list.
+constexpr int kHotMinSlots = 64;
 
 // Enqueues the launches of one factored step on stream st.
 int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float* H,
@@ -305,6 +309,10 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
   c.ex_row = s->ex_row; c.ex_val = s->ex_val; c.ex_cnt = s->ex_cnt;
   c.hkey = s->hkey; c.hmin = s->hmin; c.hcnt = s->hcnt; c.hbits = s->hbits;
   c.own = s->own; c.flags = fl; c.solve_ws = s->solve_ws;
+  // rows held by kHotMinSlots or more slots are scattered in launch 4, four
+  // waves each, when the step has enough slots for such rows to be worth it
+  c.hot_min = (m * K >= 4096) ? kHotMinSlots : 0;
+  const bool hot = c.hot_min > 0;
   const float* Hh = s->Z0;          // H^ rows
   const float* UH = s->Z0 + d;      // (U H)^T rows
 
@@ -370,7 +378,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     pt.e1 = Hh; pt.lde1 = s->ld0; pt.e2 = s->Yh; pt.lde2 = d;
     pt.s1 = s->a; pt.s2 = s->b; pt.g = grad_H; pt.ldg = d;
     pt.tile = 32;
-    L.lk = 3;
+    L.lk = hot ? 6 : 3;
     L.timing_slot = 2;
     hipEvent_t e0, e1;
     OK_OR_RETURN(prof_pair(s, PH_LAUNCH3, &e0, &e1));
@@ -378,6 +386,9 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
   }
   {  // launch 4: Q -= lr (H T^T + T H^T) ; U and U^{-T} updates ; clear the hash slots
     StepLaunch L{};
+    // the clear blocks (which also scatter the hot rows) come last: when the
+    // tiles fill more than one pass over the compute units, blocks placed
+    // first would hold back the tiles for their own latency-bound work
     L.ntask = 2;
     L.kind[0] = TK_GEMM; L.kind[1] = TK_CLEAR;
     GemmBatch& g = L.gemm;
@@ -392,7 +403,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     g.p[2] = gemm_problem(L_TN, d, d, m, vmat(s->X, d, m), vmat(H, d, m), c.Uit, d, -1.f, 1.f,
                           EPI_STORE);
     g.p[2].tile = 64;
-    L.lk = 4;
+    L.lk = hot ? 7 : 4;
     L.timing_slot = 3;
     hipEvent_t e0, e1;
     OK_OR_RETURN(prof_pair(s, PH_LAUNCH4, &e0, &e1));
@@ -517,7 +528,8 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       (rc = dalloc(s, &s->solve_ws, solve_workspace_floats(m, d))) ||
       (rc = dalloc(s, &s->ex_row, (size_t)m * K)) || (rc = dalloc(s, &s->ex_val, (size_t)m * K)) ||
       (rc = dalloc(s, &s->ex_cnt, m)) || (rc = dalloc(s, &s->hkey, hsize)) ||
-      (rc = dalloc(s, &s->hmin, hsize)) || (rc = dalloc(s, &s->hcnt, hsize)) ||
+      (rc = dalloc(s, &s->hmin, hsize)) ||
+      (rc = dalloc(s, &s->hcnt, hsize + 1 + (size_t)m * K / kHotMinSlots)) ||
       (rc = dalloc(s, &s->touched, (size_t)m * K)) ||
       (rc = dalloc(s, &s->own, (size_t)m * K)) || (rc = dalloc(s, &s->count, 1)) ||
       (rc = dalloc(s, &s->UHa, md)) || (rc = dalloc(s, &s->yyd, m)) ||
@@ -526,7 +538,7 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
     return fail(rc);
   if (fill_ints(s->hkey, -1, hsize, s->stream) != hipSuccess ||
       fill_ints(s->hmin, 0x7fffffff, hsize, s->stream) != hipSuccess ||
-      fill_ints(s->hcnt, 0, hsize, s->stream) != hipSuccess)
+      fill_ints(s->hcnt, 0, hsize + 1, s->stream) != hipSuccess)
     return fail(LST_EHIP);
   if (cfg->cond_max > 0.f && (rc = ensure_vtmp(s))) return fail(rc);
   if (hipMemcpyAsync(s->V, V, (size_t)D * d * sizeof(float), hipMemcpyDeviceToDevice, s->stream) !=

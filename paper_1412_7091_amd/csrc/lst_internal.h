@@ -119,6 +119,10 @@ hipError_t gemm_splitk_reduce(const float* ws, int splits, int M, int N, float* 
 // Everything the tasks of one factored step read or write (device pointers).
 struct StepCtx {
   int m, K, d;
+  // rows held by hot_min or more slots (hot_min 0: none) are not scattered by
+  // their owner in launch 3 but listed (hot_list) and scattered by the clear
+  // blocks of launch 4, which does not read V
+  int hot_min;
   int64_t D;
   int loss_kind;
   float eps, lr;
@@ -144,7 +148,8 @@ struct StepCtx {
   float* ex_val;
   int* ex_cnt;
   int *hkey, *hmin, *hcnt;  // hash table of the step's target rows: smallest slot
-                            // and number of slots of each
+                            // and number of slots of each; hcnt's 2^hbits counts
+                            // are followed by the hot-row list ([0]: count, then rows)
   int hbits;
   int* own;      // m x K: the row of slot i*K + k if that slot owns the row's
                  // scatter in this step (its smallest slot), else -1
@@ -158,8 +163,10 @@ enum TaskKind {
 constexpr int kMaxTasks = 6;
 
 // One heterogeneous launch: block ranges of its tasks (set by step_launch).
-// lk (1..4) selects the kernel built for that launch of the step, which
-// contains only the tasks, GEMM layouts and epilogues that launch uses.
+// lk selects the kernel built for that launch of the step, which contains only
+// the tasks, GEMM layouts and epilogues that launch uses: 1..4 the step's
+// launches, 5 the stabilisation's products, 6 and 7 launches 3 and 4 of a step
+// that scatters its hot rows in launch 4.
 struct StepLaunch {
   int lk;
   int ntask;

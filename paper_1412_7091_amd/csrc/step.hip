@@ -38,6 +38,9 @@ __device__ __forceinline__ unsigned row_hash(int r, int bits) {
   return ((unsigned)r * 2654435761u) >> (32 - bits);
 }
 
+// The hot-row list, stored after the hash table's slot counts.
+__device__ __forceinline__ int* hot_list(const StepCtx& c) { return c.hcnt + (1 << c.hbits); }
+
 // c1 = h_i^T Q h_i: the partial sums left by the first product of the step,
 // added in index order (the same bits wherever it is evaluated).
 __device__ __forceinline__ float example_c1(const StepCtx& c, int i) {
@@ -340,6 +343,7 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
     if (lane_id() == 0) {
       c.flags[F_NNZ] = nnz;
       c.flags[F_UNIQUE] = 0;
+      hot_list(c)[0] = 0;  // the list launch 3 fills
     }
   }
   const int i = local * 4 + wave_id();
@@ -1087,16 +1091,20 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
 constexpr int kScatterSlotsPerWave = 1;
 constexpr int kScatterBatch = 4;
 
+template <bool HOT>
 __device__ __forceinline__ void scatter_slot(const StepCtx& c, int e);
 
 // A wave handles kScatterSlotsPerWave consecutive slots in turn (few blocks,
-// so that they share the launch's compute units with the GEMM tiles).
+// so that they share the launch's compute units with the GEMM tiles).  With
+// HOT the owners of rows held by c.hot_min or more slots list them instead.
+template <bool HOT>
 __device__ __forceinline__ void task_scatter(const StepCtx& c, int local) {
   const int e0 = (local * 4 + wave_id()) * kScatterSlotsPerWave;
   for (int u = 0; u < kScatterSlotsPerWave; ++u)
-    if (e0 + u < c.m * c.K) scatter_slot(c, e0 + u);
+    if (e0 + u < c.m * c.K) scatter_slot<HOT>(c, e0 + u);
 }
 
+template <bool HOT>
 __device__ __forceinline__ void scatter_slot(const StepCtx& c, int e) {
   const int lane = lane_id();
   const int i = e / c.K;
@@ -1121,6 +1129,15 @@ __device__ __forceinline__ void scatter_slot(const StepCtx& c, int e) {
   // have been met, and a row held by this slot alone takes its example's row
   // of X directly (the same sum as the search would form: one term)
   const int cnt = c.hcnt[h];
+  if constexpr (HOT) {
+    if (cnt >= c.hot_min) {
+      if (lane == 0) {
+        int* hot = hot_list(c);
+        hot[1 + atomicAdd(hot, 1)] = r;
+      }
+      return;
+    }
+  }
   if (cnt == 1 && vec) {
     const float w = one_hot ? c.cs[i] : -c.val[e];
     const float* xr = c.X + (size_t)i * c.d;
@@ -1236,9 +1253,108 @@ __device__ __forceinline__ void scatter_slot(const StepCtx& c, int e) {
   }
 }
 
+// Launch 4: the scatter of the rows launch 3 listed as hot (held by so many
+// slots that one wave would add them one example at a time), by the nb clear
+// blocks.  Work item q = (listed row q / nch, 256-column chunk q % nch);
+// block b takes the items b, b + nb, ...  Its four waves split the examples
+// into fixed quarters, each adds c_j X_j over its quarter in example order,
+// and the four partial sums are added in wave order before the row is
+// written once.
+constexpr size_t kHotLdsBytes = 3 * 64 * sizeof(float4);
+
+__device__ __forceinline__ void scatter_hot(const StepCtx& c, int local, int nb,
+                                            unsigned char* sraw) {
+  float4(*part)[64] = reinterpret_cast<float4(*)[64]>(sraw);  // 3 x 64 partial sums
+  if (c.flags[F_ERR]) return;
+  const int* hot = hot_list(c);
+  const int nch = (c.d + 255) / 256;
+  const int items = hot[0] * nch;
+  const int wave = wave_id(), lane = lane_id();
+  const bool one_hot = c.loss_kind == LST_LOSS_SPHERICAL;
+  const bool vec = (c.d % 4 == 0);
+  const int span = (c.m + 3) / 4, jb = wave * span, je = min(c.m, jb + span);
+  for (int q = local; q < items; q += nb) {
+    const int r = hot[1 + q / nch];
+    const int col = (q % nch) * 256 + 4 * lane;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j0 = jb; j0 < je; j0 += 64) {
+      const int j = j0 + lane;
+      float cj = 0.f;
+      bool found = false;
+      if (j < je) {
+        const int* rows = c.ex_row + (size_t)j * c.K;
+        const float* vals = c.ex_val + (size_t)j * c.K;
+        const int n = c.ex_cnt[j];
+        int lo = 0, hi = n;
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (rows[mid] < r) lo = mid + 1; else hi = mid;
+        }
+        float sum = 0.f;
+        while (lo < n && rows[lo] == r) {
+          sum += vals[lo];
+          ++lo;
+          found = true;
+        }
+        cj = one_hot ? c.cs[j] : -sum;
+      }
+      unsigned long long bal = __ballot(found);
+      // four examples at a time: their rows of X are in flight together
+      while (bal) {
+        float w[4];
+        float4 x[4];
+        bool on[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          on[u] = bal != 0;
+          const int src = on[u] ? __ffsll((long long)bal) - 1 : 0;
+          bal &= bal - 1;
+          w[u] = __shfl(cj, src);
+          const float* xr = c.X + (size_t)(j0 + src) * c.d;
+          x[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (on[u] && col < c.d) {
+            if (vec) {
+              x[u] = *reinterpret_cast<const float4*>(xr + col);
+            } else {
+              x[u].x = xr[col];
+              if (col + 1 < c.d) x[u].y = xr[col + 1];
+              if (col + 2 < c.d) x[u].z = xr[col + 2];
+              if (col + 3 < c.d) x[u].w = xr[col + 3];
+            }
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (!on[u]) break;
+          acc.x += w[u] * x[u].x; acc.y += w[u] * x[u].y;
+          acc.z += w[u] * x[u].z; acc.w += w[u] * x[u].w;
+        }
+      }
+    }
+    if (wave > 0) part[wave - 1][lane] = acc;
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+      for (int p = 0; p < 3; ++p) {
+        const float4 o = part[p][lane];
+        acc.x += o.x; acc.y += o.y; acc.z += o.z; acc.w += o.w;
+      }
+      float* vr = c.V + (size_t)r * c.d;
+      if (col < c.d) vr[col] += acc.x;
+      if (col + 1 < c.d) vr[col + 1] += acc.y;
+      if (col + 2 < c.d) vr[col + 2] += acc.z;
+      if (col + 3 < c.d) vr[col + 3] += acc.w;
+    }
+    __syncthreads();  // part[] is free for the next item
+  }
+}
+
 // Launch 4: empty the hash slots of the rows this step touched (found from
-// own[]) and count the distinct rows (one atomic per block).
-__device__ __forceinline__ void task_clear(const StepCtx& c, int local) {
+// own[]) and count the distinct rows (one atomic per block); with HOT the
+// blocks first scatter the hot rows (the longer work, independent of the hash).
+template <bool HOT>
+__device__ __forceinline__ void task_clear(const StepCtx& c, int local, unsigned char* sraw) {
+  if constexpr (HOT) scatter_hot(c, local, (c.m * c.K + 255) / 256, sraw);
   __shared__ int s_cnt[4];
   const int t = local * 256 + threadIdx.x;
   const int r = (t < c.m * c.K) ? c.own[t] : -1;
@@ -1278,8 +1394,9 @@ __device__ unsigned long long g_step_times[4][8192][3];
 // which keeps its code small enough for the instruction cache.
 struct LaunchMasks {
   unsigned tasks, vars, epis, tiles;
+  bool hot;  // launch 3 lists the hot rows, launch 4's clear blocks scatter them
 };
-constexpr LaunchMasks kLaunchMasks[6] = {
+constexpr LaunchMasks kLaunchMasks[8] = {
     {0u, 0u, 0u, 0u},
     {(1u << TK_GEMM) | (1u << TK_TARGETS), V_NT, (1u << EPI_STORE) | (1u << EPX_ROWSUMS), TILE32},
     {(1u << TK_GEMM) | (1u << TK_SOLVE) | (1u << TK_YY) | (1u << TK_SCALARS), V_NN | V_NT,
@@ -1289,6 +1406,10 @@ constexpr LaunchMasks kLaunchMasks[6] = {
      TILE32 | TILE64},
     // the d x d products of the Appendix C stabilisation
     {1u << TK_GEMM, V_NT | V_NN, 1u << EPI_SCALED, TILE32},
+    // launches 3 and 4 of a step whose hot rows are scattered in launch 4
+    {(1u << TK_GEMM) | (1u << TK_SCATTER), V_NN, 1u << EPI_GRADT, TILE32, true},
+    {(1u << TK_GEMM) | (1u << TK_CLEAR), V_TN, (1u << EPI_SYM) | (1u << EPI_STORE),
+     TILE32 | TILE64, true},
 };
 
 // The launch-1 kernel built for m > 128 also compiles 64 x 64 tiles: a large
@@ -1331,10 +1452,10 @@ __device__ __forceinline__ void run_task(const StepCtx& c, const StepLaunch& L, 
     if (kind == TK_SOLVE) { task_solve<SMALLM>(c, local, sraw); return; }
   }
   if constexpr ((M.tasks >> TK_SCATTER) & 1u) {
-    if (kind == TK_SCATTER) { task_scatter(c, local); return; }
+    if (kind == TK_SCATTER) { task_scatter<M.hot>(c, local); return; }
   }
   if constexpr ((M.tasks >> TK_CLEAR) & 1u) {
-    if (kind == TK_CLEAR) { task_clear(c, local); return; }
+    if (kind == TK_CLEAR) { task_clear<M.hot>(c, local, sraw); return; }
   }
 }
 
@@ -1447,13 +1568,15 @@ static const void* step_kernel_for(int lk, bool small, int w16) {
     case 3: return w16 ? kfn<true, 4, 3>() : kfn<true, 1, 3>();
     case 4: return w16 ? kfn<true, 4, 4>() : kfn<true, 1, 4>();
     case 5: return w16 ? kfn<true, 4, 5>() : kfn<true, 1, 5>();
+    case 6: return w16 ? kfn<true, 4, 6>() : kfn<true, 1, 6>();
+    case 7: return w16 ? kfn<true, 4, 7>() : kfn<true, 1, 7>();
     default: return nullptr;
   }
 }
 
 hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t s,
                        hipEvent_t ev0, hipEvent_t ev1) {
-  if (L.lk < 1 || L.lk > 5) return hipErrorInvalidValue;
+  if (L.lk < 1 || L.lk > 7) return hipErrorInvalidValue;
   if (stages < 2 || (size_t)stages * kPanelStageBytes > kStepLdsMax) return hipErrorInvalidValue;
   const LaunchMasks M = launch_masks(L.lk, c.m <= 128);
   L.gemm.stages = stages;
@@ -1479,7 +1602,8 @@ hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t 
     } else {
       n = step_task_blocks(L.kind[t], c);
     }
-    const size_t b = lds_of(L.kind[t], stages, c.m, c.K);
+    size_t b = lds_of(L.kind[t], stages, c.m, c.K);
+    if (M.hot && L.kind[t] == TK_CLEAR && b < kHotLdsBytes) b = kHotLdsBytes;
     if (b > lds) lds = b;
     total += n;
   }
@@ -1503,7 +1627,7 @@ size_t solve_workspace_floats(int m_max, int d) {
 }
 
 hipError_t configure_kernels() {
-  for (int lk = 1; lk <= 5; ++lk)
+  for (int lk = 1; lk <= 7; ++lk)
     for (int small = 0; small < 2; ++small)
       for (int w16 = 0; w16 < 2; ++w16) {
         const void* k = step_kernel_for(lk, small != 0, w16);
