@@ -530,6 +530,48 @@ __device__ unsigned long long g_solve_marks[64][8];
   } while (0)
 #endif
 
+// Relative tolerance of the Neumann series, per column of Y and in the
+// infinity norm: the terms left out change no entry of a column by more than
+// 2^-20 of the largest entry of that column of B.  B is itself an fp32
+// product over d terms (P = U^-T H), whose rounding is of the same order or
+// larger, so more terms would not make the solve more accurate.
+constexpr float kNeumannTol = 9.5367431640625e-7f;  // 2^-20
+
+// Adaptive end of the series.  Y_k - Y_{k-1} = E^k B and ||E x||_inf <= r ||x||_inf,
+// so after iteration k the terms left out add at most
+// ||Y_k - Y_{k-1}||_inf r / (1 - r) to any entry of a column.  At an
+// iteration's end each lane passes its largest |Y_k - Y_{k-1}| (and, in the
+// first iteration, |B|) over its rows of column lane & 15; neumann_post folds
+// them over the lanes of the column and stores the wave's column maxima in
+// LDS (two sets of slots, by iteration parity, so a wave that runs ahead never
+// overwrites maxima another wave still reads); after the workgroup barrier
+// neumann_done folds the four waves and returns the same answer in every
+// wave.  A NaN counts as infinite, so it never ends the series early.
+__device__ __forceinline__ float fold_col16(float v) {
+  v = (v == v) ? v : INFINITY;
+  v = fmaxf(v, __shfl_xor(v, 16));
+  return fmaxf(v, __shfl_xor(v, 32));
+}
+__device__ __forceinline__ void neumann_post(float* red, int it, float dl, float bl) {
+  const int lane = lane_id(), wave = wave_id();
+  dl = fold_col16(dl);
+  bl = fold_col16(bl);
+  if (lane < 16) {
+    red[64 + 64 * (it & 1) + 16 * wave + lane] = dl;
+    if (it == 0) red[192 + 16 * wave + lane] = bl;
+  }
+}
+__device__ __forceinline__ bool neumann_done(const float* red, int it, float stop_k, float& bcol) {
+  const int col = lane_id() & 15;
+  const float* s = red + 64 + 64 * (it & 1) + col;
+  const float dmax = fmaxf(fmaxf(s[0], s[16]), fmaxf(s[32], s[48]));
+  if (it == 0) {
+    const float* b = red + 192 + col;
+    bcol = fmaxf(fmaxf(b[0], b[16]), fmaxf(b[32], b[48]));
+  }
+  return __all(dmax * stop_k <= kNeumannTol * bcol);
+}
+
 // The Neumann iterations for m > 128 (m % 4 == 0, 16-byte aligned rows of
 // H^T H): H^T H (up to 1 MB) does not fit in LDS and is read from memory each
 // iteration by every solve block, where it stays L2-resident.  Wave w owns the
@@ -543,7 +585,8 @@ __device__ unsigned long long g_solve_marks[64][8];
 template <int RBW>
 __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int ldh, int m, int mp,
                                               int iters, int LDE, const float* cinv,
-                                              const float* Bt, float* Yo, float* Yn) {
+                                              const float* Bt, float* Yo, float* Yn,
+                                              float* red, float stop_k) {
   constexpr int NB = 3;
   const int lane = lane_id(), wave = __builtin_amdgcn_readfirstlane(wave_id());
   const int nsl = mp / 16, nrb = mp / 16;
@@ -568,8 +611,13 @@ __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int 
 #pragma unroll
   for (int t = 0; t < RBW; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   const int yl = (lane & 15) * LDE + kl;
-  const int total = iters * nsl;
-  int sl = 0;  // slice of the next MFMAs
+  int total = iters * nsl;  // cut short once the series has converged
+  int sl = 0;               // slice of the next MFMAs
+  int it = 0;               // iterations completed
+  floatx4 prev[RBW];        // diag(1/c) (H^T H) Y_{k-1} of the wave's rows (Y_0 = B: zero)
+  float bcol = 0.f;
+#pragma unroll
+  for (int t = 0; t < RBW; ++t) prev[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   for (int g0 = 0; g0 < total; g0 += NB) {
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
@@ -594,18 +642,29 @@ __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int 
             bv[t] = *reinterpret_cast<const floatx4*>(Bt + (lane & 15) * LDE + row);
             cv[t] = *reinterpret_cast<const floatx4*>(cinv + row);
           }
+          float dl = 0.f, bl = 0.f;
 #pragma unroll
           for (int t = 0; t < RBW; ++t) {
             const int rb = wave + 4 * t;
-            if (rb < nrb)
-              *reinterpret_cast<floatx4*>(Yn + (lane & 15) * LDE + rb * 16 + kl) =
-                  bv[t] + acc[t] * cv[t];
+            const floatx4 y = acc[t] * cv[t];
+            if (rb < nrb) {
+              *reinterpret_cast<floatx4*>(Yn + (lane & 15) * LDE + rb * 16 + kl) = bv[t] + y;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                dl = fmaxf(dl, fabsf(y[q] - prev[t][q]));
+                bl = fmaxf(bl, fabsf(bv[t][q]));
+              }
+            }
+            prev[t] = y;
             acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
           }
+          neumann_post(red, it, dl, bl);
           lds_barrier();
           float* tt = Yo;
           Yo = Yn;
           Yn = tt;
+          if (neumann_done(red, it, stop_k, bcol)) total = g0 + j + 1;
+          ++it;
         }
       }
     }
@@ -843,8 +902,11 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
       }
     }
     int iters = 0;
+    const float stop_k = r / (1.f - r);
     if (r > 0.f) {
-      const float need = logf(5.9604645e-8f * (1.f - r)) / logf(r);  // r^(k+1)/(1-r) <= 2^-24
+      // at most: r^(k+1) / (1 - r) <= tol (a bound that holds before any
+      // iteration); the series usually ends sooner (neumann_done)
+      const float need = logf(kNeumannTol * (1.f - r)) / logf(r);
       iters = (int)ceilf(need) - 1;
       if (iters < 0) iters = 0;
       if (iters > 64) iters = 64;
@@ -901,6 +963,10 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
         }
       }
       const unsigned yl = 4u * (unsigned)((lane & 15) * LDE + 4 * (lane >> 4));
+      floatx4 prev[RBW];  // diag(1/c) (H^T H) Y_{k-1} of the wave's rows (Y_0 = B: zero)
+      float bcol = 0.f;
+#pragma unroll
+      for (int t = 0; t < RBW; ++t) prev[t] = floatx4{0.f, 0.f, 0.f, 0.f};
       for (int it = 0; it < iters; ++it) {
         floatx4 acc[RBW];
 #pragma unroll
@@ -937,6 +1003,7 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
         // the reads of slice nsl (a re-read of the last one) may be outstanding
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         const int col = lane & 15;
+        float dl = 0.f, bl = 0.f;
 #pragma unroll
         for (int t = 0; t < RBW; ++t) {
           const int rb = wave + 4 * t;
@@ -944,18 +1011,29 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const int row = rb * 16 + 4 * (lane >> 4) + q;
-            Yn[col * LDE + row] = Bt[col * LDE + row] + acc[t][q] * cinv[row];
+            const float bv = Bt[col * LDE + row], y = acc[t][q] * cinv[row];
+            Yn[col * LDE + row] = bv + y;
+            dl = fmaxf(dl, fabsf(y - prev[t][q]));
+            bl = fmaxf(bl, fabsf(bv));
+            prev[t][q] = y;
           }
         }
+        neumann_post(red, it, dl, bl);
         __syncthreads();
         float* tt = Yo;
         Yo = Yn;
         Yn = tt;
+        if (neumann_done(red, it, stop_k, bcol)) break;
       }
     } else if (gvec) {
-      Yo = (nrb <= 16) ? neumann_mem<4>(HH, ldh, m, mp, iters, LDE, cinv, Bt, Yo, Yn)
-                       : neumann_mem<8>(HH, ldh, m, mp, iters, LDE, cinv, Bt, Yo, Yn);
+      Yo = (nrb <= 16)
+               ? neumann_mem<4>(HH, ldh, m, mp, iters, LDE, cinv, Bt, Yo, Yn, red, stop_k)
+               : neumann_mem<8>(HH, ldh, m, mp, iters, LDE, cinv, Bt, Yo, Yn, red, stop_k);
     } else {
+    floatx4 prev[RBW];  // diag(1/c) (H^T H) Y_{k-1} of the wave's rows (Y_0 = B: zero)
+    float bcol = 0.f;
+#pragma unroll
+    for (int t = 0; t < RBW; ++t) prev[t] = floatx4{0.f, 0.f, 0.f, 0.f};
     for (int it = 0; it < iters; ++it) {
       floatx4 acc[RBW];
 #pragma unroll
@@ -987,6 +1065,7 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
         }
       }
       const int col = lane & 15;
+      float dl = 0.f, bl = 0.f;
 #pragma unroll
       for (int t = 0; t < RBW; ++t) {
         const int rb = wave + 4 * t;
@@ -994,13 +1073,19 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int row = rb * 16 + 4 * (lane >> 4) + q;
-          Yn[col * LDE + row] = Bt[col * LDE + row] + acc[t][q] * cinv[row];
+          const float bv = Bt[col * LDE + row], y = acc[t][q] * cinv[row];
+          Yn[col * LDE + row] = bv + y;
+          dl = fmaxf(dl, fabsf(y - prev[t][q]));
+          bl = fmaxf(bl, fabsf(bv));
+          prev[t][q] = y;
         }
       }
+      neumann_post(red, it, dl, bl);
       __syncthreads();
       float* tt = Yo;
       Yo = Yn;
       Yn = tt;
+      if (neumann_done(red, it, stop_k, bcol)) break;
     }
     }
     LST_SMARK(5);
