@@ -356,6 +356,10 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
                           1.f, 0.f, EPI_STORE);
     g.p[3] = gemm_problem(L_NT, m, m, d, vmat(s->G, d, m), vmat(UH, s->ld0, m), s->NP + 2 * m,
                           4 * m, 1.f, 0.f, EPI_STORE);
+    // m > 128: K (d) is long and 64 x 64 tiles fetch half the bytes per
+    // output of 32 x 32 ones; with up to 9 stages all of K is in flight
+    if (m > 128)
+      for (int q = 0; q < g.np; ++q) g.p[q].tile = 64;
     L.lk = 2;
     L.timing_slot = 1;
     hipEvent_t e0, e1;

@@ -1497,12 +1497,13 @@ constexpr LaunchMasks kLaunchMasks[8] = {
      TILE32 | TILE64, true},
 };
 
-// The launch-1 kernel built for m > 128 also compiles 64 x 64 tiles: a large
-// stacked product fills the chip with them and fetches half the bytes per
-// output of 32 x 32 tiles.
+// The kernels of launches 1 and 2 built for m > 128 also compile 64 x 64
+// tiles: their products are long in K there (d up to 1024), and 64 x 64 tiles
+// fetch half the bytes per output of 32 x 32 ones (launch 1 uses them when
+// they alone fill the chip, launch 2 always).
 constexpr LaunchMasks launch_masks(int lk, bool small) {
   LaunchMasks M = kLaunchMasks[lk];
-  if (!small && lk == 1) M.tiles |= TILE64;
+  if (!small && (lk == 1 || lk == 2)) M.tiles |= TILE64;
   return M;
 }
 
@@ -1642,6 +1643,11 @@ static const void* kfn() {
 
 // The kernel built for (launch kind, m <= 128, 16-byte DMA); nullptr for a
 // combination that is not built.
+// Launch kinds with a kernel of their own for m > 128 (64 x 64 tiles, and the
+// solve's memory-streamed iterations); the others run the m <= 128 kernel at
+// every m.
+constexpr bool has_large_kernel(int lk) { return lk == 1 || lk == 2; }
+
 static const void* step_kernel_for(int lk, bool small, int w16) {
   switch (lk) {
     case 1:
@@ -1663,7 +1669,9 @@ hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t 
                        hipEvent_t ev0, hipEvent_t ev1) {
   if (L.lk < 1 || L.lk > 7) return hipErrorInvalidValue;
   if (stages < 2 || (size_t)stages * kPanelStageBytes > kStepLdsMax) return hipErrorInvalidValue;
-  const LaunchMasks M = launch_masks(L.lk, c.m <= 128);
+  // the kernel that runs and the masks checked below must be the same build
+  const bool small = c.m <= 128 || !has_large_kernel(L.lk);
+  const LaunchMasks M = launch_masks(L.lk, small);
   L.gemm.stages = stages;
   L.gemm.timing_slot = L.timing_slot;
   size_t lds = 0;
@@ -1696,7 +1704,7 @@ hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t 
   if (total == 0) return hipSuccess;
   if (lds > kStepLdsMax) return hipErrorInvalidValue;
 
-  const void* fn = step_kernel_for(L.lk, c.m <= 128, w16);
+  const void* fn = step_kernel_for(L.lk, small, w16);
   if (!fn) return hipErrorInvalidValue;
   StepCtx ca = c;
   StepLaunch la = L;
