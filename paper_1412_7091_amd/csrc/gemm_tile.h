@@ -435,6 +435,9 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
         if (((epi_is<EPIS>(P, EPI_STORE) || epi_is<EPIS>(P, EPI_SCALED)) && P.beta != 0.f) ||
             (epi_is<EPIS>(P, EPI_SYM) && row <= col)) {
           pre1[i][j][r] = P.C[(size_t)row * P.ldc + col];
+        } else if (epi_is<EPIS>(P, EPI_GRADN)) {
+          pre1[i][j][r] = P.s1[row] * P.e1[(size_t)row * P.lde1 + col] +
+                          P.s2[row] * P.e2[(size_t)row * P.lde2 + col];
         } else if (epi_is<EPIS>(P, EPI_GRADT)) {
           // accumulator rows 2o and 2o + 1 (r even / odd) both feed output row o
           const int o = row >> 1;
@@ -562,6 +565,9 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
             P.g[(size_t)o * P.ldg + col] = gv;
             P.C[(size_t)o * P.ldc + col] = gv + P.alpha * nh;
           }
+        } else if (epi_is<EPIS>(P, EPI_GRADN)) {
+          P.g[(size_t)row * P.ldg + col] = pre1[i][j][r];
+          P.C[(size_t)row * P.ldc + col] = pre1[i][j][r] + P.alpha * v;
         } else if (epi_is<EPIS>(P, EPI_PARTIAL)) {
           P.C[(size_t)z * P.M * P.N + (size_t)row * P.N + col] = v;
         } else if (epi_is<EPIS>(P, EPI_SCALED)) {

@@ -43,6 +43,8 @@ struct lst_state {
   int last_slots = 0;  // m * K of the last factored step
   int hbits = 0;
   int ld0 = 0;
+  float* Nm = nullptr;  // m_max > 128: m x ldn, N = A C1 A + A C2 B + B C2^T A + B Y^T Y B
+  int ldn = 0;
   int n_c1p = 0;  // partial sums of h^T Q h per example (two per 32-column tile of H^)
   int n_hap_max = 0;  // partial sums of |H^T H| per row for m = m_max
   // naive workspace
@@ -375,10 +377,19 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     GemmBatch& g = L.gemm;
     g.np = 1;
     GemmProblem& pt = g.p[0];
-    // NP viewed as 2m x 2m (row stride 2m): row 2i = [C1 C2]_i, row 2i+1 = [C2^T Y^T Y]_i;
-    // times [a H; b H] it gives both halves of (N H^T)_i, combined in the epilogue.
-    pt = gemm_problem(L_NN, 2 * m, d, 2 * m, vmat(s->NP, 2 * m, 2 * m),
-                      vmat2(s->aH, d, m, s->bH, d, m), s->T, d, -0.5f * lr, 0.f, EPI_GRADT);
+    if (m > 128) {
+      // N formed first (m x m, elementwise), then T = grad_H - (lr/2) N H^T
+      // at the algorithmic size 2 m^2 d
+      HIPCHK(form_n(s->NP, s->a, s->b, m, s->Nm, s->ldn, st));
+      pt = gemm_problem(L_NN, m, d, m, vmat(s->Nm, s->ldn, m), vmat(H, d, m), s->T, d,
+                        -0.5f * lr, 0.f, EPI_GRADN);
+    } else {
+      // NP viewed as 2m x 2m (row stride 2m): row 2i = [C1 C2]_i, row 2i+1 = [C2^T Y^T Y]_i;
+      // times [a H; b H] it gives both halves of (N H^T)_i, combined in the
+      // epilogue: four times the multiply-adds of N H^T, but no pass to form N
+      pt = gemm_problem(L_NN, 2 * m, d, 2 * m, vmat(s->NP, 2 * m, 2 * m),
+                        vmat2(s->aH, d, m, s->bH, d, m), s->T, d, -0.5f * lr, 0.f, EPI_GRADT);
+    }
     pt.e1 = Hh; pt.lde1 = s->ld0; pt.e2 = s->Yh; pt.lde2 = d;
     pt.s1 = s->a; pt.s2 = s->b; pt.g = grad_H; pt.ldg = d;
     pt.tile = 32;
@@ -516,6 +527,7 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
   };
   if (rc != LST_OK) return fail(rc);
   s->ld0 = (3 * d + m + 3) / 4 * 4;
+  s->ldn = (m + 3) / 4 * 4;
   s->n_c1p = 2 * ((d + 31) / 32);  // the most partials (32-column tiles)
   s->n_hap_max = hap_count(d, m, 32) > hap_count(d, m, 64) ? hap_count(d, m, 32)
                                                            : hap_count(d, m, 64);
@@ -525,7 +537,8 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
   const size_t md = (size_t)m * d;
   if ((rc = dalloc(s, &s->state, 3 * (size_t)d * d)) || (rc = dalloc(s, &s->G, md)) ||
       (rc = dalloc(s, &s->Z0, (size_t)m * s->ld0)) || (rc = dalloc(s, &s->Yh, md)) ||
-      (rc = dalloc(s, &s->NP, (size_t)4 * m * m)) || (rc = dalloc(s, &s->aH, md)) ||
+      (rc = dalloc(s, &s->NP, (size_t)4 * m * m)) ||
+      (rc = dalloc(s, &s->Nm, m > 128 ? (size_t)m * s->ldn : 0)) || (rc = dalloc(s, &s->aH, md)) ||
       (rc = dalloc(s, &s->bH, md)) ||
       (rc = dalloc(s, &s->a, m)) || (rc = dalloc(s, &s->b, m)) || (rc = dalloc(s, &s->cs, m)) ||
       (rc = dalloc(s, &s->T, md)) || (rc = dalloc(s, &s->X, md)) ||

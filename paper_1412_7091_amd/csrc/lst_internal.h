@@ -40,9 +40,10 @@ enum Epi {
                     //   g = s1[i]*E1[i][c] + s2[i]*E2[i][c]; G[i][c] = g;
                     //   C[i][c] = g + alpha*(s1[i]*acc[2i][c] + s2[i]*acc[2i+1][c])
   EPI_PARTIAL = 3,  // split-K partial: slice z of a M x N workspace, reduced by gemm_splitk_reduce
-  EPI_SCALED = 4    // C = alpha * p * acc + beta * C with p = 2^(-2 ilogb(*s1)) (p = 1 when s1
+  EPI_SCALED = 4,   // C = alpha * p * acc + beta * C with p = 2^(-2 ilogb(*s1)) (p = 1 when s1
                     // is null or *s1 is not positive and finite); with g non-null the diagonal
                     // of C is also added into *g (atomically: only its exponent is used)
+  EPI_GRADN = 5     // g = s1[i]*E1[i][c] + s2[i]*E2[i][c]; G[i][c] = g; C[i][c] = g + alpha*acc[i][c]
 };
 
 // Layouts of C = op(A) op(B):  M x K times K x N.
@@ -180,6 +181,10 @@ struct StepLaunch {
 // has its own tile edge (GemmProblem::tile), all share `stages` LDS stages
 // (>= 2).  With ev0 / ev1 the launch records them at the start and the end of
 // the kernel's execution.
+// N = A C1 A + A C2 B + B C2^T A + B (Y^T Y) B (A = diag(a), B = diag(b)) into
+// an m x ldn buffer (columns m .. ldn - 1 zero) from NP = [C1 | C2 | C2^T | Y^T Y].
+hipError_t form_n(const float* NP, const float* a, const float* b, int m, float* N, int ldn,
+                  hipStream_t s);
 hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t s,
                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // 1 when every operand of the batch allows 16-byte LDS-DMA (aligned rows with

@@ -1500,10 +1500,14 @@ constexpr LaunchMasks kLaunchMasks[8] = {
 // The kernels of launches 1 and 2 built for m > 128 also compile 64 x 64
 // tiles: their products are long in K there (d up to 1024), and 64 x 64 tiles
 // fetch half the bytes per output of 32 x 32 ones (launch 1 uses them when
-// they alone fill the chip, launch 2 always).
+// they alone fill the chip, launch 2 always).  The launch-3 kernels built for
+// m > 128 compile the EPI_GRADN epilogue: there T takes N H^T from the formed
+// m x m matrix N instead of the interleaved 2m x 2m view of NP, a quarter of
+// the multiply-adds.
 constexpr LaunchMasks launch_masks(int lk, bool small) {
   LaunchMasks M = kLaunchMasks[lk];
   if (!small && (lk == 1 || lk == 2)) M.tiles |= TILE64;
+  if (!small && (lk == 3 || lk == 6)) M.epis |= 1u << EPI_GRADN;
   return M;
 }
 
@@ -1643,10 +1647,10 @@ static const void* kfn() {
 
 // The kernel built for (launch kind, m <= 128, 16-byte DMA); nullptr for a
 // combination that is not built.
-// Launch kinds with a kernel of their own for m > 128 (64 x 64 tiles, and the
-// solve's memory-streamed iterations); the others run the m <= 128 kernel at
-// every m.
-constexpr bool has_large_kernel(int lk) { return lk == 1 || lk == 2; }
+// Launch kinds with a kernel of their own for m > 128 (64 x 64 tiles, the
+// solve's memory-streamed iterations, the T product from N); the others run
+// the m <= 128 kernel at every m.
+constexpr bool has_large_kernel(int lk) { return lk == 1 || lk == 2 || lk == 3 || lk == 6; }
 
 static const void* step_kernel_for(int lk, bool small, int w16) {
   switch (lk) {
@@ -1656,13 +1660,41 @@ static const void* step_kernel_for(int lk, bool small, int w16) {
     case 2:
       if (small) return w16 ? kfn<true, 4, 2>() : kfn<true, 1, 2>();
       return w16 ? kfn<false, 4, 2>() : kfn<false, 1, 2>();
-    case 3: return w16 ? kfn<true, 4, 3>() : kfn<true, 1, 3>();
+    case 3:
+      if (small) return w16 ? kfn<true, 4, 3>() : kfn<true, 1, 3>();
+      return w16 ? kfn<false, 4, 3>() : kfn<false, 1, 3>();
     case 4: return w16 ? kfn<true, 4, 4>() : kfn<true, 1, 4>();
     case 5: return w16 ? kfn<true, 4, 5>() : kfn<true, 1, 5>();
-    case 6: return w16 ? kfn<true, 4, 6>() : kfn<true, 1, 6>();
+    case 6:
+      if (small) return w16 ? kfn<true, 4, 6>() : kfn<true, 1, 6>();
+      return w16 ? kfn<false, 4, 6>() : kfn<false, 1, 6>();
     case 7: return w16 ? kfn<true, 4, 7>() : kfn<true, 1, 7>();
     default: return nullptr;
   }
+}
+
+// One thread per element of N; row i of NP holds [C1 | C2 | C2^T | Y^T Y]_i.
+__global__ __launch_bounds__(256) void form_n_kernel(const float* __restrict__ NP,
+                                                     const float* __restrict__ a,
+                                                     const float* __restrict__ b, int m,
+                                                     float* __restrict__ N, int ldn) {
+  const int i = blockIdx.y, j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= ldn) return;
+  float v = 0.f;
+  if (j < m) {
+    const float* r = NP + (size_t)i * 4 * m;
+    const float aj = a[j], bj = b[j];
+    v = a[i] * (r[j] * aj + r[m + j] * bj) + b[i] * (r[2 * m + j] * aj + r[3 * m + j] * bj);
+  }
+  N[(size_t)i * ldn + j] = v;
+}
+
+hipError_t form_n(const float* NP, const float* a, const float* b, int m, float* N, int ldn,
+                  hipStream_t s) {
+  if (m <= 0 || ldn < m) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(form_n_kernel, dim3((ldn + 255) / 256, m), dim3(256), 0, s, NP, a, b, m, N,
+                     ldn);
+  return hipGetLastError();
 }
 
 hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t s,
