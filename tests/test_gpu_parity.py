@@ -71,7 +71,8 @@ def test_several_tiles_ragged(gpu_lib):
 def test_wide_minibatch_ragged(gpu_lib):
     """m = 260 > 128: the Woodbury solve reads H^T H from memory with 16-byte loads;
     260 is not a multiple of 16 (clamped row blocks and k slices), r is about 0.3,
-    so a dozen Neumann iterations run."""
+    so the Neumann series runs several iterations (its a-priori cap is eleven) before its
+    per-column stopping test passes."""
     cfg = _cfg(D=3000, d=64, m=260, K=3, lr=5e-3, pad_frac=0.1, entropy=112)
     reports, W_rel, _ = run_parity(cfg, 4)
     _assert(reports, W_rel)
