@@ -125,6 +125,19 @@ def test_spherical_zipf_small(gpu_lib):
     _assert(reports, W_rel)
 
 
+def test_spherical_wide_minibatch(gpu_lib):
+    """m = 203 > 128 with the spherical loss: launch 3 forms N = A C1 A + A C2 B + B C2^T A
+    + B Y^T Y B with per-example a_i = 2 / S_i and b_i = beta_i (not constants) and takes
+    T from N H^T; m is not a multiple of 4 (N's rows are padded) and Zipf classes collide.
+    At lr = 1e-2 the N H^T term is a sizeable part of T, and the Zipf head rows take large
+    updates: the fp32 grad error of either T path (m = 128 takes the interleaved one) passes
+    1e-4 after about a dozen steps, so eight are run."""
+    cfg = _cfg(D=4001, d=40, m=203, K=1, loss="spherical", lr=1e-2, idx_dist="zipf", zipf_s=1.0,
+               val_dist="one", distinct=True, h_scale=None, entropy=113)
+    reports, W_rel, _ = run_parity(cfg, 8, V_check_untouched=True)
+    _assert(reports, W_rel)
+
+
 def test_random_initial_U(gpu_lib):
     cfg = _cfg(D=800, d=20, m=8, K=5, u_init="random", entropy=105)
     reports, W_rel, _ = run_parity(cfg, 20)
