@@ -12,7 +12,9 @@
 //             scalars per example: loss, a_i, b_i, c_i, a h_i, b h_i, and the
 //                     hash table of each target row's smallest slot         (steps 3-6)
 //   launch 3  GEMM    grad_H = H^ A + Y^ diag(b), T = grad_H - (lr/2) N H^T  (step 4)
-//                     with N H^T = A [C1 C2] [AH; BH] + B [C2^T Y^T Y] [AH; BH]
+//                     with N H^T = A [C1 C2] [AH; BH] + B [C2^T Y^T Y] [AH; BH];
+//                     for m > 128 a small kernel forms N between launches 2
+//                     and 3 and the GEMM takes N H^T directly
 //             scatter V[r] += sum over examples j holding r of c_j X_j     (step 9)
 //   launch 4  GEMM    Q -= lr (H T^T + T H^T), symmetric; U -= lr (UH) A H^T;
 //                     U^{-T} -= X^T H^T                                     (steps 7, 8, 10)
