@@ -122,6 +122,104 @@ def spherical_softmax_step(W, H_rows, idx, lr: float, eps: float = 1e-3):
     return loss, grad_H.T.copy(), W_new
 
 
+def term_scales(W, H_rows, idx, val, loss, grad_H, loss_kind: str = "squared",
+                eps: float = 1e-3):
+    """Per-example magnitudes of the terms whose sums give L_i and grad_h_i.
+
+    A method that never forms o = W h evaluates the loss and the gradient as
+    sums of a few terms (eq. L and eq. gradH of section 3.1; the section 3.6
+    family for the spherical softmax):
+      squared    L_i = h^T Q h - 2 h^T W^T y + y^T y,   grad = 2 W^T W h - 2 W^T y;
+      spherical  L_i = log S_i - log(o_c^2 + eps),      grad = (2/S_i) W^T W h + b_i W^T e_c,
+                 b_i = -2 o_c / (o_c^2 + eps), S_i = sum_j (o_j^2 + eps).
+    The rounding error of any evaluation of such a sum is bounded by a multiple
+    of the sum of the terms' magnitudes, which can exceed |L_i| or ||grad_i||
+    many times when the terms cancel.  For the spherical softmax the scales
+    also carry the sensitivity of L_i and of the class term of grad_i to o_c,
+    a sum of terms of total size |w_c| |h_i| (w_c the class row of W).  Returns (loss_scale[m], grad_scale[m]):
+    sum of |term| for L_i and sum of ||term|| for grad_h_i, at W (the weights
+    the step starts from), loss and grad_H (the step's exact loss[m] and
+    gradient, m x d).  Costs O(m K d): the dense terms come from grad_H and
+    the sparse ones, log S_i from L_i.
+    """
+    W = widen(W)
+    H = widen(H_rows)                        # m x d, rows are examples
+    g = widen(grad_H)
+    idx = np.asarray(idx)
+    m = H.shape[0]
+    loss_scale = np.zeros(m)
+    grad_scale = np.zeros(m)
+    for i in range(m):
+        if loss_kind == "squared":
+            wty = np.zeros(W.shape[1])
+            yv = {}
+            for k in range(idx.shape[1]):
+                r = int(idx[i, k])
+                if r < 0:
+                    continue
+                yv[r] = yv.get(r, 0.0) + float(val[i, k])
+            for r, v in yv.items():
+                wty += v * W[r]
+            yy = sum(v * v for v in yv.values())
+            wtwh = 0.5 * g[i] + wty                   # W^T W h from grad = 2 (W^T W h - W^T y)
+            loss_scale[i] = abs(H[i] @ wtwh) + 2.0 * abs(H[i] @ wty) + yy
+            grad_scale[i] = 2.0 * np.linalg.norm(wtwh) + 2.0 * np.linalg.norm(wty)
+        elif loss_kind == "spherical":
+            c = int(idx[i, 0])
+            wc = W[c]
+            oc = float(wc @ H[i])
+            b = -2.0 * oc / (oc * oc + eps)
+            t = b * wc
+            lo = np.log(oc * oc + eps)
+            # o_c = w_c . h is itself a sum, of terms of total size |w_c| |h|; a
+            # change of o_c moves L_i by b dO_c and the class term of the
+            # gradient by b'(o_c) dO_c w_c, b' = 2 (o_c^2 - eps) / (o_c^2 + eps)^2,
+            # up to 2 / eps in size near o_c = 0
+            doc = float(np.linalg.norm(wc) * np.linalg.norm(H[i]))
+            db = 2.0 * (oc * oc - eps) / (oc * oc + eps) ** 2
+            loss_scale[i] = abs(lo) + abs(float(loss[i]) + lo) + abs(b) * doc
+            grad_scale[i] = (np.linalg.norm(g[i] - t) + np.linalg.norm(t)
+                             + abs(db) * doc * np.linalg.norm(wc))
+        else:
+            raise ValueError(f"unknown loss {loss_kind!r}")
+    return loss_scale, grad_scale
+
+
+def step_fp32(W, H_rows, idx, val, lr: float, loss_kind: str = "squared", eps: float = 1e-3):
+    """The same definition as `step`, evaluated in float32 arithmetic.
+
+    Not a reference: a yardstick.  Its distance from the fp64 trajectory shows
+    how closely any fp32 evaluation of the method can follow that trajectory
+    (the spherical softmax amplifies rounding through -2 o_c / (o_c^2 + eps),
+    whose slope at small o_c is up to 2 / eps).  Returns (loss, grad_H, W_new)
+    as float32 arrays.
+    """
+    f = np.float32
+    W = np.asarray(W, dtype=f)
+    D = W.shape[0]
+    H = np.asarray(H_rows, dtype=f).T
+    m = H.shape[1]
+    O = W @ H
+    if loss_kind == "squared":
+        Y = dense_targets(D, idx, val).astype(f)
+        R = O - Y
+        loss = np.einsum("jm,jm->m", R, R)
+        G = f(2.0) * R
+    elif loss_kind == "spherical":
+        c = np.asarray(idx)[:, 0].astype(np.int64)
+        cols = np.arange(m)
+        S = np.sum(O * O + f(eps), axis=0, dtype=f)
+        oc = O[c, cols]
+        loss = -np.log((oc * oc + f(eps)) / S)
+        G = f(2.0) * O / S
+        G[c, cols] -= f(2.0) * oc / (oc * oc + f(eps))
+    else:
+        raise ValueError(f"unknown loss {loss_kind!r}")
+    grad = (W.T @ G).T.copy()
+    W_new = W - f(lr) * (G @ H.T)
+    return loss, grad, W_new
+
+
 def step(W, H_rows, idx, val, lr: float, loss_kind: str = "squared", eps: float = 1e-3):
     """Dispatch on the loss: 'squared' or 'spherical'."""
     if loss_kind == "squared":

@@ -1,4 +1,4 @@
-"""The paper's factored algorithm, literally, in fp64 (test infrastructure only).
+"""The paper's factored representation of W, in fp64 (test infrastructure only).
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
@@ -8,14 +8,40 @@ exists to check the paper's algebra against the explicit definition in
 `oracle.explicit`: after every step V U must equal the explicitly updated W,
 Q must equal W^T W and U (U^{-T})^T must be the identity.
 
+How the step is organised here.  Every loss this package handles has an
+output gradient of the form
+
+    dL/dO = W H A + G,      A = diag(a_1 .. a_m),  G sparse on the targets,
+
+(squared error: a_i = 2 and G = -2 Y, eq. gradH; spherical softmax: see
+`spherical_minibatch_step`).  For such a loss the whole update is a function
+of (H, A, G) and the factored state, derived once in `_factored_update`:
+
+  * gradient wrt H       W^T dL/dO = (Q H) A + W^T G, with W^T G = U^T (V^T G)
+                         (section 3.1, eq. gradH, and the remark at the end of
+                         section 3.2 that W^T y is U^T (V^T y));
+  * the W update         W - lr (dL/dO) H^T is reached by
+                         U <- U (I - lr H A H^T)          (eq. updateU) and
+                         V <- V - lr G (U_new^{-T} H)^T   (eq. updateV),
+                         since V_new U_new = V U_new - lr G H^T;
+  * U^{-T}               (I - lr H A H^T)^{-1} by the Woodbury identity, which
+                         for one example is the Sherman-Morrison form of
+                         eq. updateU-T (section 3.5 and the minibatch appendix);
+  * Q                    W_new^T W_new expanded (the proof of the Q update in the
+                         appendix): Q - lr (H grad^T + grad H^T) + lr^2 H N H^T
+                         with N = (dL/dO)^T (dL/dO) built from m x m pieces.
+
 Functions
-  FactoredState.from_initial  Appendix A initialisation (V = W0, U = I, U^{-T} = I,
-                              Q = V^T V), generalised to any invertible U0.
-  minibatch_step              Appendix A, steps 1-10, squared error, in the paper's order.
-  online_step                 Algorithm 1 (one example, Sherman-Morrison update of U^{-T}).
-  sherman_morrison_inverse_T  equation (updateU-T) on its own.
-  spherical_minibatch_step    minibatch form for the spherical softmax, derived here
-                              (the paper gives no minibatch formulas for section 3.6).
+  FactoredState.from_initial  the initialisation of the minibatch appendix (V = W0,
+                              U = U^{-T} = I, Q = V^T V), generalised to any
+                              invertible U0.
+  minibatch_step              squared error, any m (a_i = 2, G = -2 Y).
+  spherical_minibatch_step    spherical softmax, one class per example (the paper
+                              lists this loss in section 3.6 without minibatch
+                              formulas; the (a, G) form above supplies them).
+  online_step                 one example, squared error, with the rank-one
+                              (Sherman-Morrison) update of U^{-T} of eq. updateU-T.
+  sherman_morrison_inverse_T  eq. updateU-T on its own.
   pristine_restore            Appendix C: V <- V U, U <- I, U^{-T} <- I.
 """
 from __future__ import annotations
@@ -36,8 +62,8 @@ class FactoredState:
 
     @classmethod
     def from_initial(cls, V0, U0=None) -> "FactoredState":
-        """Appendix A initialisation.  With U0 = I this is V = W0, Q = V^T V,
-        U = U^{-T} = I; a general invertible U0 gives W0 = V0 U0."""
+        """Initial state with W0 = V0 U0 (U0 = I unless given): U^{-T} = inv(U0)^T,
+        Q = W0^T W0.  With U0 = I this is the appendix's V = W0, Q = V^T V."""
         V = widen(V0)
         d = V.shape[1]
         U = np.eye(d) if U0 is None else widen(U0)
@@ -48,98 +74,105 @@ class FactoredState:
         return self.V @ self.U
 
 
-def minibatch_step(st: FactoredState, H_rows, idx, val, lr: float):
-    """Appendix A, steps 1-10 (squared error), applied in place to `st`.
+def _factored_update(st: FactoredState, H: np.ndarray, a: np.ndarray, G: np.ndarray,
+                     QH: np.ndarray, WtG: np.ndarray, lr: float) -> np.ndarray:
+    """Apply W <- W - lr (W H A + G) H^T to the factored state; return grad_H (d x m).
 
-    Returns (loss[m] = diag M, grad_H[m x d]).  The sum of loss is L = Tr M.
+    H is d x m (columns are examples), a the diagonal of A, G the D x m sparse
+    part of dL/dO, QH = Q H and WtG = W^T G (both d x m, from the state before
+    the update).  The new U, U^{-T}, V and Q all follow from the same
+    rank-m change  I - lr H A H^T  of U's right-hand side.
+    """
+    A = np.diag(a)
+    grad = QH @ A + WtG                                  # W^T dL/dO
+    # N = (dL/dO)^T (dL/dO) = A H^T Q H A + A H^T W^T G + G^T W H A + G^T G
+    HtWtG = H.T @ WtG
+    N = A @ (H.T @ QH) @ A + A @ HtWtG + HtWtG.T @ A + G.T @ G
+    # U_new^{-T} = U^{-T} (I - lr H A H^T)^{-1}
+    #            = U^{-T} - (U^{-T} H) (H^T H - A^{-1}/lr)^{-1} H^T          (Woodbury)
+    S = H.T @ H - np.diag(1.0 / a) / lr
+    UinvT_new = st.UinvT - (st.UinvT @ H) @ np.linalg.solve(S, H.T)
+    U_new = st.U - lr * (st.U @ H) @ A @ H.T
+    V_new = st.V - lr * G @ (UinvT_new @ H).T
+    Q_new = st.Q - lr * (H @ grad.T + grad @ H.T) + lr * lr * (H @ N) @ H.T
+    st.U, st.UinvT, st.V, st.Q = U_new, UinvT_new, V_new, Q_new
+    return grad
+
+
+def minibatch_step(st: FactoredState, H_rows, idx, val, lr: float):
+    """Squared error over a minibatch, applied in place to `st`.
+
+    Loss (eq. L, one example per column): L_i = h_i^T Q h_i - 2 h_i^T (W^T y_i)
+    + y_i^T y_i; the minibatch loss is their sum (the trace of the m x m matrix
+    whose diagonal they are).  dL/dO = 2 (W H - Y): a_i = 2, G = -2 Y.
+    Returns (loss[m], grad_H[m x d]).
     """
     D = st.V.shape[0]
     H = widen(H_rows).T                      # d x m
-    m = H.shape[1]
     Y = dense_targets(D, idx, val)           # D x m, sparse in content
-    Hhat = st.Q @ H                                          # 1
-    Yhat = st.U.T @ (st.V.T @ Y)                             # 2
-    Zhat = Hhat - Yhat                                       # 3
-    grad_H = 2.0 * Zhat                                      # 4
-    M = H.T @ Zhat - Yhat.T @ H + Y.T @ Y                    # 5
-    loss = np.diag(M).copy()                                 # 6 (L = Tr M)
-    U_new = st.U - 2.0 * lr * (st.U @ H) @ H.T               # 7
-    S = H.T @ H - np.eye(m) / (2.0 * lr)
-    UinvT_new = st.UinvT - (st.UinvT @ H) @ np.linalg.solve(S, H.T)   # 8 (Woodbury)
-    V_new = st.V + 2.0 * lr * Y @ (UinvT_new @ H).T          # 9
-    Q_new = (st.Q - 2.0 * lr * (H @ Zhat.T + Zhat @ H.T)
-             + 4.0 * lr * lr * (H @ M) @ H.T)                # 10
-    st.U, st.UinvT, st.V, st.Q = U_new, UinvT_new, V_new, Q_new
-    return loss, grad_H.T.copy()
+    QH = st.Q @ H
+    WtY = st.U.T @ (st.V.T @ Y)              # W^T Y without forming W
+    loss = (np.einsum("ji,ji->i", H, QH) - 2.0 * np.einsum("ji,ji->i", H, WtY)
+            + np.einsum("ji,ji->i", Y, Y))
+    m = H.shape[1]
+    grad = _factored_update(st, H, np.full(m, 2.0), -2.0 * Y, QH, -2.0 * WtY, lr)
+    return loss, grad.T.copy()
+
+
+def spherical_minibatch_step(st: FactoredState, H_rows, idx, lr: float, eps: float = 1e-3):
+    """Spherical softmax L_i = -log((o_c^2 + eps) / sum_j (o_j^2 + eps)), in place.
+
+    With o = W h_i:  sum_j (o_j^2 + eps) = h_i^T Q h_i + D eps =: S_i and
+    o_c = h_i^T (W^T e_c), both cheap (the section 3.6 family).  The output
+    gradient is 2 o / S_i - 2 o_c e_c / (o_c^2 + eps), i.e. the (a, G) form with
+    a_i = 2 / S_i and G = Y diag(beta), beta_i = -2 o_c / (o_c^2 + eps), Y the
+    one-hot targets.  Pinned against the explicit definition and finite
+    differences only (the paper prints no minibatch formulas for this loss).
+    Returns (loss[m], grad_H[m x d]).
+    """
+    D = st.V.shape[0]
+    H = widen(H_rows).T                                      # d x m
+    Y = dense_targets(D, idx, None, one_hot=True)            # D x m
+    QH = st.Q @ H
+    WtY = st.U.T @ (st.V.T @ Y)                              # column i: W^T e_{c_i}
+    oc = np.einsum("ji,ji->i", H, WtY)
+    S = np.einsum("ji,ji->i", H, QH) + D * eps
+    loss = -np.log((oc * oc + eps) / S)
+    beta = -2.0 * oc / (oc * oc + eps)
+    grad = _factored_update(st, H, 2.0 / S, Y * beta[None, :], QH, WtY * beta[None, :], lr)
+    return loss, grad.T.copy()
 
 
 def sherman_morrison_inverse_T(UinvT, h, lr: float):
-    """Equation (updateU-T): U_new^{-T} = U^{-T} + 2 lr / (1 - 2 lr ||h||^2) (U^{-T} h) h^T."""
+    """Eq. updateU-T: the inverse transpose of U (I - 2 lr h h^T) from that of U,
+    U^{-T} + 2 lr / (1 - 2 lr ||h||^2) (U^{-T} h) h^T."""
     h = widen(h)
     return UinvT + (2.0 * lr / (1.0 - 2.0 * lr * (h @ h))) * np.outer(UinvT @ h, h)
 
 
 def online_step(st: FactoredState, h, y_idx, y_val, lr: float):
-    """Algorithm 1 (one example, squared error), applied in place.  Returns (L, grad_h)."""
+    """One example, squared error, applied in place.  Returns (L, grad_h).
+
+    The loss and the gradient come from eq. L and eq. gradH (with
+    z = Q h - W^T y); the state then moves by rank-one changes only:
+    U by eq. updateU, U^{-T} by eq. updateU-T, V along y by eq. updateV
+    (which needs the new U^{-T} times h), and Q by eq. updateQ, whose last
+    term carries the example's loss L.
+    """
     D = st.V.shape[0]
     h = widen(h)
     y = dense_targets(D, np.asarray(y_idx).reshape(1, -1), np.asarray(y_val).reshape(1, -1))[:, 0]
-    hhat = st.Q @ h                                          # 1
-    yhat = st.U.T @ (st.V.T @ y)                             # 2
-    zhat = hhat - yhat                                       # 3
-    grad_h = 2.0 * zhat                                      # 4
-    L = h @ hhat - 2.0 * (h @ yhat) + y @ y                  # 5
-    U_new = st.U - 2.0 * lr * np.outer(st.U @ h, h)          # 6
-    UinvT_new = sherman_morrison_inverse_T(st.UinvT, h, lr)  # 7
-    V_new = st.V + 2.0 * lr * np.outer(y, UinvT_new @ h)     # 8
-    Q_new = (st.Q - 2.0 * lr * (np.outer(h, zhat) + np.outer(zhat, h))
-             + 4.0 * lr * lr * L * np.outer(h, h))           # 9
-    st.U, st.UinvT, st.V, st.Q = U_new, UinvT_new, V_new, Q_new
+    Qh = st.Q @ h
+    Wty = st.U.T @ (st.V.T @ y)
+    z = Qh - Wty
+    L = h @ Qh - 2.0 * (h @ Wty) + y @ y
+    grad_h = 2.0 * z
+    UinvT_new = sherman_morrison_inverse_T(st.UinvT, h, lr)
+    st.V = st.V + 2.0 * lr * np.outer(y, UinvT_new @ h)
+    st.U = st.U - 2.0 * lr * np.outer(st.U @ h, h)
+    st.UinvT = UinvT_new
+    st.Q = st.Q - 2.0 * lr * (np.outer(h, z) + np.outer(z, h)) + 4.0 * lr * lr * L * np.outer(h, h)
     return L, grad_h
-
-
-def spherical_minibatch_step(st: FactoredState, H_rows, idx, lr: float, eps: float = 1e-3):
-    """Factored minibatch step for L_i = -log((o_c^2 + eps) / sum_j (o_j^2 + eps)).
-
-    Derived here, following the structure of Appendix A (the paper lists the
-    loss family in section 3.6 but gives no minibatch formulas).  Write the
-    output gradient of the minibatch as  dL/dO = W H A + G,  with
-    A = diag(a_i), a_i = 2 / S_i, S_i = h_i^T Q h_i + D eps (= sum_j (o_j^2 + eps)),
-    and G = Y diag(beta_i) sparse on the targets, beta_i = -2 o_c / (o_c^2 + eps),
-    o_c = h_i^T (W^T e_c).  Then W_new = W - lr (W H A + G) H^T and, exactly as in
-    Appendix A:
-        U_new      = U - lr (U H) A H^T
-        U_new^{-T} = U^{-T} - (U^{-T} H) S_w^{-1} H^T,  S_w = H^T H - A^{-1} / lr   (Woodbury)
-        V_new      = V - lr G (U_new^{-T} H)^T
-        Q_new      = Q - lr (H grad_H^T + grad_H H^T) + lr^2 H N H^T
-    with grad_H = Q H A + W^T G and N = (dL/dO)^T (dL/dO)
-       = A H^T Q H A + A H^T (W^T G) + (W^T G)^T H A + G^T G.
-    Squared error is the special case a_i = 2, G = -2 Y.
-    Pinned against the explicit definition and finite differences only.
-    """
-    D = st.V.shape[0]
-    H = widen(H_rows).T                                      # d x m
-    m = H.shape[1]
-    Y = dense_targets(D, idx, None, one_hot=True)            # one-hot targets, D x m
-    Hhat = st.Q @ H                                          # Q H
-    Yhat = st.U.T @ (st.V.T @ Y)                             # W^T Y: column i = W^T e_{c_i}
-    oc = np.einsum("ji,ji->i", H, Yhat)                      # o_c = h^T W^T e_c
-    S = np.einsum("ji,ji->i", H, Hhat) + D * eps             # ||o||^2 + D eps
-    loss = -np.log((oc * oc + eps) / S)
-    a = 2.0 / S
-    beta = -2.0 * oc / (oc * oc + eps)
-    A = np.diag(a)
-    G = Y * beta[None, :]                                    # sparse part of dL/dO
-    WtG = Yhat * beta[None, :]                               # W^T G
-    grad_H = Hhat @ A + WtG
-    N = A @ H.T @ Hhat @ A + A @ H.T @ WtG + WtG.T @ H @ A + G.T @ G
-    U_new = st.U - lr * (st.U @ H) @ A @ H.T
-    Sw = H.T @ H - np.diag(1.0 / a) / lr
-    UinvT_new = st.UinvT - (st.UinvT @ H) @ np.linalg.solve(Sw, H.T)
-    V_new = st.V - lr * G @ (UinvT_new @ H).T
-    Q_new = st.Q - lr * (H @ grad_H.T + grad_H @ H.T) + lr * lr * (H @ N) @ H.T
-    st.U, st.UinvT, st.V, st.Q = U_new, UinvT_new, V_new, Q_new
-    return loss, grad_H.T.copy()
 
 
 def pristine_restore(st: FactoredState) -> None:

@@ -8,9 +8,10 @@ it corrects only the singular values of U that leave a safe range
 [sigma_low, sigma_high], each with a rank-one change of U, U^{-T} and V that
 leaves W = V U (hence Q = W^T W) unchanged.
 
-Functions (Appendix C, in the order the appendix introduces them)
-  fix_singular_value       the procedure that moves one singular value sigma of U,
-                           with left singular vector u, to sigma_star.
+Functions
+  fix_singular_value       moves one singular value sigma of U, with left singular
+                           vector u, to sigma_star (a symmetric rank-one left
+                           factor on U, its inverse on V).
   stabilize_svd            the appendix's procedure with a full SVD of U: every
                            singular value outside the range is moved to 1.
   top_left_singular_pair   the power iteration the appendix proposes instead of the
@@ -40,24 +41,25 @@ from .factored import FactoredState
 def fix_singular_value(st: FactoredState, sigma: float, u: np.ndarray, sigma_star: float = 1.0):
     """Move the singular value sigma of U (left singular vector u, unit norm) to sigma_star.
 
-    alpha = (sigma_star - sigma) / sigma and beta = -alpha / (1 + alpha), then
-        U      <- U + alpha u (U^T u)^T
-        V      <- V + beta (V u) u^T
-        U^{-T} <- U^{-T} + beta u (U^{-1} u)^T,  U^{-1} = (U^{-T})^T before this update.
-    With U = sum_k s_k u_k v_k^T, U^T u_k = s_k v_k, so the new U has s_k (1 + alpha)
-    = sigma_star in place of s_k and the same singular vectors; V is multiplied on
-    the right by (I + alpha u u^T)^{-1} = I + beta u u^T, so V U is unchanged.
-    Applied in place; returns (alpha, beta).
+    With U = sum_k s_k u_k v_k^T, left-multiplying U by L = I + alpha u u^T,
+    alpha = sigma_star / sigma - 1, scales the term of u by 1 + alpha and leaves
+    every other singular value and every singular vector alone.  W = V U stays
+    the same when V is right-multiplied by L^{-1} = I + beta u u^T with
+    beta = -alpha / (1 + alpha) (Sherman-Morrison for a rank-one change of the
+    identity), and since L is symmetric the new U^{-T} is L^{-1} U^{-T}.
+    Each of the three products is applied as a rank-one correction, so V costs
+    O(D d).  Applied in place; returns (alpha, beta).
     """
     u = np.asarray(u, dtype=np.float64)
-    alpha = (sigma_star - sigma) / sigma
+    alpha = sigma_star / sigma - 1.0
     beta = -alpha / (1.0 + alpha)
-    Uinv = st.UinvT.T
-    w_u = st.U.T @ u
-    w_i = Uinv @ u
-    st.U = st.U + alpha * np.outer(u, w_u)
+    # L U = U + alpha u (u^T U);  L^{-1} U^{-T} = U^{-T} + beta u (u^T U^{-T});
+    # V L^{-1} = V + beta (V u) u^T.  Row vectors u^T U and u^T U^{-T} from the old state.
+    uU = u @ st.U
+    uUinvT = u @ st.UinvT
+    st.U = st.U + alpha * np.outer(u, uU)
+    st.UinvT = st.UinvT + beta * np.outer(u, uUinvT)
     st.V = st.V + beta * np.outer(st.V @ u, u)
-    st.UinvT = st.UinvT + beta * np.outer(u, w_i)
     return alpha, beta
 
 

@@ -570,18 +570,36 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
     if (hipMemcpyAsync(Up(s), U, (size_t)d * d * sizeof(float), hipMemcpyDeviceToDevice,
                        s->stream) != hipSuccess)
       return fail(LST_EHIP);
-    // U^{-T}: invert U (fp64 Gauss-Jordan), then transpose
+    // U^{-T}: invert U (fp64 Gauss-Jordan), then transpose.  The scratch of
+    // the inversion lives only for this call.
     double* work = nullptr;
     float* inv = nullptr;
-    if ((rc = dalloc(s, &work, (size_t)d * d)) || (rc = dalloc(s, &inv, (size_t)d * d)))
-      return fail(rc);
-    if (invert_small(Up(s), d, inv, d, d, work, s->flags, 0, s->stream) != hipSuccess ||
-        transpose_square(inv, Uitp(s), d, s->stream) != hipSuccess)
-      return fail(LST_EHIP);
-    // Q = (V U)^T (V U); the product goes through the restore buffer
-    if ((rc = ensure_vtmp(s))) return fail(rc);
-    if ((rc = vu_product(s, s->stream, s->V, s->Vtmp, nullptr, nullptr))) return fail(rc);
-    if ((rc = gram_splitk(s, s->Vtmp, D, d, Qp(s), 1.f))) return fail(rc);
+    if (hipMalloc((void**)&work, (size_t)d * d * sizeof(double)) != hipSuccess)
+      return fail(LST_ENOMEM);
+    if (hipMalloc((void**)&inv, (size_t)d * d * sizeof(float)) != hipSuccess) {
+      (void)hipFree(work);
+      return fail(LST_ENOMEM);
+    }
+    const bool inv_ok = invert_small(Up(s), d, inv, d, d, work, s->flags, 0, s->stream) ==
+                            hipSuccess &&
+                        transpose_square(inv, Uitp(s), d, s->stream) == hipSuccess;
+    const bool synced = hipStreamSynchronize(s->stream) == hipSuccess;
+    (void)hipFree(work);
+    (void)hipFree(inv);
+    if (!inv_ok || !synced) return fail(LST_EHIP);
+    // Q = (V U)^T (V U).  With drift control on, the product goes through the
+    // restore buffer the state keeps anyway; otherwise through a D x d buffer
+    // freed right after.
+    float* vu = s->Vtmp;
+    if (!vu && hipMalloc((void**)&vu, (size_t)D * d * sizeof(float)) != hipSuccess)
+      return fail(LST_ENOMEM);
+    rc = vu_product(s, s->stream, s->V, vu, nullptr, nullptr);
+    if (rc == LST_OK) rc = gram_splitk(s, vu, D, d, Qp(s), 1.f);  // synchronises
+    if (vu != s->Vtmp) {
+      (void)hipStreamSynchronize(s->stream);
+      (void)hipFree(vu);
+    }
+    if (rc) return fail(rc);
   }
   int err = 0;
   if ((rc = read_flag(s, F_ERR, &err))) return fail(rc);

@@ -441,9 +441,10 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
 // needs is X = S^{-1} P^T (m x d).  A block solves S X_blk = P^T_blk for 16
 // columns.  Writing S = -diag(c) (I - E), E = diag(1/c) H^T H, gives
 // X = (I - E)^{-1} B with B = -diag(1/c) P^T.  When r = ||E||_inf < 1/2 the
-// Neumann series Y_{k+1} = B + E Y_k converges geometrically and is stopped
-// after the first k with r^(k+1) / (1 - r) <= 2^-24, below fp32 rounding of
-// the result.  Otherwise (a learning rate so large that 2 lr ||H^T H|| is not
+// Neumann series Y_{k+1} = B + E Y_k converges geometrically; a block stops it
+// once, in every one of its columns, a bound on the terms left out falls to
+// 2^-20 of that column's largest |B| entry (kNeumannTol, neumann_done), with
+// r^(k+1) / (1 - r) <= 2^-20 as the a-priori cap on k.  Otherwise (a learning rate so large that 2 lr ||H^T H|| is not
 // small) the block runs Gauss-Jordan elimination with partial pivoting on
 // [S | P^T_blk] (fp64 in LDS for m <= 128, fp32 in a global workspace above),
 // flagging LST_ESINGULAR on a pivot that is not finite or not above

@@ -1,9 +1,14 @@
 """GPU parity: the HIP library (through its C ABI) against the fp64 oracle.
 
-Bar (per step, C16 norms): |sum L_gpu - sum L_ref| / |sum L_ref| <= 1e-4 and
-||grad_gpu - grad_ref||_F / ||grad_ref||_F <= 1e-4; after the run
-||V U - W_ref||_F / ||W_ref||_F <= 1e-3; the distinct touched rows equal the
-oracle's np.unique bit for bit; rows of V no target touches stay bitwise equal.
+Bar, every step: |sum L_gpu - sum L_ref| / |sum L_ref| <= 1e-4 and
+||grad_gpu - grad_ref||_F / ||grad_ref||_F <= 1e-4 (the norms of the bar on
+loss and grad_H), and per example: |L_i,gpu - L_i,ref| and ||g_i,gpu - g_i,ref||
+within 1e-4 of the size of the terms the method sums to get L_i and g_i
+(`oracle.explicit.term_scales`: eq. L and eq. gradH, whose terms can cancel;
+for the spherical softmax also the sensitivity to o_c).  After the run
+||V U - W_ref||_F / ||W_ref||_F <= 1e-3, and at every W_every-th step when
+asked.  The distinct touched rows equal the oracle's np.unique bit for bit;
+rows of V no target touches stay bitwise equal.
 """
 import numpy as np
 import pytest
@@ -20,15 +25,20 @@ TOL_W = 1e-3
 
 
 def _assert(reports, W_rel, tol_step=TOL_STEP, tol_W=TOL_W, rows=True):
-    worst_l = max(r.loss_rel for r in reports)
-    worst_g = max(r.grad_rel for r in reports)
-    print(f"steps={len(reports)} worst loss rel={worst_l:.2e} worst grad rel={worst_g:.2e} "
-          f"W rel={W_rel:.2e}", flush=True)
+    worst = {k: max(getattr(r, k) for r in reports)
+             for k in ("loss_rel", "loss_term_rel", "grad_rel", "grad_term_rel", "loss_max_rel",
+                       "grad_row_rel")}
+    print(f"steps={len(reports)} " + " ".join(f"{k}={v:.2e}" for k, v in worst.items())
+          + f" W rel={W_rel:.2e}", flush=True)
     for r in reports:
         assert r.loss_rel <= tol_step, r
         assert r.grad_rel <= tol_step, r
+        assert r.loss_term_rel <= tol_step, r
+        assert r.grad_term_rel <= tol_step, r
         if rows:
             assert r.rows_equal, r
+        if r.W_rel is not None:
+            assert r.W_rel <= tol_W, r
     assert W_rel <= tol_W, W_rel
 
 
@@ -125,17 +135,44 @@ def test_spherical_zipf_small(gpu_lib):
     _assert(reports, W_rel)
 
 
-def test_spherical_wide_minibatch(gpu_lib):
-    """m = 203 > 128 with the spherical loss: launch 3 forms N = A C1 A + A C2 B + B C2^T A
-    + B Y^T Y B with per-example a_i = 2 / S_i and b_i = beta_i (not constants) and takes
-    T from N H^T; m is not a multiple of 4 (N's rows are padded) and Zipf classes collide.
-    At lr = 1e-2 the N H^T term is a sizeable part of T, and the Zipf head rows take large
-    updates: the fp32 grad error of either T path (m = 128 takes the interleaved one) passes
-    1e-4 after about a dozen steps, so eight are run."""
-    cfg = _cfg(D=4001, d=40, m=203, K=1, loss="spherical", lr=1e-2, idx_dist="zipf", zipf_s=1.0,
-               val_dist="one", distinct=True, h_scale=None, entropy=113)
-    reports, W_rel, _ = run_parity(cfg, 8, V_check_untouched=True)
+def _sph_cfg(m, lr, entropy):
+    return _cfg(D=4001, d=40, m=m, K=1, loss="spherical", lr=lr, idx_dist="zipf", zipf_s=1.0,
+                val_dist="one", distinct=True, h_scale=None, entropy=entropy)
+
+
+@pytest.mark.parametrize("m,entropy", [(128, 117), (203, 113)])
+def test_spherical_minibatch_60_steps(gpu_lib, m, entropy):
+    """Spherical softmax with Zipf classes that collide, 60 steps at lr = 1e-3.
+    m = 128 takes N H^T from the interleaved 2m x 2m view of NP (launch 3);
+    m = 203 > 128 forms N = A C1 A + A C2 B + B C2^T A + B Y^T Y B with
+    per-example a_i = 2 / S_i and b_i first (m not a multiple of 4: N's rows are
+    padded).  An fp32 evaluation of the definition stays within 1.1e-5 (grad)
+    and 2.3e-7 (W) of the fp64 trajectory over these 60 steps."""
+    reports, W_rel, _ = run_parity(_sph_cfg(m, 1e-3, entropy), 60, W_every=20,
+                                   V_check_untouched=True)
     _assert(reports, W_rel)
+
+
+@pytest.mark.parametrize("m,entropy", [(128, 117), (203, 113)])
+def test_spherical_stress_tracks_fp32_yardstick(gpu_lib, m, entropy):
+    """The same workloads at lr = 1e-2, where the trajectory itself is unstable
+    in fp32: the slope of b(o_c) = -2 o_c / (o_c^2 + eps) reaches 2 / eps near
+    o_c = 0, so rounding in W grows step after step.  A plain fp32 evaluation of
+    the definition (explicit W, explicit.step_fp32) leaves the 1e-4 grad bar
+    after 11 (m = 128) and 17 (m = 203) steps and reaches 1e-3 around step 24.
+    No fp32 implementation can stay on the fp64 trajectory here, so the bar is
+    relative: the library's grad error stays within 10x the largest error the
+    fp32 evaluation has shown up to that step (plus 1e-5), for 24 steps.  The
+    library's own explicit-W path (naive) is stepped alongside and reported."""
+    reports, W_rel, _ = run_parity(_sph_cfg(m, 1e-2, entropy), 24, yardstick=True,
+                                   with_naive=True, log_every=4)
+    yard = 0.0
+    for r in reports:
+        yard = max(yard, r.yard_grad_rel)
+        print(f"step {r.step}: factored {r.grad_rel:.1e} naive {r.naive_grad_rel:.1e} "
+              f"fp32 definition {r.yard_grad_rel:.1e}", flush=True)
+        assert r.grad_rel <= 10.0 * yard + 1e-5, r
+        assert r.rows_equal, r
 
 
 def test_random_initial_U(gpu_lib):
@@ -152,24 +189,32 @@ def test_naive_path_small(gpu_lib):
         _assert(reports, W_rel, rows=False)
 
 
-def test_c2_paper_prefix(gpu_lib):
-    """D = 200000, d = 500, m = 128, K = 10 at full size (the benchmarked launch)."""
-    reports, W_rel, _ = run_parity(CONFIGS["c2"], 4)
+@pytest.mark.timeout(600)
+def test_c2_paper_100_steps(gpu_lib):
+    """D = 200000, d = 500, m = 128, K = 10, lr = 1e-3 at full size (the benchmarked
+    launches): 100 steps, W checked every 25 steps."""
+    reports, W_rel, _ = run_parity(CONFIGS["c2"], 100, W_every=25, log_every=10)
     _assert(reports, W_rel)
 
 
-def test_c3_spherical_prefix(gpu_lib):
-    reports, W_rel, _ = run_parity(CONFIGS["c3"], 4)
+@pytest.mark.timeout(600)
+def test_c3_spherical_100_steps(gpu_lib):
+    """Spherical softmax with Zipf(1.0) one-hot classes at full size, 100 steps."""
+    reports, W_rel, _ = run_parity(CONFIGS["c3"], 100, W_every=25, log_every=10)
     _assert(reports, W_rel)
 
 
-def test_c4_large_vocab_prefix(gpu_lib):
-    reports, W_rel, _ = run_parity(CONFIGS["c4"], 2)
+@pytest.mark.timeout(600)
+def test_c4_large_vocab_10_steps(gpu_lib):
+    """D = 1M, d = 512, m = 256, K = 64 Zipf(1.1) counts: 10 steps."""
+    reports, W_rel, _ = run_parity(CONFIGS["c4"], 10, W_every=5, log_every=2)
     _assert(reports, W_rel)
 
 
-def test_c5_wide_prefix(gpu_lib):
-    reports, W_rel, _ = run_parity(CONFIGS["c5"], 2)
+@pytest.mark.timeout(600)
+def test_c5_wide_10_steps(gpu_lib):
+    """D = 500k, d = 1024, m = 512, K = 32: 10 steps."""
+    reports, W_rel, _ = run_parity(CONFIGS["c5"], 10, W_every=5, log_every=2)
     _assert(reports, W_rel)
 
 

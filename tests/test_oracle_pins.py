@@ -381,3 +381,55 @@ def test_planted_mistakes_are_caught():
                 caught = True
                 break
         assert caught, f"mutant {mutant.__name__} slipped through every pin"
+
+
+# ------------------------------------------ conditioning scales, fp32 yardstick
+@pytest.mark.parametrize("loss", ["squared", "spherical"])
+def test_term_scales_brute_force(loss):
+    """term_scales against the terms formed from the explicit output o = W h, and
+    the triangle inequality (each scale bounds |L_i| and ||grad_i||)."""
+    kw = dict(K=1) if loss == "spherical" else dict(pad_frac=0.2, dup_frac=0.3)
+    wl = _tiny(loss, seed=31, D=40, d=6, m=5, K=kw.pop("K", 4), **kw)
+    W = wl.init_V().astype(np.float64)
+    H, idx, val = wl.batch(0)
+    eps = 1e-3
+    L, g, _ = explicit.step(W, H, idx, val, 0.05, loss, eps)
+    ls, gs = explicit.term_scales(W, H, idx, val, L, g, loss, eps)
+    Hd = H.astype(np.float64)
+    for i in range(H.shape[0]):
+        o = W @ Hd[i]
+        if loss == "squared":
+            y = np.zeros(W.shape[0])
+            for k in range(idx.shape[1]):
+                if idx[i, k] >= 0:
+                    y[idx[i, k]] += val[i, k]
+            want_l = o @ o + 2 * abs(o @ y) + y @ y
+            want_g = 2 * np.linalg.norm(W.T @ o) + 2 * np.linalg.norm(W.T @ y)
+        else:
+            c = idx[i, 0]
+            S = np.sum(o * o + eps)
+            b = -2 * o[c] / (o[c] ** 2 + eps)
+            db = 2 * (o[c] ** 2 - eps) / (o[c] ** 2 + eps) ** 2
+            doc = np.linalg.norm(W[c]) * np.linalg.norm(Hd[i])
+            want_l = abs(np.log(o[c] ** 2 + eps)) + abs(np.log(S)) + abs(b) * doc
+            want_g = (np.linalg.norm(2 / S * (W.T @ o)) + np.linalg.norm(b * W[c])
+                      + abs(db) * doc * np.linalg.norm(W[c]))
+        assert abs(ls[i] - want_l) <= 1e-10 * want_l
+        assert abs(gs[i] - want_g) <= 1e-10 * want_g
+        assert ls[i] >= abs(L[i]) * (1 - 1e-12)
+        assert gs[i] >= np.linalg.norm(g[i]) * (1 - 1e-12)
+
+
+@pytest.mark.parametrize("loss", ["squared", "spherical"])
+def test_fp32_yardstick_is_the_definition(loss):
+    """step_fp32 is `step` evaluated in float32: on a benign tiny case it agrees to
+    fp32 accuracy (and its outputs are float32)."""
+    kw = dict(K=1) if loss == "spherical" else {}
+    wl = _tiny(loss, seed=32, D=60, d=7, m=6, K=kw.pop("K", 3), **kw)
+    W = wl.init_V()
+    H, idx, val = wl.batch(0)
+    a = explicit.step(W, H, idx, val, 0.05, loss)
+    b = explicit.step_fp32(W, H, idx, val, 0.05, loss)
+    for x, y in zip(b, a):
+        assert x.dtype == np.float32
+        assert _rel(x, y) < 2e-5
