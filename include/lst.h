@@ -51,7 +51,8 @@ enum {
   LST_ENOMEM = -4,      /* device allocation failed                               */
   LST_EHIP = -5,        /* a HIP runtime call failed                              */
   LST_ENONFINITE = -6,  /* the loss of the minibatch is not finite                */
-  LST_ESTATE = -7       /* call not valid for this kind of state                  */
+  LST_ESTATE = -7,      /* call not valid for this kind of state                  */
+  LST_ENOSCRATCH = -8   /* larger than the static workspace of lst_stabilize_noalloc */
 };
 
 /* Loss functions (sections 3.1 and 3.6). */
@@ -199,6 +200,23 @@ typedef struct lst_stab_report {
  * LST_ESTATE for a naive state, LST_ENOMEM, LST_EHIP.
  */
 int lst_stabilize(lst_state* s, const lst_stab_config* cfg, lst_stab_report* report);
+
+/*
+ * lst_stabilize_noalloc -- lst_stabilize for callers that cannot allocate
+ * device memory (code under HIP-graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same kernels and results, but the workspace is a
+ * static device array of 12 MiB that each GPU holds until the process ends,
+ * instead of the state's workspace, which lst_stabilize allocates on first
+ * use.  It fits d <= 512 with max_fixes <= 16; a larger problem returns
+ * LST_ENOSCRATCH without doing anything.  Makes no allocation of any kind.
+ * Every call on one GPU uses that GPU's array, which keeps the last call's
+ * contents (each call initialises what it reads first): calls that overlap
+ * on one GPU (two streams, two states) race and must be serialised by the
+ * caller.  With report non-NULL the call synchronises the state's stream
+ * (not capturable); pass NULL under capture.
+ * Errors: as lst_stabilize, plus LST_ENOSCRATCH.
+ */
+int lst_stabilize_noalloc(lst_state* s, const lst_stab_config* cfg, lst_stab_report* report);
 
 /*
  * lst_set_stabilize -- run lst_stabilize(cfg, NULL) after every `every`-th

@@ -26,6 +26,7 @@ LST_ENOMEM = -4
 LST_EHIP = -5
 LST_ENONFINITE = -6
 LST_ESTATE = -7
+LST_ENOSCRATCH = -8
 
 LST_LOSS_SQUARED = 0
 LST_LOSS_SPHERICAL = 1
@@ -93,6 +94,8 @@ _SIGS = {
     "lst_restore": (ctypes.c_int, [_P]),
     "lst_stabilize": (ctypes.c_int, [_P, ctypes.POINTER(lst_stab_config),
                                      ctypes.POINTER(lst_stab_report)]),
+    "lst_stabilize_noalloc": (ctypes.c_int, [_P, ctypes.POINTER(lst_stab_config),
+                                             ctypes.POINTER(lst_stab_report)]),
     "lst_set_stabilize": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(lst_stab_config)]),
     "lst_naive_init": (ctypes.c_int, [ctypes.POINTER(_P), ctypes.c_int64, ctypes.c_int32, _P,
                                       ctypes.POINTER(lst_config), _P]),
@@ -273,6 +276,17 @@ def lst_stabilize(h, sigma_low=1e-3, sigma_high=100.0, squarings=7, max_fixes=2,
     return rep
 
 
+def lst_stabilize_noalloc(h, sigma_low=1e-3, sigma_high=100.0, squarings=7, max_fixes=2,
+                          reinvert=1, report=True):
+    """lst_stabilize on the library's static workspace (no device allocation)."""
+    cfg = _stab_config(sigma_low, sigma_high, squarings, max_fixes, reinvert)
+    rep = lst_stab_report() if report else None
+    _check(load_library().lst_stabilize_noalloc(h, ctypes.byref(cfg),
+                                                ctypes.byref(rep) if rep is not None else None),
+           "lst_stabilize_noalloc")
+    return rep
+
+
 def lst_set_stabilize(h, every, sigma_low=1e-3, sigma_high=100.0, squarings=7, max_fixes=2,
                       reinvert=1):
     cfg = _stab_config(sigma_low, sigma_high, squarings, max_fixes, reinvert)
@@ -410,6 +424,9 @@ class FactoredOutputLayer(_Layer):
 
     def stabilize(self, **kw):
         return lst_stabilize(self._h, **kw)
+
+    def stabilize_noalloc(self, **kw):
+        return lst_stabilize_noalloc(self._h, **kw)
 
     def set_stabilize(self, every: int, **kw) -> None:
         lst_set_stabilize(self._h, every, **kw)

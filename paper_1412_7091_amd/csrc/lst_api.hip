@@ -15,11 +15,21 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "lst_internal.h"
 
 using namespace lst;
+
+// Workspace of lst_stabilize_noalloc: one array per GPU the library runs on,
+// held until the process ends.  12 MiB: the Appendix C workspace (two d x d
+// products, split-K partials, vectors, per-round flags) for d <= 512 and up
+// to 16 corrections at each end.  Host code takes its device address with
+// hipGetSymbolAddress (scratch_device_ptr); the array's name in host code is
+// not a device address.
+constexpr size_t kScratchFloats = (size_t)3 << 20;
+static __device__ __align__(256) float scratch[kScratchFloats];
 
 struct lst_state {
   int kind = 0;  // 0 factored, 1 naive
@@ -65,6 +75,7 @@ struct lst_state {
   uint64_t graph_clock = 0;
   int use_graphs = 0;  // direct launches: graph replay adds device-side gaps between steps
   hipStream_t cap = nullptr;  // capture stream
+  float* scratch = nullptr;   // this device's copy of the static scratch array
   // Appendix C stabilisation: workspace (allocated at first use) and the
   // periodic setting
   float* stab_f = nullptr;
@@ -81,6 +92,24 @@ struct lst_state {
 };
 
 namespace {
+
+// Device address of `scratch` on each device, taken once per device with that
+// device current (each GPU holds its own copy of the array).
+std::mutex g_scratch_mu;
+std::vector<float*> g_scratch_ptr;
+
+int scratch_device_ptr(int device, float** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (device < 0) return LST_EINVAL;
+  if ((size_t)device >= g_scratch_ptr.size()) g_scratch_ptr.resize(device + 1, nullptr);
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return LST_EHIP;
+    g_scratch_ptr[device] = static_cast<float*>(p);
+  }
+  *out = g_scratch_ptr[device];
+  return LST_OK;
+}
 
 // GEMM tile edge of launch 1: 64 when m > 128 and 64 x 64 tiles alone fill
 // the 256 compute units (half the bytes per output of 32 x 32 tiles), else 32.
@@ -201,6 +230,7 @@ int common_init(lst_state* s, int64_t D, int32_t d, const lst_config* cfg, void*
   s->stream = static_cast<hipStream_t>(hip_stream);
   HIPCHK(hipStreamCreateWithFlags(&s->cap, hipStreamNonBlocking));
   HIPCHK(configure_kernels());
+  OK_OR_RETURN(scratch_device_ptr(s->device, &s->scratch));
   OK_OR_RETURN(dalloc(s, &s->flags, F_COUNT));
   HIPCHK(hipMemsetAsync(s->flags, 0, F_COUNT * sizeof(int), s->stream));
   OK_OR_RETURN(dalloc(s, &s->V, (size_t)D * d));
@@ -447,6 +477,56 @@ int check_stab_config(const lst_stab_config* c) {
   return LST_OK;
 }
 
+// Enqueues one stabilisation on stream st with the workspace f (floats laid
+// out by stab_layout(d, ksplit, cfg.max_fixes)) and the round flags in ints.
+int enqueue_stabilize_in(lst_state* s, const lst_stab_config& cfg, hipStream_t st, float* f,
+                         int* ints, int ksplit) {
+  const StabLayout l = stab_layout(s->d, ksplit, cfg.max_fixes);
+  StabArgs a{};
+  a.D = s->D;
+  a.d = s->d;
+  a.V = s->V;
+  a.U = Up(s);
+  a.Uit = Uitp(s);
+  a.flags = s->flags;
+  a.sigma_low = cfg.sigma_low;
+  a.sigma_high = cfg.sigma_high;
+  a.squarings = cfg.squarings;
+  a.max_fixes = cfg.max_fixes;
+  a.reinvert = cfg.reinvert;
+  a.ksplit = ksplit;
+  a.G = f + l.G; a.G2 = f + l.G2; a.ws = f + l.ws; a.x = f + l.x; a.u = f + l.u; a.w = f + l.w;
+  a.wpart = f + l.wpart; a.scal = f + l.scal; a.sig = f + l.sig; a.trace = f + l.trace;
+  a.chain = ints;
+  a.stop = ints + 2 * (cfg.max_fixes + 1);
+  HIPCHK(stabilize_enqueue(a, st));
+  return LST_OK;
+}
+
+// Reads the report of the stabilisation just enqueued (synchronises).
+int read_stab_report(lst_state* s, const lst_stab_config& cfg, const float* f, const int* ints,
+                     int ksplit, lst_stab_report* report) {
+  const int R = cfg.max_fixes;
+  const StabLayout l = stab_layout(s->d, ksplit, R);
+  std::vector<int> chain(2 * (R + 1));
+  std::vector<float> sig(2 * R);
+  HIPCHK(hipStreamSynchronize(s->stream));
+  HIPCHK(hipMemcpy(chain.data(), ints, chain.size() * sizeof(int), hipMemcpyDeviceToHost));
+  HIPCHK(hipMemcpy(sig.data(), f + l.sig, sig.size() * sizeof(float), hipMemcpyDeviceToHost));
+  int fixes[2] = {0, 0};
+  float last[2] = {NAN, NAN};
+  for (int e = 0; e < 2; ++e)
+    for (int r = 0; r < R; ++r) {
+      fixes[e] += chain[e * (R + 1) + r + 1];
+      if (chain[e * (R + 1) + r]) last[e] = sig[e * R + r];
+    }
+  report->fixes_low = fixes[0];
+  report->fixes_high = fixes[1];
+  report->sigma_min = last[0];
+  report->sigma_max = last[1];
+  return LST_OK;
+}
+
 // Enqueues one stabilisation on stream st (the workspace is sized for the
 // largest max_fixes seen so far; a larger one reallocates it).
 int enqueue_stabilize(lst_state* s, const lst_stab_config& cfg, hipStream_t st) {
@@ -470,27 +550,7 @@ int enqueue_stabilize(lst_state* s, const lst_stab_config& cfg, hipStream_t st) 
     s->stab_ksplit = ks;
     s->stab_rounds = cfg.max_fixes;
   }
-  const StabLayout l = stab_layout(d, s->stab_ksplit, cfg.max_fixes);
-  StabArgs a{};
-  a.D = s->D;
-  a.d = d;
-  a.V = s->V;
-  a.U = Up(s);
-  a.Uit = Uitp(s);
-  a.flags = s->flags;
-  a.sigma_low = cfg.sigma_low;
-  a.sigma_high = cfg.sigma_high;
-  a.squarings = cfg.squarings;
-  a.max_fixes = cfg.max_fixes;
-  a.reinvert = cfg.reinvert;
-  a.ksplit = s->stab_ksplit;
-  float* f = s->stab_f;
-  a.G = f + l.G; a.G2 = f + l.G2; a.ws = f + l.ws; a.x = f + l.x; a.u = f + l.u; a.w = f + l.w;
-  a.wpart = f + l.wpart; a.scal = f + l.scal; a.sig = f + l.sig; a.trace = f + l.trace;
-  a.chain = s->stab_i;
-  a.stop = s->stab_i + 2 * (cfg.max_fixes + 1);
-  HIPCHK(stabilize_enqueue(a, st));
-  return LST_OK;
+  return enqueue_stabilize_in(s, cfg, st, s->stab_f, s->stab_i, s->stab_ksplit);
 }
 
 }  // namespace
@@ -507,6 +567,8 @@ const char* lst_strerror(int status) {
     case LST_EHIP: return "HIP runtime error";
     case LST_ENONFINITE: return "non-finite loss";
     case LST_ESTATE: return "call not valid for this kind of state";
+    case LST_ENOSCRATCH:
+      return "problem larger than the static workspace of the no-allocation entry point";
     default: return "unknown status";
   }
 }
@@ -675,26 +737,23 @@ int lst_stabilize(lst_state* s, const lst_stab_config* cfg, lst_stab_report* rep
   DeviceGuard dg(s->device);
   OK_OR_RETURN(enqueue_stabilize(s, *cfg, s->stream));
   if (!report) return LST_OK;
-  const int R = cfg->max_fixes;
-  const StabLayout l = stab_layout(s->d, s->stab_ksplit, R);
-  std::vector<int> chain(2 * (R + 1));
-  std::vector<float> sig(2 * R);
-  HIPCHK(hipStreamSynchronize(s->stream));
-  HIPCHK(hipMemcpy(chain.data(), s->stab_i, chain.size() * sizeof(int), hipMemcpyDeviceToHost));
-  HIPCHK(hipMemcpy(sig.data(), s->stab_f + l.sig, sig.size() * sizeof(float),
-                   hipMemcpyDeviceToHost));
-  int fixes[2] = {0, 0};
-  float last[2] = {NAN, NAN};
-  for (int e = 0; e < 2; ++e)
-    for (int r = 0; r < R; ++r) {
-      fixes[e] += chain[e * (R + 1) + r + 1];
-      if (chain[e * (R + 1) + r]) last[e] = sig[e * R + r];
-    }
-  report->fixes_low = fixes[0];
-  report->fixes_high = fixes[1];
-  report->sigma_min = last[0];
-  report->sigma_max = last[1];
-  return LST_OK;
+  return read_stab_report(s, *cfg, s->stab_f, s->stab_i, s->stab_ksplit, report);
+}
+
+int lst_stabilize_noalloc(lst_state* s, const lst_stab_config* cfg, lst_stab_report* report) {
+  if (!s) return LST_EINVAL;
+  OK_OR_RETURN(check_stab_config(cfg));
+  if (s->kind != 0) return LST_ESTATE;
+  if (!s->scratch) return LST_EHIP;
+  const int ks = stab_ksplit(s->d);
+  const StabLayout l = stab_layout(s->d, ks, cfg->max_fixes);
+  if (l.floats + l.ints > kScratchFloats) return LST_ENOSCRATCH;
+  DeviceGuard dg(s->device);
+  float* f = s->scratch;
+  int* ints = reinterpret_cast<int*>(s->scratch + l.floats);
+  OK_OR_RETURN(enqueue_stabilize_in(s, *cfg, s->stream, f, ints, ks));
+  if (!report) return LST_OK;
+  return read_stab_report(s, *cfg, f, ints, ks, report);
 }
 
 int lst_set_stabilize(lst_state* s, int32_t every, const lst_stab_config* cfg) {
