@@ -114,6 +114,10 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
  *   loss   (device) m floats: per-example loss L_i.
  *   grad_H (device) m x d: row i = dL/dh_i (no 1/m factor).
  * Never forms W H.  State is updated in place unless the sticky error flag is set.
+ * With m == 1 and K <= 256 the step takes the single-example form of
+ * Algorithm 1 (Sherman-Morrison update of U^{-T}, eq. updateU-T) in two
+ * launches; otherwise the minibatch steps of Appendix A.  Both compute the
+ * same update in exact arithmetic, with the same error behaviour.
  */
 int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* Y_idx,
              const float* Y_val, float lr, float* loss, float* grad_H);

@@ -1,8 +1,11 @@
 // C ABI of the library: state ownership, argument checks, and the launches of
-// one step (the kernels themselves are in step.hip, gemm.hip and small.hip).
+// one step (the kernels themselves are in step.hip, gemm.hip, small.hip and
+// online.hip).
 //
 // The factored step (Appendix A) is four heterogeneous launches on the
-// state's stream (see step.hip).  Shortcuts used, exact in real arithmetic:
+// state's stream (see step.hip); a single example with at most 256 target
+// pairs takes the two launches of online.hip instead.  Shortcuts of the
+// minibatch step, exact in real arithmetic:
 //   U_new^{-T} H = -(1/lr) P S^{-1} A^{-1}, so with X = S^{-1} P^T (m x d):
 //   U_new^{-T} = U^{-T} - X^T H^T and V_new = V - lr G (U_new^{-T} H)^T
 //   = V + sum_i (g_i / a_i) X_i, i.e. c = -val (squared) or b_i / a_i (spherical);
@@ -53,6 +56,8 @@ struct lst_state {
   int last_slots = 0;  // m * K of the last factored step
   int hbits = 0;
   int ld0 = 0;
+  float* on_ws = nullptr;  // single-example step: workspace and tickets
+  int* on_tick = nullptr;
   float* Nm = nullptr;  // m_max > 128: m x ldn, N = A C1 A + A C2 B + B C2^T A + B Y^T Y B
   int ldn = 0;
   int n_c1p = 0;  // partial sums of h^T Q h per example (two per 32-column tile of H^)
@@ -154,8 +159,11 @@ int dalloc(lst_state* s, T** p, size_t count) {
   return LST_OK;
 }
 
-enum Phase { PH_LAUNCH1 = 0, PH_LAUNCH2, PH_LAUNCH3, PH_LAUNCH4, PH_DRIFT, PH_COUNT };
-const char* const kPhaseNames[PH_COUNT] = {"launch1", "launch2", "launch3", "launch4", "drift"};
+enum Phase {
+  PH_LAUNCH1 = 0, PH_LAUNCH2, PH_LAUNCH3, PH_LAUNCH4, PH_DRIFT, PH_ONLINE_A, PH_ONLINE_B, PH_COUNT
+};
+const char* const kPhaseNames[PH_COUNT] = {"launch1", "launch2", "launch3", "launch4",
+                                           "drift",   "online_a", "online_b"};
 
 // Records the begin (end = 0) or end (end = 1) event of a phase on stream st
 // when profiling.
@@ -320,9 +328,47 @@ constexpr int kLaunch34Stages = 4;
 // their list.
 constexpr int kHotMinSlots = 64;
 
+// Drift control after a step (Appendix C, pristine restore when
+// ||U||_F ||U^{-T}||_F > cond_max d).
+int enqueue_drift(lst_state* s, hipStream_t st) {
+  if (!(s->cfg.cond_max > 0.f)) return LST_OK;
+  const int d = s->d;
+  int* fl = s->flags;
+  OK_OR_RETURN(prof_mark(s, PH_DRIFT, 0, st));
+  HIPCHK(drift_check(Up(s), Uitp(s), d, s->cfg.cond_max * (float)d, fl, st));
+  HIPCHK(copy_if(s->V, s->Vtmp, (size_t)s->D * d, fl + F_RESTORE, st));
+  OK_OR_RETURN(vu_product(s, st, s->Vtmp, s->V, fl + F_RESTORE, fl + F_ERR));
+  HIPCHK(set_identity_if(Up(s), d, fl + F_RESTORE, st));
+  HIPCHK(set_identity_if(Uitp(s), d, fl + F_RESTORE, st));
+  return prof_mark(s, PH_DRIFT, 1, st);
+}
+
+// The single-example step (two launches, Sherman-Morrison update of U^{-T}).
+int enqueue_online(lst_state* s, hipStream_t st, int32_t K, const float* H, const int32_t* Y_idx,
+                   const float* Y_val, float lr, float* loss, float* grad_H) {
+  OnlineArgs a = online_args(s->d, s->on_ws, s->on_tick);
+  a.K = K;
+  a.loss_kind = s->cfg.loss;
+  a.D = s->D;
+  a.eps = s->cfg.sph_eps;
+  a.lr = lr;
+  a.h = H; a.idx = Y_idx; a.val = Y_val;
+  a.V = s->V; a.Q = Qp(s); a.U = Up(s); a.Uit = Uitp(s);
+  a.own = s->own;
+  a.flags = s->flags;
+  a.loss = loss; a.grad = grad_H;
+  hipEvent_t e0a, e1a, e0b, e1b;
+  OK_OR_RETURN(prof_pair(s, PH_ONLINE_A, &e0a, &e1a));
+  OK_OR_RETURN(prof_pair(s, PH_ONLINE_B, &e0b, &e1b));
+  HIPCHK(online_step(a, st, e0a, e1a, e0b, e1b));
+  return enqueue_drift(s, st);
+}
+
 // Enqueues the launches of one factored step on stream st.
 int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float* H,
                  const int32_t* Y_idx, const float* Y_val, float lr, float* loss, float* grad_H) {
+  if (m == 1 && K <= kOnlineMaxK)
+    return enqueue_online(s, st, K, H, Y_idx, Y_val, lr, loss, grad_H);
   const int d = s->d;
   int* fl = s->flags;
   StepCtx c{};
@@ -454,16 +500,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     OK_OR_RETURN(prof_pair(s, PH_LAUNCH4, &e0, &e1));
     HIPCHK(step_launch(c, L, stages_for(g, kLaunch34Stages), st, e0, e1));
   }
-  if (s->cfg.cond_max > 0.f) {
-    OK_OR_RETURN(prof_mark(s, PH_DRIFT, 0, st));
-    HIPCHK(drift_check(c.U, c.Uit, d, s->cfg.cond_max * (float)d, fl, st));
-    HIPCHK(copy_if(s->V, s->Vtmp, (size_t)s->D * d, fl + F_RESTORE, st));
-    OK_OR_RETURN(vu_product(s, st, s->Vtmp, s->V, fl + F_RESTORE, fl + F_ERR));
-    HIPCHK(set_identity_if(c.U, d, fl + F_RESTORE, st));
-    HIPCHK(set_identity_if(c.Uit, d, fl + F_RESTORE, st));
-    OK_OR_RETURN(prof_mark(s, PH_DRIFT, 1, st));
-  }
-  return LST_OK;
+  return enqueue_drift(s, st);
 }
 
 int check_stab_config(const lst_stab_config* c) {
@@ -613,9 +650,12 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       (rc = dalloc(s, &s->own, (size_t)m * K)) || (rc = dalloc(s, &s->count, 1)) ||
       (rc = dalloc(s, &s->UHa, md)) || (rc = dalloc(s, &s->yyd, m)) ||
       (rc = dalloc(s, &s->c1p, (size_t)m * s->n_c1p)) ||
-      (rc = dalloc(s, &s->hap, (size_t)m * s->n_hap_max)))
+      (rc = dalloc(s, &s->hap, (size_t)m * s->n_hap_max)) ||
+      (rc = dalloc(s, &s->on_ws, online_workspace_floats(d))) ||
+      (rc = dalloc(s, &s->on_tick, 2 * (size_t)online_tiles(d))))
     return fail(rc);
   if (fill_ints(s->hkey, -1, hsize, s->stream) != hipSuccess ||
+      fill_ints(s->on_tick, 0, 2 * online_tiles(d), s->stream) != hipSuccess ||
       fill_ints(s->hmin, 0x7fffffff, hsize, s->stream) != hipSuccess ||
       fill_ints(s->hcnt, 0, hsize + 1, s->stream) != hipSuccess)
     return fail(LST_EHIP);

@@ -1,0 +1,403 @@
+// The single-example step (m = 1): Algorithm 1 of the paper, extended to the
+// loss family of section 3.6, in two launches.
+//
+// With one example the products of the minibatch step shrink to matrix-vector
+// products and the Woodbury update of U^{-T} to Sherman-Morrison
+// (eq. updateU-T), so the step is bound by reading Q, U and U^{-T} twice (for
+// the products, then for the rank-one updates) and by the round trip between
+// the two passes.  With dL/do = a W h + G (squared error: a = 2, G = -2 y;
+// spherical softmax: a = 2 / S, G = b e_c, b = -2 o_c / (o_c^2 + eps)):
+//   h^ = Q h, y^ = W^T y = U^T (V^T y), c1 = h^T h^, c2 = h^T y^, y^T y;
+//   grad = a h^ + b y^ (squared: b = -2);  N = a^2 c1 + 2 a b c2 + b^2 y^T y;
+//   T = grad - (lr / 2) N h;  den = 1 - lr a ||h||^2;
+//   Q <- Q - lr (h T^T + T h^T);  U <- U - lr a (U h) h^T;
+//   U^{-T} <- U^{-T} + (lr a / den) (U^{-T} h) h^T          (eq. updateU-T);
+//   V[r] <- V[r] - (lr / den) G_r (U^{-T} h)^T for every target row r, since
+//   U_new^{-T} h = (U^{-T} h) / den                         (eq. updateV).
+//
+//   launch A  64 x 64 tiles of Q, U, U^{-T}: the tile's partial sums of Q h,
+//             U h, U^{-T} h over its columns and of U^T g over its rows, with
+//             g = V^T y gathered from the target rows of V.  The last tile of
+//             a row block (column block) to finish, counted with an atomic
+//             ticket, adds that block's partials in tile order and leaves the
+//             finished entries plus partial dot products.  Block 0 checks the
+//             targets and merges repeated rows.
+//   launch B  blocks of R rows: every block forms the same scalars and T from
+//             the finished vectors, then updates its rows of Q, U, U^{-T}, and
+//             its share of the target rows of V.
+// Summation orders are fixed, so the step is deterministic.  Q stays bitwise
+// symmetric: entries (i, j) and (j, i) get the same correction (sym_pair).
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include "lst_internal.h"
+
+namespace lst {
+
+namespace {
+
+constexpr int kOnTile = 64;
+
+enum { PV_Q = 0, PV_U = 1, PV_P = 2, PV_Y = 3 };
+
+// partial sums of vector v from tile t (launch A)
+__device__ __forceinline__ float* on_part(const OnlineArgs& a, int v, int t) {
+  return a.part + ((size_t)v * a.nt + t) * a.d;
+}
+
+// Sum over the 64 lanes of a wave in a fixed order (xor butterfly).
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+// Block 0 of launch A: index checks (LST_EINDEX), and for each slot k whose
+// row no earlier slot holds: own[k] = its row, rsum[k] = the values of all the
+// row's slots added in slot order; other slots own[k] = -1, rsum[k] = 0.
+// Also y^T y, the number of valid pairs and of distinct rows.
+__device__ void online_targets(const OnlineArgs& a, int* skey, float* sval, float* red) {
+  const int tid = threadIdx.x, K = a.K;
+  const bool one_hot = a.loss_kind == LST_LOSS_SPHERICAL;
+  int r = -1;
+  bool valid = false;
+  if (tid < K) {
+    r = a.idx[tid];
+    valid = r >= 0 && (int64_t)r < a.D;
+    const bool bad = (r < -1) || ((int64_t)r >= a.D) || (one_hot && r == -1);
+    if (bad) atomicCAS(a.flags + F_ERR, 0, LST_EINDEX);
+    skey[tid] = valid ? r : -1;
+    sval[tid] = valid ? (one_hot ? 1.f : a.val[tid]) : 0.f;
+  }
+  __syncthreads();
+  bool owner = valid;
+  float sum = 0.f;
+  if (valid) {
+    for (int k = 0; k < tid && owner; ++k) owner = skey[k] != r;
+    if (owner)
+      for (int k = tid; k < K; ++k)
+        if (skey[k] == r) sum += sval[k];
+  }
+  if (tid < K) {
+    a.own[tid] = owner ? r : -1;
+    a.rsum[tid] = owner ? sum : 0.f;
+  }
+  const float yy = wave_sum(sum * sum);
+  const float nnz = wave_sum(valid ? 1.f : 0.f);
+  const float nuq = wave_sum(owner ? 1.f : 0.f);
+  const int w = tid >> 6;
+  if ((tid & 63) == 0) {
+    red[w] = yy;
+    red[4 + w] = nnz;
+    red[8 + w] = nuq;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    a.scal[0] = ((red[0] + red[1]) + red[2]) + red[3];
+    a.flags[F_NNZ] = (int)(((red[4] + red[5]) + red[6]) + red[7]);
+    a.flags[F_UNIQUE] = (int)(((red[8] + red[9]) + red[10]) + red[11]);
+  }
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(256) void online_a_kernel(OnlineArgs a) {
+  __shared__ float sU[kOnTile][kOnTile + 1];
+  __shared__ float sh[kOnTile], sg[4][kOnTile], scol[4][kOnTile];
+  __shared__ int skey[kOnlineMaxK];
+  __shared__ float sval[kOnlineMaxK];
+  __shared__ int s_last[2];
+  const int tid = threadIdx.x, d = a.d, K = a.K, nt = a.nt;
+  if (blockIdx.x == 0) {
+    online_targets(a, skey, sval, &scol[0][0]);
+    return;
+  }
+  const int t = blockIdx.x - 1;
+  const int bi = t / nt, bj = t - bi * nt;
+  const int r0 = bi * kOnTile, c0 = bj * kOnTile;
+
+  // the tile: thread (row i, quarter q) holds 16 consecutive columns of each matrix
+  const int i = tid >> 2, q = tid & 3;
+  const int row = r0 + i, col0 = c0 + 16 * q;
+  float vq[16], vu[16], vp[16];
+  if (VEC && row < d && col0 + 16 <= d) {
+    const float4* Qr = reinterpret_cast<const float4*>(a.Q + (size_t)row * d + col0);
+    const float4* Ur = reinterpret_cast<const float4*>(a.U + (size_t)row * d + col0);
+    const float4* Pr = reinterpret_cast<const float4*>(a.Uit + (size_t)row * d + col0);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const float4 x = Qr[c], y = Ur[c], z = Pr[c];
+      vq[4 * c] = x.x; vq[4 * c + 1] = x.y; vq[4 * c + 2] = x.z; vq[4 * c + 3] = x.w;
+      vu[4 * c] = y.x; vu[4 * c + 1] = y.y; vu[4 * c + 2] = y.z; vu[4 * c + 3] = y.w;
+      vp[4 * c] = z.x; vp[4 * c + 1] = z.y; vp[4 * c + 2] = z.z; vp[4 * c + 3] = z.w;
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const bool in = row < d && col0 + c < d;
+      const size_t o = in ? (size_t)row * d + col0 + c : 0;
+      vq[c] = in ? a.Q[o] : 0.f;
+      vu[c] = in ? a.U[o] : 0.f;
+      vp[c] = in ? a.Uit[o] : 0.f;
+    }
+  }
+  // targets (every tile gathers g over its rows; only block 0 reports errors)
+  if (tid < K) {
+    const int r = a.idx[tid];
+    const bool valid = r >= 0 && (int64_t)r < a.D;
+    skey[tid] = valid ? r : -1;
+    sval[tid] = valid ? (a.loss_kind == LST_LOSS_SPHERICAL ? 1.f : a.val[tid]) : 0.f;
+  }
+  if (tid < kOnTile) sh[tid] = (c0 + tid < d) ? a.h[c0 + tid] : 0.f;
+  __syncthreads();
+  {  // g over the tile's rows: thread (row j, slot group kq) adds slots kq, kq + 4, ...
+    const int j = tid & 63, kq = tid >> 6;
+    const int grow = r0 + j;
+    float g = 0.f;
+    if (grow < d)
+      for (int k = kq; k < K; k += 4) {
+        const int r = skey[k];
+        if (r >= 0) g += sval[k] * a.V[(size_t)r * d + grow];
+      }
+    sg[kq][j] = g;
+  }
+  // row partials of Q h, U h, U^{-T} h
+  float sq = 0.f, su = 0.f, sp = 0.f;
+#pragma unroll
+  for (int c = 0; c < 16; ++c) {
+    const float hv = sh[16 * q + c];
+    sq += vq[c] * hv;
+    su += vu[c] * hv;
+    sp += vp[c] * hv;
+    sU[i][16 * q + c] = vu[c];
+  }
+  sq += __shfl_xor(sq, 1);
+  su += __shfl_xor(su, 1);
+  sp += __shfl_xor(sp, 1);
+  sq += __shfl_xor(sq, 2);
+  su += __shfl_xor(su, 2);
+  sp += __shfl_xor(sp, 2);
+  if (q == 0 && row < d) {
+    on_part(a, PV_Q, bj)[row] = sq;
+    on_part(a, PV_U, bj)[row] = su;
+    on_part(a, PV_P, bj)[row] = sp;
+  }
+  __syncthreads();
+  {  // column partials of U^T g: thread (column j, row quarter qq)
+    const int j = tid & 63, qq = tid >> 6;
+    float s = 0.f;
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) {
+      const int ir = 16 * qq + rr;
+      const float g = ((sg[0][ir] + sg[1][ir]) + sg[2][ir]) + sg[3][ir];
+      s += sU[ir][j] * g;
+    }
+    scol[qq][j] = s;
+  }
+  __syncthreads();
+  if (tid < kOnTile && c0 + tid < d)
+    on_part(a, PV_Y, bi)[c0 + tid] = ((scol[0][tid] + scol[1][tid]) + scol[2][tid]) + scol[3][tid];
+
+  // tickets: the last tile of row block bi (column block bj) finishes its entries
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) {
+    s_last[0] = atomicAdd(a.tick + bi, 1) == nt - 1;
+    s_last[1] = atomicAdd(a.tick + nt + bj, 1) == nt - 1;
+  }
+  __syncthreads();
+  const int w = tid >> 6, lane = tid & 63;
+  if (s_last[0]) {
+    __threadfence();
+    if (w < 3) {
+      const int r = r0 + lane;
+      float s = 0.f;
+      if (r < d)
+        for (int u = 0; u < nt; ++u) s += on_part(a, w, u)[r];
+      if (r < d) a.vec[(size_t)w * d + r] = s;
+      if (w == PV_Q) {
+        const float hr = r < d ? a.h[r] : 0.f;
+        const float c1 = wave_sum(hr * s);
+        const float hh = wave_sum(hr * hr);
+        if (lane == 0) {
+          a.sp[bi] = c1;
+          a.sp[nt + bi] = hh;
+        }
+      }
+    }
+    if (tid == 0) a.tick[bi] = 0;
+  }
+  if (s_last[1]) {
+    __threadfence();
+    if (w == 3) {
+      const int c = c0 + lane;
+      float s = 0.f;
+      if (c < d)
+        for (int u = 0; u < nt; ++u) s += on_part(a, PV_Y, u)[c];
+      if (c < d) a.vec[(size_t)PV_Y * d + c] = s;
+      const float hc = c < d ? a.h[c] : 0.f;
+      const float c2 = wave_sum(hc * s);
+      if (lane == 0) a.sp[2 * nt + bj] = c2;
+    }
+    if (tid == 0) a.tick[nt + bj] = 0;
+  }
+}
+
+// a b + c d with both products rounded before the sum (no fused multiply-add),
+// so that sym_pair(a, b, c, d) and sym_pair(d, c, b, a) are the same bits.
+__device__ __forceinline__ float sym_pair(float a, float b, float c, float d) {
+#pragma clang fp contract(off)
+  return a * b + c * d;
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
+  extern __shared__ float sm[];
+  float* sT = sm;
+  float* sH = sm + a.d;
+  const int tid = threadIdx.x, d = a.d, nt = a.nt, R = a.rows_per_block;
+  const int i0 = blockIdx.x * R;
+  const int rows = min(R, d - i0);
+
+  // scalars: every block the same, from the per-block partials in block order
+  float c1 = 0.f, hh = 0.f, c2 = 0.f;
+  for (int u = 0; u < nt; ++u) {
+    c1 += a.sp[u];
+    hh += a.sp[nt + u];
+    c2 += a.sp[2 * nt + u];
+  }
+  const float yy = a.scal[0];
+  float L, av, bv;
+  if (a.loss_kind == LST_LOSS_SQUARED) {
+    L = c1 - 2.f * c2 + yy;
+    av = 2.f;
+    bv = -2.f;
+  } else {
+    const float S = c1 + (float)a.D * a.eps;
+    const float num = c2 * c2 + a.eps;
+    L = -logf(num) + logf(S);
+    av = 2.f / S;
+    bv = -2.f * c2 / num;
+  }
+  const float lr = a.lr;
+  const float N = av * av * c1 + 2.f * av * bv * c2 + bv * bv * yy;
+  const float den = 1.f - lr * av * hh;
+  int err = 0;
+  if (!isfinite(L)) err = LST_ENONFINITE;
+  else if (!(den != 0.f) || !isfinite(den)) err = LST_ESINGULAR;
+  const int err0 = a.flags[F_ERR];
+  if (blockIdx.x == 0 && tid == 0) {
+    a.loss[0] = L;
+    if (err) atomicCAS(a.flags + F_ERR, 0, err);
+  }
+  const float* hq = a.vec + (size_t)PV_Q * d;
+  const float* yh = a.vec + (size_t)PV_Y * d;
+  const float hn = -0.5f * lr * N;
+  for (int j = tid; j < d; j += 256) {
+    const float hv = a.h[j];
+    const float g = av * hq[j] + bv * yh[j];
+    sT[j] = g + hn * hv;
+    sH[j] = hv;
+    if (blockIdx.x == 0) a.grad[j] = g;
+  }
+  __syncthreads();
+  if (err0 != 0 || err != 0) return;
+
+  // rows i0 .. i0 + rows of Q, U, U^{-T}
+  const float* uv = a.vec + (size_t)PV_U * d;
+  const float* pv = a.vec + (size_t)PV_P * d;
+  const float cu = lr * av, cp = lr * av / den;
+  float* __restrict__ Q = a.Q;
+  float* __restrict__ U = a.U;
+  float* __restrict__ P = a.Uit;
+  if (VEC) {
+    const int d4 = d >> 2;
+    for (int e = tid; e < rows * d4; e += 256) {
+      const int ii = e / d4, j4 = e - ii * d4;
+      const int i = i0 + ii;
+      const size_t o = (size_t)i * d + 4 * j4;
+      float4 qv = *reinterpret_cast<const float4*>(Q + o);
+      float4 uw = *reinterpret_cast<const float4*>(U + o);
+      float4 pw = *reinterpret_cast<const float4*>(P + o);
+      const float hi = sH[i], Ti = sT[i];
+      const float wu = cu * uv[i], wp = cp * pv[i];
+      const float4 hj = *reinterpret_cast<const float4*>(sH + 4 * j4);
+      const float4 Tj = *reinterpret_cast<const float4*>(sT + 4 * j4);
+      qv.x -= lr * sym_pair(hi, Tj.x, Ti, hj.x);
+      qv.y -= lr * sym_pair(hi, Tj.y, Ti, hj.y);
+      qv.z -= lr * sym_pair(hi, Tj.z, Ti, hj.z);
+      qv.w -= lr * sym_pair(hi, Tj.w, Ti, hj.w);
+      uw.x -= wu * hj.x; uw.y -= wu * hj.y; uw.z -= wu * hj.z; uw.w -= wu * hj.w;
+      pw.x += wp * hj.x; pw.y += wp * hj.y; pw.z += wp * hj.z; pw.w += wp * hj.w;
+      *reinterpret_cast<float4*>(Q + o) = qv;
+      *reinterpret_cast<float4*>(U + o) = uw;
+      *reinterpret_cast<float4*>(P + o) = pw;
+    }
+  } else {
+    for (int e = tid; e < rows * d; e += 256) {
+      const int ii = e / d, j = e - ii * d;
+      const int i = i0 + ii;
+      const size_t o = (size_t)i * d + j;
+      const float hi = sH[i], Ti = sT[i], hj = sH[j], Tj = sT[j];
+      Q[o] -= lr * sym_pair(hi, Tj, Ti, hj);
+      U[o] -= cu * uv[i] * hj;
+      P[o] += cp * pv[i] * hj;
+    }
+  }
+  // target rows of V: slot k by block k mod (number of blocks)
+  for (int k = blockIdx.x; k < a.K; k += gridDim.x) {
+    const int r = a.own[k];
+    if (r < 0) continue;
+    const float G = a.loss_kind == LST_LOSS_SQUARED ? -2.f * a.rsum[k] : bv;
+    const float wv = -lr * G / den;
+    float* Vr = a.V + (size_t)r * d;
+    for (int j = tid; j < d; j += 256) Vr[j] += wv * pv[j];
+  }
+}
+
+}  // namespace
+
+int online_tiles(int d) { return (d + kOnTile - 1) / kOnTile; }
+
+size_t online_workspace_floats(int d) {
+  const size_t nt = (size_t)online_tiles(d);
+  return 4 * nt * d + 4 * (size_t)d + 3 * nt + 4 + kOnlineMaxK;
+}
+
+OnlineArgs online_args(int d, float* ws, int* tick) {
+  OnlineArgs a{};
+  const int nt = online_tiles(d);
+  a.d = d;
+  a.nt = nt;
+  a.part = ws;
+  a.vec = ws + 4 * (size_t)nt * d;
+  a.sp = a.vec + 4 * (size_t)d;
+  a.scal = a.sp + 3 * nt;
+  a.rsum = a.scal + 4;
+  a.tick = tick;
+  return a;
+}
+
+hipError_t online_step(const OnlineArgs& a0, hipStream_t s, hipEvent_t e0a, hipEvent_t e1a,
+                       hipEvent_t e0b, hipEvent_t e1b) {
+  OnlineArgs a = a0;
+  if (a.K < 1 || a.K > kOnlineMaxK || a.d < 1 || a.d > 4096 || a.nt != online_tiles(a.d))
+    return hipErrorInvalidValue;
+  // launch B: about 256 blocks of R rows each
+  a.rows_per_block = (a.d + 255) / 256;
+  void* args[] = {&a};
+  const bool vec = a.d % 4 == 0;
+  const dim3 ga(1 + a.nt * a.nt), gb((a.d + a.rows_per_block - 1) / a.rows_per_block);
+  const size_t ldsb = (size_t)2 * a.d * sizeof(float);
+  const void* ka = vec ? (const void*)online_a_kernel<true> : (const void*)online_a_kernel<false>;
+  const void* kb = vec ? (const void*)online_b_kernel<true> : (const void*)online_b_kernel<false>;
+  hipError_t e;
+  if (e0a && e1a)
+    e = hipExtLaunchKernel(ka, ga, dim3(256), args, 0, s, e0a, e1a, 0);
+  else
+    e = hipLaunchKernel(ka, ga, dim3(256), args, 0, s);
+  if (e != hipSuccess) return e;
+  if (e0b && e1b) return hipExtLaunchKernel(kb, gb, dim3(256), args, ldsb, s, e0b, e1b, 0);
+  return hipLaunchKernel(kb, gb, dim3(256), args, ldsb, s);
+}
+
+}  // namespace lst
