@@ -56,8 +56,7 @@ struct lst_state {
   int last_slots = 0;  // m * K of the last factored step
   int hbits = 0;
   int ld0 = 0;
-  float* on_ws = nullptr;  // single-example step: workspace and tickets
-  int* on_tick = nullptr;
+  float* on_ws = nullptr;  // single-example step workspace
   float* Nm = nullptr;  // m_max > 128: m x ldn, N = A C1 A + A C2 B + B C2^T A + B Y^T Y B
   int ldn = 0;
   int n_c1p = 0;  // partial sums of h^T Q h per example (two per 32-column tile of H^)
@@ -343,10 +342,10 @@ int enqueue_drift(lst_state* s, hipStream_t st) {
   return prof_mark(s, PH_DRIFT, 1, st);
 }
 
-// The single-example step (two launches, Sherman-Morrison update of U^{-T}).
+// The single-example step (Sherman-Morrison update of U^{-T}).
 int enqueue_online(lst_state* s, hipStream_t st, int32_t K, const float* H, const int32_t* Y_idx,
                    const float* Y_val, float lr, float* loss, float* grad_H) {
-  OnlineArgs a = online_args(s->d, s->on_ws, s->on_tick);
+  OnlineArgs a = online_args(s->d, s->on_ws);
   a.K = K;
   a.loss_kind = s->cfg.loss;
   a.D = s->D;
@@ -651,11 +650,9 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       (rc = dalloc(s, &s->UHa, md)) || (rc = dalloc(s, &s->yyd, m)) ||
       (rc = dalloc(s, &s->c1p, (size_t)m * s->n_c1p)) ||
       (rc = dalloc(s, &s->hap, (size_t)m * s->n_hap_max)) ||
-      (rc = dalloc(s, &s->on_ws, online_workspace_floats(d))) ||
-      (rc = dalloc(s, &s->on_tick, 2 * (size_t)online_tiles(d))))
+      (rc = dalloc(s, &s->on_ws, online_workspace_floats(d))))
     return fail(rc);
   if (fill_ints(s->hkey, -1, hsize, s->stream) != hipSuccess ||
-      fill_ints(s->on_tick, 0, 2 * online_tiles(d), s->stream) != hipSuccess ||
       fill_ints(s->hmin, 0x7fffffff, hsize, s->stream) != hipSuccess ||
       fill_ints(s->hcnt, 0, hsize + 1, s->stream) != hipSuccess)
     return fail(LST_EHIP);

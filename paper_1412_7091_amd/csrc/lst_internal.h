@@ -199,10 +199,12 @@ hipError_t compact_owned(const int* own, int n, int* out, int* count, hipStream_
 hipError_t fill_ints(int* p, int v, int n, hipStream_t s);
 
 // ------------------------------------------------- the single-example step
-// Two launches for m = 1 (online.hip).  Workspace: one float buffer of
-// online_workspace_floats(d) carved by online_args, and 2 * online_tiles(d)
-// ints of tickets that start at zero (each launch leaves them at zero).
+// Two launches for m = 1 (three for d > 1024; online.hip).  Workspace: one
+// float buffer of online_workspace_floats(d), carved by online_args.
 constexpr int kOnlineMaxK = 256;
+constexpr int kOnlineMaxRows = 16;    // rows per block of launch B (d <= 4096)
+constexpr int kOnlineFuseTiles = 16;  // launch B adds the partials itself up to 16 tiles a side
+constexpr int kOnlineMaxTiles = 64;   // tiles a side for d = 4096
 struct OnlineArgs {
   int d, K, nt, rows_per_block, loss_kind;
   int64_t D;
@@ -212,19 +214,18 @@ struct OnlineArgs {
   const float* val;
   float *V, *Q, *U, *Uit;
   float* part;  // 4 x nt x d: per-tile partial sums of Q h, U h, U^{-T} h, U^T V^T y
-  float* vec;   // 4 x d: the same vectors, finished
-  float* sp;    // 3 x nt: per row (column) block partials of h^T Q h, h^T h, h^T y^
+  float* vec;   // 4 x d: the same vectors, finished (d > 1024)
+  float* sp;    // 3 x nt: per-slab partials of h^T Q h, h^T h, h^T y^ (d > 1024)
   float* scal;  // [0]: y^T y
   float* rsum;  // K: summed value of each owning slot
-  int* tick;    // 2 x nt: tiles finished per row block, per column block
   int* own;     // K: the row of slot k if slot k is the row's first, else -1
   int* flags;
   float *loss, *grad;
 };
 int online_tiles(int d);
 size_t online_workspace_floats(int d);
-OnlineArgs online_args(int d, float* ws, int* tick);
-// With e0a/e1a (e0b/e1b) the launches record them at their start and end.
+OnlineArgs online_args(int d, float* ws);
+// With e0a/e1a (e0b/e1b) the first (last) launch records them at its start and end.
 hipError_t online_step(const OnlineArgs& a, hipStream_t s, hipEvent_t e0a = nullptr,
                        hipEvent_t e1a = nullptr, hipEvent_t e0b = nullptr,
                        hipEvent_t e1b = nullptr);

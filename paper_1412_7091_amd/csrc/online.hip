@@ -17,14 +17,16 @@
 //
 //   launch A  64 x 64 tiles of Q, U, U^{-T}: the tile's partial sums of Q h,
 //             U h, U^{-T} h over its columns and of U^T g over its rows, with
-//             g = V^T y gathered from the target rows of V.  The last tile of
-//             a row block (column block) to finish, counted with an atomic
-//             ticket, adds that block's partials in tile order and leaves the
-//             finished entries plus partial dot products.  Block 0 checks the
-//             targets and merges repeated rows.
-//   launch B  blocks of R rows: every block forms the same scalars and T from
-//             the finished vectors, then updates its rows of Q, U, U^{-T}, and
-//             its share of the target rows of V.
+//             g = V^T y gathered from the target rows of V.  Block 0 checks
+//             the targets and merges repeated rows.
+//   launch B  blocks of R rows: every block adds the partials of h^ and y^ in
+//             tile order (so all blocks hold the same vectors and scalars),
+//             forms T, then updates its rows of Q, U, U^{-T} and the same
+//             columns of the target rows of V.
+// For d > 1024 (more than 16 tiles a side) a third launch between them adds
+// the partials once, and launch B reads the finished vectors.  The partials
+// cross blocks only at launch boundaries: a hand-off inside launch A would
+// need device-scope fences, each of which writes back the L2 of its XCD.
 // Summation orders are fixed, so the step is deterministic.  Q stays bitwise
 // symmetric: entries (i, j) and (j, i) get the same correction (sym_pair).
 #include <hip/hip_runtime.h>
@@ -50,6 +52,20 @@ __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
   return x;
+}
+
+// p[0] + p[stride] + ... + p[(n - 1) stride] in that order, n <= MAXN, with
+// every load issued before the first add.
+template <int MAXN>
+__device__ __forceinline__ float sum_parts(const float* p, size_t stride, int n) {
+  float v[MAXN];
+#pragma unroll
+  for (int u = 0; u < MAXN; ++u) v[u] = u < n ? p[(size_t)u * stride] : 0.f;
+  float s = 0.f;
+#pragma unroll
+  for (int u = 0; u < MAXN; ++u)
+    if (u < n) s += v[u];
+  return s;
 }
 
 // Block 0 of launch A: index checks (LST_EINDEX), and for each slot k whose
@@ -105,7 +121,6 @@ __global__ __launch_bounds__(256) void online_a_kernel(OnlineArgs a) {
   __shared__ float sh[kOnTile], sg[4][kOnTile], scol[4][kOnTile];
   __shared__ int skey[kOnlineMaxK];
   __shared__ float sval[kOnlineMaxK];
-  __shared__ int s_last[2];
   const int tid = threadIdx.x, d = a.d, K = a.K, nt = a.nt;
   if (blockIdx.x == 0) {
     online_targets(a, skey, sval, &scol[0][0]);
@@ -115,7 +130,14 @@ __global__ __launch_bounds__(256) void online_a_kernel(OnlineArgs a) {
   const int bi = t / nt, bj = t - bi * nt;
   const int r0 = bi * kOnTile, c0 = bj * kOnTile;
 
-  // the tile: thread (row i, quarter q) holds 16 consecutive columns of each matrix
+  // targets first (their rows of V are the longest chain of loads), then the
+  // tile: thread (row i, quarter q) holds 16 consecutive columns of each matrix
+  int tr = -1;
+  float tv = 0.f;
+  if (tid < K) {
+    tr = a.idx[tid];
+    if (a.loss_kind != LST_LOSS_SPHERICAL) tv = a.val[tid];
+  }
   const int i = tid >> 2, q = tid & 3;
   const int row = r0 + i, col0 = c0 + 16 * q;
   float vq[16], vu[16], vp[16];
@@ -140,12 +162,11 @@ __global__ __launch_bounds__(256) void online_a_kernel(OnlineArgs a) {
       vp[c] = in ? a.Uit[o] : 0.f;
     }
   }
-  // targets (every tile gathers g over its rows; only block 0 reports errors)
+  // every tile gathers g over its rows; only block 0 reports bad indices
   if (tid < K) {
-    const int r = a.idx[tid];
-    const bool valid = r >= 0 && (int64_t)r < a.D;
-    skey[tid] = valid ? r : -1;
-    sval[tid] = valid ? (a.loss_kind == LST_LOSS_SPHERICAL ? 1.f : a.val[tid]) : 0.f;
+    const bool valid = tr >= 0 && (int64_t)tr < a.D;
+    skey[tid] = valid ? tr : -1;
+    sval[tid] = valid ? (a.loss_kind == LST_LOSS_SPHERICAL ? 1.f : tv) : 0.f;
   }
   if (tid < kOnTile) sh[tid] = (c0 + tid < d) ? a.h[c0 + tid] : 0.f;
   __syncthreads();
@@ -196,50 +217,6 @@ __global__ __launch_bounds__(256) void online_a_kernel(OnlineArgs a) {
   __syncthreads();
   if (tid < kOnTile && c0 + tid < d)
     on_part(a, PV_Y, bi)[c0 + tid] = ((scol[0][tid] + scol[1][tid]) + scol[2][tid]) + scol[3][tid];
-
-  // tickets: the last tile of row block bi (column block bj) finishes its entries
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    s_last[0] = atomicAdd(a.tick + bi, 1) == nt - 1;
-    s_last[1] = atomicAdd(a.tick + nt + bj, 1) == nt - 1;
-  }
-  __syncthreads();
-  const int w = tid >> 6, lane = tid & 63;
-  if (s_last[0]) {
-    __threadfence();
-    if (w < 3) {
-      const int r = r0 + lane;
-      float s = 0.f;
-      if (r < d)
-        for (int u = 0; u < nt; ++u) s += on_part(a, w, u)[r];
-      if (r < d) a.vec[(size_t)w * d + r] = s;
-      if (w == PV_Q) {
-        const float hr = r < d ? a.h[r] : 0.f;
-        const float c1 = wave_sum(hr * s);
-        const float hh = wave_sum(hr * hr);
-        if (lane == 0) {
-          a.sp[bi] = c1;
-          a.sp[nt + bi] = hh;
-        }
-      }
-    }
-    if (tid == 0) a.tick[bi] = 0;
-  }
-  if (s_last[1]) {
-    __threadfence();
-    if (w == 3) {
-      const int c = c0 + lane;
-      float s = 0.f;
-      if (c < d)
-        for (int u = 0; u < nt; ++u) s += on_part(a, PV_Y, u)[c];
-      if (c < d) a.vec[(size_t)PV_Y * d + c] = s;
-      const float hc = c < d ? a.h[c] : 0.f;
-      const float c2 = wave_sum(hc * s);
-      if (lane == 0) a.sp[2 * nt + bj] = c2;
-    }
-    if (tid == 0) a.tick[nt + bj] = 0;
-  }
 }
 
 // a b + c d with both products rounded before the sum (no fused multiply-add),
@@ -249,22 +226,188 @@ __device__ __forceinline__ float sym_pair(float a, float b, float c, float d) {
   return a * b + c * d;
 }
 
-template <bool VEC>
+// Launch between A and B when d > 1024: block s adds the partials of entries
+// 64 s .. 64 s + 63 of the four vectors, and the partial dot products of that
+// slab (h^T h^, h^T h, h^T y^).
+__global__ __launch_bounds__(256) void online_r_kernel(OnlineArgs a) {
+  const int tid = threadIdx.x, d = a.d, nt = a.nt, w = tid >> 6, lane = tid & 63;
+  const int r = blockIdx.x * kOnTile + lane;
+  const float s = r < d ? sum_parts<kOnlineMaxTiles>(on_part(a, w, 0) + r, d, nt) : 0.f;
+  if (r < d) a.vec[(size_t)w * d + r] = s;
+  const float hr = r < d ? a.h[r] : 0.f;
+  if (w == PV_Q) {
+    const float c1 = wave_sum(hr * s);
+    const float hh = wave_sum(hr * hr);
+    if (lane == 0) {
+      a.sp[blockIdx.x] = c1;
+      a.sp[nt + blockIdx.x] = hh;
+    }
+  } else if (w == PV_Y) {
+    const float c2 = wave_sum(hr * s);
+    if (lane == 0) a.sp[2 * nt + blockIdx.x] = c2;
+  }
+}
+
+// FUSED: launch B adds the tile partials itself (d <= 1024); otherwise it reads
+// the vectors and slab dot products of online_r_kernel.
+template <bool VEC, bool FUSED>
 __global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
   extern __shared__ float sm[];
-  float* sT = sm;
-  float* sH = sm + a.d;
+  float* sT = sm;           // h^, then T in place
+  float* sY = sm + a.d;     // y^
+  float* sH = sm + 2 * a.d;
+  __shared__ float red[3][4];
+  __shared__ float su[kOnlineMaxRows], spv[kOnlineMaxRows];
   const int tid = threadIdx.x, d = a.d, nt = a.nt, R = a.rows_per_block;
   const int i0 = blockIdx.x * R;
   const int rows = min(R, d - i0);
+  float* __restrict__ Q = a.Q;
+  float* __restrict__ U = a.U;
+  float* __restrict__ P = a.Uit;
 
-  // scalars: every block the same, from the per-block partials in block order
-  float c1 = 0.f, hh = 0.f, c2 = 0.f;
-  for (int u = 0; u < nt; ++u) {
-    c1 += a.sp[u];
-    hh += a.sp[nt + u];
-    c2 += a.sp[2 * nt + u];
+  // Loads are issued early so that their latencies overlap: the status flag,
+  // the owning slots (whose rows of V are requested as soon as they arrive),
+  // the block's first rows of Q, U, U^{-T}, then the prologue's partials.
+  const int err0 = a.flags[F_ERR];
+  constexpr int kVPre = 2;
+  const int nve = a.K * rows;
+  int vrow[kVPre];
+  float vrs[kVPre], vval[kVPre];
+#pragma unroll
+  for (int c = 0; c < kVPre; ++c) {
+    const int e = tid + 256 * c;
+    vrow[c] = -1;
+    vrs[c] = 0.f;
+    if (e < nve) {
+      vrow[c] = a.own[e / rows];
+      vrs[c] = a.rsum[e / rows];
+    }
   }
+  auto load_v = [&]() {
+#pragma unroll
+    for (int c = 0; c < kVPre; ++c) {
+      const int e = tid + 256 * c;
+      if (e < nve && vrow[c] >= 0) vval[c] = a.V[(size_t)vrow[c] * d + i0 + e % rows];
+    }
+  };
+  constexpr int kPre = 4;
+  const int d4 = d >> 2, ne4 = VEC ? rows * d4 : 0;
+  float4 pq[kPre], pu[kPre], pp[kPre];
+  if (VEC) {
+#pragma unroll
+    for (int c = 0; c < kPre; ++c) {
+      const int e = tid + 256 * c;
+      if (e < ne4) {
+        const int ii = e / d4;
+        const size_t o = (size_t)(i0 + ii) * d + 4 * (e - ii * d4);
+        pq[c] = *reinterpret_cast<const float4*>(Q + o);
+        pu[c] = *reinterpret_cast<const float4*>(U + o);
+        pp[c] = *reinterpret_cast<const float4*>(P + o);
+      }
+    }
+  }
+
+  // h^, y^ and the dot products: every block the same, in the same order
+  float c1 = 0.f, hh = 0.f, c2 = 0.f;
+  if (FUSED) {
+    // thread t: entries 4t .. 4t + 3 (d <= 1024); all of its partials are
+    // requested before the first is added
+    const int j0 = 4 * tid;
+    const bool act = j0 < d;
+    float x[4] = {0.f, 0.f, 0.f, 0.f}, y[4] = {0.f, 0.f, 0.f, 0.f};
+    if (VEC) {
+      float4 px[kOnlineFuseTiles], py[kOnlineFuseTiles];
+      if (act) {
+#pragma unroll
+        for (int u = 0; u < kOnlineFuseTiles; ++u)
+          if (u < nt) {
+            px[u] = *reinterpret_cast<const float4*>(on_part(a, PV_Q, u) + j0);
+            py[u] = *reinterpret_cast<const float4*>(on_part(a, PV_Y, u) + j0);
+          }
+      }
+      load_v();
+      if (act) {
+#pragma unroll
+        for (int u = 0; u < kOnlineFuseTiles; ++u)
+          if (u < nt) {
+            x[0] += px[u].x; x[1] += px[u].y; x[2] += px[u].z; x[3] += px[u].w;
+            y[0] += py[u].x; y[1] += py[u].y; y[2] += py[u].z; y[3] += py[u].w;
+          }
+      }
+    } else {
+      float px[kOnlineFuseTiles][4], py[kOnlineFuseTiles][4];
+      if (act) {
+#pragma unroll
+        for (int u = 0; u < kOnlineFuseTiles; ++u)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const bool in = u < nt && j0 + c < d;
+            px[u][c] = in ? on_part(a, PV_Q, u)[j0 + c] : 0.f;
+            py[u][c] = in ? on_part(a, PV_Y, u)[j0 + c] : 0.f;
+          }
+      }
+      load_v();
+      if (act) {
+#pragma unroll
+        for (int u = 0; u < kOnlineFuseTiles; ++u)
+          if (u < nt)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+              x[c] += px[u][c];
+              y[c] += py[u][c];
+            }
+      }
+    }
+    if (act) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int j = j0 + c;
+        if (j < d) {
+          const float hv = a.h[j];
+          sT[j] = x[c];
+          sY[j] = y[c];
+          sH[j] = hv;
+          c1 += hv * x[c];
+          c2 += hv * y[c];
+          hh += hv * hv;
+        }
+      }
+    }
+    c1 = wave_sum(c1);
+    c2 = wave_sum(c2);
+    hh = wave_sum(hh);
+    if ((tid & 63) == 0) {
+      red[0][tid >> 6] = c1;
+      red[1][tid >> 6] = c2;
+      red[2][tid >> 6] = hh;
+    }
+    if (tid < rows) {
+      su[tid] = sum_parts<kOnlineFuseTiles>(on_part(a, PV_U, 0) + i0 + tid, d, nt);
+    } else if (tid >= 64 && tid < 64 + rows) {
+      spv[tid - 64] = sum_parts<kOnlineFuseTiles>(on_part(a, PV_P, 0) + i0 + tid - 64, d, nt);
+    }
+    __syncthreads();
+    c1 = ((red[0][0] + red[0][1]) + red[0][2]) + red[0][3];
+    c2 = ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3];
+    hh = ((red[2][0] + red[2][1]) + red[2][2]) + red[2][3];
+  } else {
+    load_v();
+    for (int u = 0; u < nt; ++u) {
+      c1 += a.sp[u];
+      hh += a.sp[nt + u];
+      c2 += a.sp[2 * nt + u];
+    }
+#pragma unroll 4
+    for (int j = tid; j < d; j += 256) {
+      sT[j] = a.vec[(size_t)PV_Q * d + j];
+      sY[j] = a.vec[(size_t)PV_Y * d + j];
+      sH[j] = a.h[j];
+    }
+    if (tid < rows) su[tid] = a.vec[(size_t)PV_U * d + i0 + tid];
+    else if (tid >= 64 && tid < 64 + rows) spv[tid - 64] = a.vec[(size_t)PV_P * d + i0 + tid - 64];
+    __syncthreads();
+  }
+
   const float yy = a.scal[0];
   float L, av, bv;
   if (a.loss_kind == LST_LOSS_SQUARED) {
@@ -284,42 +427,29 @@ __global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
   int err = 0;
   if (!isfinite(L)) err = LST_ENONFINITE;
   else if (!(den != 0.f) || !isfinite(den)) err = LST_ESINGULAR;
-  const int err0 = a.flags[F_ERR];
   if (blockIdx.x == 0 && tid == 0) {
     a.loss[0] = L;
     if (err) atomicCAS(a.flags + F_ERR, 0, err);
   }
-  const float* hq = a.vec + (size_t)PV_Q * d;
-  const float* yh = a.vec + (size_t)PV_Y * d;
   const float hn = -0.5f * lr * N;
   for (int j = tid; j < d; j += 256) {
-    const float hv = a.h[j];
-    const float g = av * hq[j] + bv * yh[j];
-    sT[j] = g + hn * hv;
-    sH[j] = hv;
+    const float g = av * sT[j] + bv * sY[j];
+    sT[j] = g + hn * sH[j];
     if (blockIdx.x == 0) a.grad[j] = g;
   }
   __syncthreads();
   if (err0 != 0 || err != 0) return;
 
   // rows i0 .. i0 + rows of Q, U, U^{-T}
-  const float* uv = a.vec + (size_t)PV_U * d;
-  const float* pv = a.vec + (size_t)PV_P * d;
   const float cu = lr * av, cp = lr * av / den;
-  float* __restrict__ Q = a.Q;
-  float* __restrict__ U = a.U;
-  float* __restrict__ P = a.Uit;
   if (VEC) {
-    const int d4 = d >> 2;
-    for (int e = tid; e < rows * d4; e += 256) {
+    // entry e of the block's rows: float4 j4 of row ii
+    auto update = [&](int e, float4 qv, float4 uw, float4 pw) {
       const int ii = e / d4, j4 = e - ii * d4;
       const int i = i0 + ii;
       const size_t o = (size_t)i * d + 4 * j4;
-      float4 qv = *reinterpret_cast<const float4*>(Q + o);
-      float4 uw = *reinterpret_cast<const float4*>(U + o);
-      float4 pw = *reinterpret_cast<const float4*>(P + o);
       const float hi = sH[i], Ti = sT[i];
-      const float wu = cu * uv[i], wp = cp * pv[i];
+      const float wu = cu * su[ii], wp = cp * spv[ii];
       const float4 hj = *reinterpret_cast<const float4*>(sH + 4 * j4);
       const float4 Tj = *reinterpret_cast<const float4*>(sT + 4 * j4);
       qv.x -= lr * sym_pair(hi, Tj.x, Ti, hj.x);
@@ -331,6 +461,15 @@ __global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
       *reinterpret_cast<float4*>(Q + o) = qv;
       *reinterpret_cast<float4*>(U + o) = uw;
       *reinterpret_cast<float4*>(P + o) = pw;
+    };
+#pragma unroll
+    for (int c = 0; c < kPre; ++c)
+      if (tid + 256 * c < ne4) update(tid + 256 * c, pq[c], pu[c], pp[c]);
+    for (int e = tid + 256 * kPre; e < ne4; e += 256) {
+      const int ii = e / d4;
+      const size_t o = (size_t)(i0 + ii) * d + 4 * (e - ii * d4);
+      update(e, *reinterpret_cast<const float4*>(Q + o), *reinterpret_cast<const float4*>(U + o),
+             *reinterpret_cast<const float4*>(P + o));
     }
   } else {
     for (int e = tid; e < rows * d; e += 256) {
@@ -339,18 +478,26 @@ __global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
       const size_t o = (size_t)i * d + j;
       const float hi = sH[i], Ti = sT[i], hj = sH[j], Tj = sT[j];
       Q[o] -= lr * sym_pair(hi, Tj, Ti, hj);
-      U[o] -= cu * uv[i] * hj;
-      P[o] += cp * pv[i] * hj;
+      U[o] -= cu * su[ii] * hj;
+      P[o] += cp * spv[ii] * hj;
     }
   }
-  // target rows of V: slot k by block k mod (number of blocks)
-  for (int k = blockIdx.x; k < a.K; k += gridDim.x) {
+  // columns i0 .. i0 + rows of the target rows of V
+  const float cv = -lr / den;
+#pragma unroll
+  for (int c = 0; c < kVPre; ++c) {
+    const int e = tid + 256 * c;
+    if (e < nve && vrow[c] >= 0) {
+      const float G = a.loss_kind == LST_LOSS_SQUARED ? -2.f * vrs[c] : bv;
+      a.V[(size_t)vrow[c] * d + i0 + e % rows] = vval[c] + (cv * G) * spv[e % rows];
+    }
+  }
+  for (int e = tid + 256 * kVPre; e < nve; e += 256) {
+    const int k = e / rows, ii = e - k * rows;
     const int r = a.own[k];
     if (r < 0) continue;
     const float G = a.loss_kind == LST_LOSS_SQUARED ? -2.f * a.rsum[k] : bv;
-    const float wv = -lr * G / den;
-    float* Vr = a.V + (size_t)r * d;
-    for (int j = tid; j < d; j += 256) Vr[j] += wv * pv[j];
+    a.V[(size_t)r * d + i0 + ii] += (cv * G) * spv[ii];
   }
 }
 
@@ -363,7 +510,7 @@ size_t online_workspace_floats(int d) {
   return 4 * nt * d + 4 * (size_t)d + 3 * nt + 4 + kOnlineMaxK;
 }
 
-OnlineArgs online_args(int d, float* ws, int* tick) {
+OnlineArgs online_args(int d, float* ws) {
   OnlineArgs a{};
   const int nt = online_tiles(d);
   a.d = d;
@@ -373,7 +520,6 @@ OnlineArgs online_args(int d, float* ws, int* tick) {
   a.sp = a.vec + 4 * (size_t)d;
   a.scal = a.sp + 3 * nt;
   a.rsum = a.scal + 4;
-  a.tick = tick;
   return a;
 }
 
@@ -382,20 +528,27 @@ hipError_t online_step(const OnlineArgs& a0, hipStream_t s, hipEvent_t e0a, hipE
   OnlineArgs a = a0;
   if (a.K < 1 || a.K > kOnlineMaxK || a.d < 1 || a.d > 4096 || a.nt != online_tiles(a.d))
     return hipErrorInvalidValue;
-  // launch B: about 256 blocks of R rows each
+  // launch B: about 256 blocks of R <= 16 rows each
   a.rows_per_block = (a.d + 255) / 256;
   void* args[] = {&a};
-  const bool vec = a.d % 4 == 0;
+  const bool vec = a.d % 4 == 0, fused = a.nt <= kOnlineFuseTiles;
   const dim3 ga(1 + a.nt * a.nt), gb((a.d + a.rows_per_block - 1) / a.rows_per_block);
-  const size_t ldsb = (size_t)2 * a.d * sizeof(float);
+  const size_t ldsb = (size_t)3 * a.d * sizeof(float);
   const void* ka = vec ? (const void*)online_a_kernel<true> : (const void*)online_a_kernel<false>;
-  const void* kb = vec ? (const void*)online_b_kernel<true> : (const void*)online_b_kernel<false>;
+  const void* kb = fused ? (vec ? (const void*)online_b_kernel<true, true>
+                                : (const void*)online_b_kernel<false, true>)
+                         : (vec ? (const void*)online_b_kernel<true, false>
+                                : (const void*)online_b_kernel<false, false>);
   hipError_t e;
   if (e0a && e1a)
     e = hipExtLaunchKernel(ka, ga, dim3(256), args, 0, s, e0a, e1a, 0);
   else
     e = hipLaunchKernel(ka, ga, dim3(256), args, 0, s);
   if (e != hipSuccess) return e;
+  if (!fused) {
+    e = hipLaunchKernel((const void*)online_r_kernel, dim3(a.nt), dim3(256), args, 0, s);
+    if (e != hipSuccess) return e;
+  }
   if (e0b && e1b) return hipExtLaunchKernel(kb, gb, dim3(256), args, ldsb, s, e0b, e1b, 0);
   return hipLaunchKernel(kb, gb, dim3(256), args, ldsb, s);
 }

@@ -54,10 +54,11 @@ def _layer(cfg, **kw):
 
 # ------------------------------------------------ against the factored oracle
 @pytest.mark.parametrize("d,pad,dup", [(16, 0.0, 0.0), (37, 0.2, 0.3), (130, 0.1, 0.2),
-                                       (500, 0.0, 0.0)])
+                                       (500, 0.0, 0.0), (1030, 0.1, 0.1), (1088, 0.0, 0.2)])
 def test_online_state_matches_factored_oracle(gpu_lib, d, pad, dup):
-    """d = 37 and 130: rows not 16-byte aligned and a ragged last tile; padding slots
-    and indices repeated inside the example."""
+    """d = 37, 130 and 1030: rows not 16-byte aligned and a ragged last tile; padding
+    slots and indices repeated inside the example.  d = 1030 and 1088 exceed 16 tiles
+    a side: the partials are finished by a launch of their own."""
     cfg = _cfg(d=d, pad_frac=pad, dup_frac=dup, entropy=301 + d)
     wl, layer = _layer(cfg)
     st = factored.FactoredState.from_initial(wl.init_V())
