@@ -70,10 +70,18 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-naive", action="store_true")
     ap.add_argument("--no-stabilize", action="store_true")
+    ap.add_argument("--step-only", action="store_true",
+                    help="only the timed and profiled minibatch steps (for counter runs): no "
+                         "split-task pass, single-example, stabilise, input-layer, naive or CPU "
+                         "parts")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the benchmark line: factored vs naive step time over the "
                          "vocabulary size D at d = 300, m = 128 (the paper's timing figure and "
                          "speedup table)")
+    ap.add_argument("--tasks", action="store_true",
+                    help="instead of the benchmark line: every task of the step as a launch of "
+                         "its own (lst_set_split_tasks), with per-task times and the HBM "
+                         "fraction of the gather and the scatter")
     ap.add_argument("--crossover", action="store_true",
                     help="instead of the benchmark line: the Woodbury step against a solve from "
                          "scratch, over m at d = 500 and 1024 (D = 200000, K = 10)")
@@ -82,6 +90,8 @@ def main():
         return sweep(args)
     if args.crossover:
         return crossover(args)
+    if args.tasks:
+        return tasks_only(args)
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the step has no "
@@ -149,9 +159,10 @@ def main():
     u, nnz = st.last_unique, st.last_nnz
     kernels = {}
     best = None
-    from paper_1412_7091_amd.profiling import measured_traffic
+    from paper_1412_7091_amd.profiling import measured_mfma, measured_traffic
 
     traffic = measured_traffic(cfg.name) or {}
+    mfma = measured_mfma(cfg.name) or {}
     for name, tot in phases.items():
         avg_us = 1e3 * tot / max(nsteps, 1)
         if avg_us <= 0:
@@ -160,6 +171,9 @@ def main():
         entry = {"avg_us": round(avg_us, 3)}
         if name in traffic:
             entry["hbm_bytes_measured"] = traffic[name]["hbm_bytes"]
+        if name in mfma:
+            entry["mfma_busy_counter"] = mfma[name]["busy_frac"]
+            entry["mfma_flops_counter"] = mfma[name]["mfma_flops"]
         if avg_us > 0 and (flops > 0 or nbytes > 0):
             tf = flops / (avg_us * 1e-6) / 1e12
             gb = nbytes / (avg_us * 1e-6) / 1e9
@@ -180,8 +194,21 @@ def main():
         roofline = {"kernel": best, "bound": "hbm", "achieved": dom["hbm_gbs"],
                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": dom["hbm_frac"],
                     "traffic": dom_traffic}
+    if args.step_only:
+        args.no_stabilize = args.no_naive = args.no_cpu_baseline = True
+    tasks = single = None
+    if not args.step_only:
+        tasks = task_times(layer, run, cfg, u, args.steps)
+        log("per-task us (split launches): " + ", ".join(f"{k}={v['avg_us']:.1f}"
+                                                        for k, v in tasks.items()))
+    roofline["mfma_busy_counter"] = dom.get("mfma_busy_counter")
     layer.close()
     del layer
+
+    if not args.step_only:
+        single = single_example_cost(lst, torch, cfg, V0_t, dev)
+        log(f"single example: {single['us_per_step']:.2f} us/step pipelined, "
+            f"{single['latency_us_median']:.1f} us latency")
 
     stab = None
     if not args.no_stabilize:
@@ -252,12 +279,143 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "naive": naive,
+        "single_example": single,
         "stabilize": stab,
         "input_layer": inp,
         "kernels": kernels,
+        "tasks": tasks,
         "last_step": {"distinct_rows": u, "pairs": nnz},
     }
     print(json.dumps(out), flush=True)
+
+
+def task_times(layer, run, cfg, u, steps):
+    """Per-task launch times of the minibatch step with every task launched on its
+    own (HIP events around each launch, a profiled pass of `steps` steps).
+
+    The gather (launch1.targets: target preparation, Y^T Y and G = V^T Y)
+    must read the u distinct target rows of V at least once: 4 u d bytes.  The
+    scatter (launch3.scatter, plus launch4.clear, which scatters the rows held
+    by 64 or more slots when the step has 4096 or more slots) reads and
+    writes them: 8 u d bytes."""
+    layer.set_split_tasks(True)
+    run(20)
+    layer.profile(True)
+    run(steps)
+    phases, n = layer.profile_read()
+    layer.profile(False)
+    layer.set_split_tasks(False)
+    if layer.sync() != 0:
+        log("device error in split-task steps")
+        sys.exit(1)
+    out = {}
+    for name, tot in phases.items():
+        if "." in name and tot > 0:
+            out[name] = {"avg_us": round(1e3 * tot / max(n, 1), 3)}
+    hot = cfg.m * cfg.K >= 4096
+    for name, nbytes, parts in (("gather", 4.0 * u * cfg.d, ["launch1.targets"]),
+                                ("scatter", 8.0 * u * cfg.d,
+                                 ["launch3.scatter"] + (["launch4.clear"] if hot else []))):
+        t = sum(out[p]["avg_us"] for p in parts if p in out)
+        if t > 0:
+            gbs = nbytes / (t * 1e-6) / 1e9
+            out[name] = {"tasks": parts, "avg_us": round(t, 3), "bytes": nbytes,
+                         "hbm_gbs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+    return out
+
+
+def tasks_only(args):
+    """`--tasks`: the split-task measurement alone (for a kernel trace)."""
+    import torch
+
+    import paper_1412_7091_amd as lst
+    from synth import Workload, get_config
+
+    cfg = get_config(args.config)
+    wl = Workload(cfg)
+    dev = torch.device("cuda:0")
+    V0_t = torch.from_numpy(wl.init_V()).to(dev)
+    pool = [tuple(torch.from_numpy(x).to(dev) for x in wl.batch(s)) for s in range(16)]
+    loss_t = torch.empty(cfg.m, device=dev)
+    grad_t = torch.empty((cfg.m, cfg.d), device=dev)
+    layer = lst.FactoredOutputLayer(V0_t, loss=cfg.loss, sph_eps=cfg.sph_eps, m_max=cfg.m,
+                                    K_max=cfg.K)
+
+    def run(n, offset=0):
+        for s in range(n):
+            H, idx, val = pool[(s + offset) % len(pool)]
+            layer.step(H, idx, val, cfg.lr, out=(loss_t, grad_t))
+
+    layer.set_split_tasks(True)
+    run(args.warmup)
+    u = layer.stats().last_unique
+    tasks = task_times(layer, run, cfg, u, args.steps)
+    layer.close()
+    print(json.dumps({"tasks": tasks, "distinct_rows": u, "steps": args.steps,
+                      "config": {"workload": cfg.name, "D": cfg.D, "d": cfg.d, "m": cfg.m,
+                                 "K": cfg.K}}), flush=True)
+
+
+def single_example_cost(lst, torch, cfg, V0_t, dev, steps=2000):
+    """The m = 1 step (Algorithm 1 with the Sherman-Morrison update of U^-T) on
+    the workload's D, d and K: pipelined time per step (HIP events around
+    `steps` back-to-back steps), latency of one step (host clock from the call
+    to the end of a synchronisation, median of 200), and its launches.
+
+    Algorithmic bytes: launch A reads Q, U, U^-T (3 d^2 floats) and the u
+    target rows of V; launch B reads and writes Q, U, U^-T and its columns of
+    the target rows (2 (3 d^2 + u d) floats)."""
+    import dataclasses
+
+    from synth import Workload
+
+    c1 = dataclasses.replace(cfg, m=1)
+    wl1 = Workload(c1)
+    pool = [tuple(torch.from_numpy(x).to(dev) for x in wl1.batch(s)) for s in range(16)]
+    layer = lst.FactoredOutputLayer(V0_t, loss=cfg.loss, sph_eps=cfg.sph_eps, m_max=1,
+                                    K_max=cfg.K)
+    out = (torch.empty(1, device=dev), torch.empty((1, cfg.d), device=dev))
+
+    def run(n):
+        for s in range(n):
+            layer.step(*pool[s % 16], cfg.lr, out=out)
+
+    run(50)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    run(steps)
+    e1.record()
+    torch.cuda.synchronize()
+    us = 1e3 * e0.elapsed_time(e1) / steps
+    lat = []
+    for s in range(200):
+        t0 = time.perf_counter()
+        layer.step(*pool[s % 16], cfg.lr, out=out)
+        torch.cuda.synchronize()
+        lat.append(1e6 * (time.perf_counter() - t0))
+    layer.profile(True)
+    run(500)
+    phases, n = layer.profile_read()
+    layer.profile(False)
+    u = layer.stats().last_unique
+    if layer.sync() != 0:
+        log("device error in single-example steps")
+        sys.exit(1)
+    layer.close()
+    launches = {}
+    for name, tot in phases.items():
+        if tot <= 0:
+            continue
+        avg = 1e3 * tot / max(n, 1)
+        nb = {"online_a": 4.0 * (3 * cfg.d * cfg.d + u * cfg.d),
+              "online_b": 8.0 * (3 * cfg.d * cfg.d + u * cfg.d)}.get(name, 0.0)
+        launches[name] = {"avg_us": round(avg, 3), "bytes": nb,
+                          "hbm_frac": round(nb / (avg * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    return {"us_per_step": round(us, 3), "latency_us_median": round(float(np.median(lat)), 2),
+            "examples_per_s": round(1e6 / us, 1), "launches": launches,
+            "minibatch_path_m1_us": "26-31 (four-launch minibatch step with m = 1, before "
+                                    "the single-example path)"}
 
 
 def stabilize_cost(lst, torch, cfg, V0_t, dev):
@@ -527,30 +685,56 @@ def input_layer_cost(lst, torch, cfg, wl, V0_t, pool):
     return res
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+
+    return platform.processor() or platform.machine()
+
+
 def cpu_baseline(cfg, wl, V0, seconds):
-    """The fp64 oracle (explicit W, O(D d) per example) on a bounded prefix of the same steps."""
+    """The fp64 oracle (explicit W, O(D d) per example) on a bounded prefix of the
+    same steps: median time per step over the steps run, the CPU model, and the
+    BLAS library numpy calls (vendor, version, threads)."""
     from oracle import explicit
 
+    blas = {}
     try:
         from threadpoolctl import threadpool_info
 
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()
-                       if i.get("user_api") == "blas"] or [1])
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                blas = {"vendor": i.get("internal_api"), "version": i.get("version"),
+                        "threads": i.get("num_threads"), "arch": i.get("architecture")}
+                break
     except Exception:  # pragma: no cover - threadpoolctl missing
-        threads = len(os.sched_getaffinity(0))
+        pass
+    threads = blas.get("threads") or len(os.sched_getaffinity(0))
     W = V0.astype(np.float64)
+    times = []
     t0 = time.perf_counter()
     n = 0
     while True:
         H, idx, val = wl.batch(n)
+        ts = time.perf_counter()
         _, _, W = explicit.step(W, H, idx, val, cfg.lr, cfg.loss, cfg.sph_eps)
+        times.append(time.perf_counter() - ts)
         n += 1
         el = time.perf_counter() - t0
-        if (el >= seconds and n >= 2) or n >= 1000:
+        if (el >= seconds and n >= 3) or n >= 1000:
             break
-    return {"value": round(cfg.m * n / el, 3), "unit": "examples/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{n} consecutive steps of {cfg.name} from its initial W, fp64 numpy, "
+    med = float(np.median(times))
+    return {"value": round(cfg.m / med, 3), "unit": "examples/s", "cores": threads,
+            "kind": "oracle", "statistic": "median",
+            "cpu_model": _cpu_model(), "blas": blas,
+            "sample": f"{n} consecutive steps of {cfg.name} from its initial W, fp64 numpy; "
+                      f"median {med * 1e3:.1f} ms per step (mean {1e3 * float(np.mean(times)):.1f}), "
                       f"{el:.1f}s wall"}
 
 

@@ -260,6 +260,19 @@ int lst_naive_step(lst_state* s, int32_t m, int32_t K, const float* H, const int
 int lst_set_graphs(lst_state* s, int32_t enable);
 
 /*
+ * lst_set_split_tasks -- measurement aid for the minibatch step (Appendix A):
+ * with enable != 0 every task that a launch of lst_step runs side by side (the
+ * GEMM tiles, the target preparation and gather of V^T Y, Y^T Y, the per-example
+ * scalars, the Woodbury solve, the scatter into V, the clear) runs as a launch
+ * of its own, in the same order, so that a kernel trace or the profile phases
+ * ("launch<L>.<task>") time each task alone.  The tasks of one launch are
+ * independent: results are bitwise the same, the step is slower.  0 restores
+ * the default.  Factored states only (LST_ESTATE otherwise); synchronises the
+ * stream and releases the cached graphs.
+ */
+int lst_set_split_tasks(lst_state* s, int32_t enable);
+
+/*
  * lst_sync -- wait for the state's stream; return and clear the sticky device
  * error (LST_OK if none).
  */

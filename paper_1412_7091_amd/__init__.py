@@ -103,6 +103,7 @@ _SIGS = {
                                       ctypes.c_float, _P, _P]),
     "lst_sync": (ctypes.c_int, [_P]),
     "lst_set_graphs": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "lst_set_split_tasks": (ctypes.c_int, [_P, ctypes.c_int32]),
     "lst_stats": (ctypes.c_int, [_P, ctypes.POINTER(lst_stats_t)]),
     "lst_profile_enable": (ctypes.c_int, [_P, ctypes.c_int32]),
     "lst_profile_read": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_double), ctypes.c_int32,
@@ -303,6 +304,10 @@ def lst_set_graphs(h, enable: bool = True) -> None:
     _check(load_library().lst_set_graphs(h, 1 if enable else 0), "lst_set_graphs")
 
 
+def lst_set_split_tasks(h, enable: bool = True) -> None:
+    _check(load_library().lst_set_split_tasks(h, 1 if enable else 0), "lst_set_split_tasks")
+
+
 def lst_stats(h) -> lst_stats_t:
     st = lst_stats_t()
     _check(load_library().lst_stats(h, ctypes.byref(st)), "lst_stats")
@@ -421,6 +426,9 @@ class FactoredOutputLayer(_Layer):
 
     def restore(self):
         lst_restore(self._h)
+
+    def set_split_tasks(self, enable: bool = True) -> None:
+        lst_set_split_tasks(self._h, enable)
 
     def stabilize(self, **kw):
         return lst_stabilize(self._h, **kw)

@@ -15,6 +15,7 @@
 // raise a device error of this step, and skips when the error flag is set.
 #include <math.h>
 #include <stdlib.h>
+#include <stdio.h>
 #include <string.h>
 
 #include <algorithm>
@@ -77,6 +78,7 @@ struct lst_state {
   };
   std::vector<GraphEntry> graphs;
   uint64_t graph_clock = 0;
+  int split = 0;       // every task of a step as a launch of its own (profiling aid)
   int use_graphs = 0;  // direct launches: graph replay adds device-side gaps between steps
   hipStream_t cap = nullptr;  // capture stream
   float* scratch = nullptr;   // this device's copy of the static scratch array
@@ -158,11 +160,34 @@ int dalloc(lst_state* s, T** p, size_t count) {
   return LST_OK;
 }
 
+// Phases of a step for the profile: the launches, and with split tasks
+// (lst_set_split_tasks) each task of launch L as a launch of its own,
+// PH_TASK0 + (L - 1) * kTaskKinds + its task kind.
+constexpr int kTaskKinds = TK_CLEAR + 1;
 enum Phase {
-  PH_LAUNCH1 = 0, PH_LAUNCH2, PH_LAUNCH3, PH_LAUNCH4, PH_DRIFT, PH_ONLINE_A, PH_ONLINE_B, PH_COUNT
+  PH_LAUNCH1 = 0, PH_LAUNCH2, PH_LAUNCH3, PH_LAUNCH4, PH_DRIFT, PH_ONLINE_A, PH_ONLINE_B,
+  PH_TASK0, PH_COUNT = PH_TASK0 + 4 * kTaskKinds
 };
-const char* const kPhaseNames[PH_COUNT] = {"launch1", "launch2", "launch3", "launch4",
-                                           "drift",   "online_a", "online_b"};
+const char* const kTaskNames[kTaskKinds] = {"gemm",  "targets", "yy",   "scalars",
+                                            "solve", "scatter", "clear"};
+const char* const kLaunchNames[PH_TASK0] = {"launch1", "launch2", "launch3", "launch4",
+                                            "drift",   "online_a", "online_b"};
+// "launch<L>.<task>" for the split-task phases
+struct PhaseNames {
+  char buf[PH_COUNT][32];
+  PhaseNames() {
+    for (int p = 0; p < PH_COUNT; ++p) {
+      if (p < PH_TASK0) {
+        snprintf(buf[p], sizeof buf[p], "%s", kLaunchNames[p]);
+      } else {
+        const int q = p - PH_TASK0;
+        snprintf(buf[p], sizeof buf[p], "launch%d.%s", 1 + q / kTaskKinds,
+                 kTaskNames[q % kTaskKinds]);
+      }
+    }
+  }
+};
+const PhaseNames kPhaseNames;
 
 // Records the begin (end = 0) or end (end = 1) event of a phase on stream st
 // when profiling.
@@ -327,6 +352,27 @@ constexpr int kLaunch34Stages = 4;
 // their list.
 constexpr int kHotMinSlots = 64;
 
+// Launch `phase` (PH_LAUNCH1 .. PH_LAUNCH4) of the minibatch step: one grid for
+// all of its tasks, or with split tasks one launch per task, in task order
+// (the tasks of a launch are independent, so the results are the same).
+int run_launch(lst_state* s, const StepCtx& c, StepLaunch& L, int stages, hipStream_t st,
+               int phase) {
+  hipEvent_t e0, e1;
+  if (!s->split) {
+    OK_OR_RETURN(prof_pair(s, phase, &e0, &e1));
+    HIPCHK(step_launch(c, L, stages, st, e0, e1));
+    return LST_OK;
+  }
+  for (int t = 0; t < L.ntask; ++t) {
+    StepLaunch one = L;
+    one.ntask = 1;
+    one.kind[0] = L.kind[t];
+    OK_OR_RETURN(prof_pair(s, PH_TASK0 + (phase - PH_LAUNCH1) * kTaskKinds + L.kind[t], &e0, &e1));
+    HIPCHK(step_launch(c, one, stages, st, e0, e1));
+  }
+  return LST_OK;
+}
+
 // Drift control after a step (Appendix C, pristine restore when
 // ||U||_F ||U^{-T}||_F > cond_max d).
 int enqueue_drift(lst_state* s, hipStream_t st) {
@@ -407,10 +453,9 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     p1.dot_h = H; p1.ld_doth = d;
     L.lk = 1;
     L.timing_slot = 0;
-    hipEvent_t e0, e1;
-    OK_OR_RETURN(prof_pair(s, PH_LAUNCH1, &e0, &e1));
-    HIPCHK(step_launch(c, L, stages_for(L.gemm, t1 == 64 ? kLaunch1Stages64 : kMaxStages), st,
-                       e0, e1));
+    OK_OR_RETURN(run_launch(s, c, L,
+                            stages_for(L.gemm, t1 == 64 ? kLaunch1Stages64 : kMaxStages), st,
+                            PH_LAUNCH1));
   }
   {  // launch 2: Y^, C1, C2, C2^T ; solve ; Y^T Y ; per-example scalars
     StepLaunch L{};
@@ -439,9 +484,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
       for (int q = 0; q < g.np; ++q) g.p[q].tile = 64;
     L.lk = 2;
     L.timing_slot = 1;
-    hipEvent_t e0, e1;
-    OK_OR_RETURN(prof_pair(s, PH_LAUNCH2, &e0, &e1));
-    HIPCHK(step_launch(c, L, stages_for(g), st, e0, e1));
+    OK_OR_RETURN(run_launch(s, c, L, stages_for(g), st, PH_LAUNCH2));
   }
   {  // launch 3: grad_H and T ; scatter into V
     StepLaunch L{};
@@ -470,9 +513,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     pt.tile = 32;
     L.lk = hot ? 6 : 3;
     L.timing_slot = 2;
-    hipEvent_t e0, e1;
-    OK_OR_RETURN(prof_pair(s, PH_LAUNCH3, &e0, &e1));
-    HIPCHK(step_launch(c, L, stages_for(g, kLaunch34Stages), st, e0, e1));
+    OK_OR_RETURN(run_launch(s, c, L, stages_for(g, kLaunch34Stages), st, PH_LAUNCH3));
   }
   {  // launch 4: Q -= lr (H T^T + T H^T) ; U and U^{-T} updates ; clear the hash slots
     StepLaunch L{};
@@ -495,9 +536,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     g.p[2].tile = 64;
     L.lk = hot ? 7 : 4;
     L.timing_slot = 3;
-    hipEvent_t e0, e1;
-    OK_OR_RETURN(prof_pair(s, PH_LAUNCH4, &e0, &e1));
-    HIPCHK(step_launch(c, L, stages_for(g, kLaunch34Stages), st, e0, e1));
+    OK_OR_RETURN(run_launch(s, c, L, stages_for(g, kLaunch34Stages), st, PH_LAUNCH4));
   }
   return enqueue_drift(s, st);
 }
@@ -991,7 +1030,19 @@ int lst_profile_read(lst_state* s, double* ms_total, int32_t capacity, int32_t* 
 
 const char* lst_profile_phase_name(int32_t phase) {
   if (phase < 0 || phase >= PH_COUNT) return nullptr;
-  return kPhaseNames[phase];
+  return kPhaseNames.buf[phase];
+}
+
+int lst_set_split_tasks(lst_state* s, int32_t enable) {
+  if (!s) return LST_EINVAL;
+  if (s->kind != 0) return LST_ESTATE;
+  DeviceGuard dg(s->device);
+  HIPCHK(hipStreamSynchronize(s->stream));
+  s->split = enable ? 1 : 0;
+  // captured steps hold the other launch sequence
+  for (auto& g : s->graphs) (void)hipGraphExecDestroy(g.exec);
+  s->graphs.clear();
+  return LST_OK;
 }
 
 int lst_set_graphs(lst_state* s, int32_t enable) {

@@ -1736,7 +1736,12 @@ hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t 
     total += n;
   }
   L.begin[L.ntask] = total;
-  if (total == 0) return hipSuccess;
+  if (total == 0) {
+    // nothing to run: the events still mark this (empty) launch on the stream
+    if (ev0 && ev1 && (hipEventRecord(ev0, s) != hipSuccess || hipEventRecord(ev1, s) != hipSuccess))
+      return hipErrorUnknown;
+    return hipSuccess;
+  }
   if (lds > kStepLdsMax) return hipErrorInvalidValue;
 
   const void* fn = step_kernel_for(L.lk, small, w16);

@@ -256,6 +256,35 @@ def test_determinism(gpu_lib):
         assert torch.equal(la, lb) and torch.equal(ga, gb)
 
 
+@pytest.mark.parametrize("m,K,d", [(32, 8, 48), (150, 30, 70)])
+def test_split_tasks_bitwise_equal(gpu_lib, m, K, d):
+    """Every task of a step launched alone (the measurement aid) gives bitwise the
+    results of the default launches; m = 150 takes the m > 128 task order and,
+    with m K >= 4096, the hot-row scatter of launch 4."""
+    import paper_1412_7091_amd as lst
+
+    cfg = _cfg(D=3000, d=d, m=m, K=K, lr=5e-3, idx_dist="zipf", zipf_s=1.1, entropy=119)
+    wl = Workload(cfg)
+    dev = torch.device("cuda:0")
+    V0 = torch.from_numpy(wl.init_V()).to(dev)
+    layers = [lst.FactoredOutputLayer(V0, m_max=m, K_max=K) for _ in range(2)]
+    layers[1].set_split_tasks(True)
+    outs = [[], []]
+    for s in range(6):
+        H, idx, val = (torch.from_numpy(x).to(dev) for x in wl.batch(s))
+        for li, layer in enumerate(layers):
+            loss_t, grad_t = layer.step(H, idx, val, cfg.lr)
+            outs[li].append((loss_t.clone(), grad_t.clone()))
+    for layer in layers:
+        assert layer.sync() == 0
+    for (la, ga), (lb, gb) in zip(*outs):
+        assert torch.equal(la, lb) and torch.equal(ga, gb)
+    for x, y in zip(layers[0].get_state(), layers[1].get_state()):
+        assert torch.equal(x, y)
+    assert torch.equal(layers[0].get_V(), layers[1].get_V())
+    assert np.array_equal(layers[0].touched_rows(), layers[1].touched_rows())
+
+
 def test_graph_replay_matches_eager(gpu_lib):
     """Captured steps replayed several times (three input buffers cycled, with eager
     work and synchronisations in between) give bitwise the same results as the
