@@ -83,8 +83,9 @@ def main():
                          "its own (lst_set_split_tasks), with per-task times and the HBM "
                          "fraction of the gather and the scatter")
     ap.add_argument("--crossover", action="store_true",
-                    help="instead of the benchmark line: the Woodbury step against a solve from "
-                         "scratch, over m at d = 500 and 1024 (D = 200000, K = 10)")
+                    help="instead of the benchmark line: the Woodbury step (lst_step) against the "
+                         "solve-from-scratch step (lst_step_solve), over m at d = 500 and 1024 "
+                         "(D = 200000, K = 10)")
     args = ap.parse_args()
     if args.sweep:
         return sweep(args)
@@ -551,24 +552,24 @@ def sweep(args):
     return 0
 
 
-CROSS_M = (1, 16, 64, 128, 256, 512)
+CROSS_M = (1, 2, 4, 8, 16, 32, 64, 128, 256, 512)
 CROSS_D = (500, 1024)
 
 
 def crossover(args):
-    """Woodbury update of U^{-T} against solving for U_new^{-T} H from scratch.
+    """Woodbury update of U^{-T} (lst_step) against solving U_new^T Z = H from
+    scratch (lst_step_solve), both the library's own kernels, over m at d = 500
+    and 1024 (D = 200000, K = 10, squared error).
 
     The paper notes that for large m it may pay to solve the d x d system with
     U_new every minibatch instead of keeping U^{-T} through the Woodbury
-    identity (its m x m inverse).  Per step the Woodbury form spends 2 d^2 m on
-    the U^{-T} panel of the first product, about 2 n m^2 d on the Neumann
-    solve (n iterations) and 2 d^2 m on the U^{-T} update; the from-scratch
-    form spends (2/3) d^3 on a pivoted factorisation of U_new and 2 d^2 m on
-    the two triangular solves.  This prints, for each d and m, the factored
-    step's time and its launches (HIP events), the flop-model crossover, and
-    the time of a vendor factorisation and solve of the same d x d system
-    (rocSOLVER through torch.linalg, timed as a yardstick only; the library
-    has no from-scratch path).  Prints one JSON object.
+    identity.  Per step the Woodbury form spends 2 d^2 m on the U^{-T} panel of
+    the first product, about 2 n m^2 d on the Neumann solve (n iterations) and
+    2 d^2 m on the U^{-T} update; the from-scratch form spends (2/3) d^3 on the
+    pivoted factorisation of U_new and 2 d^2 m on the triangular solves.  For
+    each d and m: both steps' time (HIP events around back-to-back steps), the
+    from-scratch step's factorisation and solve phases, and the flop model.
+    Prints one JSON object.
     """
     import torch
 
@@ -584,75 +585,57 @@ def crossover(args):
         wl = Workload(cfg)
         V0_t = torch.from_numpy(wl.init_V()).to(dev)
         pool = [tuple(torch.from_numpy(x).to(dev) for x in wl.batch(s)) for s in range(4)]
-        layer = lst.FactoredOutputLayer(V0_t, m_max=cfg.m, K_max=cfg.K)
+        wood = lst.FactoredOutputLayer(V0_t, m_max=cfg.m, K_max=cfg.K)
+        scr = lst.FactoredOutputLayer(V0_t, m_max=cfg.m, K_max=cfg.K)
         loss_t = torch.empty(cfg.m, device=dev)
         grad_t = torch.empty((cfg.m, d), device=dev)
-        # the flop-model crossover: 2 d^2 m + 2 n m^2 d = (2/3) d^3 with n = 4
         n_it = 4
-        m_flop = (-2 * d * d + np.sqrt(4 * d ** 4 + 4 * 2 * n_it * d * (2 / 3) * d ** 3)) / (
-            2 * 2 * n_it * d)
         for m in CROSS_M:
             sub = [tuple(x[:m].contiguous() for x in b) for b in pool]
-
-            def run(n, offset=0):
-                for s in range(n):
-                    H, idx, val = sub[(offset + s) % len(sub)]
-                    layer.step(H, idx, val, cfg.lr, out=(loss_t[:m], grad_t[:m]))
-
-            run(10)
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            run(100, 10)
-            e1.record()
-            torch.cuda.synchronize()
-            assert layer.sync() == 0
-            step_us = 1e3 * e0.elapsed_time(e1) / 100
-            layer.profile(True)
-            run(50)
-            phases, nsteps = layer.profile_read()
-            layer.profile(False)
-            launches = {k: round(1e3 * v / max(nsteps, 1), 2) for k, v in phases.items()
-                        if k.startswith("launch")}
-            row = {"d": d, "m": m, "step_us": round(step_us, 2), "launch_us": launches,
-                   "woodbury_flops": 4 * d * d * m + 2 * n_it * m * m * d,
+            row = {"d": d, "m": m, "woodbury_flops": 4 * d * d * m + 2 * n_it * m * m * d,
                    "scratch_flops": int(2 * d ** 3 / 3) + 2 * d * d * m}
+            for name, layer, fn in (("woodbury", wood, wood.step), ("scratch", scr, scr.step_solve)):
+                nsteps = 100 if name == "woodbury" else 30
+
+                def run(n, offset=0):
+                    for s in range(n):
+                        H, idx, val = sub[(offset + s) % len(sub)]
+                        fn(H, idx, val, cfg.lr, out=(loss_t[:m], grad_t[:m]))
+
+                run(5)
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                run(nsteps, 5)
+                e1.record()
+                torch.cuda.synchronize()
+                if layer.sync() != 0:
+                    log(f"device error in the {name} step at d={d} m={m}")
+                    sys.exit(1)
+                row[f"{name}_us"] = round(1e3 * e0.elapsed_time(e1) / nsteps, 2)
+                if name == "scratch":
+                    layer.profile(True)
+                    run(10)
+                    phases, n = layer.profile_read()
+                    layer.profile(False)
+                    row["scratch_phases_us"] = {k: round(1e3 * v / max(n, 1), 1)
+                                                for k, v in phases.items() if v > 0}
+            row["faster"] = "woodbury" if row["woodbury_us"] <= row["scratch_us"] else "scratch"
             out.append(row)
             log(json.dumps(row))
-        layer.close()
-        # vendor factorisation and solve of U^T Z = H for a d x d U near I
-        U = torch.eye(d, device=dev) + 0.01 * torch.randn(d, d, device=dev)
-        for m in CROSS_M:
-            H = torch.randn(d, m, device=dev)
-            for _ in range(3):
-                LU, piv = torch.linalg.lu_factor(U)
-                torch.linalg.lu_solve(LU, piv, H, adjoint=True)
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for _ in range(20):
-                LU, piv = torch.linalg.lu_factor(U)
-            e1.record()
-            torch.cuda.synchronize()
-            f_us = 1e3 * e0.elapsed_time(e1) / 20
-            e0.record()
-            for _ in range(20):
-                Z = torch.linalg.lu_solve(LU, piv, H, adjoint=True)
-            e1.record()
-            torch.cuda.synchronize()
-            s_us = 1e3 * e0.elapsed_time(e1) / 20
-            resid = float((U.T @ Z - H).abs().max())
-            for row in out:
-                if row["d"] == d and row["m"] == m:
-                    row.update(vendor_factor_us=round(f_us, 1), vendor_solve_us=round(s_us, 1),
-                               vendor_resid=resid, m_flop_crossover=round(float(m_flop), 1))
-                    log(json.dumps({k: row[k] for k in ("d", "m", "vendor_factor_us",
-                                                         "vendor_solve_us")}))
+        wood.close()
+        scr.close()
         del V0_t, pool
         torch.cuda.empty_cache()
-    print(json.dumps({"crossover": "Woodbury step vs a from-scratch solve of U_new^T Z = H",
+    cross = {}
+    for d in CROSS_D:
+        ms = [r["m"] for r in out if r["d"] == d and r["faster"] == "scratch"]
+        cross[str(d)] = min(ms) if ms else None
+    print(json.dumps({"crossover": "Woodbury step (lst_step) vs solve-from-scratch step "
+                                   "(lst_step_solve)",
                       "D": 200_000, "K": 10, "loss": "squared", "dtype": "f32",
-                      "data": "synthetic", "rows": out}), flush=True)
+                      "data": "synthetic", "first_m_scratch_faster": cross, "rows": out}),
+          flush=True)
     return 0
 
 

@@ -123,6 +123,23 @@ int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* 
              const float* Y_val, float lr, float* loss, float* grad_H);
 
 /*
+ * lst_step_solve -- the same step as lst_step, with U^{-T} replaced by a solve
+ * from scratch (section 3.5, last paragraph: for large m it can pay to solve
+ * the d x d system with U_new each minibatch instead of keeping U^{-T} through
+ * the m x m Woodbury inverse).  Per step: A = U_new^T is formed and factored
+ * (partial pivoting), and U_new^T Z = H is solved for Z = U_new^{-T} H, which
+ * gives the update of V (eq. updateV); Q and U move as in lst_step.  Same
+ * arguments, outputs and device errors (LST_ESINGULAR: a zero pivot of U_new).
+ * Requires d <= 1024 (LST_EINVAL otherwise).  Never captured into graphs; drift
+ * control does not run (it needs U^{-T}).  Allocates its workspace (d^2 +
+ * m_max d floats, 2 d ints) at the first call.  Afterwards the state's U^{-T}
+ * no longer matches U: lst_step, lst_stabilize and lst_stabilize_noalloc
+ * return LST_ESTATE until lst_restore (which sets U = U^{-T} = I).
+ */
+int lst_step_solve(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* Y_idx,
+                   const float* Y_val, float lr, float* loss, float* grad_H);
+
+/*
  * lst_materialize_W -- debug: W = V U into W (device, D x d).  O(D d^2).
  * For a naive state, copies its explicit W.
  */

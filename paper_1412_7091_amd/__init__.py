@@ -87,6 +87,8 @@ _SIGS = {
                                 ctypes.POINTER(lst_config), _P]),
     "lst_step": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, ctypes.c_float,
                                 _P, _P]),
+    "lst_step_solve": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P, _P, _P,
+                                      ctypes.c_float, _P, _P]),
     "lst_materialize_W": (ctypes.c_int, [_P, _P]),
     "lst_get_state": (ctypes.c_int, [_P, _P, _P, _P]),
     "lst_get_V": (ctypes.c_int, [_P, _P]),
@@ -220,6 +222,10 @@ def _step(fn_name, h, H, Y_idx, Y_val, lr, loss_out, grad_out):
 
 def lst_step(h, H, Y_idx, Y_val, lr, loss_out, grad_out):
     _step("lst_step", h, H, Y_idx, Y_val, lr, loss_out, grad_out)
+
+
+def lst_step_solve(h, H, Y_idx, Y_val, lr, loss_out, grad_out):
+    _step("lst_step_solve", h, H, Y_idx, Y_val, lr, loss_out, grad_out)
 
 
 def lst_naive_step(h, H, Y_idx, Y_val, lr, loss_out, grad_out):
@@ -404,6 +410,12 @@ class FactoredOutputLayer(_Layer):
     def step(self, H, Y_idx, Y_val, lr, out: Optional[Tuple] = None):
         loss, grad = out if out is not None else self._alloc_outputs(H.shape[0])
         lst_step(self._h, H, Y_idx, Y_val, lr, loss, grad)
+        return loss, grad
+
+    def step_solve(self, H, Y_idx, Y_val, lr, out: Optional[Tuple] = None):
+        """The step with U_new^T Z = H solved from scratch (lst_step_solve)."""
+        loss, grad = out if out is not None else self._alloc_outputs(H.shape[0])
+        lst_step_solve(self._h, H, Y_idx, Y_val, lr, loss, grad)
         return loss, grad
 
     def get_state(self):

@@ -58,6 +58,12 @@ struct lst_state {
   int hbits = 0;
   int ld0 = 0;
   float* on_ws = nullptr;  // single-example step workspace
+  // solve-from-scratch step: A = U_new^T and its LU factors, pivots, the
+  // permutation, Z^T; allocated at its first call.  uit_stale: U^{-T} no
+  // longer matches U (lst_step refuses the state until lst_restore).
+  float *lu_F = nullptr, *lu_Z = nullptr;
+  int *lu_ipiv = nullptr, *lu_perm = nullptr;
+  int uit_stale = 0;
   float* Nm = nullptr;  // m_max > 128: m x ldn, N = A C1 A + A C2 B + B C2^T A + B Y^T Y B
   int ldn = 0;
   int n_c1p = 0;  // partial sums of h^T Q h per example (two per 32-column tile of H^)
@@ -166,12 +172,13 @@ int dalloc(lst_state* s, T** p, size_t count) {
 constexpr int kTaskKinds = TK_CLEAR + 1;
 enum Phase {
   PH_LAUNCH1 = 0, PH_LAUNCH2, PH_LAUNCH3, PH_LAUNCH4, PH_DRIFT, PH_ONLINE_A, PH_ONLINE_B,
-  PH_TASK0, PH_COUNT = PH_TASK0 + 4 * kTaskKinds
+  PH_SCRATCH_FACTOR, PH_SCRATCH_SOLVE, PH_TASK0, PH_COUNT = PH_TASK0 + 4 * kTaskKinds
 };
 const char* const kTaskNames[kTaskKinds] = {"gemm",  "targets", "yy",   "scalars",
                                             "solve", "scatter", "clear"};
-const char* const kLaunchNames[PH_TASK0] = {"launch1", "launch2", "launch3", "launch4",
-                                            "drift",   "online_a", "online_b"};
+const char* const kLaunchNames[PH_TASK0] = {"launch1",  "launch2",  "launch3",
+                                            "launch4",  "drift",    "online_a",
+                                            "online_b", "scratch.factor", "scratch.solve"};
 // "launch<L>.<task>" for the split-task phases
 struct PhaseNames {
   char buf[PH_COUNT][32];
@@ -410,9 +417,15 @@ int enqueue_online(lst_state* s, hipStream_t st, int32_t K, const float* H, cons
 }
 
 // Enqueues the launches of one factored step on stream st.
+// scratch: the solve-from-scratch form (section 3.5, last paragraph) instead of
+// the Woodbury update: no U^{-T} in launch 1 and no Woodbury solve in launch 2;
+// after launch 3, A = U_new^T is formed, factored and solved for Z = U_new^{-T} H
+// (lu.hip), then the scatter, the Q and U updates and the clear run as launches
+// of their own.  U^{-T} is left as it was.
 int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float* H,
-                 const int32_t* Y_idx, const float* Y_val, float lr, float* loss, float* grad_H) {
-  if (m == 1 && K <= kOnlineMaxK)
+                 const int32_t* Y_idx, const float* Y_val, float lr, float* loss, float* grad_H,
+                 bool scratch = false) {
+  if (!scratch && m == 1 && K <= kOnlineMaxK)
     return enqueue_online(s, st, K, H, Y_idx, Y_val, lr, loss, grad_H);
   const int d = s->d;
   int* fl = s->flags;
@@ -445,10 +458,14 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     L.kind[0] = TK_GEMM; L.kind[1] = TK_TARGETS;
     L.gemm.np = 1;
     GemmProblem& p1 = L.gemm.p[0];
-    p1 = gemm_problem(L_NT, m, 3 * d + m, d, vmat(H, d, m), vmat2(s->state, d, 3 * d, H, d, m),
-                      s->Z0, s->ld0, 1.f, 0.f, EPI_STORE);
+    // [Q; U; U^{-T}; H^T] (scratch: [Q; U; H^T], H^T H lands in the P columns)
+    const int nst = scratch ? 2 : 3;
+    p1 = gemm_problem(L_NT, m, nst * d + m, d, vmat(H, d, m),
+                      vmat2(s->state, d, nst * d, H, d, m), s->Z0, s->ld0, 1.f, 0.f, EPI_STORE);
     p1.dotp = s->c1p; p1.ld_dotp = s->n_c1p; p1.dot_ncols = d;  // h_i^T H^_i partials
-    p1.absp = s->hap; p1.ld_absp = c.n_hap; p1.abs_col0 = 3 * d;  // |H^T H| row partials
+    if (!scratch) {
+      p1.absp = s->hap; p1.ld_absp = c.n_hap; p1.abs_col0 = 3 * d;  // |H^T H| row partials
+    }
     p1.tile = t1;
     p1.dot_h = H; p1.ld_doth = d;
     L.lk = 1;
@@ -466,6 +483,10 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
       // outlasts the GEMM tiles, and the merges of Y^T Y take long for long
       // target lists: their blocks go first
       L.kind[0] = TK_SOLVE; L.kind[1] = TK_YY; L.kind[2] = TK_GEMM;
+    }
+    if (scratch) {
+      L.ntask = 3;
+      L.kind[0] = TK_GEMM; L.kind[1] = TK_YY; L.kind[2] = TK_SCALARS;
     }
     GemmBatch& g = L.gemm;
     g.np = 4;
@@ -513,7 +534,40 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     pt.tile = 32;
     L.lk = hot ? 6 : 3;
     L.timing_slot = 2;
+    if (scratch) {
+      L.ntask = 1;
+      L.kind[0] = TK_GEMM;
+    }
     OK_OR_RETURN(run_launch(s, c, L, stages_for(g, kLaunch34Stages), st, PH_LAUNCH3));
+  }
+  if (scratch) {
+    // A = U_new^T = U^T - lr H^T (U H A): factor it, Z = A^{-1} H, X_i = -lr a_i z_i
+    OK_OR_RETURN(prof_mark(s, PH_SCRATCH_FACTOR, 0, st));
+    HIPCHK(transpose_square(c.U, s->lu_F, d, st));
+    {
+      StepLaunch F{};
+      F.lk = 4;
+      F.ntask = 1;
+      F.kind[0] = TK_GEMM;
+      F.gemm.np = 1;
+      F.gemm.p[0] = gemm_problem(L_TN, d, d, m, vmat(H, d, m), vmat(s->UHa, d, m), s->lu_F, d,
+                                 -lr, 1.f, EPI_STORE);
+      F.gemm.p[0].tile = 64;
+      HIPCHK(step_launch(c, F, stages_for(F.gemm, kLaunch34Stages), st));
+    }
+    HIPCHK(lu_factor(s->lu_F, d, s->lu_ipiv, s->lu_perm, fl, st));
+    OK_OR_RETURN(prof_mark(s, PH_SCRATCH_FACTOR, 1, st));
+    OK_OR_RETURN(prof_mark(s, PH_SCRATCH_SOLVE, 0, st));
+    HIPCHK(lu_solve_rows(s->lu_F, s->lu_perm, d, H, m, s->lu_Z, s->X, s->a, lr, st));
+    OK_OR_RETURN(prof_mark(s, PH_SCRATCH_SOLVE, 1, st));
+    StepLaunch L{};
+    L.ntask = 1;
+    L.kind[0] = TK_SCATTER;
+    L.lk = hot ? 6 : 3;
+    L.timing_slot = 2;
+    hipEvent_t e0, e1;
+    OK_OR_RETURN(prof_pair(s, PH_TASK0 + 2 * kTaskKinds + TK_SCATTER, &e0, &e1));
+    HIPCHK(step_launch(c, L, kLaunch34Stages, st, e0, e1));
   }
   {  // launch 4: Q -= lr (H T^T + T H^T) ; U and U^{-T} updates ; clear the hash slots
     StepLaunch L{};
@@ -536,7 +590,22 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     g.p[2].tile = 64;
     L.lk = hot ? 7 : 4;
     L.timing_slot = 3;
+    if (scratch) {
+      g.np = 2;  // no U^{-T}
+      L.ntask = 1;
+    }
     OK_OR_RETURN(run_launch(s, c, L, stages_for(g, kLaunch34Stages), st, PH_LAUNCH4));
+    if (scratch) {
+      StepLaunch C{};
+      C.ntask = 1;
+      C.kind[0] = TK_CLEAR;
+      C.lk = L.lk;
+      C.timing_slot = 3;
+      hipEvent_t e0, e1;
+      OK_OR_RETURN(prof_pair(s, PH_TASK0 + 3 * kTaskKinds + TK_CLEAR, &e0, &e1));
+      HIPCHK(step_launch(c, C, kLaunch34Stages, st, e0, e1));
+      return LST_OK;  // drift control needs U^{-T}
+    }
   }
   return enqueue_drift(s, st);
 }
@@ -750,7 +819,7 @@ int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* 
              const float* Y_val, float lr, float* loss, float* grad_H) {
   int rc = check_step_args(s, m, K, H, Y_idx, Y_val, lr, loss, grad_H);
   if (rc != LST_OK) return rc;
-  if (s->kind != 0) return LST_ESTATE;
+  if (s->kind != 0 || s->uit_stale) return LST_ESTATE;
   DeviceGuard dg(s->device);
   if (s->prof || !s->use_graphs) {
     if (s->prof) s->prof_steps += 1;
@@ -806,10 +875,34 @@ int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* 
   return LST_OK;
 }
 
+int lst_step_solve(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* Y_idx,
+                   const float* Y_val, float lr, float* loss, float* grad_H) {
+  int rc = check_step_args(s, m, K, H, Y_idx, Y_val, lr, loss, grad_H);
+  if (rc != LST_OK) return rc;
+  if (s->kind != 0) return LST_ESTATE;
+  if (s->d > kLuMaxD) return LST_EINVAL;
+  DeviceGuard dg(s->device);
+  if (!s->lu_F) {
+    const int d = s->d;
+    if ((rc = dalloc(s, &s->lu_F, (size_t)d * d)) ||
+        (rc = dalloc(s, &s->lu_Z, (size_t)s->cfg.m_max * d)) || (rc = dalloc(s, &s->lu_ipiv, d)) ||
+        (rc = dalloc(s, &s->lu_perm, d)))
+      return rc;
+  }
+  if (s->prof) s->prof_steps += 1;
+  rc = enqueue_step(s, s->stream, m, K, H, Y_idx, Y_val, lr, loss, grad_H, true);
+  if (rc == LST_OK) {
+    s->steps += 1;
+    s->last_slots = m * K;
+    s->uit_stale = 1;
+  }
+  return rc;
+}
+
 int lst_stabilize(lst_state* s, const lst_stab_config* cfg, lst_stab_report* report) {
   if (!s) return LST_EINVAL;
   OK_OR_RETURN(check_stab_config(cfg));
-  if (s->kind != 0) return LST_ESTATE;
+  if (s->kind != 0 || s->uit_stale) return LST_ESTATE;
   DeviceGuard dg(s->device);
   OK_OR_RETURN(enqueue_stabilize(s, *cfg, s->stream));
   if (!report) return LST_OK;
@@ -819,7 +912,7 @@ int lst_stabilize(lst_state* s, const lst_stab_config* cfg, lst_stab_report* rep
 int lst_stabilize_noalloc(lst_state* s, const lst_stab_config* cfg, lst_stab_report* report) {
   if (!s) return LST_EINVAL;
   OK_OR_RETURN(check_stab_config(cfg));
-  if (s->kind != 0) return LST_ESTATE;
+  if (s->kind != 0 || s->uit_stale) return LST_ESTATE;
   if (!s->scratch) return LST_EHIP;
   const int ks = stab_ksplit(s->d);
   const StabLayout l = stab_layout(s->d, ks, cfg->max_fixes);
@@ -901,6 +994,7 @@ int lst_restore(lst_state* s) {
   OK_OR_RETURN(vu_product(s, s->stream, s->Vtmp, s->V, nullptr, nullptr));
   HIPCHK(set_identity_if(Up(s), s->d, nullptr, s->stream));
   HIPCHK(set_identity_if(Uitp(s), s->d, nullptr, s->stream));
+  s->uit_stale = 0;
   return LST_OK;
 }
 

@@ -230,6 +230,18 @@ hipError_t online_step(const OnlineArgs& a, hipStream_t s, hipEvent_t e0a = null
                        hipEvent_t e1a = nullptr, hipEvent_t e0b = nullptr,
                        hipEvent_t e1b = nullptr);
 
+// ----------------------------------------- the solve-from-scratch step (lu.hip)
+constexpr int kLuMaxD = 1024;
+// In place P A = L R of the d x d row-major A (partial pivoting); ipiv[k] = the
+// row swapped with row k at step k, perm[j] = the row of A that ends at row j.
+// LST_ESINGULAR in flags[F_ERR] on a zero or non-finite pivot (the
+// factorisation runs on; its output is then meaningless).
+hipError_t lu_factor(float* A, int d, int* ipiv, int* perm, int* flags, hipStream_t s);
+// With F, perm from lu_factor of A: row i of H (m x d) is h_i^T; writes
+// z_i = A^{-1} h_i to row i of X2 and -lr acoef[i] z_i to row i of Xout.
+hipError_t lu_solve_rows(const float* F, const int* perm, int d, const float* H, int m, float* X2,
+                         float* Xout, const float* acoef, float lr, hipStream_t s);
+
 // ------------------------------------------------------------ small dense
 // Sinv = S^{-1} (Gauss-Jordan, partial pivoting); sets F_ERR = LST_ESINGULAR on a zero pivot.
 hipError_t invert_small(const float* S, int lds, float* Sinv, int ldi, int m, double* work,

@@ -52,13 +52,15 @@ def _compare(s, loss_g, grad_g, loss_r, grad_r, W_before, H, idx, val, cfg, rows
 
 def run_parity(cfg: WorkloadConfig, steps: int, *, cond_max: float = 0.0, check_rows: bool = True,
                W_every: int = 0, naive: bool = False, V_check_untouched: bool = False,
-               yardstick: bool = False, with_naive: bool = False, log_every: int = 0):
+               yardstick: bool = False, with_naive: bool = False, log_every: int = 0,
+               solve: bool = False):
     """Steps the GPU library and the explicit-W oracle from the same initial W.
 
     yardstick: also step the definition in fp32 on the host (explicit.step_fp32)
     and record its grad distance from the oracle (StepReport.yard_grad_rel).
     with_naive: also step the library's explicit-W (naive) path on the GPU and
     record its grad distance (StepReport.naive_grad_rel).
+    solve: step with lst_step_solve (U_new^T Z = H solved from scratch).
     Returns (reports, W_rel_final, extra) where extra holds the final layer object."""
     import torch
 
@@ -92,7 +94,8 @@ def run_parity(cfg: WorkloadConfig, steps: int, *, cond_max: float = 0.0, check_
         H_t = torch.from_numpy(H).to(dev)
         i_t = torch.from_numpy(idx).to(dev)
         v_t = torch.from_numpy(val).to(dev)
-        loss_t, grad_t = layer.step(H_t, i_t, v_t, cfg.lr)
+        stepper = layer.step_solve if solve else layer.step
+        loss_t, grad_t = stepper(H_t, i_t, v_t, cfg.lr)
         code = layer.sync()
         assert code == 0, f"step {s}: device status {code}"
         loss_g = loss_t.cpu().numpy()
