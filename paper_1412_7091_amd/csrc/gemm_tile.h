@@ -433,7 +433,7 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
         pre2[i][j][r] = 0.f;
         if (row >= P.M || col >= P.N) continue;
         if (((epi_is<EPIS>(P, EPI_STORE) || epi_is<EPIS>(P, EPI_SCALED)) && P.beta != 0.f) ||
-            (epi_is<EPIS>(P, EPI_SYM) && row <= col)) {
+            (epi_is<EPIS>(P, EPI_SYM) && row <= col && P.beta != 0.f)) {
           pre1[i][j][r] = P.C[(size_t)row * P.ldc + col];
         } else if (epi_is<EPIS>(P, EPI_GRADN)) {
           pre1[i][j][r] = P.s1[row] * P.e1[(size_t)row * P.lde1 + col] +

@@ -354,6 +354,7 @@ int stages_for(const GemmBatch& b, int max_stages = kMaxStages) {
 // Launches 3 and 4 keep at most 4 stages (64 KB): two blocks share a compute
 // unit, so the short tasks run beside the GEMM tiles.
 constexpr int kLaunch34Stages = 4;
+constexpr int kLaunch2Stages64 = 4;
 // Slots a row needs to be scattered by the launch-4 clear blocks instead of its
 // owner in launch 3; at most m K / kHotMinSlots rows qualify, which sizes
 // their list.
@@ -500,12 +501,21 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     g.p[3] = gemm_problem(L_NT, m, m, d, vmat(s->G, d, m), vmat(UH, s->ld0, m), s->NP + 2 * m,
                           4 * m, 1.f, 0.f, EPI_STORE);
     // m > 128: K (d) is long and 64 x 64 tiles fetch half the bytes per
-    // output of 32 x 32 ones; with up to 9 stages all of K is in flight
-    if (m > 128)
+    // output of 32 x 32 ones; with up to 9 stages all of K is in flight.  N is
+    // formed before launch 3 from C2 itself, so C2^T is not computed, and the
+    // symmetric C1 = H^T Q H runs on its upper-triangle tiles only.
+    if (m > 128) {
+      g.np = 3;
+      g.p[1].epi = EPI_SYM;
       for (int q = 0; q < g.np; ++q) g.p[q].tile = 64;
+    }
     L.lk = 2;
     L.timing_slot = 1;
-    OK_OR_RETURN(run_launch(s, c, L, stages_for(g), st, PH_LAUNCH2));
+    // m > 128: four stages (64 KB) so that a GEMM tile and a solve block (whose
+    // B stays in registers) share a compute unit and the tiles need not wait
+    // for the solve to end
+    OK_OR_RETURN(run_launch(s, c, L, stages_for(g, m > 128 ? kLaunch2Stages64 : kMaxStages), st,
+                            PH_LAUNCH2));
   }
   {  // launch 3: grad_H and T ; scatter into V
     StepLaunch L{};

@@ -35,7 +35,8 @@ struct VMat {
 
 enum Epi {
   EPI_STORE = 0,    // C = alpha*acc + beta*C
-  EPI_SYM = 1,      // upper-triangle tiles only: C[r][c] = C[c][r] = C[r][c] + alpha*acc (r <= c)
+  EPI_SYM = 1,      // upper-triangle tiles only: C[r][c] = C[c][r] = beta_r + alpha*acc (r <= c),
+                    // beta_r = C[r][c] when beta != 0, else 0
   EPI_GRADT = 2,    // output rows 2i, 2i+1 pair up into row i (M = 2 x rows of C):
                     //   g = s1[i]*E1[i][c] + s2[i]*E2[i][c]; G[i][c] = g;
                     //   C[i][c] = g + alpha*(s1[i]*acc[2i][c] + s2[i]*acc[2i+1][c])

@@ -513,8 +513,11 @@ __host__ __device__ inline int solve_lde(int mp) { return mp + 4; }
 __host__ __device__ inline size_t solve_lds_bytes(int m) {
   const int mp = (m + 15) & ~15;
   const int lde = solve_lde(mp);
+  // m <= 128: 1/c, B^T, Y^T twice and H^T H; m > 128: 1/c and Y^T twice (each
+  // wave keeps its rows of B in registers, so that a GEMM tile fits beside)
   const size_t neumann =
-      (size_t)(mp + 3 * kSolveCols * lde + (m <= 128 ? mp * mp : 0)) * sizeof(float);
+      (size_t)(mp + (m <= 128 ? 3 : 2) * kSolveCols * lde + (m <= 128 ? mp * mp : 0)) *
+      sizeof(float);
   const size_t gj = m <= 128 ? (size_t)m * (m + kSolveCols) * sizeof(double) : 0;
   const size_t extra = 256 * sizeof(float) + 512 * sizeof(double) + 64;  // red, colk, scalars
   return (neumann > gj ? neumann : gj) + extra;
@@ -587,13 +590,19 @@ __device__ __forceinline__ bool neumann_done(const float* red, int it, float sto
 // they meet rows of Y_k that are zero.  Returns the buffer holding the result.
 template <int RBW>
 __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int ldh, int m, int mp,
-                                              int iters, int LDE, const float* cinv,
-                                              const float* Bt, float* Yo, float* Yn,
-                                              float* red, float stop_k) {
+                                              int iters, int LDE, const float* cinv, float* Yo,
+                                              float* Yn, float* red, float stop_k) {
   constexpr int NB = 3;
   const int lane = lane_id(), wave = __builtin_amdgcn_readfirstlane(wave_id());
   const int nsl = mp / 16, nrb = mp / 16;
   const int kl = 4 * (lane >> 4);
+  // B's entries of the wave's rows (Y_0 = B), kept in registers
+  floatx4 bv[RBW];
+#pragma unroll
+  for (int t = 0; t < RBW; ++t) {
+    const int row = min(wave + 4 * t, nrb - 1) * 16 + kl;
+    bv[t] = *reinterpret_cast<const floatx4*>(Yo + (lane & 15) * LDE + row);
+  }
   unsigned rofs[RBW];
 #pragma unroll
   for (int t = 0; t < RBW; ++t)
@@ -636,15 +645,12 @@ __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int 
           for (int t = 0; t < RBW; ++t)
             acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[j][t][q], fb[q], acc[t], 0, 0, 0);
         if (++sl == nsl) {
-          // Y_{k+1} rows of the wave's blocks: every read first, then the writes
+          // Y_{k+1} rows of the wave's blocks
           sl = 0;
-          floatx4 bv[RBW], cv[RBW];
+          floatx4 cv[RBW];
 #pragma unroll
-          for (int t = 0; t < RBW; ++t) {
-            const int row = min(wave + 4 * t, nrb - 1) * 16 + kl;
-            bv[t] = *reinterpret_cast<const floatx4*>(Bt + (lane & 15) * LDE + row);
-            cv[t] = *reinterpret_cast<const floatx4*>(cinv + row);
-          }
+          for (int t = 0; t < RBW; ++t)
+            cv[t] = *reinterpret_cast<const floatx4*>(cinv + min(wave + 4 * t, nrb - 1) * 16 + kl);
           float dl = 0.f, bl = 0.f;
 #pragma unroll
           for (int t = 0; t < RBW; ++t) {
@@ -675,6 +681,120 @@ __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int 
   return Yo;
 }
 
+// neumann_mem for 256 < m <= 512: a wave owns eight 16-row blocks, taken as
+// two passes of four per iteration (the same stream of H^T H rows, each row
+// read once per iteration), so that the fragments in flight and the
+// accumulators are those of four blocks: the kernel then needs at most 256
+// VGPRs and two workgroups share a compute unit.
+__device__ __forceinline__ float* neumann_mem_two_pass(const float* __restrict__ HH, int ldh, int m,
+                                                       int mp, int iters, int LDE,
+                                                       const float* cinv, float* Yo, float* Yn,
+                                                       float* red, float stop_k) {
+  constexpr int NB = 3, RB = 4;
+  const int lane = lane_id(), wave = __builtin_amdgcn_readfirstlane(wave_id());
+  const int nsl = mp / 16, nrb = mp / 16;
+  const int kl = 4 * (lane >> 4);
+  // B's entries of the wave's rows (Y_0 = B), by pass
+  floatx4 bv0[RB], bv1[RB];
+  unsigned rofs0[RB], rofs1[RB];
+#pragma unroll
+  for (int t = 0; t < RB; ++t) {
+    const int r0 = min(wave + 4 * t, nrb - 1) * 16, r1 = min(wave + 16 + 4 * t, nrb - 1) * 16;
+    bv0[t] = *reinterpret_cast<const floatx4*>(Yo + (lane & 15) * LDE + r0 + kl);
+    bv1[t] = *reinterpret_cast<const floatx4*>(Yo + (lane & 15) * LDE + r1 + kl);
+    rofs0[t] = (unsigned)min(r0 + (lane & 15), m - 1) * (unsigned)ldh;
+    rofs1[t] = (unsigned)min(r1 + (lane & 15), m - 1) * (unsigned)ldh;
+  }
+  floatx4 fa[NB][RB];
+  auto load = [&](floatx4(&f)[RB], int sl, int ps) {
+    const unsigned ko = (unsigned)min(sl * 16 + kl, m - 4);
+#pragma unroll
+    for (int t = 0; t < RB; ++t)
+      f[t] = *reinterpret_cast<const floatx4*>(HH + ((ps ? rofs1[t] : rofs0[t]) + ko));
+  };
+  int lsl = 0, lps = 0;  // slice and pass of the next load
+  auto advance = [&](int& a, int& b) {
+    if (++a == nsl) {
+      a = 0;
+      b ^= 1;
+    }
+  };
+#pragma unroll
+  for (int j = 0; j + 1 < NB; ++j) {
+    load(fa[j], lsl, lps);
+    advance(lsl, lps);
+  }
+  floatx4 acc[RB];
+#pragma unroll
+  for (int t = 0; t < RB; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int yl = (lane & 15) * LDE + kl;
+  int total = iters * 2 * nsl;  // cut short once the series has converged
+  int sl = 0, ps = 0;           // slice and pass of the next MFMAs
+  int it = 0;                   // iterations completed
+  floatx4 prev0[RB], prev1[RB];  // diag(1/c) (H^T H) Y_{k-1} of the wave's rows
+  float bcol = 0.f, dl = 0.f, bl = 0.f;
+#pragma unroll
+  for (int t = 0; t < RB; ++t) {
+    prev0[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    prev1[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int g0 = 0; g0 < total; g0 += NB) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      // the loads run unconditionally (past the end they re-read H^T H)
+      load(fa[(j + NB - 1) % NB], lsl, lps);
+      advance(lsl, lps);
+      if (g0 + j < total) {
+        const floatx4 fb = *reinterpret_cast<const floatx4*>(Yo + yl + sl * 16);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int t = 0; t < RB; ++t)
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[j][t][q], fb[q], acc[t], 0, 0, 0);
+        if (++sl == nsl) {
+          // Y_{k+1} rows of the pass's blocks
+          sl = 0;
+#pragma unroll
+          for (int t = 0; t < RB; ++t) {
+            const int rb = wave + 16 * ps + 4 * t;
+            const floatx4 cv =
+                *reinterpret_cast<const floatx4*>(cinv + min(rb, nrb - 1) * 16 + kl);
+            const floatx4 y = acc[t] * cv;
+            const floatx4 b = ps ? bv1[t] : bv0[t];
+            const floatx4 pv = ps ? prev1[t] : prev0[t];
+            if (rb < nrb) {
+              *reinterpret_cast<floatx4*>(Yn + (lane & 15) * LDE + rb * 16 + kl) = b + y;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                dl = fmaxf(dl, fabsf(y[q] - pv[q]));
+                bl = fmaxf(bl, fabsf(b[q]));
+              }
+            }
+            if (ps)
+              prev1[t] = y;
+            else
+              prev0[t] = y;
+            acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+          }
+          if (ps) {  // both passes done: the iteration ends
+            neumann_post(red, it, dl, bl);
+            lds_barrier();
+            float* tt = Yo;
+            Yo = Yn;
+            Yn = tt;
+            if (neumann_done(red, it, stop_k, bcol)) total = g0 + j + 1;
+            ++it;
+            dl = 0.f;
+            bl = 0.f;
+          }
+          ps ^= 1;
+        }
+      }
+    }
+  }
+  return Yo;
+}
+
 template <bool SMALL>
 __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned char* sraw) {
   LST_SMARK(0);
@@ -691,8 +811,8 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   double* colk = reinterpret_cast<double*>(red + 256);
   int* s_int = reinterpret_cast<int*>(colk + 512);  // s_p, s_bad
   float* cinv = reinterpret_cast<float*>(sraw);        // mp: 1 / c_i = lr a_i
-  float* Bt = cinv + mp;                               // kSolveCols x LDE: B^T
-  float* Y0 = Bt + kSolveCols * LDE;                   // kSolveCols x LDE: Y^T
+  float* Bt = cinv + mp;  // kSolveCols x LDE: B^T (m <= 128; above, the waves keep B)
+  float* Y0 = SMALL ? Bt + kSolveCols * LDE : cinv + mp;  // kSolveCols x LDE: Y^T
   float* Y1 = Y0 + kSolveCols * LDE;
   float* Hs = Y1 + kSolveCols * LDE;                   // mp x mp: H^T H (SMALL only)
 
@@ -810,37 +930,50 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
     r = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   } else {
     LST_SMARK(2);
-    // At most two rows per thread (m <= 512) with at most 34 partials each:
-    // every load is issued, at a clamped valid address, before the first is
-    // used (partials past the 34th, never present for m <= 512, are summed
-    // one by one).
-    constexpr int kMaxHapBig = 2 * (512 / 32 + 1);
+    // The partials, m x nh floats stored row after row (m <= 512 and nh <= 34: two
+    // per tile column over the m columns of H^T H), are
+    // read as one flat array, every load issued before the first is used (each
+    // wave's load covers consecutive addresses), then summed row by row through
+    // LDS in chunks of 64 rows (Y1 is free until the iterations start).
+    constexpr int kChunkRows = 64, kChunks = 4;  // per pass; two passes cover 512 rows
+    constexpr int kPerChunk = (kChunkRows * 34 + 255) / 256;
     const int nh = c.n_hap;
-    float hv[2][kMaxHapBig];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const float* hp = c.hap + (size_t)min(tid + 256 * h, m - 1) * nh;
-#pragma unroll
-      for (int p = 0; p < kMaxHapBig; ++p) hv[h][p] = hp[min(p, nh - 1)];
-    }
+    float* stage = Y1;
     float rmax = 0.f;
+    for (int pass = 0; pass < 2; ++pass) {
+    float hv[kChunks][kPerChunk];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int i = tid + 256 * h;
-      float sabs = 0.f;
+    for (int cq = 0; cq < kChunks; ++cq) {
+      const int ch = pass * kChunks + cq;
+      const int nflat = max(0, min(kChunkRows, m - ch * kChunkRows)) * nh;
+      const float* base = c.hap + (size_t)ch * kChunkRows * nh;
 #pragma unroll
-      for (int p = 0; p < kMaxHapBig; ++p) sabs += p < nh ? hv[h][p] : 0.f;
-      if (i < m) {
-        for (int p = kMaxHapBig; p < nh; ++p) sabs += c.hap[(size_t)i * nh + p];
-        const float ri = sabs * cinv[i];
-        rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
+      for (int u = 0; u < kPerChunk; ++u) {
+        const int e = tid + 256 * u;
+        hv[cq][u] = e < nflat ? base[e] : 0.f;
       }
     }
-    for (int i = tid + 512; i < m; i += 256) {  // m > 512: not reached (m_max <= 512)
-      float sabs = 0.f;
-      for (int p = 0; p < nh; ++p) sabs += c.hap[(size_t)i * nh + p];
-      const float ri = sabs * cinv[i];
-      rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
+#pragma unroll
+    for (int cq = 0; cq < kChunks; ++cq) {
+      const int ch = pass * kChunks + cq;
+      if (ch * kChunkRows < m) {
+        const int nflat = min(kChunkRows, m - ch * kChunkRows) * nh;
+#pragma unroll
+        for (int u = 0; u < kPerChunk; ++u) {
+          const int e = tid + 256 * u;
+          if (e < nflat) stage[e] = hv[cq][u];
+        }
+        __syncthreads();
+        const int i = ch * kChunkRows + tid;
+        if (tid < kChunkRows && i < m) {
+          float sabs = 0.f;
+          for (int p = 0; p < nh; ++p) sabs += stage[tid * nh + p];
+          const float ri = sabs * cinv[i];
+          rmax = (ri == ri) ? fmaxf(rmax, ri) : INFINITY;
+        }
+        __syncthreads();
+      }
+    }
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, off));
@@ -856,7 +989,7 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
                     ((uintptr_t)HH & 15) == 0 && ((uintptr_t)P & 15) == 0;
   if (r < 0.5f) {
     if (gvec) {
-      // B^T = -(P^T_blk) diag(1/c)^T, Y0 = B^T: 16-byte loads, slot e = row
+      // Y0 = B = -(P^T_blk) diag(1/c)^T: 16-byte loads, slot e = row
       // e / 4, columns c0 + 4 (e % 4) ... + 3 (all in or all out of range)
       const int nq = 4 * mp;
       for (int e0 = 0; e0 < nq; e0 += 256 * 8) {
@@ -874,16 +1007,12 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
             const int i = e >> 2, cq = 4 * (e & 3);
             const bool ok = i < m && c0 + cq < d;
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-              const float val = ok ? -pv[u][v] * cinv[i] : 0.f;
-              Bt[(cq + v) * LDE + i] = val;
-              Y0[(cq + v) * LDE + i] = val;
-            }
+            for (int v = 0; v < 4; ++v) Y0[(cq + v) * LDE + i] = ok ? -pv[u][v] * cinv[i] : 0.f;
           }
         }
       }
     } else if (!SMALL) {
-      // B^T = -(P^T_blk) diag(1/c)^T, Y0 = B^T.
+      // Y0 = B = -(P^T_blk) diag(1/c)^T.
       for (int e0 = 0; e0 < kSolveCols * mp; e0 += 256 * 8) {
         float pv[8];
 #pragma unroll
@@ -897,9 +1026,7 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
           const int e = e0 + tid + 256 * u;
           if (e < kSolveCols * mp) {
             const int i = e / kSolveCols, cc = e - i * kSolveCols;
-            const float v = (i < m && c0 + cc < d) ? -pv[u] * cinv[i] : 0.f;
-            Bt[cc * LDE + i] = v;
-            Y0[cc * LDE + i] = v;
+            Y0[cc * LDE + i] = (i < m && c0 + cc < d) ? -pv[u] * cinv[i] : 0.f;
           }
         }
       }
@@ -1030,57 +1157,85 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
       }
     } else if (gvec) {
       Yo = (nrb <= 16)
-               ? neumann_mem<4>(HH, ldh, m, mp, iters, LDE, cinv, Bt, Yo, Yn, red, stop_k)
-               : neumann_mem<8>(HH, ldh, m, mp, iters, LDE, cinv, Bt, Yo, Yn, red, stop_k);
+               ? neumann_mem<4>(HH, ldh, m, mp, iters, LDE, cinv, Yo, Yn, red, stop_k)
+               : neumann_mem_two_pass(HH, ldh, m, mp, iters, LDE, cinv, Yo, Yn, red, stop_k);
     } else {
     floatx4 prev[RBW];  // diag(1/c) (H^T H) Y_{k-1} of the wave's rows (Y_0 = B: zero)
+    floatx4 bvr[RBW];   // B's entries of the wave's rows, read from Y_0 = B
     float bcol = 0.f;
 #pragma unroll
-    for (int t = 0; t < RBW; ++t) prev[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < RBW; ++t) {
+      prev[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+      const int rb = min(wave + 4 * t, nrb - 1);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) bvr[t][q] = Yo[(lane & 15) * LDE + rb * 16 + 4 * (lane >> 4) + q];
+    }
     for (int it = 0; it < iters; ++it) {
-      floatx4 acc[RBW];
-#pragma unroll
-      for (int t = 0; t < RBW; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-      constexpr int NB = 3;
-      float4 fb[NB], fa[NB][RBW];
-      // Every wave multiplies all RBW of its row blocks (a block past the last
-      // reads a clamped one and is never stored): the waves run side by side,
-      // so the extra MFMAs cost no time and the loop carries no branches.
-      auto mma = [&](const float4& b, const float4 (&a)[RBW]) {
-#pragma unroll
-        for (int t = 0; t < RBW; ++t) {
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].x, b.x, acc[t], 0, 0, 0);
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].y, b.y, acc[t], 0, 0, 0);
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].z, b.z, acc[t], 0, 0, 0);
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].w, b.w, acc[t], 0, 0, 0);
-        }
-      };
-      // Three fragment buffers rotate: slice s + 1 is read while slice s is
-      // multiplied, into the buffer of slice s - 2 (whose MFMAs are done).
-      const int nsl = mp / 16;
-      frag(Yo, 0, fb[0], fa[0]);
-      for (int sl = 0; sl < nsl; sl += NB) {
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          if (sl + j >= nsl) break;
-          frag(Yo, min(sl + j + 1, nsl - 1) * 16, fb[(j + 1) % NB], fa[(j + 1) % NB]);
-          mma(fb[j], fa[j]);
-        }
-      }
       const int col = lane & 15;
+      const int nsl = mp / 16;
       float dl = 0.f, bl = 0.f;
+      // the wave's row blocks in passes of four (fragments and accumulators of
+      // four blocks at a time keep the kernel within 256 VGPRs)
 #pragma unroll
-      for (int t = 0; t < RBW; ++t) {
-        const int rb = wave + 4 * t;
-        if (rb >= nrb) break;
+      for (int ps = 0; ps < RBW / 4; ++ps) {
+        floatx4 acc[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int row = rb * 16 + 4 * (lane >> 4) + q;
-          const float bv = Bt[col * LDE + row], y = acc[t][q] * cinv[row];
-          Yn[col * LDE + row] = bv + y;
-          dl = fmaxf(dl, fabsf(y - prev[t][q]));
-          bl = fmaxf(bl, fabsf(bv));
-          prev[t][q] = y;
+        for (int t = 0; t < 4; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+        constexpr int NB = 3;
+        float4 fb[NB], fa[NB][4];
+        auto frag4 = [&](int kk, float4& fbv, float4 (&fav)[4]) {
+          const int k = kk + 4 * (lane >> 4);
+          fbv = *reinterpret_cast<const float4*>(Yo + (lane & 15) * LDE + k);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int arow = min((wave + 4 * (4 * ps + t)) * 16, mp - 16) + (lane & 15);
+            const float* hr = HH + (size_t)min(arow, m - 1) * ldh;
+            const float x0 = hr[min(k, m - 1)], x1 = hr[min(k + 1, m - 1)];
+            const float x2 = hr[min(k + 2, m - 1)], x3 = hr[min(k + 3, m - 1)];
+            const bool ok = arow < m;
+            fav[t].x = (ok && k < m) ? x0 : 0.f;
+            fav[t].y = (ok && k + 1 < m) ? x1 : 0.f;
+            fav[t].z = (ok && k + 2 < m) ? x2 : 0.f;
+            fav[t].w = (ok && k + 3 < m) ? x3 : 0.f;
+          }
+        };
+        // Every wave multiplies all four row blocks of the pass (a block past
+        // the last reads a clamped one and is never stored): the waves run side
+        // by side, so the extra MFMAs cost no time and the loop has no branches.
+        auto mma = [&](const float4& b, const float4 (&av)[4]) {
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[t].x, b.x, acc[t], 0, 0, 0);
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[t].y, b.y, acc[t], 0, 0, 0);
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[t].z, b.z, acc[t], 0, 0, 0);
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[t].w, b.w, acc[t], 0, 0, 0);
+          }
+        };
+        // Three fragment buffers rotate: slice s + 1 is read while slice s is
+        // multiplied, into the buffer of slice s - 2 (whose MFMAs are done).
+        frag4(0, fb[0], fa[0]);
+        for (int sl = 0; sl < nsl; sl += NB) {
+#pragma unroll
+          for (int j = 0; j < NB; ++j) {
+            if (sl + j >= nsl) break;
+            frag4(min(sl + j + 1, nsl - 1) * 16, fb[(j + 1) % NB], fa[(j + 1) % NB]);
+            mma(fb[j], fa[j]);
+          }
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int T = 4 * ps + t;
+          const int rb = wave + 4 * T;
+          if (rb >= nrb) break;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int row = rb * 16 + 4 * (lane >> 4) + q;
+            const float bv = bvr[T][q], y = acc[t][q] * cinv[row];
+            Yn[col * LDE + row] = bv + y;
+            dl = fmaxf(dl, fabsf(y - prev[T][q]));
+            bl = fmaxf(bl, fabsf(bv));
+            prev[T][q] = y;
+          }
         }
       }
       neumann_post(red, it, dl, bl);
@@ -1503,13 +1658,16 @@ constexpr LaunchMasks kLaunchMasks[8] = {
 // The kernels of launches 1 and 2 built for m > 128 also compile 64 x 64
 // tiles: their products are long in K there (d up to 1024), and 64 x 64 tiles
 // fetch half the bytes per output of 32 x 32 ones (launch 1 uses them when
-// they alone fill the chip, launch 2 always).  The launch-3 kernels built for
+// they alone fill the chip, launch 2 always).  Launch 2's also compiles the
+// symmetric epilogue: there C1 = H^T Q H is computed on its upper-triangle
+// tiles and mirrored, and C2^T is not computed at all (N is formed from C2).  The launch-3 kernels built for
 // m > 128 compile the EPI_GRADN epilogue: there T takes N H^T from the formed
 // m x m matrix N instead of the interleaved 2m x 2m view of NP, a quarter of
 // the multiply-adds.
 constexpr LaunchMasks launch_masks(int lk, bool small) {
   LaunchMasks M = kLaunchMasks[lk];
   if (!small && (lk == 1 || lk == 2)) M.tiles |= TILE64;
+  if (!small && lk == 2) M.epis |= 1u << EPI_SYM;  // C1 = H^T H^ on its upper triangle
   if (!small && (lk == 3 || lk == 6)) M.epis |= 1u << EPI_GRADN;
   return M;
 }
@@ -1553,7 +1711,8 @@ __device__ __forceinline__ void run_task(const StepCtx& c, const StepLaunch& L, 
 }
 
 template <bool SMALLM, int W, int LK>
-__global__ __launch_bounds__(256) void step_kernel(StepCtx c, StepLaunch L) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SMALLM || LK != 2 ? 1 : 2)))
+void step_kernel(StepCtx c, StepLaunch L) {
   extern __shared__ __attribute__((aligned(16))) unsigned char sraw[];
   const int blk = blockIdx.x;
   int t = 0;
@@ -1677,26 +1836,45 @@ static const void* step_kernel_for(int lk, bool small, int w16) {
 }
 
 // One thread per element of N; row i of NP holds [C1 | C2 | C2^T | Y^T Y]_i.
+// N_ij = a_i a_j C1_ij + a_i b_j C2_ij + b_i a_j C2_ji + b_i b_j (Y^T Y)_ij from
+// NP = [C1 | C2 | . | Y^T Y] (C2^T is read as C2 transposed): 32 x 32 tiles of N,
+// the C2_ji tile through LDS so that every read is along a row.
 __global__ __launch_bounds__(256) void form_n_kernel(const float* __restrict__ NP,
                                                      const float* __restrict__ a,
                                                      const float* __restrict__ b, int m,
                                                      float* __restrict__ N, int ldn) {
-  const int i = blockIdx.y, j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= ldn) return;
-  float v = 0.f;
-  if (j < m) {
-    const float* r = NP + (size_t)i * 4 * m;
-    const float aj = a[j], bj = b[j];
-    v = a[i] * (r[j] * aj + r[m + j] * bj) + b[i] * (r[2 * m + j] * aj + r[3 * m + j] * bj);
+  __shared__ float T[32][33];
+  const int I0 = blockIdx.y * 32, J0 = blockIdx.x * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 8 rows of 32 per pass
+  const size_t ldp = (size_t)4 * m;
+  float c2t[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {  // C2[J0 + r][I0 + tx] for r = ty + 8 u
+    const int r = J0 + ty + 8 * u, col = I0 + tx;
+    c2t[u] = (r < m && col < m) ? NP[(size_t)r * ldp + m + col] : 0.f;
   }
-  N[(size_t)i * ldn + j] = v;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) T[ty + 8 * u][tx] = c2t[u];
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = I0 + ty + 8 * u, j = J0 + tx;
+    if (i >= m || j >= ldn) continue;
+    float v = 0.f;
+    if (j < m) {
+      const float* r = NP + (size_t)i * ldp;
+      const float aj = a[j], bj = b[j];
+      v = a[i] * (r[j] * aj + r[m + j] * bj) + b[i] * (T[tx][ty + 8 * u] * aj + r[3 * m + j] * bj);
+    }
+    N[(size_t)i * ldn + j] = v;
+  }
 }
 
 hipError_t form_n(const float* NP, const float* a, const float* b, int m, float* N, int ldn,
                   hipStream_t s) {
   if (m <= 0 || ldn < m) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(form_n_kernel, dim3((ldn + 255) / 256, m), dim3(256), 0, s, NP, a, b, m, N,
-                     ldn);
+  hipLaunchKernelGGL(form_n_kernel, dim3((ldn + 31) / 32, (m + 31) / 32), dim3(256), 0, s, NP, a,
+                     b, m, N, ldn);
   return hipGetLastError();
 }
 
