@@ -271,6 +271,23 @@ __device__ __forceinline__ float merge_dot(const int* ri, const float* vi, int n
   return acc;
 }
 
+// The same sum for lists whose rows are distinct: every step advances the
+// side(s) with the smaller row, with no branch inside the loop, so the lanes
+// of a wave (each merging its own pair) stay in step.
+__device__ __forceinline__ float merge_dot_distinct(const int* ri, const float* vi, int ni,
+                                                    const int* rj, const float* vj, int nj) {
+  float acc = 0.f;
+  int a = 0, b = 0;
+  while (a < ni && b < nj) {
+    const int ra = ri[a], rb = rj[b];
+    const float va = vi[a], vb = vj[b];
+    acc += (ra == rb) ? va * vb : 0.f;
+    a += (ra <= rb);
+    b += (rb <= ra);
+  }
+  return acc;
+}
+
 __device__ __forceinline__ void task_yy(const StepCtx& c, int local, unsigned char* sraw) {
   int(*srow)[kGramLd] = reinterpret_cast<int(*)[kGramLd]>(sraw);
   float(*sval)[kGramLd] = reinterpret_cast<float(*)[kGramLd]>(sraw + 32 * kGramLd * 4);
@@ -311,13 +328,37 @@ __device__ __forceinline__ void task_yy(const StepCtx& c, int local, unsigned ch
     }
     if (threadIdx.x < 32) scnt[threadIdx.x] = cnt;
     __syncthreads();
+    // Merge the repeats inside each list (adjacent, the lists being ordered):
+    // one list per wave at a time; each run's first entry takes the run's
+    // values summed in order and moves to its rank among the runs.  A wave's
+    // reads all complete before its writes (its LDS accesses run in order).
+    const int lane = lane_id(), w = wave_id();
+    for (int l = w; l < 32; l += 4) {
+      const int n = scnt[l];
+      const int k = lane;
+      const int r = k < n ? srow[l][k] : -1;
+      const bool head = k < n && (k == 0 || srow[l][k - 1] != r);
+      float sum = 0.f;
+      if (head)
+        for (int k2 = k; k2 < n && srow[l][k2] == r; ++k2) sum += sval[l][k2];
+      const unsigned long long heads = __ballot(head);
+      const int pos = __popcll(heads & ((1ull << k) - 1ull));
+      asm volatile("" ::: "memory");
+      if (head) {
+        srow[l][pos] = r;
+        sval[l][pos] = sum;
+      }
+      if (lane == 0) scnt[l] = __popcll(heads);
+    }
+    __syncthreads();
   }
   const int li = threadIdx.x >> 4, lj = threadIdx.x & 15;
   const int i = I0 + li, j = J0 + lj;
   if (i >= c.m || j >= c.m || i > j) return;
   float acc;
   if (staged)
-    acc = merge_dot(srow[li], sval[li], scnt[li], srow[16 + lj], sval[16 + lj], scnt[16 + lj]);
+    acc = merge_dot_distinct(srow[li], sval[li], scnt[li], srow[16 + lj], sval[16 + lj],
+                             scnt[16 + lj]);
   else
     acc = merge_dot(c.ex_row + (size_t)i * c.K, c.ex_val + (size_t)i * c.K, c.ex_cnt[i],
                     c.ex_row + (size_t)j * c.K, c.ex_val + (size_t)j * c.K, c.ex_cnt[j]);
