@@ -182,8 +182,7 @@ VMat vmat(const float* p, int ld, int rows, const float* rscale) {
   VMat v{};
   v.p[0] = p;
   v.ld[0] = ld;
-  v.r0[0] = 0;
-  v.r0[1] = rows;
+  v.r1 = rows;
   v.nb = 1;
   v.vec = (ld % 4 == 0) && aligned16(p);
   v.rscale = rscale;
@@ -196,9 +195,8 @@ VMat vmat2(const float* p0, int ld0, int rows0, const float* p1, int ld1, int ro
   v.ld[0] = ld0;
   v.p[1] = p1;
   v.ld[1] = ld1;
-  v.r0[0] = 0;
-  v.r0[1] = rows0;
-  v.r0[2] = rows0 + rows1;
+  v.r1 = rows0;  // block 1 holds rows [rows0, rows0 + rows1)
+  (void)rows1;
   v.nb = 2;
   v.vec = (ld0 % 4 == 0) && (ld1 % 4 == 0) && aligned16(p0) && aligned16(p1);
   v.rscale = nullptr;

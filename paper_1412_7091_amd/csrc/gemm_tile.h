@@ -46,9 +46,7 @@ static __device__ unsigned long long g_gemm_marks[4][8192][5];
 __device__ __forceinline__ const float* vm_row(const VMat& v, int row) {
   const float* base = v.p[0];
   int ld = v.ld[0], r0 = 0;
-  if (v.nb > 1 && row >= v.r0[1]) { base = v.p[1]; ld = v.ld[1]; r0 = v.r0[1]; }
-  if (v.nb > 2 && row >= v.r0[2]) { base = v.p[2]; ld = v.ld[2]; r0 = v.r0[2]; }
-  if (v.nb > 3 && row >= v.r0[3]) { base = v.p[3]; ld = v.ld[3]; r0 = v.r0[3]; }
+  if (v.nb > 1 && row >= v.r1) { base = v.p[1]; ld = v.ld[1]; r0 = v.r1; }
   return base + (size_t)(row - r0) * (size_t)ld;
 }
 
@@ -412,11 +410,12 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
   constexpr int IB = G::IB;
   const int S = bt.stages;
   const int m0 = tm * T, n0 = tn * T;
+  const GemmExtras& X = bt.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   constexpr bool kRowSums = (EPIS >> EPX_ROWSUMS) & 1u;
-  const bool dot = kRowSums && P.dotp != nullptr && n0 < P.dot_ncols;
-  const bool absr = kRowSums && P.absp != nullptr && n0 + T > P.abs_col0;
+  const bool dot = kRowSums && X.dotp != nullptr && n0 < X.dot_ncols;
+  const bool absr = kRowSums && X.absp != nullptr && n0 + T > X.abs_col0;
   LST_MARK(0);
 
   // Operands of the epilogue, fetched before the first chunk.
@@ -436,20 +435,20 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
             (epi_is<EPIS>(P, EPI_SYM) && row <= col && P.beta != 0.f)) {
           pre1[i][j][r] = P.C[(size_t)row * P.ldc + col];
         } else if (epi_is<EPIS>(P, EPI_GRADN)) {
-          pre1[i][j][r] = P.s1[row] * P.e1[(size_t)row * P.lde1 + col] +
-                          P.s2[row] * P.e2[(size_t)row * P.lde2 + col];
+          pre1[i][j][r] = X.s1[row] * X.e1[(size_t)row * X.lde1 + col] +
+                          X.s2[row] * X.e2[(size_t)row * X.lde2 + col];
         } else if (epi_is<EPIS>(P, EPI_GRADT)) {
           // accumulator rows 2o and 2o + 1 (r even / odd) both feed output row o
           const int o = row >> 1;
           if ((r & 1) == 0) {
-            pre1[i][j][r] = P.s1[o] * P.e1[(size_t)o * P.lde1 + col];
-            pre2[i][j][r] = P.s2[o] * P.e2[(size_t)o * P.lde2 + col];
+            pre1[i][j][r] = X.s1[o] * X.e1[(size_t)o * X.lde1 + col];
+            pre2[i][j][r] = X.s2[o] * X.e2[(size_t)o * X.lde2 + col];
           } else {
-            pre1[i][j][r] = P.s1[o];
-            pre2[i][j][r] = P.s2[o];
+            pre1[i][j][r] = X.s1[o];
+            pre2[i][j][r] = X.s2[o];
           }
         }
-        if (dot && col < P.dot_ncols) pre2[i][j][r] = P.dot_h[(size_t)row * P.ld_doth + col];
+        if (dot && col < X.dot_ncols) pre2[i][j][r] = X.dot_h[(size_t)row * X.ld_doth + col];
       }
 
   Accum<T> acs;
@@ -527,8 +526,8 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
   // EPI_SCALED: the power-of-two scale from the trace of the previous product
   // (exact, so the vector the products converge to does not depend on it).
   float pscale = 1.f, tsum = 0.f;
-  if (epi_is<EPIS>(P, EPI_SCALED) && P.s1 != nullptr) {
-    const float t = *P.s1;
+  if (epi_is<EPIS>(P, EPI_SCALED) && X.s1 != nullptr) {
+    const float t = *X.s1;
     if (t > 0.f && isfinite(t)) pscale = ldexpf(1.f, max(-126, min(126, -2 * ilogbf(t))));
   }
   // Element r of acc[i][j]: row 4*(lane/16) + r, column lane % 16 of its 16 x 16 block.
@@ -549,8 +548,8 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
         const float v = acc[i][j][r];
         if (epi_is<EPIS>(P, EPI_STORE)) {
           P.C[(size_t)row * P.ldc + col] = P.alpha * v + P.beta * pre1[i][j][r];
-          if (dot && col < P.dot_ncols) dsum[i][r] += pre2[i][j][r] * v;
-          if (absr && col >= P.abs_col0) asum[i][r] += fabsf(v);
+          if (dot && col < X.dot_ncols) dsum[i][r] += pre2[i][j][r] * v;
+          if (absr && col >= X.abs_col0) asum[i][r] += fabsf(v);
         } else if (epi_is<EPIS>(P, EPI_SYM)) {
           if (row <= col) {
             const float o = pre1[i][j][r] + P.alpha * v;
@@ -562,12 +561,16 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
             const int o = row >> 1;
             const float gv = pre1[i][j][r] + pre2[i][j][r];
             const float nh = pre1[i][j][r + 1] * v + pre2[i][j][r + 1] * acc[i][j][r + 1];
-            P.g[(size_t)o * P.ldg + col] = gv;
+            X.g[(size_t)o * X.ldg + col] = gv;
             P.C[(size_t)o * P.ldc + col] = gv + P.alpha * nh;
           }
         } else if (epi_is<EPIS>(P, EPI_GRADN)) {
-          P.g[(size_t)row * P.ldg + col] = pre1[i][j][r];
+          X.g[(size_t)row * X.ldg + col] = pre1[i][j][r];
           P.C[(size_t)row * P.ldc + col] = pre1[i][j][r] + P.alpha * v;
+        } else if (epi_is<EPIS>(P, EPI_STORE_T)) {
+          const float o = P.alpha * v;
+          P.C[(size_t)row * P.ldc + col] = o;
+          P.C[(size_t)P.ct_off + (size_t)col * P.ldc + row] = o;
         } else if (epi_is<EPIS>(P, EPI_PARTIAL)) {
           P.C[(size_t)z * P.M * P.N + (size_t)row * P.N + col] = v;
         } else if (epi_is<EPIS>(P, EPI_SCALED)) {
@@ -576,11 +579,11 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
           if (row == col) tsum += o;
         }
       }
-  if (epi_is<EPIS>(P, EPI_SCALED) && P.g != nullptr && tm == tn) {
+  if (epi_is<EPIS>(P, EPI_SCALED) && X.g != nullptr && tm == tn) {
     // the diagonal of a tile on the diagonal: one atomic per wave
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) tsum += __shfl_xor(tsum, off);
-    if (lane == 0) atomicAdd(P.g, tsum);
+    if (lane == 0) atomicAdd(X.g, tsum);
   }
   if (dot) {
     // Row sums over this wave's columns, reduced across the 16 lanes of a row
@@ -595,11 +598,11 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
         v += __shfl_xor(v, 4);
         v += __shfl_xor(v, 8);
         const int row = m0 + wm * G::WT + i * 16 + 4 * (lane >> 4) + r;
-        if ((lane & 15) == 0 && row < P.M) P.dotp[(size_t)row * P.ld_dotp + 2 * tn + wn] = v;
+        if ((lane & 15) == 0 && row < P.M) X.dotp[(size_t)row * X.ld_dotp + 2 * tn + wn] = v;
       }
   }
   if (absr) {  // the same for the sums of |C| (a wave left of abs_col0 writes 0)
-    const int pc = 2 * (tn - P.abs_col0 / T) + wn;
+    const int pc = 2 * (tn - X.abs_col0 / T) + wn;
 #pragma unroll
     for (int i = 0; i < IB; ++i)
 #pragma unroll
@@ -610,7 +613,7 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
         v += __shfl_xor(v, 4);
         v += __shfl_xor(v, 8);
         const int row = m0 + wm * G::WT + i * 16 + 4 * (lane >> 4) + r;
-        if ((lane & 15) == 0 && row < P.M) P.absp[(size_t)row * P.ld_absp + pc] = v;
+        if ((lane & 15) == 0 && row < P.M) X.absp[(size_t)row * X.ld_absp + pc] = v;
       }
   }
   LST_MARK(4);

@@ -359,6 +359,7 @@ constexpr int kLaunch2Stages64 = 4;
 // owner in launch 3; at most m K / kHotMinSlots rows qualify, which sizes
 // their list.
 constexpr int kHotMinSlots = 64;
+static_assert(kHotMinSlots <= kSlotCap + 1, "rows scattered in launch 3 must fit their slot list");
 
 // Launch `phase` (PH_LAUNCH1 .. PH_LAUNCH4) of the minibatch step: one grid for
 // all of its tasks, or with split tasks one launch per task, in task order
@@ -463,12 +464,13 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     const int nst = scratch ? 2 : 3;
     p1 = gemm_problem(L_NT, m, nst * d + m, d, vmat(H, d, m),
                       vmat2(s->state, d, nst * d, H, d, m), s->Z0, s->ld0, 1.f, 0.f, EPI_STORE);
-    p1.dotp = s->c1p; p1.ld_dotp = s->n_c1p; p1.dot_ncols = d;  // h_i^T H^_i partials
+    GemmExtras& x1 = L.gemm.x;
+    x1.dotp = s->c1p; x1.ld_dotp = s->n_c1p; x1.dot_ncols = d;  // h_i^T H^_i partials
     if (!scratch) {
-      p1.absp = s->hap; p1.ld_absp = c.n_hap; p1.abs_col0 = 3 * d;  // |H^T H| row partials
+      x1.absp = s->hap; x1.ld_absp = c.n_hap; x1.abs_col0 = 3 * d;  // |H^T H| row partials
     }
     p1.tile = t1;
-    p1.dot_h = H; p1.ld_doth = d;
+    x1.dot_h = H; x1.ld_doth = d;
     L.lk = 1;
     L.timing_slot = 0;
     OK_OR_RETURN(run_launch(s, c, L,
@@ -490,23 +492,23 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
       L.kind[0] = TK_GEMM; L.kind[1] = TK_YY; L.kind[2] = TK_SCALARS;
     }
     GemmBatch& g = L.gemm;
-    g.np = 4;
+    g.np = 3;
     g.p[0] = gemm_problem(L_NN, m, d, d, vmat(s->G, d, m), vmat(c.U, d, d), s->Yh, d, 1.f, 0.f,
                           EPI_STORE);
-    // C1, C2 and C2^T go into NP = [C1 | C2 | C2^T | Y^T Y] (row stride 4m)
+    // C1, C2 and C2^T go into NP = [C1 | C2 | C2^T | Y^T Y] (row stride 4m); C2^T is
+    // stored by C2's tiles
     g.p[1] = gemm_problem(L_NT, m, m, d, vmat(H, d, m), vmat(Hh, s->ld0, m), s->NP, 4 * m, 1.f,
                           0.f, EPI_STORE);
     g.p[2] = gemm_problem(L_NT, m, m, d, vmat(UH, s->ld0, m), vmat(s->G, d, m), s->NP + m, 4 * m,
-                          1.f, 0.f, EPI_STORE);
-    g.p[3] = gemm_problem(L_NT, m, m, d, vmat(s->G, d, m), vmat(UH, s->ld0, m), s->NP + 2 * m,
-                          4 * m, 1.f, 0.f, EPI_STORE);
+                          1.f, 0.f, EPI_STORE_T);
+    g.p[2].ct_off = m;
     // m > 128: K (d) is long and 64 x 64 tiles fetch half the bytes per
     // output of 32 x 32 ones; with up to 9 stages all of K is in flight.  N is
     // formed before launch 3 from C2 itself, so C2^T is not computed, and the
     // symmetric C1 = H^T Q H runs on its upper-triangle tiles only.
     if (m > 128) {
-      g.np = 3;
       g.p[1].epi = EPI_SYM;
+      g.p[2].epi = EPI_STORE;
       for (int q = 0; q < g.np; ++q) g.p[q].tile = 64;
     }
     L.lk = 2;
@@ -539,8 +541,9 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
       pt = gemm_problem(L_NN, 2 * m, d, 2 * m, vmat(s->NP, 2 * m, 2 * m),
                         vmat2(s->aH, d, m, s->bH, d, m), s->T, d, -0.5f * lr, 0.f, EPI_GRADT);
     }
-    pt.e1 = Hh; pt.lde1 = s->ld0; pt.e2 = s->Yh; pt.lde2 = d;
-    pt.s1 = s->a; pt.s2 = s->b; pt.g = grad_H; pt.ldg = d;
+    GemmExtras& xt = g.x;
+    xt.e1 = Hh; xt.lde1 = s->ld0; xt.e2 = s->Yh; xt.lde2 = d;
+    xt.s1 = s->a; xt.s2 = s->b; xt.g = grad_H; xt.ldg = d;
     pt.tile = 32;
     L.lk = hot ? 6 : 3;
     L.timing_slot = 2;
@@ -761,7 +764,7 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       (rc = dalloc(s, &s->solve_ws, solve_workspace_floats(m, d))) ||
       (rc = dalloc(s, &s->ex_row, (size_t)m * K)) || (rc = dalloc(s, &s->ex_val, (size_t)m * K)) ||
       (rc = dalloc(s, &s->ex_cnt, m)) || (rc = dalloc(s, &s->hkey, hsize)) ||
-      (rc = dalloc(s, &s->hmin, hsize)) ||
+      (rc = dalloc(s, &s->hmin, (size_t)hsize * (1 + kSlotCap))) ||
       (rc = dalloc(s, &s->hcnt, hsize + 1 + (size_t)m * K / kHotMinSlots)) ||
       (rc = dalloc(s, &s->touched, (size_t)m * K)) ||
       (rc = dalloc(s, &s->own, (size_t)m * K)) || (rc = dalloc(s, &s->count, 1)) ||

@@ -25,12 +25,12 @@ enum {
 // virtual matrix lives in block b with r0[b] <= r < r0[b+1].  An optional
 // per-row scale multiplies every element of a row as it is loaded.
 struct VMat {
-  const float* p[4];
-  int ld[4];
-  int r0[5];
+  const float* p[2];
+  const float* rscale;  // per-row scale or nullptr
+  int ld[2];
+  int r1;               // first row of block 1 (nb == 2)
   int nb;
   int vec;              // 1: every block has ld % 4 == 0 and a 16-byte aligned base
-  const float* rscale;  // per-row scale or nullptr
 };
 
 enum Epi {
@@ -44,8 +44,11 @@ enum Epi {
   EPI_SCALED = 4,   // C = alpha * p * acc + beta * C with p = 2^(-2 ilogb(*s1)) (p = 1 when s1
                     // is null or *s1 is not positive and finite); with g non-null the diagonal
                     // of C is also added into *g (atomically: only its exponent is used)
-  EPI_GRADN = 5     // g = s1[i]*E1[i][c] + s2[i]*E2[i][c]; G[i][c] = g; C[i][c] = g + alpha*acc[i][c]
+  EPI_GRADN = 5,    // g = s1[i]*E1[i][c] + s2[i]*E2[i][c]; G[i][c] = g; C[i][c] = g + alpha*acc[i][c]
+  EPI_STORE_T = 6   // C[r][c] = alpha*acc and its transpose at C + ct_off: C[ct_off + c*ldc + r]
 };
+// s1, s2, E1, E2, G (and the row sums of EPI_STORE) are the batch's extras
+// (GemmExtras): only batches of one problem use them.
 
 // Layouts of C = op(A) op(B):  M x K times K x N.
 enum Layout {
@@ -54,37 +57,43 @@ enum Layout {
   L_TN = 2    // A rows are K (M contiguous), B rows are K (N contiguous)
 };
 
-struct GemmProblem {
+struct alignas(64) GemmProblem {  // whole kernel-argument cache lines each
   int M, N, K;
   int a_kc, b_kc;   // 1: the operand's rows are the output dimension (K contiguous)
-  VMat A, B;
-  float* C;
   int ldc;
   float alpha, beta;
   int epi;
   int ksplit;       // EPI_PARTIAL: number of K slices (>= 1)
   int tile;         // step GEMMs: output tile edge, 32 or 64 (0: 32)
   int tiles_m, tiles_n, tile_begin;
-  // EPI_GRADT operands
-  const float* e1; int lde1;
-  const float* e2; int lde2;
+  int ct_off;       // EPI_STORE_T: offset of the transpose from C
+  VMat A, B;
+  float* C;
+};
+
+// Epilogue operands that only a batch of one problem uses (its p[0]).
+struct GemmExtras {
+  // EPI_GRADT / EPI_GRADN (and s1, g of EPI_SCALED)
+  const float* e1;
+  const float* e2;
   const float* s1;
   const float* s2;
-  float* g; int ldg;
+  float* g;
   // EPI_STORE only: per-row partial dot products of the first dot_ncols
   // output columns with dot_h (same row and column), one per (tile column,
   // wave column): dotp[row * ld_dotp + 2 * tile_n + wave_n].
-  float* dotp; int ld_dotp;
-  int dot_ncols;
-  const float* dot_h; int ld_doth;
+  float* dotp;
+  const float* dot_h;
   // EPI_STORE only: per-row partial sums of |C| over the output columns
   // >= abs_col0, one per (tile column, wave column) from the tile column
   // abs_col0 / tile on: absp[row * ld_absp + 2 * (tile_n - abs_col0 / tile) + wave_n].
-  float* absp; int ld_absp;
-  int abs_col0;
+  float* absp;
+  int lde1, lde2, ldg;
+  int ld_dotp, dot_ncols, ld_doth;
+  int ld_absp, abs_col0;
 };
 
-constexpr int kMaxProblems = 4;
+constexpr int kMaxProblems = 3;
 
 struct GemmBatch {
   // Header first: a block finds its problem and its options from these
@@ -99,6 +108,7 @@ struct GemmBatch {
   const int* skip_if;          // nonzero *skip_if: every block returns at once
   const int* run_if;           // zero *run_if: every block returns at once
   const int* skip_updates_if;  // nonzero: blocks of problems >= first_update return at once
+  GemmExtras x;                // with np == 1: the extra operands of p[0]'s epilogue
   GemmProblem p[kMaxProblems];
 };
 
@@ -119,6 +129,22 @@ hipError_t gemm_splitk_reduce(const float* ws, int splits, int M, int N, float* 
 
 // ------------------------------------------------------------ the step
 // Everything the tasks of one factored step read or write (device pointers).
+// Slots of a row that its hash entry lists (a row held by more is found by
+// searching the examples' target lists instead).
+constexpr int kSlotCap = 64;
+
+// Slots per scatter wave: one while a step has at most kScatterOneSlot slots;
+// above, about kScatterWaves waves, few enough to be resident together beside
+// launch 3's tiles, so that the step's slots are looked up in one pass of
+// memory latency instead of one per round of workgroups.
+constexpr int kScatterOneSlot = 2048;
+constexpr int kScatterWaves = 1024;
+__host__ __device__ inline int scatter_slots_per_wave(int slots) {
+  if (slots <= kScatterOneSlot) return 1;
+  const int s = (slots + kScatterWaves - 1) / kScatterWaves;
+  return s > 64 ? 64 : s;
+}
+
 struct StepCtx {
   int m, K, d;
   // rows held by hot_min or more slots (hot_min 0: none) are not scattered by
@@ -152,7 +178,9 @@ struct StepCtx {
   int *hkey, *hmin, *hcnt;  // hash table of the step's target rows: smallest slot
                             // and number of slots of each; hcnt's 2^hbits counts
                             // are followed by the hot-row list ([0]: count, then rows)
-  int hbits;
+  int hbits;   // hmin's 2^hbits entries are followed by 2^hbits x kSlotCap more: the
+               // slots of each row, in no particular order (the first kSlotCap of
+               // them; entries past the row's count are stale)
   int* own;      // m x K: the row of slot i*K + k if that slot owns the row's
                  // scatter in this step (its smallest slot), else -1
   int* flags;

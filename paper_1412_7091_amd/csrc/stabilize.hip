@@ -287,8 +287,8 @@ hipError_t tile_product(const StabArgs& a, int layout, const float* A, const flo
   L.gemm.skip_if = stop;
   GemmProblem& p = L.gemm.p[0];
   p = gemm_problem(layout, d, d, d, vmat(A, d, d), vmat(B, d, d), C, d, alpha, beta, EPI_SCALED);
-  p.s1 = scale_in;
-  p.g = trace_out;
+  L.gemm.x.s1 = scale_in;
+  L.gemm.x.g = trace_out;
   p.tile = 32;
   int stages = (d + 63) / 64;  // every K chunk resident when it fits
   if (stages > 9) stages = 9;

@@ -42,6 +42,7 @@ __device__ __forceinline__ unsigned row_hash(int r, int bits) {
 
 // The hot-row list, stored after the hash table's slot counts.
 __device__ __forceinline__ int* hot_list(const StepCtx& c) { return c.hcnt + (1 << c.hbits); }
+__device__ __forceinline__ int* hslot_of(const StepCtx& c) { return c.hmin + (1 << c.hbits); }
 
 // c1 = h_i^T Q h_i: the partial sums left by the first product of the step,
 // added in index order (the same bits wherever it is evaluated).
@@ -393,8 +394,11 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
   if (i >= c.m) return;
   const int lane = lane_id(), d = c.d;
   // Record, for every target row, the smallest slot i*K + k holding it (the
-  // owner of the row's scatter in launch 3) and the number of slots holding it:
-  // open addressing, at most half full.
+  // owner of the row's scatter in launch 3), the number of slots holding it and
+  // (the first kSlotCap of) those slots: open addressing, at most half full.
+  // The list entry of a lane's first slot is written at the end of the task,
+  // so that waiting for its position overlaps the rest of the work.
+  int first_at = -1, first_slot = 0;
   {
     const int mask = (1 << c.hbits) - 1;
     for (int k = lane; k < c.K; k += 64) {
@@ -406,7 +410,13 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
         const int prev = atomicCAS(c.hkey + h, -1, r);
         if (prev == -1 || prev == r) {
           atomicMin(c.hmin + h, slot);
-          atomicAdd(c.hcnt + h, 1);
+          const int pos = atomicAdd(c.hcnt + h, 1);
+          if (k == lane) {
+            first_at = pos < kSlotCap ? (int)h * kSlotCap + pos : -1;
+            first_slot = slot;
+          } else if (pos < kSlotCap) {
+            hslot_of(c)[(size_t)h * kSlotCap + pos] = slot;
+          }
           break;
         }
         h = (h + 1) & mask;
@@ -468,6 +478,7 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
       }
     }
   }
+  if (first_at >= 0) hslot_of(c)[first_at] = first_slot;
   if (lane != 0) return;
   c.loss[i] = L;
   c.a[i] = a;
@@ -1368,162 +1379,179 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
 // ----------------------------------------------------------------- scatter
 // Step 9: V[r, :] += sum over the examples j whose target holds row r of
 // c_j X[j, :], c_j = -(sum of j's values at r) (squared) or cs_j (spherical),
-// in increasing j.  One wave per (example, slot) pair; only the pair with the
-// smallest slot of its row (read from the hash table) does the work, so every
-// row is written once and in a fixed order.  Each pair records in own[] the
-// row it owns (or -1); launch 4 clears the hash slots from that record.
-constexpr int kScatterSlotsPerWave = 1;
+// in increasing j.  Only the slot (example i, pair k; index i K + k) with the
+// smallest index of its row, read from the hash table, does the row's work, so
+// every row is written once and in a fixed order.  Each slot records in own[]
+// the row it owns (or -1); launch 4 clears the hash slots from that record.
+//
+// A row held by one slot is written kScatterRows at a time, with all their
+// rows of X and V in flight before the first is added.  A row held by several
+// slots reads their list from its hash entry, sorts it into slot order and
+// adds the examples' rows of X in that order, 16 in flight; a row held by
+// more than kSlotCap slots searches the examples' sorted target lists instead
+// (kScatterBatch rows in flight).
 constexpr int kScatterBatch = 4;
+constexpr int kScatterRows = 8;
 
-template <bool HOT>
-__device__ __forceinline__ void scatter_slot(const StepCtx& c, int e);
-
-// A wave handles kScatterSlotsPerWave consecutive slots in turn (few blocks,
-// so that they share the launch's compute units with the GEMM tiles).  With
-// HOT the owners of rows held by c.hot_min or more slots list them instead.
-template <bool HOT>
-__device__ __forceinline__ void task_scatter(const StepCtx& c, int local) {
-  const int e0 = (local * 4 + wave_id()) * kScatterSlotsPerWave;
-  for (int u = 0; u < kScatterSlotsPerWave; ++u)
-    if (e0 + u < c.m * c.K) scatter_slot<HOT>(c, e0 + u);
+// The value of x in lane src (the same src in every lane): a scalar read of
+// the lane, not a cross-lane shuffle through LDS.
+__device__ __forceinline__ int from_lane(int x, int src) {
+  return __builtin_amdgcn_readlane(x, src);
+}
+__device__ __forceinline__ float from_lane(float x, int src) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), src));
 }
 
-template <bool HOT>
-__device__ __forceinline__ void scatter_slot(const StepCtx& c, int e) {
+// Ascending sort of one int per lane across the wave (bitonic network).
+__device__ __forceinline__ int wave_sort_asc(int x) {
   const int lane = lane_id();
-  const int i = e / c.K;
-  const int r = c.idx[e];
-  bool owner = false;
-  unsigned h = 0;
-  if (r >= 0 && (int64_t)r < c.D) {
-    const int mask = (1 << c.hbits) - 1;
-    h = row_hash(r, c.hbits);
-    int probe = 0;
-    while (probe <= mask && c.hkey[h] != r) {
-      h = (h + 1) & mask;
-      ++probe;
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const int o = __shfl_xor(x, j);
+      const bool up = (lane & k) == 0, low = (lane & j) == 0;
+      x = (low == up) ? min(x, o) : max(x, o);
     }
-    owner = probe <= mask && c.hmin[h] == e;
-  }
-  if (lane == 0) c.own[e] = owner ? r : -1;
-  if (!owner || c.flags[F_ERR]) return;
-  const bool one_hot = c.loss_kind == LST_LOSS_SPHERICAL;
-  const bool vec = (c.d % 4 == 0);
-  // slots holding r in this step: the examples are searched only until all
-  // have been met, and a row held by this slot alone takes its example's row
-  // of X directly (the same sum as the search would form: one term)
-  const int cnt = c.hcnt[h];
-  if constexpr (HOT) {
-    if (cnt >= c.hot_min) {
-      if (lane == 0) {
-        int* hot = hot_list(c);
-        hot[1 + atomicAdd(hot, 1)] = r;
+  return x;
+}
+
+// acc (columns cg + 256 q + 4 lane, q < NQ) += w_l X[j_l, :] over the lanes l
+// set in bal, in lane order; with d % 4 == 0, B rows of X in flight at a time
+// (a row of a common target, in nearly every example, would otherwise pay the
+// memory latency once per example).
+template <int NQ, int B>
+__device__ __forceinline__ void add_x_rows(const StepCtx& c, int cg, unsigned long long bal,
+                                           float w_l, int j_l, float4 (&acc)[4]) {
+  const int lane = lane_id();
+  if (c.d % 4 == 0) {
+    while (bal) {
+      float w[B];
+      float4 x[B][NQ];
+      bool on[B];
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        on[u] = bal != 0;
+        const int src = on[u] ? __ffsll((long long)bal) - 1 : 0;
+        bal &= bal - 1;
+        w[u] = from_lane(w_l, src);
+        const int j = from_lane(j_l, src);
+        const float* xr = c.X + (size_t)j * c.d;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+          const int col = cg + q * 256 + lane * 4;
+          if (on[u] && col < c.d) x[u][q] = *reinterpret_cast<const float4*>(xr + col);
+        }
       }
-      return;
-    }
-  }
-  if (cnt == 1 && vec) {
-    const float w = one_hot ? c.cs[i] : -c.val[e];
-    const float* xr = c.X + (size_t)i * c.d;
-    float* vr = c.V + (size_t)r * c.d;
-    for (int col = 4 * lane; col < c.d; col += 256) {
-      const float4 x = *reinterpret_cast<const float4*>(xr + col);
-      float4 v = *reinterpret_cast<float4*>(vr + col);
-      v.x += 0.f + w * x.x; v.y += 0.f + w * x.y; v.z += 0.f + w * x.z; v.w += 0.f + w * x.w;
-      *reinterpret_cast<float4*>(vr + col) = v;
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        if (!on[u]) break;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+          const int col = cg + q * 256 + lane * 4;
+          if (col >= c.d) continue;
+          acc[q].x += w[u] * x[u][q].x; acc[q].y += w[u] * x[u][q].y;
+          acc[q].z += w[u] * x[u][q].z; acc[q].w += w[u] * x[u][q].w;
+        }
+      }
     }
     return;
   }
-  // columns in groups of 1024 (four 256-column chunks held in registers)
-  for (int cg = 0; cg < c.d; cg += 1024) {
+  while (bal) {
+    const int src = __ffsll((long long)bal) - 1;
+    bal &= bal - 1;
+    const float w = from_lane(w_l, src);
+    const float* xr = c.X + (size_t)from_lane(j_l, src) * c.d;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int col = cg + q * 256 + lane * 4;
+      if (col >= c.d) continue;
+      acc[q].x += w * xr[col];
+      if (col + 1 < c.d) acc[q].y += w * xr[col + 1];
+      if (col + 2 < c.d) acc[q].z += w * xr[col + 2];
+      if (col + 3 < c.d) acc[q].w += w * xr[col + 3];
+    }
+  }
+}
+
+// The row r held by cnt slots, owned by slot e (hash entry h): the whole wave.
+__device__ __forceinline__ void scatter_row(const StepCtx& c, int r, int h, int cnt, int e) {
+  const int lane = lane_id();
+  const bool one_hot = c.loss_kind == LST_LOSS_SPHERICAL;
+  const bool listed = cnt <= kSlotCap;
+  // listed: lane l < cnt holds the l-th slot of the row in slot order; the
+  // first lane of each example's run carries that example and its c_j
+  float cj = 0.f;
+  int jl = 0;
+  unsigned long long lead = 0;
+  if (listed) {
+    const bool in = lane < cnt;
+    const int sl = wave_sort_asc(in ? hslot_of(c)[(size_t)h * kSlotCap + lane] : 0x7fffffff);
+    jl = in ? sl / c.K : -1;
+    const float v = (in && !one_hot) ? c.val[sl] : 0.f;
+    const int jp = __shfl_up(jl, 1);
+    const bool leader = in && (lane == 0 || jp != jl);
+    // the values of a run, added in slot order by its first lane
+    float sum = v;
+    bool more = leader;
+    for (int t = 1; t < 64 && __ballot(more) != 0; ++t) {
+      const float vt = __shfl_down(v, t);
+      const int jt = __shfl_down(jl, t);
+      more = more && lane + t < cnt && jt == jl;
+      if (more) sum += vt;
+    }
+    if (leader) cj = one_hot ? c.cs[jl] : -sum;
+    lead = __ballot(leader);
+  }
+  const int i = e / c.K;
+  // columns in groups of 512 (listed: 16 rows of X in flight) or 1024 (the
+  // search, done once per group)
+  const int gcols = listed ? 512 : 1024;
+  for (int cg = 0; cg < c.d; cg += gcols) {
     float4 acc[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) acc[q] = make_float4(0.f, 0.f, 0.f, 0.f);
-    int met = 0;
-    for (int j0 = i; j0 < c.m && met < cnt; j0 += 64) {
-      const int j = j0 + lane;
-      float cj = 0.f;
-      bool found = false;
-      int nrun = 0;
-      if (j < c.m) {
-        const int* rows = c.ex_row + (size_t)j * c.K;
-        const float* vals = c.ex_val + (size_t)j * c.K;
-        const int n = c.ex_cnt[j];
-        int lo = 0, hi = n;
-        while (lo < hi) {
-          const int mid = (lo + hi) >> 1;
-          if (rows[mid] < r) lo = mid + 1; else hi = mid;
-        }
-        float sum = 0.f;
-        while (lo < n && rows[lo] == r) {
-          sum += vals[lo];
-          ++lo;
-          ++nrun;
-          found = true;
-        }
-        cj = one_hot ? c.cs[j] : -sum;
-      }
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) nrun += __shfl_xor(nrun, off);
-      met += nrun;
-      unsigned long long bal = __ballot(found);
-      if (vec) {
-        // kScatterBatch examples at a time: their rows of X are all in flight
-        // before the first is added (a row of a common target, in nearly every
-        // example, would otherwise pay the memory latency once per example);
-        // the additions keep increasing example order.
-        while (bal) {
-          float w[kScatterBatch];
-          float4 x[kScatterBatch][4];
-          bool on[kScatterBatch];
-#pragma unroll
-          for (int u = 0; u < kScatterBatch; ++u) {
-            on[u] = bal != 0;
-            const int src = on[u] ? __ffsll((long long)bal) - 1 : 0;
-            bal &= bal - 1;
-            w[u] = __shfl(cj, src);
-            const float* xr = c.X + (size_t)(j0 + src) * c.d;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int col = cg + q * 256 + lane * 4;
-              if (col < c.d) x[u][q] = *reinterpret_cast<const float4*>(xr + col);
-            }
+    if (listed) {
+      add_x_rows<2, 16>(c, cg, lead, cj, jl, acc);
+    } else {
+      // examples i, i + 1, ... (i holds the row's smallest slot), 64 at a
+      // time, until all cnt slots have been met
+      int met = 0;
+      for (int j0 = i; j0 < c.m && met < cnt; j0 += 64) {
+        const int j = j0 + lane;
+        float cw = 0.f;
+        bool found = false;
+        int nrun = 0;
+        if (j < c.m) {
+          const int* rows = c.ex_row + (size_t)j * c.K;
+          const float* vals = c.ex_val + (size_t)j * c.K;
+          const int n = c.ex_cnt[j];
+          int lo = 0, hi = n;
+          while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (rows[mid] < r) lo = mid + 1; else hi = mid;
           }
-#pragma unroll
-          for (int u = 0; u < kScatterBatch; ++u) {
-            if (!on[u]) break;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int col = cg + q * 256 + lane * 4;
-              if (col >= c.d) continue;
-              acc[q].x += w[u] * x[u][q].x; acc[q].y += w[u] * x[u][q].y;
-              acc[q].z += w[u] * x[u][q].z; acc[q].w += w[u] * x[u][q].w;
-            }
+          float sum = 0.f;
+          while (lo < n && rows[lo] == r) {
+            sum += vals[lo];
+            ++lo;
+            ++nrun;
+            found = true;
           }
+          cw = one_hot ? c.cs[j] : -sum;
         }
-      }
-      while (bal) {
-        const int src = __ffsll((long long)bal) - 1;
-        bal &= bal - 1;
-        const float w = __shfl(cj, src);
-        const float* xr = c.X + (size_t)(j0 + src) * c.d;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int col = cg + q * 256 + lane * 4;
-          if (col >= c.d) continue;
-          acc[q].x += w * xr[col];
-          if (col + 1 < c.d) acc[q].y += w * xr[col + 1];
-          if (col + 2 < c.d) acc[q].z += w * xr[col + 2];
-          if (col + 3 < c.d) acc[q].w += w * xr[col + 3];
-        }
+        for (int off = 32; off > 0; off >>= 1) nrun += __shfl_xor(nrun, off);
+        met += nrun;
+        add_x_rows<4, kScatterBatch>(c, cg, __ballot(found), cw, j, acc);
       }
     }
     float* vr = c.V + (size_t)r * c.d;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int col = cg + q * 256 + lane * 4;
-      if (col >= c.d) continue;
-      if (vec) {
+      if (col >= c.d || col >= cg + gcols) continue;
+      if (c.d % 4 == 0) {
         float4 v = *reinterpret_cast<float4*>(vr + col);
         v.x += acc[q].x; v.y += acc[q].y; v.z += acc[q].z; v.w += acc[q].w;
         *reinterpret_cast<float4*>(vr + col) = v;
@@ -1534,6 +1562,139 @@ __device__ __forceinline__ void scatter_slot(const StepCtx& c, int e) {
         if (col + 3 < c.d) vr[col + 3] += acc[q].w;
       }
     }
+  }
+}
+
+// Rows held by one slot each (d % 4 == 0): V[r_l] += w_l X[i_l] for the lanes
+// l set in bal, kScatterRows rows at a time, 512 columns at a time.  The sum
+// has one term, written as the several-slot rows write theirs (0 + w x, then
+// added to V), so a row gives the same bits either way.
+__device__ __forceinline__ void scatter_single(const StepCtx& c, unsigned long long bal, int r_l,
+                                               int i_l, float w_l) {
+  const int lane = lane_id();
+  for (int cg = 0; cg < c.d; cg += 512) {
+    unsigned long long b = bal;
+    while (b) {
+      float* vr[kScatterRows];
+      float4 x[kScatterRows][2], v[kScatterRows][2];
+      int src[kScatterRows];
+      bool on[kScatterRows];
+#pragma unroll
+      for (int u = 0; u < kScatterRows; ++u) {
+        on[u] = b != 0;
+        src[u] = on[u] ? __ffsll((long long)b) - 1 : 0;
+        b &= b - 1;
+        const int ru = from_lane(r_l, src[u]), iu = from_lane(i_l, src[u]);
+        const float* xr = c.X + (size_t)iu * c.d;
+        vr[u] = c.V + (size_t)ru * c.d;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int col = cg + q * 256 + lane * 4;
+          if (on[u] && col < c.d) {
+            x[u][q] = *reinterpret_cast<const float4*>(xr + col);
+            v[u][q] = *reinterpret_cast<const float4*>(vr[u] + col);
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kScatterRows; ++u) {
+        if (!on[u]) break;
+        // the weight's load (issued before the rows') has landed by now
+        const float w = from_lane(w_l, src[u]);
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int col = cg + q * 256 + lane * 4;
+          if (col >= c.d) continue;
+          float4 o = v[u][q];
+          o.x += 0.f + w * x[u][q].x; o.y += 0.f + w * x[u][q].y;
+          o.z += 0.f + w * x[u][q].z; o.w += 0.f + w * x[u][q].w;
+          *reinterpret_cast<float4*>(vr[u] + col) = o;
+        }
+      }
+    }
+  }
+}
+
+__host__ __device__ inline int scatter_lookup_blocks(const StepCtx& c) {
+  const int spw = scatter_slots_per_wave(c.m * c.K);
+  return (c.m * c.K + 4 * spw - 1) / (4 * spw);
+}
+__host__ __device__ inline int scatter_entry_blocks(const StepCtx& c) {
+  return scatter_slots_per_wave(c.m * c.K) == 1 ? 0 : ((1 << c.hbits) + 255) / 256;
+}
+
+// Blocks [0, scatter_lookup_blocks) take scatter_slots_per_wave(m K)
+// consecutive slots per wave and look them up together; a slot that owns its
+// row records it in own[], and the rows held by one slot are written here.
+// The blocks after them take the hash entries, 64 per wave, and write the
+// rows held by several slots (with d % 4 != 0, every row): the hash spreads
+// these rows evenly over the waves, whereas the slots that own them cluster
+// in the first examples when targets repeat.  With one slot per wave (small
+// steps) there are no entry blocks and the wave writes the row its slot owns,
+// whatever the row's count.  With HOT the rows held by c.hot_min or more
+// slots are listed for launch 4 instead.
+template <bool HOT>
+__device__ __forceinline__ void task_scatter(const StepCtx& c, int local) {
+  const int lane = lane_id();
+  const int spw = scatter_slots_per_wave(c.m * c.K);
+  const int nlook = scatter_lookup_blocks(c);
+  const bool vec = c.d % 4 == 0;
+  // launches 1 and 2 set the error flag: read it while the slots are looked up
+  const int err = c.flags[F_ERR];
+  int r = -1, cnt = 0, e = 0, h = 0;
+  bool mine = false;  // this lane's row is written by scatter_row below
+  if (local >= nlook) {
+    if (err) return;
+    h = ((local - nlook) * 4 + wave_id()) * 64 + lane;
+    if (h < (1 << c.hbits)) {
+      r = c.hkey[h];
+      if (r >= 0) {
+        cnt = c.hcnt[h];
+        e = c.hmin[h];
+      }
+    }
+    mine = r >= 0 && !(cnt == 1 && vec);
+  } else {
+    e = (local * 4 + wave_id()) * spw + lane;
+    bool owner = false;
+    if (lane < spw && e < c.m * c.K) {
+      r = c.idx[e];
+      if (r >= 0 && (int64_t)r < c.D) {
+        const int mask = (1 << c.hbits) - 1;
+        unsigned hh = row_hash(r, c.hbits);
+        int probe = 0;
+        while (probe <= mask && c.hkey[hh] != r) {
+          hh = (hh + 1) & mask;
+          ++probe;
+        }
+        owner = probe <= mask && c.hmin[hh] == e;
+        if (owner) cnt = c.hcnt[hh];
+        h = (int)hh;
+      }
+      c.own[e] = owner ? r : -1;
+    }
+    if (err) return;
+    const bool single = owner && cnt == 1 && vec;
+    const unsigned long long one = __ballot(single);
+    if (one) {
+      const int i = e / c.K;
+      const float w = single ? (c.loss_kind == LST_LOSS_SPHERICAL ? c.cs[i] : -c.val[e]) : 0.f;
+      scatter_single(c, one, r, i, w);
+    }
+    mine = spw == 1 && owner && !single;
+  }
+  if constexpr (HOT) {
+    if (mine && cnt >= c.hot_min) {
+      int* hot = hot_list(c);
+      hot[1 + atomicAdd(hot, 1)] = r;
+      mine = false;
+    }
+  }
+  unsigned long long several = __ballot(mine);
+  while (several) {
+    const int src = __ffsll((long long)several) - 1;
+    several &= several - 1;
+    scatter_row(c, from_lane(r, src), from_lane(h, src), from_lane(cnt, src), from_lane(e, src));
   }
 }
 
@@ -1593,7 +1754,7 @@ __device__ __forceinline__ void scatter_hot(const StepCtx& c, int local, int nb,
           on[u] = bal != 0;
           const int src = on[u] ? __ffsll((long long)bal) - 1 : 0;
           bal &= bal - 1;
-          w[u] = __shfl(cj, src);
+          w[u] = from_lane(cj, src);
           const float* xr = c.X + (size_t)(j0 + src) * c.d;
           x[u] = make_float4(0.f, 0.f, 0.f, 0.f);
           if (on[u] && col < c.d) {
@@ -1684,7 +1845,7 @@ constexpr LaunchMasks kLaunchMasks[8] = {
     {0u, 0u, 0u, 0u},
     {(1u << TK_GEMM) | (1u << TK_TARGETS), V_NT, (1u << EPI_STORE) | (1u << EPX_ROWSUMS), TILE32},
     {(1u << TK_GEMM) | (1u << TK_SOLVE) | (1u << TK_YY) | (1u << TK_SCALARS), V_NN | V_NT,
-     1u << EPI_STORE, TILE32},
+     (1u << EPI_STORE) | (1u << EPI_STORE_T), TILE32},
     {(1u << TK_GEMM) | (1u << TK_SCATTER), V_NN, 1u << EPI_GRADT, TILE32},
     {(1u << TK_GEMM) | (1u << TK_CLEAR), V_TN, (1u << EPI_SYM) | (1u << EPI_STORE),
      TILE32 | TILE64},
@@ -1820,7 +1981,7 @@ int step_task_blocks(int kind, const StepCtx& c) {
     case TK_YY: { const int nb = (c.m + 15) / 16; return nb * (nb + 1) / 2; }
     case TK_SCALARS: return (c.m + 3) / 4;
     case TK_SOLVE: return (c.d + kSolveCols - 1) / kSolveCols;
-    case TK_SCATTER: return (c.m * c.K + 4 * kScatterSlotsPerWave - 1) / (4 * kScatterSlotsPerWave);
+    case TK_SCATTER: return scatter_lookup_blocks(c) + scatter_entry_blocks(c);
     case TK_CLEAR: return (c.m * c.K + 255) / 256;
     default: return 0;
   }
@@ -1936,10 +2097,14 @@ hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t 
     L.begin[t] = total;
     int n = 0;
     if (L.kind[t] == TK_GEMM) {
+      // the extras belong to a batch of one problem
+      const GemmExtras& x = L.gemm.x;
+      const bool rowsums = (x.dotp != nullptr || x.absp != nullptr);
+      const bool extras = rowsums || x.e1 || x.e2 || x.s1 || x.s2 || x.g;
+      if (extras && L.gemm.np != 1) return hipErrorInvalidValue;
       for (int q = 0; q < L.gemm.np; ++q) {
         const GemmProblem& p = L.gemm.p[q];
         const unsigned tbit = (p.tile == 64) ? TILE64 : (p.tile == 32 || p.tile == 0) ? TILE32 : 0u;
-        const bool rowsums = (p.dotp != nullptr || p.absp != nullptr);
         if (!(M.vars & problem_variant(p)) || !((M.epis >> p.epi) & 1u) || !(M.tiles & tbit) ||
             (rowsums && (p.epi != EPI_STORE || !((M.epis >> EPX_ROWSUMS) & 1u))))
           return hipErrorInvalidValue;

@@ -122,6 +122,22 @@ def test_hot_rows_zipf(gpu_lib, d):
     _assert(reports, W_rel)
 
 
+@pytest.mark.parametrize("m,d", [(40, 40), (40, 37), (30, 40)])
+def test_scatter_lists_and_search(gpu_lib, m, d):
+    """Zipf 1.3 targets with repeats below the hot-row threshold, at m K = 2560
+    (lookup waves plus hash-entry waves) and 1920 (one slot per wave): rows held by
+    one slot, by 2..64 slots (the hash entry lists them) and by more than 64 (the
+    examples' target lists are searched); with d = 37 every row is written from its
+    hash entry."""
+    cfg = _cfg(D=400, d=d, m=m, K=64, lr=5e-3, idx_dist="zipf", zipf_s=1.3, distinct=False,
+               dup_frac=0.3, entropy=130)
+    _, idx, _ = Workload(cfg).batch(0)
+    _, cnt = np.unique(idx[idx >= 0], return_counts=True)
+    assert cnt.max() > 64 and ((cnt > 1) & (cnt <= 64)).any() and (cnt == 1).any()
+    reports, W_rel, _ = run_parity(cfg, 3, V_check_untouched=True)
+    _assert(reports, W_rel)
+
+
 def test_single_example(gpu_lib):
     cfg = _cfg(D=300, d=16, m=1, K=4, lr=2e-2, entropy=103)
     reports, W_rel, _ = run_parity(cfg, 30)
