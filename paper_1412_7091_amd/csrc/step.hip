@@ -640,10 +640,44 @@ __device__ __forceinline__ bool neumann_done(const float* red, int it, float sto
 // once; only the B fragment, read from Y_k in LDS, waits for the barrier that
 // ends an iteration.  Columns k >= m of H^T H are read at a clamped position:
 // they meet rows of Y_k that are zero.  Returns the buffer holding the result.
+//
+// r = ||E||_inf is formed from the absolute row sums of H^T H that the first
+// iteration accumulates from the fragments it multiplies (every block
+// streams all of H^T H in the same order, so all find the same r).  With r
+// known the series is capped (r^(k+1) / (1 - r) <= 2^-20) and the adaptive
+// stop applies; r >= 1/2 (or not finite) ends it at once, and the caller
+// then runs Gauss-Jordan instead.
+constexpr int kNeumannMaxIters = 64;
+
+// The iteration cap for r (as many iterations as the a-priori bound needs,
+// at least the one already run).
+__device__ __forceinline__ int neumann_cap(float r) {
+  if (!(r > 0.f)) return 1;
+  const float need = logf(kNeumannTol * (1.f - r)) / logf(r);
+  return max(1, min(kNeumannMaxIters, (int)ceilf(need) - 1));
+}
+
+// The wave's absolute row sums (one per lane & 15 and row block, lanes that
+// share a row hold the same sum after the fold) times 1/c, maximised over the
+// wave's valid rows and posted to red[8 + wave]; NaN counts as infinite.
+__device__ __forceinline__ void neumann_post_r(float* red, float rw) {
+  rw = (rw == rw) ? rw : INFINITY;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) rw = fmaxf(rw, __shfl_xor(rw, off));
+  if (lane_id() == 0) red[8 + wave_id()] = rw;
+}
+__device__ __forceinline__ float neumann_read_r(const float* red) {
+  return fmaxf(fmaxf(red[8], red[9]), fmaxf(red[10], red[11]));
+}
+__device__ __forceinline__ float row_abs_fold(float v) {
+  v += __shfl_xor(v, 16);
+  return v + __shfl_xor(v, 32);
+}
+
 template <int RBW>
 __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int ldh, int m, int mp,
-                                              int iters, int LDE, const float* cinv, float* Yo,
-                                              float* Yn, float* red, float stop_k) {
+                                              int LDE, const float* cinv, float* Yo, float* Yn,
+                                              float* red, float& r) {
   constexpr int NB = 3;
   const int lane = lane_id(), wave = __builtin_amdgcn_readfirstlane(wave_id());
   const int nsl = mp / 16, nrb = mp / 16;
@@ -675,13 +709,17 @@ __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int 
 #pragma unroll
   for (int t = 0; t < RBW; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   const int yl = (lane & 15) * LDE + kl;
-  int total = iters * nsl;  // cut short once the series has converged
+  int total = kNeumannMaxIters * nsl;  // capped once r is known, cut short at convergence
   int sl = 0;               // slice of the next MFMAs
   int it = 0;               // iterations completed
   floatx4 prev[RBW];        // diag(1/c) (H^T H) Y_{k-1} of the wave's rows (Y_0 = B: zero)
-  float bcol = 0.f;
+  float rs[RBW];            // first iteration: absolute row sums of the wave's rows (partial)
+  float bcol = 0.f, stop_k = 0.f;
 #pragma unroll
-  for (int t = 0; t < RBW; ++t) prev[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < RBW; ++t) {
+    prev[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    rs[t] = 0.f;
+  }
   for (int g0 = 0; g0 < total; g0 += NB) {
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
@@ -696,6 +734,12 @@ __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int 
 #pragma unroll
           for (int t = 0; t < RBW; ++t)
             acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[j][t][q], fb[q], acc[t], 0, 0, 0);
+        if (it == 0 && sl * 16 + kl < m) {
+#pragma unroll
+          for (int t = 0; t < RBW; ++t)
+            rs[t] += (fabsf(fa[j][t][0]) + fabsf(fa[j][t][1])) +
+                     (fabsf(fa[j][t][2]) + fabsf(fa[j][t][3]));
+        }
         if (++sl == nsl) {
           // Y_{k+1} rows of the wave's blocks
           sl = 0;
@@ -703,6 +747,16 @@ __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int 
 #pragma unroll
           for (int t = 0; t < RBW; ++t)
             cv[t] = *reinterpret_cast<const floatx4*>(cinv + min(wave + 4 * t, nrb - 1) * 16 + kl);
+          if (it == 0) {
+            float rw = 0.f;
+#pragma unroll
+            for (int t = 0; t < RBW; ++t) {
+              const float sum = row_abs_fold(rs[t]);
+              const int row = (wave + 4 * t) * 16 + (lane & 15);
+              if (row < m) rw = fmaxf(rw, (sum == sum) ? sum * cinv[row] : INFINITY);
+            }
+            neumann_post_r(red, rw);
+          }
           float dl = 0.f, bl = 0.f;
 #pragma unroll
           for (int t = 0; t < RBW; ++t) {
@@ -724,6 +778,12 @@ __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int 
           float* tt = Yo;
           Yo = Yn;
           Yn = tt;
+          if (it == 0) {
+            r = neumann_read_r(red);
+            stop_k = r / (1.f - r);
+            if (!(r < 0.5f)) total = g0 + j + 1;  // the caller falls back
+            else total = min(total, neumann_cap(r) * nsl);
+          }
           if (neumann_done(red, it, stop_k, bcol)) total = g0 + j + 1;
           ++it;
         }
@@ -739,9 +799,8 @@ __device__ __forceinline__ float* neumann_mem(const float* __restrict__ HH, int 
 // accumulators are those of four blocks: the kernel then needs at most 256
 // VGPRs and two workgroups share a compute unit.
 __device__ __forceinline__ float* neumann_mem_two_pass(const float* __restrict__ HH, int ldh, int m,
-                                                       int mp, int iters, int LDE,
-                                                       const float* cinv, float* Yo, float* Yn,
-                                                       float* red, float stop_k) {
+                                                       int mp, int LDE, const float* cinv,
+                                                       float* Yo, float* Yn, float* red, float& r) {
   constexpr int NB = 3, RB = 4;
   const int lane = lane_id(), wave = __builtin_amdgcn_readfirstlane(wave_id());
   const int nsl = mp / 16, nrb = mp / 16;
@@ -780,15 +839,17 @@ __device__ __forceinline__ float* neumann_mem_two_pass(const float* __restrict__
 #pragma unroll
   for (int t = 0; t < RB; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   const int yl = (lane & 15) * LDE + kl;
-  int total = iters * 2 * nsl;  // cut short once the series has converged
+  int total = kNeumannMaxIters * 2 * nsl;  // capped once r is known, cut short at convergence
   int sl = 0, ps = 0;           // slice and pass of the next MFMAs
   int it = 0;                   // iterations completed
   floatx4 prev0[RB], prev1[RB];  // diag(1/c) (H^T H) Y_{k-1} of the wave's rows
-  float bcol = 0.f, dl = 0.f, bl = 0.f;
+  float rs[RB];                  // first iteration: absolute row sums of the pass's rows (partial)
+  float bcol = 0.f, dl = 0.f, bl = 0.f, rw = 0.f, stop_k = 0.f;
 #pragma unroll
   for (int t = 0; t < RB; ++t) {
     prev0[t] = floatx4{0.f, 0.f, 0.f, 0.f};
     prev1[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    rs[t] = 0.f;
   }
   for (int g0 = 0; g0 < total; g0 += NB) {
 #pragma unroll
@@ -803,9 +864,25 @@ __device__ __forceinline__ float* neumann_mem_two_pass(const float* __restrict__
 #pragma unroll
           for (int t = 0; t < RB; ++t)
             acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[j][t][q], fb[q], acc[t], 0, 0, 0);
+        if (it == 0 && sl * 16 + kl < m) {
+#pragma unroll
+          for (int t = 0; t < RB; ++t)
+            rs[t] += (fabsf(fa[j][t][0]) + fabsf(fa[j][t][1])) +
+                     (fabsf(fa[j][t][2]) + fabsf(fa[j][t][3]));
+        }
         if (++sl == nsl) {
           // Y_{k+1} rows of the pass's blocks
           sl = 0;
+          if (it == 0) {
+#pragma unroll
+            for (int t = 0; t < RB; ++t) {
+              const float sum = row_abs_fold(rs[t]);
+              const int row = (wave + 16 * ps + 4 * t) * 16 + (lane & 15);
+              if (row < m) rw = fmaxf(rw, (sum == sum) ? sum * cinv[row] : INFINITY);
+              rs[t] = 0.f;
+            }
+            if (ps) neumann_post_r(red, rw);
+          }
 #pragma unroll
           for (int t = 0; t < RB; ++t) {
             const int rb = wave + 16 * ps + 4 * t;
@@ -834,6 +911,12 @@ __device__ __forceinline__ float* neumann_mem_two_pass(const float* __restrict__
             float* tt = Yo;
             Yo = Yn;
             Yn = tt;
+            if (it == 0) {
+              r = neumann_read_r(red);
+              stop_k = r / (1.f - r);
+              if (!(r < 0.5f)) total = g0 + j + 1;  // the caller falls back
+              else total = min(total, neumann_cap(r) * 2 * nsl);
+            }
             if (neumann_done(red, it, stop_k, bcol)) total = g0 + j + 1;
             ++it;
             dl = 0.f;
@@ -879,6 +962,11 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   // slot s ^ (j & hsw) (bank-conflict-free reads down a column and across 16
   // rows); rows and columns beyond m are zero.
   const int hsw = (mp % 32 == 0) ? 7 : 3;  // the XOR must stay inside a row's mp/4 slots
+  // m > 128 with m % 4 == 0 and 16-byte aligned rows of H^T H and P: vector
+  // loads (the right-hand side and the iterations), and r is found by the
+  // first iteration instead of from the partials
+  const bool gvec = !SMALL && m % 4 == 0 && d % 4 == 0 && ldh % 4 == 0 &&
+                    ((uintptr_t)HH & 15) == 0 && ((uintptr_t)P & 15) == 0;
   float r;
   if (SMALL) {
     // Waves 2 and 3 fetch this block's columns of P and the partial sums
@@ -980,6 +1068,10 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
     wait_vm_le(0);  // H^T H has landed
     lds_barrier();
     r = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  } else if (gvec) {
+    // r comes from the first iteration, which streams every row of H^T H
+    LST_SMARK(2);
+    r = 0.f;
   } else {
     LST_SMARK(2);
     // The partials, m x nh floats stored row after row (m <= 512 and nh <= 34: two
@@ -1035,11 +1127,7 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
   }
   LST_SMARK(3);
 
-  // m > 128 with m % 4 == 0 and 16-byte aligned rows of H^T H and P: vector
-  // loads (the right-hand side and the iterations)
-  const bool gvec = !SMALL && m % 4 == 0 && d % 4 == 0 && ldh % 4 == 0 &&
-                    ((uintptr_t)HH & 15) == 0 && ((uintptr_t)P & 15) == 0;
-  if (r < 0.5f) {
+  if (gvec || r < 0.5f) {
     if (gvec) {
       // Y0 = B = -(P^T_blk) diag(1/c)^T: 16-byte loads, slot e = row
       // e / 4, columns c0 + 4 (e % 4) ... + 3 (all in or all out of range)
@@ -1083,15 +1171,15 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
         }
       }
     }
-    int iters = 0;
+    int iters = gvec ? kNeumannMaxIters : 0;  // gvec: capped once r is known
     const float stop_k = r / (1.f - r);
-    if (r > 0.f) {
+    if (!gvec && r > 0.f) {
       // at most: r^(k+1) / (1 - r) <= tol (a bound that holds before any
       // iteration); the series usually ends sooner (neumann_done)
       const float need = logf(kNeumannTol * (1.f - r)) / logf(r);
       iters = (int)ceilf(need) - 1;
       if (iters < 0) iters = 0;
-      if (iters > 64) iters = 64;
+      if (iters > kNeumannMaxIters) iters = kNeumannMaxIters;
     }
     if (!SMALL) __syncthreads();
     LST_SMARK(4);
@@ -1208,9 +1296,8 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
         if (neumann_done(red, it, stop_k, bcol)) break;
       }
     } else if (gvec) {
-      Yo = (nrb <= 16)
-               ? neumann_mem<4>(HH, ldh, m, mp, iters, LDE, cinv, Yo, Yn, red, stop_k)
-               : neumann_mem_two_pass(HH, ldh, m, mp, iters, LDE, cinv, Yo, Yn, red, stop_k);
+      Yo = (nrb <= 16) ? neumann_mem<4>(HH, ldh, m, mp, LDE, cinv, Yo, Yn, red, r)
+                       : neumann_mem_two_pass(HH, ldh, m, mp, LDE, cinv, Yo, Yn, red, r);
     } else {
     floatx4 prev[RBW];  // diag(1/c) (H^T H) Y_{k-1} of the wave's rows (Y_0 = B: zero)
     floatx4 bvr[RBW];   // B's entries of the wave's rows, read from Y_0 = B
@@ -1299,12 +1386,14 @@ __device__ __forceinline__ void task_solve(const StepCtx& c, int local, unsigned
     }
     }
     LST_SMARK(5);
-    for (int e = tid; e < kSolveCols * m; e += 256) {
-      const int i = e / kSolveCols, cc = e - i * kSolveCols;
-      if (c0 + cc < d) c.X[(size_t)i * d + c0 + cc] = Yo[cc * LDE + i];
+    if (!gvec || r < 0.5f) {  // gvec: r from the first iteration decides only now
+      for (int e = tid; e < kSolveCols * m; e += 256) {
+        const int i = e / kSolveCols, cc = e - i * kSolveCols;
+        if (c0 + cc < d) c.X[(size_t)i * d + c0 + cc] = Yo[cc * LDE + i];
+      }
+      LST_SMARK(6);
+      return;
     }
-    LST_SMARK(6);
-    return;
   }
 
   // Fallback: Gauss-Jordan on [S | P^T_blk], S = H^T H - diag(c).  c_i moves
