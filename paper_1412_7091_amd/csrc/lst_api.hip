@@ -764,7 +764,7 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       (rc = dalloc(s, &s->solve_ws, solve_workspace_floats(m, d))) ||
       (rc = dalloc(s, &s->ex_row, (size_t)m * K)) || (rc = dalloc(s, &s->ex_val, (size_t)m * K)) ||
       (rc = dalloc(s, &s->ex_cnt, m)) || (rc = dalloc(s, &s->hkey, hsize)) ||
-      (rc = dalloc(s, &s->hmin, (size_t)hsize * (1 + kSlotCap))) ||
+      (rc = dalloc(s, &s->hmin, (size_t)hsize * (1 + kSlotCap) + 1 + hsize / 4)) ||
       (rc = dalloc(s, &s->hcnt, hsize + 1 + (size_t)m * K / kHotMinSlots)) ||
       (rc = dalloc(s, &s->touched, (size_t)m * K)) ||
       (rc = dalloc(s, &s->own, (size_t)m * K)) || (rc = dalloc(s, &s->count, 1)) ||

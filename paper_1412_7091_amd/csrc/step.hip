@@ -43,6 +43,12 @@ __device__ __forceinline__ unsigned row_hash(int r, int bits) {
 // The hot-row list, stored after the hash table's slot counts.
 __device__ __forceinline__ int* hot_list(const StepCtx& c) { return c.hcnt + (1 << c.hbits); }
 __device__ __forceinline__ int* hslot_of(const StepCtx& c) { return c.hmin + (1 << c.hbits); }
+// After the slot lists: the number of rows held by two or more slots this step,
+// then their hash entries (appended when a row's second slot arrives; at most
+// m K / 2 <= 2^hbits / 4 of them).
+__device__ __forceinline__ int* multi_rows(const StepCtx& c) {
+  return c.hmin + (size_t)(1 << c.hbits) * (1 + kSlotCap);
+}
 
 // c1 = h_i^T Q h_i: the partial sums left by the first product of the step,
 // added in index order (the same bits wherever it is evaluated).
@@ -151,6 +157,7 @@ __device__ __forceinline__ void task_targets(const StepCtx& c, int local, unsign
   const int w = wave_id(), lane = lane_id();
   const int i = local * 4 + w;
   if (i >= c.m) return;
+  if (i == 0 && lane == 0) multi_rows(c)[0] = 0;  // filled in launch 2, read in launch 3
   LST_TMARK(0);
   const int K = c.K, d = c.d;
   unsigned long long* keys = reinterpret_cast<unsigned long long*>(sraw) + (size_t)w * K;
@@ -395,7 +402,8 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
   const int lane = lane_id(), d = c.d;
   // Record, for every target row, the smallest slot i*K + k holding it (the
   // owner of the row's scatter in launch 3), the number of slots holding it and
-  // (the first kSlotCap of) those slots: open addressing, at most half full.
+  // (the first kSlotCap of) those slots, and list the rows held by two or more:
+  // open addressing, at most half full.
   // The list entry of a lane's first slot is written at the end of the task,
   // so that waiting for its position overlaps the rest of the work.
   int first_at = -1, first_slot = 0;
@@ -416,6 +424,10 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
             first_slot = slot;
           } else if (pos < kSlotCap) {
             hslot_of(c)[(size_t)h * kSlotCap + pos] = slot;
+          }
+          if (pos == 1) {  // the row's second slot: list the row once
+            int* mr = multi_rows(c);
+            mr[1 + atomicAdd(mr, 1)] = (int)h;
           }
           break;
         }
@@ -1708,20 +1720,23 @@ __host__ __device__ inline int scatter_lookup_blocks(const StepCtx& c) {
   const int spw = scatter_slots_per_wave(c.m * c.K);
   return (c.m * c.K + 4 * spw - 1) / (4 * spw);
 }
+// Waves that write the rows held by several slots (taken from the list in
+// turn: wave g the rows g, g + kEntryWaves, ...).
+constexpr int kEntryWaves = 2048;
 __host__ __device__ inline int scatter_entry_blocks(const StepCtx& c) {
-  return scatter_slots_per_wave(c.m * c.K) == 1 ? 0 : ((1 << c.hbits) + 255) / 256;
+  return scatter_slots_per_wave(c.m * c.K) == 1 ? 0 : kEntryWaves / 4;
 }
 
 // Blocks [0, scatter_lookup_blocks) take scatter_slots_per_wave(m K)
 // consecutive slots per wave and look them up together; a slot that owns its
 // row records it in own[], and the rows held by one slot are written here.
-// The blocks after them take the hash entries, 64 per wave, and write the
-// rows held by several slots (with d % 4 != 0, every row): the hash spreads
-// these rows evenly over the waves, whereas the slots that own them cluster
-// in the first examples when targets repeat.  With one slot per wave (small
-// steps) there are no entry blocks and the wave writes the row its slot owns,
-// whatever the row's count.  With HOT the rows held by c.hot_min or more
-// slots are listed for launch 4 instead.
+// The kEntryWaves waves after them write the rows held by several slots,
+// spread evenly over the waves by the list launch 2 made of them (their owner
+// slots cluster in the first examples when targets repeat, so the lookup
+// waves would get them unevenly).  With one slot per wave (small steps) there
+// are no entry waves and the wave writes the row its slot owns, whatever the
+// row's count.  With HOT the rows held by c.hot_min or more slots are listed
+// for launch 4 instead.
 template <bool HOT>
 __device__ __forceinline__ void task_scatter(const StepCtx& c, int local) {
   const int lane = lane_id();
@@ -1734,15 +1749,15 @@ __device__ __forceinline__ void task_scatter(const StepCtx& c, int local) {
   bool mine = false;  // this lane's row is written by scatter_row below
   if (local >= nlook) {
     if (err) return;
-    h = ((local - nlook) * 4 + wave_id()) * 64 + lane;
-    if (h < (1 << c.hbits)) {
+    const int* mr = multi_rows(c);
+    const int q = ((local - nlook) * 4 + wave_id()) + lane * kEntryWaves;
+    if (q < mr[0]) {
+      h = mr[1 + q];
       r = c.hkey[h];
-      if (r >= 0) {
-        cnt = c.hcnt[h];
-        e = c.hmin[h];
-      }
+      cnt = c.hcnt[h];
+      e = c.hmin[h];
+      mine = true;
     }
-    mine = r >= 0 && !(cnt == 1 && vec);
   } else {
     e = (local * 4 + wave_id()) * spw + lane;
     bool owner = false;
@@ -1770,7 +1785,9 @@ __device__ __forceinline__ void task_scatter(const StepCtx& c, int local) {
       const float w = single ? (c.loss_kind == LST_LOSS_SPHERICAL ? c.cs[i] : -c.val[e]) : 0.f;
       scatter_single(c, one, r, i, w);
     }
-    mine = spw == 1 && owner && !single;
+    // with one slot per wave every owned row is written here; otherwise the
+    // rows held by one slot of an unaligned V (the entry waves take the rest)
+    mine = owner && !single && (spw == 1 || cnt == 1);
   }
   if constexpr (HOT) {
     if (mine && cnt >= c.hot_min) {
