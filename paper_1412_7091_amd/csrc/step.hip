@@ -77,13 +77,28 @@ __device__ __forceinline__ float example_a(const StepCtx& c, int i) {
 // ----------------------------------------------------------------- targets
 // Launch 1, one wave per example i (four per block, no block barrier):
 //  - load and validate its K (index, value) pairs (LST_EINDEX on a bad index);
-//  - order the pairs by (row, slot) into ex_row / ex_val (rank sort in this
-//    wave's part of LDS) and count them;
+//  - order the pairs by (row, slot) into ex_row / ex_val (a sort across the
+//    wave's lanes for K <= 64, else a rank sort in its part of LDS) and count
+//    them;
 //  - (Y^T Y)_ii = sum over distinct rows of (sum of the row's values)^2, each
 //    row's values added in slot order;
 //  - G_i = sum_k y_ik V[r_ik, :] (Appendix A step 2, the sparse product),
 //    slots in order, up to 16 rows of V in flight.
 constexpr unsigned long long kNoKey = ~0ull;
+
+// Ascending sort of one 64-bit key per lane across the wave (bitonic network).
+__device__ __forceinline__ unsigned long long wave_sort_asc_u64(unsigned long long x) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const unsigned long long o = __shfl_xor(x, j);
+      const bool up = (lane & k) == 0, low = (lane & j) == 0;
+      x = (low == up) ? (o < x ? o : x) : (o > x ? o : x);
+    }
+  return x;
+}
 
 __host__ __device__ inline size_t targets_lds_bytes(int K) {
   return (size_t)4 * K * (sizeof(unsigned long long) + sizeof(float));
@@ -193,7 +208,31 @@ __device__ __forceinline__ void task_targets(const StepCtx& c, int local, unsign
 
   LST_TMARK(2);
   float yy = 0.f;
-  for (int k0 = 0; k0 < K; k0 += 64) {
+  if (K <= 64) {
+    // One key per lane, sorted across the wave: lane l then holds the l-th
+    // pair in (row, slot) order, and the first lane of each row's run adds
+    // the run's values in slot order.
+    const unsigned long long key = wave_sort_asc_u64(lane < K ? keys[lane] : kNoKey);
+    const bool valid = key != kNoKey;
+    const int row = valid ? (int)(unsigned)(key >> 32) : -1;
+    const float v = valid ? vals[(unsigned)key] : 0.f;
+    const int prev_row = __shfl_up(row, 1);  // every lane takes part in the shuffle
+    const bool first = valid && (lane == 0 || prev_row != row);
+    float run = v;
+    bool more = first;
+    for (int t = 1; t < 64 && __ballot(more) != 0ull; ++t) {
+      const float vt = __shfl_down(v, t);
+      const int rt = __shfl_down(row, t);
+      more = more && lane + t < 64 && rt == row;
+      if (more) run += vt;
+    }
+    if (first) yy = run * run;
+    if (lane < K) {
+      c.ex_row[(size_t)i * K + lane] = row;
+      c.ex_val[(size_t)i * K + lane] = v;
+    }
+  }
+  for (int k0 = 0; K > 64 && k0 < K; k0 += 64) {
     const int k = k0 + lane;
     if (k < K) {
       const unsigned long long key = keys[k];
