@@ -129,8 +129,10 @@ int scratch_device_ptr(int device, float** out) {
 int launch1_tile(int d, int m) {
   return (m > 128 && (size_t)((m + 63) / 64) * ((3 * d + m + 63) / 64) >= 256) ? 64 : 32;
 }
-// Stages of launch 1's 64 x 64 tiles: four (64 KB), so that two tiles share a
-// compute unit and the tiles run in one round.
+// Stages of launch 1's tiles for m > 128 or more tiles than compute units:
+// four (64 KB), so that two tiles share a compute unit and the tiles run in
+// one round (c4: 448 tiles of 32 x 32 with eight stages took two rounds, 22
+// against 17 us).
 constexpr int kLaunch1Stages64 = 4;
 
 struct DeviceGuard {
@@ -470,11 +472,12 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
       x1.absp = s->hap; x1.ld_absp = c.n_hap; x1.abs_col0 = 3 * d;  // |H^T H| row partials
     }
     p1.tile = t1;
+    const int tiles1 = ((m + t1 - 1) / t1) * ((nst * d + m + t1 - 1) / t1);
     x1.dot_h = H; x1.ld_doth = d;
     L.lk = 1;
     L.timing_slot = 0;
     OK_OR_RETURN(run_launch(s, c, L,
-                            stages_for(L.gemm, t1 == 64 ? kLaunch1Stages64 : kMaxStages), st,
+                            stages_for(L.gemm, (m > 128 || tiles1 > 256) ? kLaunch1Stages64 : kMaxStages), st,
                             PH_LAUNCH1));
   }
   {  // launch 2: Y^, C1, C2, C2^T ; solve ; Y^T Y ; per-example scalars
