@@ -356,6 +356,19 @@ int stages_for(const GemmBatch& b, int max_stages = kMaxStages) {
 // Launches 3 and 4 keep at most 4 stages (64 KB): two blocks share a compute
 // unit, so the short tasks run beside the GEMM tiles.
 constexpr int kLaunch34Stages = 4;
+// Above two tiles per compute unit (c5: 1040 tiles in launch 4) two stages
+// (32 KB), so that five tiles share a unit and hide each other's loads:
+// launch 4 at c5 89 -> 75 us; with fewer tiles the deeper ring wins (c2 +0.8 us).
+constexpr int kManyTiles = 512;
+int launch34_stages(GemmBatch& g) {
+  int tiles = 0;
+  for (int q = 0; q < g.np; ++q) {
+    const int t = g.p[q].tile == 64 ? 64 : 32;
+    const int tm = (g.p[q].M + t - 1) / t, tn = (g.p[q].N + t - 1) / t;
+    tiles += g.p[q].epi == EPI_SYM ? tm * (tm + 1) / 2 : tm * tn;
+  }
+  return tiles > kManyTiles ? 2 : kLaunch34Stages;
+}
 constexpr int kLaunch2Stages64 = 4;
 // Slots a row needs to be scattered by the launch-4 clear blocks instead of its
 // owner in launch 3; at most m K / kHotMinSlots rows qualify, which sizes
@@ -610,7 +623,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
       g.np = 2;  // no U^{-T}
       L.ntask = 1;
     }
-    OK_OR_RETURN(run_launch(s, c, L, stages_for(g, kLaunch34Stages), st, PH_LAUNCH4));
+    OK_OR_RETURN(run_launch(s, c, L, stages_for(g, launch34_stages(g)), st, PH_LAUNCH4));
     if (scratch) {
       StepLaunch C{};
       C.ntask = 1;
