@@ -9,7 +9,9 @@ generators, which hold none of the method's arithmetic.
 Modules
   explicit  the plain definition: W kept explicit, O(Dd) per example
             (sections 2.3, 3.1 and 3.2 of the paper, and its loss-family
-            extension in section 3.6 for the spherical softmax).
+            extension in section 3.6 for the spherical softmax, in the
+            (o_c^2 + eps) form and in the shifted (o_c + eps)^2 form the
+            section prints).
   factored  the paper's factored algorithm in fp64 (Algorithm 1, the minibatch
             algorithm of Appendix A, the pristine restore of Appendix C), used
             only to check the paper's identities against the explicit
@@ -22,7 +24,8 @@ Modules
 
 Pin status (what fixes each function other than itself) is listed in each
 function's docstring; the only function without a pin by the paper is the
-minibatch form of the spherical-softmax factored step, which is pinned by the
-explicit definition and by finite differences instead.
+minibatch forms of the two spherical-softmax factored steps, which are pinned
+by the explicit definition (itself pinned by closed forms, finite differences
+and the normalisation of the class probabilities) instead.
 """
 from . import explicit, factored, input_layer, stabilize  # noqa: F401

@@ -22,7 +22,11 @@ Readings of the paper taken here:
     unused slot and a repeated index adds its values;
   * spherical softmax: L_i = -log((o_c^2 + eps) / sum_k (o_k^2 + eps)) with one
     target class c per example, eps = 1e-3; this is a member of the family of
-    section 3.6 (a function of o_c and ||o||^2 only).
+    section 3.6 (a function of o_c and ||o||^2 only);
+  * shifted spherical softmax: the form section 3.6 prints,
+    L_i = -log((o_c + eps)^2 / sum_k (o_k + eps)^2), one class per example.  It
+    also needs sum_k o_k, so it lies just outside the family as the paper states
+    it; the factored oracle carries the extra terms (oracle.factored).
 """
 from __future__ import annotations
 
@@ -122,6 +126,36 @@ def spherical_softmax_step(W, H_rows, idx, lr: float, eps: float = 1e-3):
     return loss, grad_H.T.copy(), W_new
 
 
+def shifted_spherical_step(W, H_rows, idx, lr: float, eps: float = 1e-3):
+    """One minibatch step of the spherical softmax in the form section 3.6 prints.
+
+        L_i = -log((o_c + eps)^2 / sum_j (o_j + eps)^2),   o = W h_i,
+    c = idx[i, 0] the target class.  With u = o + eps (every output shifted by
+    eps) and S_i = sum_j u_j^2, the output gradient is
+        dL_i/do = 2 u / S_i - 2 e_c / u_c,
+    back-propagated as grad_h = W^T dL/do and applied as W_new = W - lr dL/dW.
+
+    Returns (loss[m], grad_H[m x d], W_new[D x d]), fp64.
+    """
+    W = widen(W)
+    D = W.shape[0]
+    H = widen(H_rows).T                     # d x m
+    m = H.shape[1]
+    c = np.asarray(idx)[:, 0].astype(np.int64)
+    if np.any(c < 0) or np.any(c >= D):
+        raise IndexError("spherical softmax needs one target class in [0, D) per example")
+    Uo = W @ H + eps                        # D x m, the shifted outputs
+    cols = np.arange(m)
+    S = np.sum(Uo * Uo, axis=0)
+    uc = Uo[c, cols]
+    loss = -np.log(uc * uc / S)
+    G = 2.0 * Uo / S
+    G[c, cols] -= 2.0 / uc
+    grad_H = W.T @ G
+    W_new = W - lr * (G @ H.T)
+    return loss, grad_H.T.copy(), W_new
+
+
 def term_scales(W, H_rows, idx, val, loss, grad_H, loss_kind: str = "squared",
                 eps: float = 1e-3):
     """Per-example magnitudes of the terms whose sums give L_i and grad_h_i.
@@ -131,7 +165,10 @@ def term_scales(W, H_rows, idx, val, loss, grad_H, loss_kind: str = "squared",
     family for the spherical softmax):
       squared    L_i = h^T Q h - 2 h^T W^T y + y^T y,   grad = 2 W^T W h - 2 W^T y;
       spherical  L_i = log S_i - log(o_c^2 + eps),      grad = (2/S_i) W^T W h + b_i W^T e_c,
-                 b_i = -2 o_c / (o_c^2 + eps), S_i = sum_j (o_j^2 + eps).
+                 b_i = -2 o_c / (o_c^2 + eps), S_i = sum_j (o_j^2 + eps);
+      shifted    L_i = log S_i - log(u_c^2),  grad = (2/S_i)(W^T W h + eps s) + b_i W^T e_c,
+                 u = o + eps, b_i = -2 / u_c, s = W^T 1, and
+                 S_i = h^T W^T W h + 2 eps s^T h + D eps^2 a sum of three terms.
     The rounding error of any evaluation of such a sum is bounded by a multiple
     of the sum of the terms' magnitudes, which can exceed |L_i| or ||grad_i||
     many times when the terms cancel.  For the spherical softmax the scales
@@ -149,6 +186,7 @@ def term_scales(W, H_rows, idx, val, loss, grad_H, loss_kind: str = "squared",
     m = H.shape[0]
     loss_scale = np.zeros(m)
     grad_scale = np.zeros(m)
+    s1 = W.sum(axis=0) if loss_kind == "spherical_shifted" else None
     for i in range(m):
         if loss_kind == "squared":
             wty = np.zeros(W.shape[1])
@@ -180,6 +218,26 @@ def term_scales(W, H_rows, idx, val, loss, grad_H, loss_kind: str = "squared",
             loss_scale[i] = abs(lo) + abs(float(loss[i]) + lo) + abs(b) * doc
             grad_scale[i] = (np.linalg.norm(g[i] - t) + np.linalg.norm(t)
                              + abs(db) * doc * np.linalg.norm(wc))
+        elif loss_kind == "spherical_shifted":
+            c = int(idx[i, 0])
+            wc = W[c]
+            uc = float(wc @ H[i]) + eps
+            b = -2.0 / uc
+            t = b * wc
+            S = uc * uc * np.exp(float(loss[i]))          # L_i = log S_i - log u_c^2
+            sterm = (2.0 * eps / S) * s1                  # (2/S) eps s
+            qterm = g[i] - t - sterm                      # (2/S) W^T W h
+            hn = float(np.linalg.norm(H[i]))
+            # S_i is formed from terms of total size s_terms; its relative error
+            # moves log S_i and scales the dense part of the gradient
+            s_terms = 0.5 * S * abs(float(H[i] @ qterm)) + 2.0 * eps * np.linalg.norm(s1) * hn \
+                + W.shape[0] * eps * eps
+            doc = float(np.linalg.norm(wc)) * hn
+            db = 2.0 / (uc * uc)                          # slope of b in o_c
+            lu = np.log(uc * uc)
+            loss_scale[i] = abs(lu) + abs(float(loss[i]) + lu) + abs(b) * doc + s_terms / S
+            grad_scale[i] = ((np.linalg.norm(qterm) + np.linalg.norm(sterm)) * (1.0 + s_terms / S)
+                             + np.linalg.norm(t) + db * doc * np.linalg.norm(wc))
         else:
             raise ValueError(f"unknown loss {loss_kind!r}")
     return loss_scale, grad_scale
@@ -213,6 +271,15 @@ def step_fp32(W, H_rows, idx, val, lr: float, loss_kind: str = "squared", eps: f
         loss = -np.log((oc * oc + f(eps)) / S)
         G = f(2.0) * O / S
         G[c, cols] -= f(2.0) * oc / (oc * oc + f(eps))
+    elif loss_kind == "spherical_shifted":
+        c = np.asarray(idx)[:, 0].astype(np.int64)
+        cols = np.arange(m)
+        Uo = O + f(eps)
+        S = np.sum(Uo * Uo, axis=0, dtype=f)
+        uc = Uo[c, cols]
+        loss = -np.log(uc * uc / S)
+        G = f(2.0) * Uo / S
+        G[c, cols] -= f(2.0) / uc
     else:
         raise ValueError(f"unknown loss {loss_kind!r}")
     grad = (W.T @ G).T.copy()
@@ -221,11 +288,13 @@ def step_fp32(W, H_rows, idx, val, lr: float, loss_kind: str = "squared", eps: f
 
 
 def step(W, H_rows, idx, val, lr: float, loss_kind: str = "squared", eps: float = 1e-3):
-    """Dispatch on the loss: 'squared' or 'spherical'."""
+    """Dispatch on the loss: 'squared', 'spherical' or 'spherical_shifted'."""
     if loss_kind == "squared":
         return squared_error_step(W, H_rows, idx, val, lr)
     if loss_kind == "spherical":
         return spherical_softmax_step(W, H_rows, idx, lr, eps)
+    if loss_kind == "spherical_shifted":
+        return shifted_spherical_step(W, H_rows, idx, lr, eps)
     raise ValueError(f"unknown loss {loss_kind!r}")
 
 

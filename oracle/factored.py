@@ -3,7 +3,10 @@
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
 W is never stored: it is V U (D x d times d x d, section 3.2), and the side
-matrices Q = W^T W and U^{-T} are kept up to date (section 3.3).  This module
+matrices Q = W^T W and U^{-T} are kept up to date (section 3.3).  For the
+spherical softmax in the shifted form of section 3.6 the state also carries a
+row c shared by all D rows and the column sums s = W^T 1, so that
+W = V U + 1 c^T (c stays zero for the other losses).  This module
 exists to check the paper's algebra against the explicit definition in
 `oracle.explicit`: after every step V U must equal the explicitly updated W,
 Q must equal W^T W and U (U^{-T})^T must be the identity.
@@ -11,25 +14,32 @@ Q must equal W^T W and U (U^{-T})^T must be the identity.
 How the step is organised here.  Every loss this package handles has an
 output gradient of the form
 
-    dL/dO = W H A + G,      A = diag(a_1 .. a_m),  G sparse on the targets,
+    dL/dO = W H A + 1 g^T + G,   A = diag(a_1 .. a_m),  G sparse on the targets,
 
-(squared error: a_i = 2 and G = -2 Y, eq. gradH; spherical softmax: see
-`spherical_minibatch_step`).  For such a loss the whole update is a function
-of (H, A, G) and the factored state, derived once in `_factored_update`:
+(squared error: a_i = 2, g = 0 and G = -2 Y, eq. gradH; spherical softmax:
+see `spherical_minibatch_step`; its shifted form has g != 0, see
+`shifted_spherical_minibatch_step`).  For such a loss the whole update is a
+function of (H, A, g, G) and the factored state, derived once in
+`_factored_update`:
 
-  * gradient wrt H       W^T dL/dO = (Q H) A + W^T G, with W^T G = U^T (V^T G)
-                         (section 3.1, eq. gradH, and the remark at the end of
-                         section 3.2 that W^T y is U^T (V^T y));
+  * gradient wrt H       W^T dL/dO = (Q H) A + s g^T + W^T G, with
+                         W^T G = U^T (V^T G) + c (1^T G) (section 3.1, eq. gradH,
+                         and the remark at the end of section 3.2 that W^T y is
+                         U^T (V^T y));
   * the W update         W - lr (dL/dO) H^T is reached by
-                         U <- U (I - lr H A H^T)          (eq. updateU) and
-                         V <- V - lr G (U_new^{-T} H)^T   (eq. updateV),
+                         U <- U (I - lr H A H^T)          (eq. updateU),
+                         V <- V - lr G (U_new^{-T} H)^T   (eq. updateV), and
+                         c <- (I - lr H A H^T) c - lr H g,
                          since V_new U_new = V U_new - lr G H^T;
+  * s = W^T 1            s - lr H (dL/dO)^T 1, with
+                         (dL/dO)^T 1 = A H^T s + D g + G^T 1;
   * U^{-T}               (I - lr H A H^T)^{-1} by the Woodbury identity, which
                          for one example is the Sherman-Morrison form of
                          eq. updateU-T (section 3.5 and the minibatch appendix);
   * Q                    W_new^T W_new expanded (the proof of the Q update in the
                          appendix): Q - lr (H grad^T + grad H^T) + lr^2 H N H^T
-                         with N = (dL/dO)^T (dL/dO) built from m x m pieces.
+                         with N = (dL/dO)^T (dL/dO) built from m x m pieces
+                         (for g != 0 also n g^T-type pieces, n = H^T s).
 
 Functions
   FactoredState.from_initial  the initialisation of the minibatch appendix (V = W0,
@@ -39,10 +49,17 @@ Functions
   spherical_minibatch_step    spherical softmax, one class per example (the paper
                               lists this loss in section 3.6 without minibatch
                               formulas; the (a, G) form above supplies them).
+  shifted_spherical_minibatch_step  the same loss in the form section 3.6 prints,
+                              (o_c + eps)^2 / sum_j (o_j + eps)^2 (g = eps a).
   online_step                 one example, squared error, with the rank-one
                               (Sherman-Morrison) update of U^{-T} of eq. updateU-T.
   sherman_morrison_inverse_T  eq. updateU-T on its own.
   pristine_restore            Appendix C: V <- V U, U <- I, U^{-T} <- I.
+
+Pin status: every step function is pinned against the explicit definition
+(`oracle.explicit`) after each of many steps; the squared-error step also by the
+paper's own identities.  The minibatch forms of both spherical steps have no
+printed values in the paper.
 """
 from __future__ import annotations
 
@@ -59,35 +76,53 @@ class FactoredState:
     U: np.ndarray      # d x d
     UinvT: np.ndarray  # d x d, (U^{-1})^T
     Q: np.ndarray      # d x d, W^T W
+    c: np.ndarray      # d, the row shared by all rows of W (W = V U + 1 c^T)
+    s: np.ndarray      # d, W^T 1
 
     @classmethod
     def from_initial(cls, V0, U0=None) -> "FactoredState":
         """Initial state with W0 = V0 U0 (U0 = I unless given): U^{-T} = inv(U0)^T,
-        Q = W0^T W0.  With U0 = I this is the appendix's V = W0, Q = V^T V."""
+        Q = W0^T W0, c = 0, s = W0^T 1.  With U0 = I this is the appendix's V = W0,
+        Q = V^T V."""
         V = widen(V0)
         d = V.shape[1]
         U = np.eye(d) if U0 is None else widen(U0)
         W = V @ U
-        return cls(V=V, U=U, UinvT=np.linalg.inv(U).T, Q=W.T @ W)
+        return cls(V=V, U=U, UinvT=np.linalg.inv(U).T, Q=W.T @ W, c=np.zeros(d),
+                   s=W.sum(axis=0))
 
     def W(self) -> np.ndarray:
-        return self.V @ self.U
+        return self.V @ self.U + self.c[None, :]
+
+    def WtG(self, G: np.ndarray) -> np.ndarray:
+        """W^T G for a D x m G without forming W: U^T (V^T G) + c (1^T G)."""
+        return self.U.T @ (self.V.T @ G) + np.outer(self.c, G.sum(axis=0))
 
 
 def _factored_update(st: FactoredState, H: np.ndarray, a: np.ndarray, G: np.ndarray,
-                     QH: np.ndarray, WtG: np.ndarray, lr: float) -> np.ndarray:
-    """Apply W <- W - lr (W H A + G) H^T to the factored state; return grad_H (d x m).
+                     QH: np.ndarray, WtG: np.ndarray, lr: float, g=None) -> np.ndarray:
+    """Apply W <- W - lr (W H A + 1 g^T + G) H^T to the factored state; return
+    grad_H (d x m).
 
-    H is d x m (columns are examples), a the diagonal of A, G the D x m sparse
-    part of dL/dO, QH = Q H and WtG = W^T G (both d x m, from the state before
-    the update).  The new U, U^{-T}, V and Q all follow from the same
-    rank-m change  I - lr H A H^T  of U's right-hand side.
+    H is d x m (columns are examples), a the diagonal of A, g the m weights of
+    the all-ones direction (None: zero), G the D x m sparse part of dL/dO,
+    QH = Q H and WtG = W^T G (both d x m, from the state before the update).
+    The new U, U^{-T}, V and Q all follow from the same rank-m change
+    I - lr H A H^T  of U's right-hand side; c and s from O(m d) products.
     """
+    D = st.V.shape[0]
+    m = H.shape[1]
+    g = np.zeros(m) if g is None else np.asarray(g, dtype=np.float64)
     A = np.diag(a)
-    grad = QH @ A + WtG                                  # W^T dL/dO
+    n = H.T @ st.s                                       # n_i = 1^T W h_i
+    grad = QH @ A + np.outer(st.s, g) + WtG              # W^T dL/dO
     # N = (dL/dO)^T (dL/dO) = A H^T Q H A + A H^T W^T G + G^T W H A + G^T G
+    #     + A n g^T + g n^T A + D g g^T + g (1^T G) + (G^T 1) g^T
     HtWtG = H.T @ WtG
-    N = A @ (H.T @ QH) @ A + A @ HtWtG + HtWtG.T @ A + G.T @ G
+    Gsum = G.sum(axis=0)                                 # 1^T G
+    N = (A @ (H.T @ QH) @ A + A @ HtWtG + HtWtG.T @ A + G.T @ G
+         + np.outer(a * n, g) + np.outer(g, a * n) + D * np.outer(g, g)
+         + np.outer(g, Gsum) + np.outer(Gsum, g))
     # U_new^{-T} = U^{-T} (I - lr H A H^T)^{-1}
     #            = U^{-T} - (U^{-T} H) (H^T H - A^{-1}/lr)^{-1} H^T          (Woodbury)
     S = H.T @ H - np.diag(1.0 / a) / lr
@@ -95,7 +130,9 @@ def _factored_update(st: FactoredState, H: np.ndarray, a: np.ndarray, G: np.ndar
     U_new = st.U - lr * (st.U @ H) @ A @ H.T
     V_new = st.V - lr * G @ (UinvT_new @ H).T
     Q_new = st.Q - lr * (H @ grad.T + grad @ H.T) + lr * lr * (H @ N) @ H.T
-    st.U, st.UinvT, st.V, st.Q = U_new, UinvT_new, V_new, Q_new
+    c_new = st.c - lr * H @ (a * (H.T @ st.c) + g)
+    s_new = st.s - lr * H @ (a * n + D * g + Gsum)
+    st.U, st.UinvT, st.V, st.Q, st.c, st.s = U_new, UinvT_new, V_new, Q_new, c_new, s_new
     return grad
 
 
@@ -111,7 +148,7 @@ def minibatch_step(st: FactoredState, H_rows, idx, val, lr: float):
     H = widen(H_rows).T                      # d x m
     Y = dense_targets(D, idx, val)           # D x m, sparse in content
     QH = st.Q @ H
-    WtY = st.U.T @ (st.V.T @ Y)              # W^T Y without forming W
+    WtY = st.WtG(Y)                          # W^T Y without forming W
     loss = (np.einsum("ji,ji->i", H, QH) - 2.0 * np.einsum("ji,ji->i", H, WtY)
             + np.einsum("ji,ji->i", Y, Y))
     m = H.shape[1]
@@ -134,12 +171,37 @@ def spherical_minibatch_step(st: FactoredState, H_rows, idx, lr: float, eps: flo
     H = widen(H_rows).T                                      # d x m
     Y = dense_targets(D, idx, None, one_hot=True)            # D x m
     QH = st.Q @ H
-    WtY = st.U.T @ (st.V.T @ Y)                              # column i: W^T e_{c_i}
+    WtY = st.WtG(Y)                                          # column i: W^T e_{c_i}
     oc = np.einsum("ji,ji->i", H, WtY)
     S = np.einsum("ji,ji->i", H, QH) + D * eps
     loss = -np.log((oc * oc + eps) / S)
     beta = -2.0 * oc / (oc * oc + eps)
     grad = _factored_update(st, H, 2.0 / S, Y * beta[None, :], QH, WtY * beta[None, :], lr)
+    return loss, grad.T.copy()
+
+
+def shifted_spherical_minibatch_step(st: FactoredState, H_rows, idx, lr: float,
+                                     eps: float = 1e-3):
+    """L_i = -log((o_c + eps)^2 / sum_j (o_j + eps)^2), in place (section 3.6).
+
+    With u = o + eps 1 and s = W^T 1:  S_i = sum_j u_j^2 = h_i^T Q h_i
+    + 2 eps s^T h_i + D eps^2 and u_c = h_i^T (W^T e_c) + eps.  The output
+    gradient 2 u / S_i - 2 e_c / u_c is the form above with a_i = 2 / S_i,
+    g = eps a (the all-ones direction) and G = Y diag(beta), beta_i = -2 / u_c.
+    Pinned against the explicit definition only (the paper prints no minibatch
+    formulas for this loss).  Returns (loss[m], grad_H[m x d]).
+    """
+    D = st.V.shape[0]
+    H = widen(H_rows).T                                      # d x m
+    Y = dense_targets(D, idx, None, one_hot=True)            # D x m
+    QH = st.Q @ H
+    WtY = st.WtG(Y)                                          # column i: W^T e_{c_i}
+    uc = np.einsum("ji,ji->i", H, WtY) + eps
+    S = np.einsum("ji,ji->i", H, QH) + 2.0 * eps * (H.T @ st.s) + D * eps * eps
+    loss = -np.log(uc * uc / S)
+    a = 2.0 / S
+    beta = -2.0 / uc
+    grad = _factored_update(st, H, a, Y * beta[None, :], QH, WtY * beta[None, :], lr, g=eps * a)
     return loss, grad.T.copy()
 
 
@@ -157,8 +219,11 @@ def online_step(st: FactoredState, h, y_idx, y_val, lr: float):
     z = Q h - W^T y); the state then moves by rank-one changes only:
     U by eq. updateU, U^{-T} by eq. updateU-T, V along y by eq. updateV
     (which needs the new U^{-T} times h), and Q by eq. updateQ, whose last
-    term carries the example's loss L.
+    term carries the example's loss L.  The state's shared row c must be zero
+    (it is for this loss); s = W^T 1 is kept up to date.
     """
+    if np.any(st.c):
+        raise ValueError("online_step handles states with c = 0 only")
     D = st.V.shape[0]
     h = widen(h)
     y = dense_targets(D, np.asarray(y_idx).reshape(1, -1), np.asarray(y_val).reshape(1, -1))[:, 0]
@@ -172,6 +237,7 @@ def online_step(st: FactoredState, h, y_idx, y_val, lr: float):
     st.U = st.U - 2.0 * lr * np.outer(st.U @ h, h)
     st.UinvT = UinvT_new
     st.Q = st.Q - 2.0 * lr * (np.outer(h, z) + np.outer(z, h)) + 4.0 * lr * lr * L * np.outer(h, h)
+    st.s = st.s - 2.0 * lr * (st.s @ h - np.sum(y)) * h   # s - lr h (dL/do)^T 1
     return L, grad_h
 
 

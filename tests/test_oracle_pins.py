@@ -201,6 +201,140 @@ def test_spherical_probabilities_sum_to_one():
     np.testing.assert_allclose(tot, np.ones(m), rtol=1e-13)
 
 
+# ------------------------------------- shifted spherical softmax (section 3.6)
+def _shift(W, H, idx, val, lr):
+    return explicit.shifted_spherical_step(W, H, idx, lr)
+
+
+def check_shift_zero_weights(step_fn):
+    """W = 0: every shifted output is eps, so each class has probability
+    eps^2 / (D eps^2) = 1/D, L_i = log D, and dL/do = (2 / (D eps)) 1 - (2 / eps) e_c:
+    grad_h = W^T dL/do = 0 and W_new = -lr dL/dO H^T."""
+    D, d, m, eps, lr = 13, 4, 3, 1e-3, 0.1
+    H = np.random.default_rng(3).standard_normal((m, d)).astype(np.float32)
+    idx = np.array([[5], [0], [5]], np.int32)
+    loss, grad, W_new = step_fn(np.zeros((D, d), np.float32), H, idx, None, lr)
+    np.testing.assert_allclose(loss, np.full(m, math.log(D)), rtol=1e-14)
+    np.testing.assert_allclose(grad, np.zeros((m, d)), atol=1e-12)
+    Hd = H.astype(np.float64)
+    want = np.tile(-lr * (2.0 / (D * eps)) * Hd.sum(axis=0), (D, 1))
+    want[5] += lr * (2.0 / eps) * (Hd[0] + Hd[2])
+    want[0] += lr * (2.0 / eps) * Hd[1]
+    np.testing.assert_allclose(W_new, want, rtol=1e-12, atol=1e-12)
+
+
+def check_shift_sums_to_one(step_fn):
+    """p_c = exp(-L) = (o_c + eps)^2 / sum_j (o_j + eps)^2 over all classes c sums to 1."""
+    D, d, m = 11, 3, 2
+    rng = np.random.default_rng(6)
+    W = rng.standard_normal((D, d)).astype(np.float32)
+    H = rng.standard_normal((m, d)).astype(np.float32)
+    tot = np.zeros(m)
+    for c in range(D):
+        loss, _, _ = step_fn(W, H, np.full((m, 1), c, np.int32), None, 0.0)
+        p = np.exp(-loss)
+        assert np.all(p > 0) and np.all(p <= 1)
+        tot += p
+    np.testing.assert_allclose(tot, np.ones(m), rtol=1e-13)
+
+
+def check_shift_fd_grad_h(step_fn):
+    check_fd_grad_h(step_fn, idx_for=_one_class)
+
+
+def check_shift_fd_update_W(step_fn):
+    check_fd_update_W(step_fn, idx_for=_one_class)
+
+
+def test_shifted_zero_weights_closed_form():
+    check_shift_zero_weights(_shift)
+
+
+def test_shifted_probabilities_sum_to_one():
+    check_shift_sums_to_one(_shift)
+
+
+def test_fd_grad_h_shifted():
+    check_shift_fd_grad_h(_shift)
+
+
+def test_fd_update_W_shifted():
+    check_shift_fd_update_W(_shift)
+
+
+def test_shifted_is_unshifted_with_a_constant_input():
+    """Appending a constant input eps to h and a column of ones to W turns o + eps
+    into the plain output o' = [W 1] [h; eps], and the shifted loss into the
+    spherical softmax of o' at eps = 0 (a different function, pinned on its own):
+    equal losses, grad_h the first d components, W_new the first d columns."""
+    wl = _tiny(seed=37, D=19, d=4, m=5, K=1)
+    W = wl.init_V().astype(np.float64)
+    H, idx, _ = wl.batch(0)
+    idx = _one_class(idx)
+    eps, lr = 0.3, 0.05   # a large eps, so that dropping it anywhere shows
+    L1, g1, W1 = explicit.shifted_spherical_step(W, H, idx, lr, eps)
+    Wa = np.hstack([W, np.ones((W.shape[0], 1))])
+    Ha = np.hstack([H.astype(np.float64), np.full((H.shape[0], 1), eps)])
+    L2, g2, W2 = explicit.spherical_softmax_step(Wa, Ha, idx, lr, 0.0)
+    np.testing.assert_allclose(L1, L2, rtol=1e-13)
+    np.testing.assert_allclose(g1, g2[:, :-1], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(W1, W2[:, :-1], rtol=1e-12, atol=1e-13)
+
+
+def _shift_mutants():
+    """Plausible mistakes in the shifted loss, planted in the oracle's outputs."""
+    eps = 1e-3
+
+    def unshifted_form(W, H, idx, val, lr):       # (o_c^2 + eps) / sum (o_j^2 + eps)
+        return explicit.spherical_softmax_step(W, H, idx, lr, eps)
+
+    def ones_direction_dropped(W, H, idx, val, lr):  # W update without the eps 1 a^T term
+        loss, g, Wn = _shift(W, H, idx, val, lr)
+        Wd = np.asarray(W, float)
+        Hd = np.asarray(H, float)
+        Uo = Wd @ Hd.T + eps
+        a = 2.0 / np.sum(Uo * Uo, axis=0)
+        return loss, g, Wn - lr * eps * np.outer(np.ones(Wd.shape[0]), a @ Hd)
+
+    def grad_without_s(W, H, idx, val, lr):        # grad_h missing (2 eps / S) W^T 1
+        loss, g, Wn = _shift(W, H, idx, val, lr)
+        Wd = np.asarray(W, float)
+        Uo = Wd @ np.asarray(H, float).T + eps
+        a = 2.0 / np.sum(Uo * Uo, axis=0)
+        return loss, g - eps * np.outer(a, Wd.sum(axis=0)), Wn
+
+    def class_term_squared(W, H, idx, val, lr):    # -2 u_c / u_c^2 written as -2 u_c
+        Wd = np.asarray(W, float)
+        Hd = np.asarray(H, float)
+        loss, g, Wn = _shift(W, H, idx, val, lr)
+        c = np.asarray(idx)[:, 0]
+        uc = np.einsum("id,id->i", Wd[c], Hd) + eps
+        dG = 2.0 / uc - 2.0 * uc                   # replaces -2/u_c by -2 u_c
+        g2 = g + dG[:, None] * Wd[c]
+        Wn2 = Wn.copy()
+        for i in range(len(c)):
+            Wn2[c[i]] -= lr * dG[i] * Hd[i]
+        return loss, g2, Wn2
+
+    return [unshifted_form, ones_direction_dropped, grad_without_s, class_term_squared]
+
+
+def test_shifted_planted_mistakes_are_caught():
+    pins = [check_shift_zero_weights, check_shift_sums_to_one, check_shift_fd_grad_h,
+            check_shift_fd_update_W]
+    for fn in pins:
+        fn(_shift)
+    for mutant in _shift_mutants():
+        caught = False
+        for fn in pins:
+            try:
+                fn(mutant)
+            except AssertionError:
+                caught = True
+                break
+        assert caught, f"mutant {mutant.__name__} slipped through every pin"
+
+
 def test_loss_and_gradient_identities():
     """eq. L and eq. gradH (section 3.1): L = h^T Q h - 2 h^T W^T y + y^T y and
     grad_h = 2 (Q h - W^T y), with Q = W^T W."""
@@ -251,7 +385,7 @@ def test_index_handling_brute_force():
 
 
 # ------------------------------------------- factored algorithm vs definition
-def _factored_vs_explicit(loss_kind, steps=20, u_init="random", **kw):
+def _factored_vs_explicit(loss_kind, steps=20, u_init="random", eps=1e-3, **kw):
     wl = _tiny(loss=loss_kind, seed=23, D=40, d=6, m=4, K=3, u_init=u_init, **kw)
     V0, U0 = wl.init_V(), wl.init_U()
     W = V0.astype(np.float64) @ U0.astype(np.float64)
@@ -263,13 +397,19 @@ def _factored_vs_explicit(loss_kind, steps=20, u_init="random", **kw):
         if loss_kind == "squared":
             loss_e, grad_e, W = explicit.squared_error_step(W, H, idx, val, lr)
             loss_f, grad_f = factored.minibatch_step(st, H, idx, val, lr)
-        else:
+        elif loss_kind == "spherical":
             idx1 = _one_class(idx)
             loss_e, grad_e, W = explicit.spherical_softmax_step(W, H, idx1, lr)
             loss_f, grad_f = factored.spherical_minibatch_step(st, H, idx1, lr)
+        else:
+            idx1 = _one_class(idx)
+            loss_e, grad_e, W = explicit.shifted_spherical_step(W, H, idx1, lr, eps)
+            loss_f, grad_f = factored.shifted_spherical_minibatch_step(st, H, idx1, lr, eps)
         Wf = st.W()
         worst = max(worst, _rel(Wf, W), _rel(st.Q, W.T @ W), _rel(loss_f, loss_e), _rel(grad_f, grad_e),
-                    float(np.abs(st.U @ st.UinvT.T - np.eye(6)).max()))
+                    _rel(st.s, W.sum(axis=0)), float(np.abs(st.U @ st.UinvT.T - np.eye(6)).max()))
+        if loss_kind != "spherical_shifted":
+            assert not np.any(st.c)
     return worst
 
 
@@ -281,6 +421,13 @@ def test_factored_minibatch_equals_explicit_squared():
 def test_factored_minibatch_equals_explicit_spherical():
     """Derived minibatch form for the spherical softmax (pinned against the definition)."""
     assert _factored_vs_explicit("spherical") < 1e-12
+
+
+def test_factored_minibatch_equals_explicit_shifted():
+    """The shifted form with W = V U + 1 c^T and s = W^T 1 (pinned against the
+    definition); a large eps makes the all-ones terms large."""
+    assert _factored_vs_explicit("spherical_shifted") < 1e-12
+    assert _factored_vs_explicit("spherical_shifted", eps=0.5) < 1e-12
 
 
 def test_first_step_from_identity_closed_form():
@@ -384,11 +531,11 @@ def test_planted_mistakes_are_caught():
 
 
 # ------------------------------------------ conditioning scales, fp32 yardstick
-@pytest.mark.parametrize("loss", ["squared", "spherical"])
+@pytest.mark.parametrize("loss", ["squared", "spherical", "spherical_shifted"])
 def test_term_scales_brute_force(loss):
     """term_scales against the terms formed from the explicit output o = W h, and
     the triangle inequality (each scale bounds |L_i| and ||grad_i||)."""
-    kw = dict(K=1) if loss == "spherical" else dict(pad_frac=0.2, dup_frac=0.3)
+    kw = dict(K=1) if loss != "squared" else dict(pad_frac=0.2, dup_frac=0.3)
     wl = _tiny(loss, seed=31, D=40, d=6, m=5, K=kw.pop("K", 4), **kw)
     W = wl.init_V().astype(np.float64)
     H, idx, val = wl.batch(0)
@@ -405,6 +552,17 @@ def test_term_scales_brute_force(loss):
                     y[idx[i, k]] += val[i, k]
             want_l = o @ o + 2 * abs(o @ y) + y @ y
             want_g = 2 * np.linalg.norm(W.T @ o) + 2 * np.linalg.norm(W.T @ y)
+        elif loss == "spherical_shifted":
+            c = idx[i, 0]
+            u = o + eps
+            S = u @ u
+            s1 = W.sum(axis=0)
+            b = -2 / u[c]
+            doc = np.linalg.norm(W[c]) * np.linalg.norm(Hd[i])
+            s_terms = o @ o + 2 * eps * np.linalg.norm(s1) * np.linalg.norm(Hd[i]) + W.shape[0] * eps ** 2
+            want_l = abs(np.log(u[c] ** 2)) + abs(np.log(S)) + abs(b) * doc + s_terms / S
+            want_g = ((np.linalg.norm(2 / S * (W.T @ o)) + np.linalg.norm(2 * eps / S * s1))
+                      * (1 + s_terms / S) + np.linalg.norm(b * W[c]) + 2 / u[c] ** 2 * doc * np.linalg.norm(W[c]))
         else:
             c = idx[i, 0]
             S = np.sum(o * o + eps)
@@ -420,11 +578,11 @@ def test_term_scales_brute_force(loss):
         assert gs[i] >= np.linalg.norm(g[i]) * (1 - 1e-12)
 
 
-@pytest.mark.parametrize("loss", ["squared", "spherical"])
+@pytest.mark.parametrize("loss", ["squared", "spherical", "spherical_shifted"])
 def test_fp32_yardstick_is_the_definition(loss):
     """step_fp32 is `step` evaluated in float32: on a benign tiny case it agrees to
     fp32 accuracy (and its outputs are float32)."""
-    kw = dict(K=1) if loss == "spherical" else {}
+    kw = dict(K=1) if loss != "squared" else {}
     wl = _tiny(loss, seed=32, D=60, d=7, m=6, K=kw.pop("K", 3), **kw)
     W = wl.init_V()
     H, idx, val = wl.batch(0)

@@ -48,7 +48,7 @@ def _check_fix(st0, st1, k_moved, s_before, target):
 
 def _copy(st):
     return factored.FactoredState(V=st.V.copy(), U=st.U.copy(), UinvT=st.UinvT.copy(),
-                                  Q=st.Q.copy())
+                                  Q=st.Q.copy(), c=st.c.copy(), s=st.s.copy())
 
 
 @pytest.mark.parametrize("k", [0, 3, 6])
