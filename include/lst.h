@@ -58,13 +58,20 @@ enum {
 /* Loss functions (sections 3.1 and 3.6). */
 enum {
   LST_LOSS_SQUARED = 0,   /* L_i = ||W h_i - y_i||^2                                    */
-  LST_LOSS_SPHERICAL = 1  /* L_i = -log((o_c^2 + eps) / sum_j (o_j^2 + eps)), o = W h_i,
+  LST_LOSS_SPHERICAL = 1, /* L_i = -log((o_c^2 + eps) / sum_j (o_j^2 + eps)), o = W h_i,
                              c = Y_idx[i][0] the target class; requires K == 1 and
                              ignores Y_val                                           */
+  LST_LOSS_SPHERICAL_SHIFTED = 2
+                          /* L_i = -log((o_c + eps)^2 / sum_j (o_j + eps)^2), the form
+                             section 3.6 prints; K == 1, Y_val ignored.  Its gradient
+                             moves every row of W along the all-ones direction, so a
+                             factored state keeps W = V U + 1 c^T and s = W^T 1
+                             (lst_get_shift); the minibatch steps then add O(m d) work
+                             and one small launch before and after the update       */
 };
 
 typedef struct lst_config {
-  int32_t loss;      /* LST_LOSS_SQUARED or LST_LOSS_SPHERICAL                         */
+  int32_t loss;      /* LST_LOSS_SQUARED, LST_LOSS_SPHERICAL or LST_LOSS_SPHERICAL_SHIFTED */
   float sph_eps;     /* eps of the spherical softmax (> 0); unused for squared error   */
   int32_t m_max;     /* largest minibatch any lst_step call will pass (1..512)         */
   int32_t K_max;     /* largest K any lst_step call will pass (1..1024); m_max*K_max
@@ -95,7 +102,8 @@ typedef struct lst_stats_t {
  *   cfg   (host)   configuration, copied.
  *   hip_stream     hipStream_t every later call of this state is ordered on
  *                  (NULL = the default stream).
- * Computes U^{-T} (the identity when U is NULL) and Q = (V U)^T (V U).
+ * Computes U^{-T} (the identity when U is NULL) and Q = (V U)^T (V U); for
+ * LST_LOSS_SPHERICAL_SHIFTED also s = (V U)^T 1, with c = 0.
  * Synchronous: returns after the state is ready.
  */
 int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float* U,
@@ -116,8 +124,9 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
  * Never forms W H.  State is updated in place unless the sticky error flag is set.
  * With m == 1 and K <= 256 the step takes the single-example form of
  * Algorithm 1 (Sherman-Morrison update of U^{-T}, eq. updateU-T) in two
- * launches; otherwise the minibatch steps of Appendix A.  Both compute the
- * same update in exact arithmetic, with the same error behaviour.
+ * launches (not for LST_LOSS_SPHERICAL_SHIFTED, which always takes the
+ * minibatch steps); otherwise the minibatch steps of Appendix A.  Both compute
+ * the same update in exact arithmetic, with the same error behaviour.
  */
 int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* Y_idx,
              const float* Y_val, float lr, float* loss, float* grad_H);
@@ -140,10 +149,18 @@ int lst_step_solve(lst_state* s, int32_t m, int32_t K, const float* H, const int
                    const float* Y_val, float lr, float* loss, float* grad_H);
 
 /*
- * lst_materialize_W -- debug: W = V U into W (device, D x d).  O(D d^2).
- * For a naive state, copies its explicit W.
+ * lst_materialize_W -- debug: W = V U (+ 1 c^T for LST_LOSS_SPHERICAL_SHIFTED)
+ * into W (device, D x d).  O(D d^2).  For a naive state, copies its explicit W.
  */
 int lst_materialize_W(lst_state* s, float* W);
+
+/*
+ * lst_get_shift -- debug: copy the shifted spherical loss's extra state of a
+ * factored state (section 3.6): c (device, d floats; W = V U + 1 c^T) and
+ * s = W^T 1 (device, d floats); either may be NULL.  States of the other
+ * losses hold c = 0 and an s that is not kept up to date: LST_ESTATE.
+ */
+int lst_get_shift(lst_state* s, float* c, float* s_out);
 
 /*
  * lst_get_state -- debug: copy Q, U and U^{-T} (each d x d, device; any may be

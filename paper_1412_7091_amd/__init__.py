@@ -30,8 +30,10 @@ LST_ENOSCRATCH = -8
 
 LST_LOSS_SQUARED = 0
 LST_LOSS_SPHERICAL = 1
+LST_LOSS_SPHERICAL_SHIFTED = 2
 
-_LOSS = {"squared": LST_LOSS_SQUARED, "spherical": LST_LOSS_SPHERICAL}
+_LOSS = {"squared": LST_LOSS_SQUARED, "spherical": LST_LOSS_SPHERICAL,
+         "spherical_shifted": LST_LOSS_SPHERICAL_SHIFTED}
 
 
 class lst_config(ctypes.Structure):
@@ -92,6 +94,7 @@ _SIGS = {
     "lst_materialize_W": (ctypes.c_int, [_P, _P]),
     "lst_get_state": (ctypes.c_int, [_P, _P, _P, _P]),
     "lst_get_V": (ctypes.c_int, [_P, _P]),
+    "lst_get_shift": (ctypes.c_int, [_P, _P, _P]),
     "lst_touched_rows": (ctypes.c_int, [_P, _P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
     "lst_restore": (ctypes.c_int, [_P]),
     "lst_stabilize": (ctypes.c_int, [_P, ctypes.POINTER(lst_stab_config),
@@ -251,6 +254,13 @@ def lst_get_V(h, V_out):
     import torch
 
     _check(load_library().lst_get_V(h, _ptr(V_out, torch.float32, "V")), "lst_get_V")
+
+
+def lst_get_shift(h, c_out=None, s_out=None):
+    import torch
+
+    _check(load_library().lst_get_shift(h, _ptr(c_out, torch.float32, "c"),
+                                        _ptr(s_out, torch.float32, "s")), "lst_get_shift")
 
 
 def lst_touched_rows(h, capacity: int):
@@ -432,6 +442,14 @@ class FactoredOutputLayer(_Layer):
         V = torch.empty((self.D, self.d), dtype=torch.float32, device=self.device)
         lst_get_V(self._h, V)
         return V
+
+    def get_shift(self):
+        """(c, s) of the shifted spherical loss: W = V U + 1 c^T, s = W^T 1."""
+        import torch
+
+        c, s = (torch.empty(self.d, dtype=torch.float32, device=self.device) for _ in range(2))
+        lst_get_shift(self._h, c, s)
+        return c, s
 
     def touched_rows(self):
         return lst_touched_rows(self._h, self.m_max * self.K_max)

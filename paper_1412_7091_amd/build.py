@@ -19,7 +19,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liblst.so")
 
 SOURCES = ["gemm.hip", "step.hip", "small.hip", "stabilize.hip", "input_layer.hip", "online.hip",
-           "lu.hip", "lst_api.hip"]
+           "lu.hip", "shifted.hip", "lst_api.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -66,6 +66,9 @@ struct lst_state {
   int uit_stale = 0;
   float* Nm = nullptr;  // m_max > 128: m x ldn, N = A C1 A + A C2 B + B C2^T A + B Y^T Y B
   int ldn = 0;
+  // shifted spherical loss: sv = [c | s] (W = V U + 1 c^T, s = W^T 1) and the
+  // per-example [c^T h_i, s^T h_i] of the current step
+  float *sv = nullptr, *nt = nullptr;
   int n_c1p = 0;  // partial sums of h^T Q h per example (two per 32-column tile of H^)
   int n_hap_max = 0;  // partial sums of |H^T H| per row for m = m_max
   // naive workspace
@@ -253,8 +256,10 @@ float* Uitp(lst_state* s) { return s->state + 2 * (size_t)s->d * s->d; }
 
 int check_config(const lst_config* cfg) {
   if (!cfg) return LST_EINVAL;
-  if (cfg->loss != LST_LOSS_SQUARED && cfg->loss != LST_LOSS_SPHERICAL) return LST_EINVAL;
-  if (cfg->loss == LST_LOSS_SPHERICAL && !(cfg->sph_eps > 0.f && isfinite(cfg->sph_eps)))
+  if (cfg->loss != LST_LOSS_SQUARED && cfg->loss != LST_LOSS_SPHERICAL &&
+      cfg->loss != LST_LOSS_SPHERICAL_SHIFTED)
+    return LST_EINVAL;
+  if (cfg->loss != LST_LOSS_SQUARED && !(cfg->sph_eps > 0.f && isfinite(cfg->sph_eps)))
     return LST_EINVAL;
   if (cfg->m_max < 1 || cfg->m_max > 512) return LST_EINVAL;
   if (cfg->K_max < 1 || cfg->K_max > 1024) return LST_EINVAL;
@@ -310,6 +315,20 @@ int vu_product(lst_state* s, hipStream_t st, const float* Vsrc, float* Wdst, con
   return LST_OK;
 }
 
+// Shifted spherical loss: s = W0^T 1 from the D x d W0 (synchronises); other
+// losses keep s = 0.
+int init_column_sums(lst_state* s, const float* W0) {
+  if (s->cfg.loss != LST_LOSS_SPHERICAL_SHIFTED) return LST_OK;
+  float* part = nullptr;
+  if (hipMalloc((void**)&part, (size_t)column_sum_parts(s->D) * s->d * sizeof(float)) !=
+      hipSuccess)
+    return LST_ENOMEM;
+  const bool ok = column_sums(W0, s->D, s->d, part, s->sv + s->d, s->stream) == hipSuccess;
+  const bool synced = hipStreamSynchronize(s->stream) == hipSuccess;
+  (void)hipFree(part);
+  return ok && synced ? LST_OK : LST_EHIP;
+}
+
 int ensure_vtmp(lst_state* s) {
   if (s->Vtmp) return LST_OK;
   return dalloc(s, &s->Vtmp, (size_t)s->D * s->d);
@@ -327,7 +346,7 @@ int check_step_args(lst_state* s, int32_t m, int32_t K, const float* H, const in
   if (m < 1 || m > s->cfg.m_max || K < 1 || K > s->cfg.K_max) return LST_EINVAL;
   if (!H || !Y_idx || !loss || !grad_H) return LST_EINVAL;
   if (s->cfg.loss == LST_LOSS_SQUARED && !Y_val) return LST_EINVAL;
-  if (s->cfg.loss == LST_LOSS_SPHERICAL && K != 1) return LST_EINVAL;
+  if (s->cfg.loss != LST_LOSS_SQUARED && K != 1) return LST_EINVAL;
   if (!(lr > 0.f) || !isfinite(lr)) return LST_EINVAL;
   return LST_OK;
 }
@@ -442,7 +461,8 @@ int enqueue_online(lst_state* s, hipStream_t st, int32_t K, const float* H, cons
 int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float* H,
                  const int32_t* Y_idx, const float* Y_val, float lr, float* loss, float* grad_H,
                  bool scratch = false) {
-  if (!scratch && m == 1 && K <= kOnlineMaxK)
+  const bool shifted = s->cfg.loss == LST_LOSS_SPHERICAL_SHIFTED;
+  if (!scratch && m == 1 && K <= kOnlineMaxK && !shifted)
     return enqueue_online(s, st, K, H, Y_idx, Y_val, lr, loss, grad_H);
   const int d = s->d;
   int* fl = s->flags;
@@ -462,6 +482,10 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
   c.ex_row = s->ex_row; c.ex_val = s->ex_val; c.ex_cnt = s->ex_cnt;
   c.hkey = s->hkey; c.hmin = s->hmin; c.hcnt = s->hcnt; c.hbits = s->hbits;
   c.own = s->own; c.flags = fl; c.solve_ws = s->solve_ws;
+  if (shifted) {
+    c.sv = s->sv;
+    c.nt = s->nt;
+  }
   // rows held by kHotMinSlots or more slots are scattered in launch 4, four
   // waves each, when the step has enough slots for such rows to be worth it
   c.hot_min = (m * K >= 4096) ? kHotMinSlots : 0;
@@ -535,6 +559,8 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     OK_OR_RETURN(run_launch(s, c, L, stages_for(g, m > 128 ? kLaunch2Stages64 : kMaxStages), st,
                             PH_LAUNCH2));
   }
+  // shifted spherical loss: the all-ones terms of grad_H and N
+  if (shifted) HIPCHK(shift_terms(c, m <= 128, st));
   {  // launch 3: grad_H and T ; scatter into V
     StepLaunch L{};
     L.ntask = 2;
@@ -624,6 +650,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
       L.ntask = 1;
     }
     OK_OR_RETURN(run_launch(s, c, L, stages_for(g, launch34_stages(g)), st, PH_LAUNCH4));
+    if (shifted) HIPCHK(shift_update(c, st));
     if (scratch) {
       StepLaunch C{};
       C.ntask = 1;
@@ -787,8 +814,11 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       (rc = dalloc(s, &s->UHa, md)) || (rc = dalloc(s, &s->yyd, m)) ||
       (rc = dalloc(s, &s->c1p, (size_t)m * s->n_c1p)) ||
       (rc = dalloc(s, &s->hap, (size_t)m * s->n_hap_max)) ||
-      (rc = dalloc(s, &s->on_ws, online_workspace_floats(d))))
+      (rc = dalloc(s, &s->on_ws, online_workspace_floats(d))) ||
+      (rc = dalloc(s, &s->sv, 2 * (size_t)d)) || (rc = dalloc(s, &s->nt, 2 * (size_t)m)))
     return fail(rc);
+  if (hipMemsetAsync(s->sv, 0, 2 * (size_t)d * sizeof(float), s->stream) != hipSuccess)
+    return fail(LST_EHIP);
   if (fill_ints(s->hkey, -1, hsize, s->stream) != hipSuccess ||
       fill_ints(s->hmin, 0x7fffffff, hsize, s->stream) != hipSuccess ||
       fill_ints(s->hcnt, 0, hsize + 1, s->stream) != hipSuccess)
@@ -802,6 +832,7 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
         set_identity_if(Uitp(s), d, nullptr, s->stream) != hipSuccess)
       return fail(LST_EHIP);
     if ((rc = gram_splitk(s, s->V, D, d, Qp(s), 1.f))) return fail(rc);
+    if ((rc = init_column_sums(s, s->V))) return fail(rc);
   } else {
     if (hipMemcpyAsync(Up(s), U, (size_t)d * d * sizeof(float), hipMemcpyDeviceToDevice,
                        s->stream) != hipSuccess)
@@ -831,6 +862,7 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       return fail(LST_ENOMEM);
     rc = vu_product(s, s->stream, s->V, vu, nullptr, nullptr);
     if (rc == LST_OK) rc = gram_splitk(s, vu, D, d, Qp(s), 1.f);  // synchronises
+    if (rc == LST_OK) rc = init_column_sums(s, vu);
     if (vu != s->Vtmp) {
       (void)hipStreamSynchronize(s->stream);
       (void)hipFree(vu);
@@ -973,7 +1005,20 @@ int lst_materialize_W(lst_state* s, float* W) {
                           s->stream));
     return LST_OK;
   }
-  return vu_product(s, s->stream, s->V, W, nullptr, nullptr);
+  OK_OR_RETURN(vu_product(s, s->stream, s->V, W, nullptr, nullptr));
+  if (s->cfg.loss == LST_LOSS_SPHERICAL_SHIFTED)
+    HIPCHK(add_row_vector(W, s->D, s->d, s->sv, s->stream));
+  return LST_OK;
+}
+
+int lst_get_shift(lst_state* s, float* c, float* s_out) {
+  if (!s) return LST_EINVAL;
+  if (s->kind != 0 || s->cfg.loss != LST_LOSS_SPHERICAL_SHIFTED) return LST_ESTATE;
+  DeviceGuard dg(s->device);
+  const size_t bytes = (size_t)s->d * sizeof(float);
+  if (c) HIPCHK(hipMemcpyAsync(c, s->sv, bytes, hipMemcpyDeviceToDevice, s->stream));
+  if (s_out) HIPCHK(hipMemcpyAsync(s_out, s->sv + s->d, bytes, hipMemcpyDeviceToDevice, s->stream));
+  return LST_OK;
 }
 
 int lst_get_state(lst_state* s, float* Q, float* U, float* UinvT) {

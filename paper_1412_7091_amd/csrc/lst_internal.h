@@ -145,6 +145,8 @@ __host__ __device__ inline int scatter_slots_per_wave(int slots) {
   return s > 64 ? 64 : s;
 }
 
+// The scalars come first and the pointers after them, so that the struct (a
+// kernel argument of every launch of the step) holds no padding.
 struct StepCtx {
   int m, K, d;
   // rows held by hot_min or more slots (hot_min 0: none) are not scattered by
@@ -154,21 +156,24 @@ struct StepCtx {
   int64_t D;
   int loss_kind;
   float eps, lr;
+  int ld0;            // row stride of Z0
+  int ld_c1p, n_c1p;  // row stride and number of partials per example of c1p
+  int n_hap;          // partials per example of hap
+  int hbits;   // hmin's 2^hbits entries are followed by 2^hbits x kSlotCap more: the
+               // slots of each row, in no particular order (the first kSlotCap of
+               // them; entries past the row's count are stale)
   const float* H;
   const int32_t* idx;
   const float* val;
   float *V, *Q, *U, *Uit;
   float* Z0;   // m x ld0: [H^ | UH | P | H^T H] (rows = examples)
-  int ld0;
   float *G, *Yh;
   float* NP;   // m x 4m: [C1 | C2 | C2^T | Y^T Y] with C1 = H^T H^, C2 = H^T Y^
   float *X, *T;
   float* UHa;         // m x d: a_i (U h_i)^T, the left factor of the U update
   float *aH, *bH;     // m x d: a_i h_i^T and b_i h_i^T
   float* c1p;         // m x ld_c1p: partial sums of h_i^T Q h_i (from launch 1)
-  int ld_c1p, n_c1p;  // row stride and number of partials per example
   float* hap;         // m x n_hap: partial sums of |H^T H| along row i (from launch 1)
-  int n_hap;
   float *a, *b, *cs;  // per example
   float* yyd;         // per example: (Y^T Y)_ii
   float *loss, *grad;
@@ -178,14 +183,16 @@ struct StepCtx {
   int *hkey, *hmin, *hcnt;  // hash table of the step's target rows: smallest slot
                             // and number of slots of each; hcnt's 2^hbits counts
                             // are followed by the hot-row list ([0]: count, then rows)
-  int hbits;   // hmin's 2^hbits entries are followed by 2^hbits x kSlotCap more: the
-               // slots of each row, in no particular order (the first kSlotCap of
-               // them; entries past the row's count are stale)
   int* own;      // m x K: the row of slot i*K + k if that slot owns the row's
                  // scatter in this step (its smallest slot), else -1
   int* flags;
   float* solve_ws;
+  // shifted spherical loss only (else null): sv = [c | s] (2 d floats) with
+  // W = V U + 1 c^T and s = W^T 1; nt = per example [t_i, n_i] = [c^T h_i, s^T h_i]
+  const float* sv;
+  float* nt;
 };
+static_assert(sizeof(StepCtx) == 336, "StepCtx is a kernel argument of every launch: keep it small");
 
 enum TaskKind {
   TK_GEMM = 0, TK_TARGETS, TK_YY, TK_SCALARS, TK_SOLVE, TK_SCATTER, TK_CLEAR
@@ -212,6 +219,20 @@ struct StepLaunch {
 // the kernel's execution.
 // N = A C1 A + A C2 B + B C2^T A + B (Y^T Y) B (A = diag(a), B = diag(b)) into
 // an m x ldn buffer (columns m .. ldn - 1 zero) from NP = [C1 | C2 | C2^T | Y^T Y].
+// The shifted spherical loss (shifted.hip; c.sv = [c | s], W = V U + 1 c^T,
+// s = W^T 1): shift_terms adds its all-ones terms to H^, Y^, C1 and C2 (and
+// C2^T when with_c2t) between launches 2 and 3; shift_update moves c and s
+// after launch 4 (skipped when the step's error flag is set).
+hipError_t shift_terms(const StepCtx& c, bool with_c2t, hipStream_t s);
+hipError_t shift_update(const StepCtx& c, hipStream_t s);
+// out[k] = sum of column k of the rows x cols row-major A, through
+// column_sum_parts(rows) x cols floats of partials in part.
+int column_sum_parts(int64_t rows);
+hipError_t column_sums(const float* A, int64_t rows, int cols, float* part, float* out,
+                       hipStream_t s);
+// A[r][k] += v[k] for every row r of the rows x cols row-major A.
+hipError_t add_row_vector(float* A, int64_t rows, int cols, const float* v, hipStream_t s);
+
 hipError_t form_n(const float* NP, const float* a, const float* b, int m, float* N, int ldn,
                   hipStream_t s);
 hipError_t step_launch(const StepCtx& c, StepLaunch& L, int stages, hipStream_t s,

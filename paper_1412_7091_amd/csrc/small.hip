@@ -230,6 +230,8 @@ hipError_t transpose_square(const float* A, float* At, int d, hipStream_t s) {
 // output row o_i = W h_i (stored in O) into dL/do_i / (2 for squared error):
 //   squared:   O_i <- o_i - y_i,  loss_i = ||o_i - y_i||^2
 //   spherical: O_i <- (2/S) o_i + b e_c,  loss_i = -log(o_c^2+eps) + log S
+//   shifted:   O_i <- (2/S) (o_i + eps) - (2/u_c) e_c, u_c = o_c + eps,
+//              S = sum_j (o_j + eps)^2,  loss_i = -log(u_c^2) + log S
 // Sums run in fp64 in a fixed tree order.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void naive_rowstats_kernel(float* __restrict__ O, int64_t ldo,
@@ -248,7 +250,7 @@ __global__ __launch_bounds__(1024) void naive_rowstats_kernel(float* __restrict_
     for (int k = 0; k < K; ++k) {
       const int r = idx[(size_t)i * K + k];
       const bool bad = (r < -1) || ((int64_t)r >= D) ||
-                       (loss_kind == LST_LOSS_SPHERICAL && r == -1);
+                       (loss_kind != LST_LOSS_SQUARED && r == -1);
       if (bad) {
         atomicCAS(flags + F_ERR, 0, LST_EINDEX);
         continue;
@@ -262,8 +264,13 @@ __global__ __launch_bounds__(1024) void naive_rowstats_kernel(float* __restrict_
     }
   }
   __syncthreads();
+  const bool shifted = loss_kind == LST_LOSS_SPHERICAL_SHIFTED;
+  const double sh = shifted ? (double)eps : 0.0;
   double acc = 0.0;
-  for (int64_t r = threadIdx.x; r < D; r += blockDim.x) acc += (double)o[r] * o[r];
+  for (int64_t r = threadIdx.x; r < D; r += blockDim.x) {
+    const double u = (double)o[r] + sh;
+    acc += u * u;
+  }
   red[threadIdx.x] = acc;
   __syncthreads();
   for (int off = blockDim.x / 2; off > 0; off >>= 1) {
@@ -280,13 +287,13 @@ __global__ __launch_bounds__(1024) void naive_rowstats_kernel(float* __restrict_
     return;
   }
   const int c = s_c;
-  const double S = sumsq + (double)D * eps;
-  const double oc = (c >= 0) ? (double)o[c] : 0.0;
-  const double num = oc * oc + eps;
+  const double S = shifted ? sumsq : sumsq + (double)D * eps;
+  const double oc = (c >= 0) ? (double)o[c] + sh : 0.0;
+  const double num = shifted ? oc * oc : oc * oc + eps;
   const float a = (float)(2.0 / S);
-  const float b = (float)(-2.0 * oc / num);
+  const float b = shifted ? (float)(-2.0 / oc) : (float)(-2.0 * oc / num);
   __syncthreads();  // every thread has read o[c] before it is rescaled
-  for (int64_t r = threadIdx.x; r < D; r += blockDim.x) o[r] *= a;
+  for (int64_t r = threadIdx.x; r < D; r += blockDim.x) o[r] = a * (float)((double)o[r] + sh);
   __syncthreads();
   if (threadIdx.x == 0) {
     if (c >= 0) o[c] += b;

@@ -23,6 +23,12 @@
 // dL/dO = W H A + G: squared error a_i = 2, G = -2 Y; spherical softmax
 // a_i = 2 / S_i, G = Y diag(b_i), S_i = h_i^T Q h_i + D eps,
 // b_i = -2 o_c / (o_c^2 + eps), o_c = h_i^T W^T y_i.  N = (dL/dO)^T dL/dO.
+// The shifted spherical softmax (section 3.6 as printed, u = o + eps) adds
+// eps 1 a^T to dL/dO, with S_i = h_i^T Q h_i + 2 eps n_i + D eps^2 and
+// b_i = -2 / u_c; W = V U + 1 c^T, s = W^T 1, t_i = c^T h_i and n_i = s^T h_i
+// (from the targets task of launch 1).  Its extra terms are added by two small
+// kernels (shifted.hip): to C1, C2, H^ and Y^ between launches 2 and 3, and to
+// c and s after launch 4.
 // Every update of the state (the scatter, launch 4) skips when the step's
 // error flag is set; all checks that can set it run in launches 1 and 2.
 #include <hip/hip_ext.h>
@@ -68,10 +74,18 @@ __device__ __forceinline__ float example_c1(const StepCtx& c, int i) {
   return s;
 }
 
-// a_i of example i (squared error: 2; spherical: 2 / S_i, S_i = c1 + D eps).
+// S_i of the spherical losses from c1 = h_i^T Q h_i: sum_j (o_j^2 + eps) =
+// c1 + D eps, or for the shifted form sum_j (o_j + eps)^2 = c1 + 2 eps n_i + D eps^2.
+__device__ __forceinline__ float example_S(const StepCtx& c, int i, float c1) {
+  if (c.loss_kind == LST_LOSS_SPHERICAL_SHIFTED)
+    return c1 + 2.f * c.eps * c.nt[2 * i + 1] + (float)c.D * c.eps * c.eps;
+  return c1 + (float)c.D * c.eps;
+}
+
+// a_i of example i (squared error: 2; spherical: 2 / S_i).
 __device__ __forceinline__ float example_a(const StepCtx& c, int i) {
   if (c.loss_kind == LST_LOSS_SQUARED) return 2.f;
-  return 2.f / (example_c1(c, i) + (float)c.D * c.eps);
+  return 2.f / example_S(c, i, example_c1(c, i));
 }
 
 // ----------------------------------------------------------------- targets
@@ -175,10 +189,28 @@ __device__ __forceinline__ void task_targets(const StepCtx& c, int local, unsign
   if (i == 0 && lane == 0) multi_rows(c)[0] = 0;  // filled in launch 2, read in launch 3
   LST_TMARK(0);
   const int K = c.K, d = c.d;
+  if (c.loss_kind == LST_LOSS_SPHERICAL_SHIFTED) {  // t_i = c^T h_i, n_i = s^T h_i
+    const float* hr = c.H + (size_t)i * d;
+    float tt = 0.f, nn = 0.f;
+    for (int j = lane; j < d; j += 64) {
+      const float h = hr[j];
+      tt += c.sv[j] * h;
+      nn += c.sv[d + j] * h;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      tt += __shfl_xor(tt, off);
+      nn += __shfl_xor(nn, off);
+    }
+    if (lane == 0) {
+      c.nt[2 * i] = tt;
+      c.nt[2 * i + 1] = nn;
+    }
+  }
   unsigned long long* keys = reinterpret_cast<unsigned long long*>(sraw) + (size_t)w * K;
   float* vals = reinterpret_cast<float*>(sraw + (size_t)4 * K * sizeof(unsigned long long)) +
                 (size_t)w * K;
-  const bool one_hot = c.loss_kind == LST_LOSS_SPHERICAL;
+  const bool one_hot = c.loss_kind != LST_LOSS_SQUARED;
   const int32_t* ix = c.idx + (size_t)i * K;
   int nvalid = 0;
   for (int k0 = 0; k0 < K; k0 += 64) {
@@ -420,6 +452,8 @@ __device__ __forceinline__ void task_yy(const StepCtx& c, int local, unsigned ch
 //   squared:   loss = c1 - 2 c2 + (Y^T Y)_ii (= M_ii, Appendix A step 6), a = 2, b = -2
 //   spherical: loss = -log(c2^2 + eps) + log(c1 + D eps), a = 2/(c1 + D eps),
 //              b = -2 c2 / (c2^2 + eps), cs = b / a (the scatter weight)
+//   shifted:   u_c = c2 + t_i + eps, S = c1 + 2 eps n_i + D eps^2,
+//              loss = log S - 2 log|u_c|, a = 2/S, b = -2/u_c, cs = b / a
 // and the row a (U h)^T of the U update's left factor; also inserts the
 // example's target rows into the hash table that decides the scatter's
 // owners.  Block 0 also counts the step's target pairs and resets the
@@ -475,7 +509,7 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
     }
   }
   const float c1 = example_c1(c, i);
-  const float Si = c1 + (float)c.D * c.eps;
+  const float Si = (c.loss_kind == LST_LOSS_SQUARED) ? 0.f : example_S(c, i, c1);
   const float a = (c.loss_kind == LST_LOSS_SQUARED) ? 2.f : 2.f / Si;
   const float* uh = c.Z0 + (size_t)i * c.ld0 + d;
   const float* gr = c.G + (size_t)i * d;
@@ -506,10 +540,15 @@ __device__ __forceinline__ void task_scalars(const StepCtx& c, int local) {
     L = c1 - 2.f * c2 + c.yyd[i];
     b = -2.f;
     cs = 0.f;
-  } else {
+  } else if (c.loss_kind == LST_LOSS_SPHERICAL) {
     const float num = c2 * c2 + c.eps;
     L = -logf(num) + logf(Si);
     b = -2.f * c2 / num;
+    cs = b / a;
+  } else {
+    const float uc = c2 + c.nt[2 * i] + c.eps;
+    L = logf(Si) - 2.f * logf(fabsf(uc));
+    b = -2.f / uc;
     cs = b / a;
   }
   // a h_i and b h_i: the right factor of the product that gives N H^T
@@ -1617,7 +1656,7 @@ __device__ __forceinline__ void add_x_rows(const StepCtx& c, int cg, unsigned lo
 // The row r held by cnt slots, owned by slot e (hash entry h): the whole wave.
 __device__ __forceinline__ void scatter_row(const StepCtx& c, int r, int h, int cnt, int e) {
   const int lane = lane_id();
-  const bool one_hot = c.loss_kind == LST_LOSS_SPHERICAL;
+  const bool one_hot = c.loss_kind != LST_LOSS_SQUARED;
   const bool listed = cnt <= kSlotCap;
   // listed: lane l < cnt holds the l-th slot of the row in slot order; the
   // first lane of each example's run carries that example and its c_j
@@ -1821,7 +1860,7 @@ __device__ __forceinline__ void task_scatter(const StepCtx& c, int local) {
     const unsigned long long one = __ballot(single);
     if (one) {
       const int i = e / c.K;
-      const float w = single ? (c.loss_kind == LST_LOSS_SPHERICAL ? c.cs[i] : -c.val[e]) : 0.f;
+      const float w = single ? (c.loss_kind != LST_LOSS_SQUARED ? c.cs[i] : -c.val[e]) : 0.f;
       scatter_single(c, one, r, i, w);
     }
     // with one slot per wave every owned row is written here; otherwise the
@@ -1860,7 +1899,7 @@ __device__ __forceinline__ void scatter_hot(const StepCtx& c, int local, int nb,
   const int nch = (c.d + 255) / 256;
   const int items = hot[0] * nch;
   const int wave = wave_id(), lane = lane_id();
-  const bool one_hot = c.loss_kind == LST_LOSS_SPHERICAL;
+  const bool one_hot = c.loss_kind != LST_LOSS_SQUARED;
   const bool vec = (c.d % 4 == 0);
   const int span = (c.m + 3) / 4, jb = wave * span, je = min(c.m, jb + span);
   for (int q = local; q < items; q += nb) {

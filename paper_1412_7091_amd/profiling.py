@@ -37,7 +37,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 REPO = os.path.dirname(PKG)
 PROFILES = os.path.join(REPO, "profiles")
 SOURCES = ["gemm_tile.h", "lst_internal.h", "step.hip", "lst_api.hip", "gemm.hip", "small.hip",
-           "stabilize.hip", "online.hip", "lu.hip"]
+           "stabilize.hip", "online.hip", "lu.hip", "shifted.hip"]
 CALIBRATION_BYTES = 64 << 20  # the benchmark's plain device-to-device copy
 
 
