@@ -65,6 +65,10 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="c2")
+    ap.add_argument("--loss", default=None,
+                    help="override the workload's loss: squared, spherical or spherical_shifted "
+                         "(the (o_c + eps)^2 form; a class-per-example workload, K = 1)")
+    ap.add_argument("--sph-eps", type=float, default=None, help="override the workload's eps")
     ap.add_argument("--naive-steps", type=int, default=10)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -109,6 +113,10 @@ def main():
         sys.exit(1)
     lst.load_library()
     cfg = get_config(args.config)
+    if args.loss is not None and args.loss != cfg.loss:
+        cfg = cfg.replace(loss=args.loss, name=f"{cfg.name}+{args.loss}")
+    if args.sph_eps is not None:
+        cfg = cfg.replace(sph_eps=args.sph_eps, name=f"{cfg.name}+eps{args.sph_eps:g}")
     wl = Workload(cfg)
     dev = torch.device("cuda:0")
     t0 = time.time()

@@ -67,7 +67,7 @@ enum {
                              moves every row of W along the all-ones direction, so a
                              factored state keeps W = V U + 1 c^T and s = W^T 1
                              (lst_get_shift); the minibatch steps then add O(m d) work
-                             and one small launch before and after the update       */
+                             and one small launch between their second and third    */
 };
 
 typedef struct lst_config {

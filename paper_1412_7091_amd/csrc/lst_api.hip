@@ -67,7 +67,7 @@ struct lst_state {
   float* Nm = nullptr;  // m_max > 128: m x ldn, N = A C1 A + A C2 B + B C2^T A + B Y^T Y B
   int ldn = 0;
   // shifted spherical loss: sv = [c | s] (W = V U + 1 c^T, s = W^T 1) and the
-  // per-example [c^T h_i, s^T h_i] of the current step
+  // per-example [c^T h_i, s^T h_i] of the current step, then a copy of [c | s]
   float *sv = nullptr, *nt = nullptr;
   int n_c1p = 0;  // partial sums of h^T Q h per example (two per 32-column tile of H^)
   int n_hap_max = 0;  // partial sums of |H^T H| per row for m = m_max
@@ -559,7 +559,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     OK_OR_RETURN(run_launch(s, c, L, stages_for(g, m > 128 ? kLaunch2Stages64 : kMaxStages), st,
                             PH_LAUNCH2));
   }
-  // shifted spherical loss: the all-ones terms of grad_H and N
+  // shifted spherical loss: the all-ones terms of grad_H and N; c and s move
   if (shifted) HIPCHK(shift_terms(c, m <= 128, st));
   {  // launch 3: grad_H and T ; scatter into V
     StepLaunch L{};
@@ -650,7 +650,6 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
       L.ntask = 1;
     }
     OK_OR_RETURN(run_launch(s, c, L, stages_for(g, launch34_stages(g)), st, PH_LAUNCH4));
-    if (shifted) HIPCHK(shift_update(c, st));
     if (scratch) {
       StepLaunch C{};
       C.ntask = 1;
@@ -815,7 +814,7 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       (rc = dalloc(s, &s->c1p, (size_t)m * s->n_c1p)) ||
       (rc = dalloc(s, &s->hap, (size_t)m * s->n_hap_max)) ||
       (rc = dalloc(s, &s->on_ws, online_workspace_floats(d))) ||
-      (rc = dalloc(s, &s->sv, 2 * (size_t)d)) || (rc = dalloc(s, &s->nt, 2 * (size_t)m)))
+      (rc = dalloc(s, &s->sv, 2 * (size_t)d)) || (rc = dalloc(s, &s->nt, 2 * ((size_t)m + d))))
     return fail(rc);
   if (hipMemsetAsync(s->sv, 0, 2 * (size_t)d * sizeof(float), s->stream) != hipSuccess)
     return fail(LST_EHIP);

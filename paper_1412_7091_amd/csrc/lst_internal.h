@@ -188,7 +188,8 @@ struct StepCtx {
   int* flags;
   float* solve_ws;
   // shifted spherical loss only (else null): sv = [c | s] (2 d floats) with
-  // W = V U + 1 c^T and s = W^T 1; nt = per example [t_i, n_i] = [c^T h_i, s^T h_i]
+  // W = V U + 1 c^T and s = W^T 1; nt = per example [t_i, n_i] = [c^T h_i, s^T h_i],
+  // then a copy of [c | s] as the step found them
   const float* sv;
   float* nt;
 };
@@ -220,11 +221,11 @@ struct StepLaunch {
 // N = A C1 A + A C2 B + B C2^T A + B (Y^T Y) B (A = diag(a), B = diag(b)) into
 // an m x ldn buffer (columns m .. ldn - 1 zero) from NP = [C1 | C2 | C2^T | Y^T Y].
 // The shifted spherical loss (shifted.hip; c.sv = [c | s], W = V U + 1 c^T,
-// s = W^T 1): shift_terms adds its all-ones terms to H^, Y^, C1 and C2 (and
-// C2^T when with_c2t) between launches 2 and 3; shift_update moves c and s
-// after launch 4 (skipped when the step's error flag is set).
+// s = W^T 1): between launches 2 and 3, shift_terms adds its all-ones terms to
+// H^, Y^, C1 and C2 (and C2^T when with_c2t), and moves c and s (skipped when
+// the step's error flag is set).  c.nt holds 2 m + 2 d floats: [t_i, n_i] per
+// example, then the copy of [c | s] the targets task of launch 1 makes.
 hipError_t shift_terms(const StepCtx& c, bool with_c2t, hipStream_t s);
-hipError_t shift_update(const StepCtx& c, hipStream_t s);
 // out[k] = sum of column k of the rows x cols row-major A, through
 // column_sum_parts(rows) x cols floats of partials in part.
 int column_sum_parts(int64_t rows);

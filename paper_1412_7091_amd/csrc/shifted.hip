@@ -14,24 +14,85 @@
 //   s       <- s - lr H (A (n + D eps 1) + b)           (s - lr H (dL/dO)^T 1)
 // while U, U^{-T}, V (with the scatter weight b_i / a_i) and Q (Appendix B,
 // which holds for any dL/dO once grad_H and N are right) move as for the
-// other losses.  shift_terms adds the eps and c terms to H^ = Q H, Y^ and NP
-// between launches 2 and 3; shift_update moves c and s after launch 4.
+// other losses.  shift_terms, between launches 2 and 3, adds the eps and c
+// terms to H^ = Q H, Y^ and NP, and moves c and s: every check that can fail
+// the step has run by then (launches 1 and 2), and no later launch reads them.
 #include "lst_internal.h"
 
 namespace lst {
 
 namespace {
 
-// One block row per example i, one thread per column: H^_i += eps s, Y^_i += c
-// (j < d) and the corrections of C1', C2' (and C2'^T when it is stored) (j < m).
-__global__ __launch_bounds__(256) void shift_terms_kernel(StepCtx c, int with_c2t) {
-  const int i = blockIdx.y;
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+// Blocks [0, nupd): c and s, 16 columns per block, its 16 groups of 16 threads
+// taking every 16th example (eight at a time, loads first), summed in a fixed
+// order (skipped when the step's error flag is set, like every state update of
+// the step).  The other blocks: one 256-wide column chunk of one example's row:
+// H^_i += eps s, Y^_i += c (column < d) and the corrections of C1', C2' (and
+// C2'^T when it is stored) (column < m).  These read the copy of [c | s] the
+// targets task left after nt, not c.sv, which the first blocks move.
+constexpr int kUpdCols = 16;
+constexpr int kUpdGroups = 16;
+
+__global__ __launch_bounds__(256) void shift_terms_kernel(StepCtx c, int with_c2t, int nupd,
+                                                          int chunks) {
   const int m = c.m, d = c.d;
   const float eps = c.eps;
+  if ((int)blockIdx.x < nupd) {
+    if (c.flags[F_ERR] != 0) return;  // the whole block
+    __shared__ float red[2][kUpdGroups][kUpdCols];
+    const int col = threadIdx.x % kUpdCols, g = threadIdx.x / kUpdCols;
+    const int k = blockIdx.x * kUpdCols + col;
+    const float De = (float)c.D * eps;
+    float dc = 0.f, ds = 0.f;
+    if (k < d) {
+      constexpr int U = 8;
+      int i = g;
+      for (; i + (U - 1) * kUpdGroups < m; i += U * kUpdGroups) {
+        float h[U], a[U], b[U], tt[U], nn[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int e = i + u * kUpdGroups;
+          h[u] = c.H[(size_t)e * d + k];
+          a[u] = c.a[e];
+          b[u] = c.b[e];
+          tt[u] = c.nt[2 * e];
+          nn[u] = c.nt[2 * e + 1];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          dc += a[u] * (tt[u] + eps) * h[u];
+          ds += (a[u] * (nn[u] + De) + b[u]) * h[u];
+        }
+      }
+      for (; i < m; i += kUpdGroups) {
+        const float h = c.H[(size_t)i * d + k], a = c.a[i];
+        dc += a * (c.nt[2 * i] + eps) * h;
+        ds += (a * (c.nt[2 * i + 1] + De) + c.b[i]) * h;
+      }
+    }
+    red[0][g][col] = dc;
+    red[1][g][col] = ds;
+    __syncthreads();
+    if (g == 0 && k < d) {
+      float tc = 0.f, ts = 0.f;
+#pragma unroll
+      for (int q = 0; q < kUpdGroups; ++q) {
+        tc += red[0][q][col];
+        ts += red[1][q][col];
+      }
+      float* sv = const_cast<float*>(c.sv);
+      sv[k] -= c.lr * tc;
+      sv[d + k] -= c.lr * ts;
+    }
+    return;
+  }
+  const int q = blockIdx.x - nupd;
+  const int i = q / chunks;
+  const int j = (q - i * chunks) * 256 + threadIdx.x;
+  const float* snap = c.nt + 2 * m;  // [c | s] as the step found them
   if (j < d) {
-    c.Z0[(size_t)i * c.ld0 + j] += eps * c.sv[d + j];
-    c.Yh[(size_t)i * d + j] += c.sv[j];
+    c.Z0[(size_t)i * c.ld0 + j] += eps * snap[d + j];
+    c.Yh[(size_t)i * d + j] += snap[j];
   }
   if (j < m) {
     float* r = c.NP + (size_t)i * 4 * m;
@@ -40,26 +101,6 @@ __global__ __launch_bounds__(256) void shift_terms_kernel(StepCtx c, int with_c2
     r[m + j] += ti + eps;
     if (with_c2t) r[2 * m + j] += c.nt[2 * j] + eps;
   }
-}
-
-// One thread per column k of c and s; the m examples are summed in order.
-// Skips (like every state update of the step) when the error flag is set.
-__global__ __launch_bounds__(256) void shift_update_kernel(StepCtx c) {
-  if (c.flags[F_ERR] != 0) return;
-  const int k = blockIdx.x * blockDim.x + threadIdx.x;
-  const int d = c.d;
-  if (k >= d) return;
-  const float eps = c.eps, De = (float)c.D * eps;
-  float dc = 0.f, ds = 0.f;
-  for (int i = 0; i < c.m; ++i) {
-    const float h = c.H[(size_t)i * d + k];
-    const float a = c.a[i];
-    dc += a * (c.nt[2 * i] + eps) * h;
-    ds += (a * (c.nt[2 * i + 1] + De) + c.b[i]) * h;
-  }
-  float* sv = const_cast<float*>(c.sv);
-  sv[k] -= c.lr * dc;
-  sv[d + k] -= c.lr * ds;
 }
 
 // Partial column sums over row blocks of at least kColRows rows (at most
@@ -108,14 +149,10 @@ __global__ __launch_bounds__(256) void add_row_kernel(float* __restrict__ A, int
 hipError_t shift_terms(const StepCtx& c, bool with_c2t, hipStream_t s) {
   if (c.m < 1 || c.d < 1 || !c.sv || !c.nt) return hipErrorInvalidValue;
   const int w = c.d > c.m ? c.d : c.m;
-  hipLaunchKernelGGL(shift_terms_kernel, dim3((w + 255) / 256, c.m), dim3(256), 0, s, c,
-                     with_c2t ? 1 : 0);
-  return hipGetLastError();
-}
-
-hipError_t shift_update(const StepCtx& c, hipStream_t s) {
-  if (c.m < 1 || c.d < 1 || !c.sv || !c.nt) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(shift_update_kernel, dim3((c.d + 255) / 256), dim3(256), 0, s, c);
+  const int chunks = (w + 255) / 256;
+  const int nupd = (c.d + kUpdCols - 1) / kUpdCols;
+  hipLaunchKernelGGL(shift_terms_kernel, dim3(nupd + chunks * c.m), dim3(256), 0, s, c,
+                     with_c2t ? 1 : 0, nupd, chunks);
   return hipGetLastError();
 }
 

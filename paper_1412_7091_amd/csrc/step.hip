@@ -26,9 +26,9 @@
 // The shifted spherical softmax (section 3.6 as printed, u = o + eps) adds
 // eps 1 a^T to dL/dO, with S_i = h_i^T Q h_i + 2 eps n_i + D eps^2 and
 // b_i = -2 / u_c; W = V U + 1 c^T, s = W^T 1, t_i = c^T h_i and n_i = s^T h_i
-// (from the targets task of launch 1).  Its extra terms are added by two small
-// kernels (shifted.hip): to C1, C2, H^ and Y^ between launches 2 and 3, and to
-// c and s after launch 4.
+// (from the targets task of launch 1, which also copies [c | s] after nt).  A
+// small kernel between launches 2 and 3 (shifted.hip) adds the extra terms to
+// C1, C2, H^ and Y^ from that copy and moves c and s.
 // Every update of the state (the scatter, launch 4) skips when the step's
 // error flag is set; all checks that can set it run in launches 1 and 2.
 #include <hip/hip_ext.h>
@@ -189,13 +189,28 @@ __device__ __forceinline__ void task_targets(const StepCtx& c, int local, unsign
   if (i == 0 && lane == 0) multi_rows(c)[0] = 0;  // filled in launch 2, read in launch 3
   LST_TMARK(0);
   const int K = c.K, d = c.d;
-  if (c.loss_kind == LST_LOSS_SPHERICAL_SHIFTED) {  // t_i = c^T h_i, n_i = s^T h_i
+  if (c.loss_kind == LST_LOSS_SPHERICAL_SHIFTED) {
+    // t_i = c^T h_i, n_i = s^T h_i; and a copy of [c | s] after nt (its 2 m
+    // entries), striped over the examples' waves, which the terms added between
+    // launches 2 and 3 read while the same kernel moves c and s
     const float* hr = c.H + (size_t)i * d;
     float tt = 0.f, nn = 0.f;
-    for (int j = lane; j < d; j += 64) {
-      const float h = hr[j];
-      tt += c.sv[j] * h;
-      nn += c.sv[d + j] * h;
+    for (int j0 = 0; j0 < d; j0 += 512) {
+      float hv[8], cv[8], sv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = min(j0 + lane + 64 * u, d - 1);
+        hv[u] = hr[j];
+        cv[u] = c.sv[j];
+        sv[u] = c.sv[d + j];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (j0 + lane + 64 * u < d) {
+          tt += cv[u] * hv[u];
+          nn += sv[u] * hv[u];
+        }
+      }
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
@@ -206,6 +221,8 @@ __device__ __forceinline__ void task_targets(const StepCtx& c, int local, unsign
       c.nt[2 * i] = tt;
       c.nt[2 * i + 1] = nn;
     }
+    float* snap = c.nt + 2 * c.m;
+    for (int j = 64 * i + lane; j < 2 * d; j += 64 * c.m) snap[j] = c.sv[j];
   }
   unsigned long long* keys = reinterpret_cast<unsigned long long*>(sraw) + (size_t)w * K;
   float* vals = reinterpret_cast<float*>(sraw + (size_t)4 * K * sizeof(unsigned long long)) +

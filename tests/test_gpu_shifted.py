@@ -26,7 +26,7 @@ import torch
 
 from oracle import explicit, factored
 from parity_util import _compare, rel, run_parity
-from synth import Workload, WorkloadConfig
+from synth import CONFIGS, Workload, WorkloadConfig
 from test_gpu_parity import _assert
 
 pytestmark = pytest.mark.gpu
@@ -60,6 +60,17 @@ def test_shifted_minibatch_60_steps(gpu_lib, m, entropy):
     C1 and C2 first."""
     cfg = _cfg(D=4001, d=40, m=m, lr=1e-3, entropy=entropy)
     reports, W_rel, _ = run_parity(cfg, 60, W_every=20, V_check_untouched=True)
+    _assert(reports, W_rel)
+
+
+@pytest.mark.timeout(600)
+def test_shifted_c3_shape_30_steps(gpu_lib):
+    """The full spherical workload (D = 200000, d = 500, m = 128, Zipf(1.0)
+    classes, lr = 1e-3) with the shifted loss at eps = 0.1, four standard
+    deviations of o_c: |u_c| stays above 2e-2 and the fp32 definition within
+    1e-6 (grad) of fp64 over these steps."""
+    cfg = CONFIGS["c3"].replace(loss="spherical_shifted", sph_eps=0.1)
+    reports, W_rel, _ = run_parity(cfg, 30, W_every=10, log_every=5)
     _assert(reports, W_rel)
 
 
