@@ -560,7 +560,8 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
                             PH_LAUNCH2));
   }
   // shifted spherical loss: the all-ones terms of grad_H and N; c and s move
-  if (shifted) HIPCHK(shift_terms(c, m <= 128, st));
+  // (for the solve-from-scratch form after its factorisation, which can fail)
+  if (shifted) HIPCHK(shift_terms(c, m <= 128, true, !scratch, st));
   {  // launch 3: grad_H and T ; scatter into V
     StepLaunch L{};
     L.ntask = 2;
@@ -614,6 +615,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
     OK_OR_RETURN(prof_mark(s, PH_SCRATCH_FACTOR, 1, st));
     OK_OR_RETURN(prof_mark(s, PH_SCRATCH_SOLVE, 0, st));
     HIPCHK(lu_solve_rows(s->lu_F, s->lu_perm, d, H, m, s->lu_Z, s->X, s->a, lr, st));
+    if (shifted) HIPCHK(shift_terms(c, m <= 128, false, true, st));
     OK_OR_RETURN(prof_mark(s, PH_SCRATCH_SOLVE, 1, st));
     StepLaunch L{};
     L.ntask = 1;

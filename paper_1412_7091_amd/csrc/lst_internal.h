@@ -221,11 +221,12 @@ struct StepLaunch {
 // N = A C1 A + A C2 B + B C2^T A + B (Y^T Y) B (A = diag(a), B = diag(b)) into
 // an m x ldn buffer (columns m .. ldn - 1 zero) from NP = [C1 | C2 | C2^T | Y^T Y].
 // The shifted spherical loss (shifted.hip; c.sv = [c | s], W = V U + 1 c^T,
-// s = W^T 1): between launches 2 and 3, shift_terms adds its all-ones terms to
-// H^, Y^, C1 and C2 (and C2^T when with_c2t), and moves c and s (skipped when
-// the step's error flag is set).  c.nt holds 2 m + 2 d floats: [t_i, n_i] per
-// example, then the copy of [c | s] the targets task of launch 1 makes.
-hipError_t shift_terms(const StepCtx& c, bool with_c2t, hipStream_t s);
+// s = W^T 1): after launch 2, shift_terms adds its all-ones terms to H^, Y^,
+// C1 and C2 (and C2^T when with_c2t) when terms is set, and moves c and s when
+// update is set (skipped when the step's error flag is set).  c.nt holds
+// 2 m + 2 d floats: [t_i, n_i] per example, then the copy of [c | s] the
+// targets task of launch 1 makes.
+hipError_t shift_terms(const StepCtx& c, bool with_c2t, bool terms, bool update, hipStream_t s);
 // out[k] = sum of column k of the rows x cols row-major A, through
 // column_sum_parts(rows) x cols floats of partials in part.
 int column_sum_parts(int64_t rows);

@@ -17,6 +17,8 @@
 // other losses.  shift_terms, between launches 2 and 3, adds the eps and c
 // terms to H^ = Q H, Y^ and NP, and moves c and s: every check that can fail
 // the step has run by then (launches 1 and 2), and no later launch reads them.
+// The solve-from-scratch form can still fail later (a zero pivot of U_new),
+// so there c and s move in a second, update-only launch after the factorisation.
 #include "lst_internal.h"
 
 namespace lst {
@@ -146,13 +148,15 @@ __global__ __launch_bounds__(256) void add_row_kernel(float* __restrict__ A, int
 
 }  // namespace
 
-hipError_t shift_terms(const StepCtx& c, bool with_c2t, hipStream_t s) {
+hipError_t shift_terms(const StepCtx& c, bool with_c2t, bool terms, bool update, hipStream_t s) {
   if (c.m < 1 || c.d < 1 || !c.sv || !c.nt) return hipErrorInvalidValue;
   const int w = c.d > c.m ? c.d : c.m;
   const int chunks = (w + 255) / 256;
-  const int nupd = (c.d + kUpdCols - 1) / kUpdCols;
-  hipLaunchKernelGGL(shift_terms_kernel, dim3(nupd + chunks * c.m), dim3(256), 0, s, c,
-                     with_c2t ? 1 : 0, nupd, chunks);
+  const int nupd = update ? (c.d + kUpdCols - 1) / kUpdCols : 0;
+  const int blocks = nupd + (terms ? chunks * c.m : 0);
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(shift_terms_kernel, dim3(blocks), dim3(256), 0, s, c, with_c2t ? 1 : 0,
+                     nupd, chunks);
   return hipGetLastError();
 }
 
