@@ -82,6 +82,24 @@ def test_worked_example_spherical():
                                rtol=1e-14, atol=1e-15)
 
 
+def test_worked_example_shifted():
+    """The hand-derived shifted example (section 3.6 as printed), in rationals."""
+    g = _golden()["shifted"]
+    loss, grad, W_new = explicit.shifted_spherical_step(
+        np.array(g["W"], np.float32), np.array(g["H"], np.float32),
+        np.array(g["idx"], np.int32), g["lr"], g["eps"],
+    )
+    S = Fraction(*g["S_rational"])
+    uc2 = Fraction(*g["uc2_rational"])
+    assert abs(loss[0] - math.log(S / uc2)) < 1e-14
+    want = np.array([float(Fraction(*q)) for q in g["grad_rational"]])
+    np.testing.assert_allclose(grad[0], want, rtol=1e-14, atol=0)
+    h = np.array(g["H"][0], float)
+    dLdo = np.array([float(Fraction(*q)) for q in g["dLdo_rational"]])
+    np.testing.assert_allclose(W_new, np.array(g["W"], float) - g["lr"] * np.outer(dLdo, h),
+                               rtol=1e-14, atol=1e-15)
+
+
 # ---------------------------------------------------------------- closed forms
 def test_identity_weights_closed_form():
     """D = d, W = I: o = h, so L = ||h - y||^2 and grad_h = 2 (h - y)."""
