@@ -462,7 +462,7 @@ int enqueue_step(lst_state* s, hipStream_t st, int32_t m, int32_t K, const float
                  const int32_t* Y_idx, const float* Y_val, float lr, float* loss, float* grad_H,
                  bool scratch = false) {
   const bool shifted = s->cfg.loss == LST_LOSS_SPHERICAL_SHIFTED;
-  if (!scratch && m == 1 && K <= kOnlineMaxK && !shifted)
+  if (!scratch && m == 1 && K <= kOnlineMaxK)
     return enqueue_online(s, st, K, H, Y_idx, Y_val, lr, loss, grad_H);
   const int d = s->d;
   int* fl = s->flags;
@@ -798,7 +798,10 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
   while ((1 << s->hbits) < 2 * m * K) ++s->hbits;
   const int hsize = 1 << s->hbits;
   const size_t md = (size_t)m * d;
-  if ((rc = dalloc(s, &s->state, 3 * (size_t)d * d)) || (rc = dalloc(s, &s->G, md)) ||
+  // [Q; U; U^{-T}] then [c | s] of the shifted loss (the single-example kernels
+  // find c and s right after U^{-T})
+  if ((rc = dalloc(s, &s->state, 3 * (size_t)d * d + 2 * (size_t)d)) ||
+      (rc = dalloc(s, &s->G, md)) ||
       (rc = dalloc(s, &s->Z0, (size_t)m * s->ld0)) || (rc = dalloc(s, &s->Yh, md)) ||
       (rc = dalloc(s, &s->NP, (size_t)4 * m * m)) ||
       (rc = dalloc(s, &s->Nm, m > 128 ? (size_t)m * s->ldn : 0)) || (rc = dalloc(s, &s->aH, md)) ||
@@ -816,8 +819,9 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
       (rc = dalloc(s, &s->c1p, (size_t)m * s->n_c1p)) ||
       (rc = dalloc(s, &s->hap, (size_t)m * s->n_hap_max)) ||
       (rc = dalloc(s, &s->on_ws, online_workspace_floats(d))) ||
-      (rc = dalloc(s, &s->sv, 2 * (size_t)d)) || (rc = dalloc(s, &s->nt, 2 * ((size_t)m + d))))
+      (rc = dalloc(s, &s->nt, 2 * ((size_t)m + d))))
     return fail(rc);
+  s->sv = s->state + 3 * (size_t)d * d;
   if (hipMemsetAsync(s->sv, 0, 2 * (size_t)d * sizeof(float), s->stream) != hipSuccess)
     return fail(LST_EHIP);
   if (fill_ints(s->hkey, -1, hsize, s->stream) != hipSuccess ||

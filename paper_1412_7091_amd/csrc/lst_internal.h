@@ -269,7 +269,9 @@ struct OnlineArgs {
   float* vec;   // 4 x d: the same vectors, finished (d > 1024)
   float* sp;    // 3 x nt: per-slab partials of h^T Q h, h^T h, h^T y^ (d > 1024)
   float* scal;  // [0]: y^T y
-  float* rsum;  // K: summed value of each owning slot
+  float* rsum;  // K: summed value of each owning slot, followed by kOnlineMaxK - K
+                // unused entries and 2 d floats: the copy of [c | s] that launch A
+                // makes for the shifted loss, whose [c | s] follow U^{-T} (Uit + d^2)
   int* own;     // K: the row of slot k if slot k is the row's first, else -1
   int* flags;
   float *loss, *grad;

@@ -9,6 +9,10 @@
 // spherical softmax: a = 2 / S, G = b e_c, b = -2 o_c / (o_c^2 + eps)):
 //   h^ = Q h, y^ = W^T y = U^T (V^T y), c1 = h^T h^, c2 = h^T y^, y^T y;
 //   grad = a h^ + b y^ (squared: b = -2);  N = a^2 c1 + 2 a b c2 + b^2 y^T y;
+// the shifted spherical softmax (W = V U + 1 c^T, s = W^T 1, u = o + eps 1)
+// adds eps s to h^ and c to y^ (so c2 = u_c - eps), with S = c1 + 2 eps s^T h
+// + D eps^2, a = 2 / S, b = -2 / u_c, N = a^2 S + 2 a b u_c + b^2, and moves
+// c -= lr a (c^T h + eps) h, s -= lr (a (s^T h + D eps) + b) h;
 //   T = grad - (lr / 2) N h;  den = 1 - lr a ||h||^2;
 //   Q <- Q - lr (h T^T + T h^T);  U <- U - lr a (U h) h^T;
 //   U^{-T} <- U^{-T} + (lr a / den) (U^{-T} h) h^T          (eq. updateU-T);
@@ -68,13 +72,20 @@ __device__ __forceinline__ float sum_parts(const float* p, size_t stride, int n)
   return s;
 }
 
+// The shifted loss's [c | s] (after U^{-T}) and launch A's copy of them (after
+// the slot sums), which launch B reads while its blocks move c and s.
+__device__ __forceinline__ float* shift_state(const OnlineArgs& a) {
+  return a.Uit + (size_t)a.d * a.d;
+}
+__device__ __forceinline__ float* shift_copy(const OnlineArgs& a) { return a.rsum + kOnlineMaxK; }
+
 // Block 0 of launch A: index checks (LST_EINDEX), and for each slot k whose
 // row no earlier slot holds: own[k] = its row, rsum[k] = the values of all the
 // row's slots added in slot order; other slots own[k] = -1, rsum[k] = 0.
 // Also y^T y, the number of valid pairs and of distinct rows.
 __device__ void online_targets(const OnlineArgs& a, int* skey, float* sval, float* red) {
   const int tid = threadIdx.x, K = a.K;
-  const bool one_hot = a.loss_kind == LST_LOSS_SPHERICAL;
+  const bool one_hot = a.loss_kind != LST_LOSS_SQUARED;
   int r = -1;
   bool valid = false;
   if (tid < K) {
@@ -124,6 +135,11 @@ __global__ __launch_bounds__(256) void online_a_kernel(OnlineArgs a) {
   const int tid = threadIdx.x, d = a.d, K = a.K, nt = a.nt;
   if (blockIdx.x == 0) {
     online_targets(a, skey, sval, &scol[0][0]);
+    if (a.loss_kind == LST_LOSS_SPHERICAL_SHIFTED) {
+      const float* sv = shift_state(a);
+      float* cp = shift_copy(a);
+      for (int j = tid; j < 2 * d; j += 256) cp[j] = sv[j];
+    }
     return;
   }
   const int t = blockIdx.x - 1;
@@ -136,7 +152,7 @@ __global__ __launch_bounds__(256) void online_a_kernel(OnlineArgs a) {
   float tv = 0.f;
   if (tid < K) {
     tr = a.idx[tid];
-    if (a.loss_kind != LST_LOSS_SPHERICAL) tv = a.val[tid];
+    if (a.loss_kind == LST_LOSS_SQUARED) tv = a.val[tid];
   }
   const int i = tid >> 2, q = tid & 3;
   const int row = r0 + i, col0 = c0 + 16 * q;
@@ -166,7 +182,7 @@ __global__ __launch_bounds__(256) void online_a_kernel(OnlineArgs a) {
   if (tid < K) {
     const bool valid = tr >= 0 && (int64_t)tr < a.D;
     skey[tid] = valid ? tr : -1;
-    sval[tid] = valid ? (a.loss_kind == LST_LOSS_SPHERICAL ? 1.f : tv) : 0.f;
+    sval[tid] = valid ? (a.loss_kind != LST_LOSS_SQUARED ? 1.f : tv) : 0.f;
   }
   if (tid < kOnTile) sh[tid] = (c0 + tid < d) ? a.h[c0 + tid] : 0.f;
   __syncthreads();
@@ -256,7 +272,7 @@ __global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
   float* sT = sm;           // h^, then T in place
   float* sY = sm + a.d;     // y^
   float* sH = sm + 2 * a.d;
-  __shared__ float red[3][4];
+  __shared__ float red[5][4];
   __shared__ float su[kOnlineMaxRows], spv[kOnlineMaxRows];
   const int tid = threadIdx.x, d = a.d, nt = a.nt, R = a.rows_per_block;
   const int i0 = blockIdx.x * R;
@@ -308,7 +324,10 @@ __global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
   }
 
   // h^, y^ and the dot products: every block the same, in the same order
-  float c1 = 0.f, hh = 0.f, c2 = 0.f;
+  // (shifted loss: h^ + eps s and y^ + c, and tt = c^T h, nn = s^T h)
+  const bool shifted = a.loss_kind == LST_LOSS_SPHERICAL_SHIFTED;
+  const float* cs = shift_copy(a);
+  float c1 = 0.f, hh = 0.f, c2 = 0.f, tt = 0.f, nn = 0.f;
   if (FUSED) {
     // thread t: entries 4t .. 4t + 3 (d <= 1024); all of its partials are
     // requested before the first is added
@@ -364,11 +383,19 @@ __global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
         const int j = j0 + c;
         if (j < d) {
           const float hv = a.h[j];
-          sT[j] = x[c];
-          sY[j] = y[c];
+          float hx = x[c], yv = y[c];
+          if (shifted) {
+            const float cj = cs[j], sj = cs[d + j];
+            hx += a.eps * sj;
+            yv += cj;
+            tt += hv * cj;
+            nn += hv * sj;
+          }
+          sT[j] = hx;
+          sY[j] = yv;
           sH[j] = hv;
           c1 += hv * x[c];
-          c2 += hv * y[c];
+          c2 += hv * yv;
           hh += hv * hv;
         }
       }
@@ -376,10 +403,16 @@ __global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
     c1 = wave_sum(c1);
     c2 = wave_sum(c2);
     hh = wave_sum(hh);
+    if (shifted) {
+      tt = wave_sum(tt);
+      nn = wave_sum(nn);
+    }
     if ((tid & 63) == 0) {
       red[0][tid >> 6] = c1;
       red[1][tid >> 6] = c2;
       red[2][tid >> 6] = hh;
+      red[3][tid >> 6] = tt;
+      red[4][tid >> 6] = nn;
     }
     if (tid < rows) {
       su[tid] = sum_parts<kOnlineFuseTiles>(on_part(a, PV_U, 0) + i0 + tid, d, nt);
@@ -390,6 +423,8 @@ __global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
     c1 = ((red[0][0] + red[0][1]) + red[0][2]) + red[0][3];
     c2 = ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3];
     hh = ((red[2][0] + red[2][1]) + red[2][2]) + red[2][3];
+    tt = ((red[3][0] + red[3][1]) + red[3][2]) + red[3][3];
+    nn = ((red[4][0] + red[4][1]) + red[4][2]) + red[4][3];
   } else {
     load_v();
     for (int u = 0; u < nt; ++u) {
@@ -399,30 +434,60 @@ __global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
     }
 #pragma unroll 4
     for (int j = tid; j < d; j += 256) {
-      sT[j] = a.vec[(size_t)PV_Q * d + j];
-      sY[j] = a.vec[(size_t)PV_Y * d + j];
-      sH[j] = a.h[j];
+      const float hv = a.h[j];
+      float hx = a.vec[(size_t)PV_Q * d + j], yv = a.vec[(size_t)PV_Y * d + j];
+      if (shifted) {
+        const float cj = cs[j], sj = cs[d + j];
+        hx += a.eps * sj;
+        yv += cj;
+        tt += hv * cj;
+        nn += hv * sj;
+      }
+      sT[j] = hx;
+      sY[j] = yv;
+      sH[j] = hv;
     }
     if (tid < rows) su[tid] = a.vec[(size_t)PV_U * d + i0 + tid];
     else if (tid >= 64 && tid < 64 + rows) spv[tid - 64] = a.vec[(size_t)PV_P * d + i0 + tid - 64];
+    if (shifted) {
+      tt = wave_sum(tt);
+      nn = wave_sum(nn);
+      if ((tid & 63) == 0) {
+        red[3][tid >> 6] = tt;
+        red[4][tid >> 6] = nn;
+      }
+    }
     __syncthreads();
+    if (shifted) {
+      tt = ((red[3][0] + red[3][1]) + red[3][2]) + red[3][3];
+      nn = ((red[4][0] + red[4][1]) + red[4][2]) + red[4][3];
+      c2 += tt;  // h^T (y^ + c)
+    }
   }
 
   const float yy = a.scal[0];
-  float L, av, bv;
+  float L, av, bv, N;
   if (a.loss_kind == LST_LOSS_SQUARED) {
     L = c1 - 2.f * c2 + yy;
     av = 2.f;
     bv = -2.f;
-  } else {
+    N = av * av * c1 + 2.f * av * bv * c2 + bv * bv * yy;
+  } else if (!shifted) {
     const float S = c1 + (float)a.D * a.eps;
     const float num = c2 * c2 + a.eps;
     L = -logf(num) + logf(S);
     av = 2.f / S;
     bv = -2.f * c2 / num;
+    N = av * av * c1 + 2.f * av * bv * c2 + bv * bv * yy;
+  } else {
+    const float S = c1 + 2.f * a.eps * nn + (float)a.D * a.eps * a.eps;
+    const float uc = c2 + a.eps;
+    L = logf(S) - 2.f * logf(fabsf(uc));
+    av = 2.f / S;
+    bv = -2.f / uc;
+    N = av * av * S + 2.f * av * bv * uc + bv * bv * yy;
   }
   const float lr = a.lr;
-  const float N = av * av * c1 + 2.f * av * bv * c2 + bv * bv * yy;
   const float den = 1.f - lr * av * hh;
   int err = 0;
   if (!isfinite(L)) err = LST_ENONFINITE;
@@ -439,6 +504,12 @@ __global__ __launch_bounds__(256) void online_b_kernel(OnlineArgs a) {
   }
   __syncthreads();
   if (err0 != 0 || err != 0) return;
+  if (shifted && tid < rows) {  // this block's entries of c and s
+    float* sv = shift_state(a);
+    const int i = i0 + tid;
+    sv[i] -= lr * av * (tt + a.eps) * sH[i];
+    sv[d + i] -= lr * (av * (nn + (float)a.D * a.eps) + bv) * sH[i];
+  }
 
   // rows i0 .. i0 + rows of Q, U, U^{-T}
   const float cu = lr * av, cp = lr * av / den;
@@ -507,7 +578,7 @@ int online_tiles(int d) { return (d + kOnTile - 1) / kOnTile; }
 
 size_t online_workspace_floats(int d) {
   const size_t nt = (size_t)online_tiles(d);
-  return 4 * nt * d + 4 * (size_t)d + 3 * nt + 4 + kOnlineMaxK;
+  return 4 * nt * d + 4 * (size_t)d + 3 * nt + 4 + kOnlineMaxK + 2 * (size_t)d;
 }
 
 OnlineArgs online_args(int d, float* ws) {

@@ -74,12 +74,38 @@ def test_shifted_c3_shape_30_steps(gpu_lib):
     _assert(reports, W_rel)
 
 
-def test_shifted_single_example(gpu_lib):
-    """m = 1 takes the minibatch launches (the two-launch single-example form
-    has no all-ones terms)."""
-    cfg = _cfg(D=500, d=16, m=1, lr=2e-2, entropy=305)
+@pytest.mark.parametrize("d,entropy", [(16, 305), (37, 312), (1088, 313)])
+def test_shifted_single_example(gpu_lib, d, entropy):
+    """m = 1 takes the two-launch single-example form (Algorithm 1 with the
+    all-ones terms); d = 37 takes its 4-byte loads, d = 1088 (17 tiles a side)
+    the extra launch that finishes the partial sums."""
+    cfg = _cfg(D=500, d=d, m=1, lr=2e-2 if d < 1000 else 2e-3, entropy=entropy)
     reports, W_rel, _ = run_parity(cfg, 30)
     _assert(reports, W_rel)
+
+
+def test_shifted_single_example_c_and_s(gpu_lib):
+    """c and s of the single-example form against the factored oracle, and the
+    single-example step against the minibatch launches (lst_step_solve takes
+    those at m = 1 too): the same loss, gradient and state within 1e-5."""
+    import paper_1412_7091_amd as lst
+
+    cfg = _cfg(D=700, d=48, m=1, lr=1e-2, sph_eps=0.3, entropy=314)
+    wl = Workload(cfg)
+    dev = torch.device("cuda:0")
+    V0 = wl.init_V()
+    layer = lst.FactoredOutputLayer(torch.from_numpy(V0).to(dev), loss=cfg.loss,
+                                    sph_eps=cfg.sph_eps, m_max=1, K_max=1)
+    st = factored.FactoredState.from_initial(V0)
+    for s in range(20):
+        H, idx, val = wl.batch(s)
+        layer.step(*(torch.from_numpy(x).to(dev) for x in (H, idx, val)), cfg.lr)
+        assert layer.sync() == 0
+        factored.shifted_spherical_minibatch_step(st, H, idx, cfg.lr, cfg.sph_eps)
+        c_g, s_g = (x.cpu().numpy() for x in layer.get_shift())
+        assert rel(c_g, st.c) <= 1e-4 and rel(s_g, st.s) <= 1e-4, (s, rel(c_g, st.c), rel(s_g, st.s))
+    Q, U, Uit = (x.cpu().numpy() for x in layer.get_state())
+    assert rel(Q, st.Q) <= 1e-4 and rel(U, st.U) <= 1e-4 and rel(Uit, st.UinvT) <= 1e-4
 
 
 def test_shifted_solve_from_scratch(gpu_lib):
