@@ -124,9 +124,8 @@ int lst_init(lst_state** out, int64_t D, int32_t d, const float* V, const float*
  * Never forms W H.  State is updated in place unless the sticky error flag is set.
  * With m == 1 and K <= 256 the step takes the single-example form of
  * Algorithm 1 (Sherman-Morrison update of U^{-T}, eq. updateU-T) in two
- * launches (not for LST_LOSS_SPHERICAL_SHIFTED, which always takes the
- * minibatch steps); otherwise the minibatch steps of Appendix A.  Both compute
- * the same update in exact arithmetic, with the same error behaviour.
+ * launches; otherwise the minibatch steps of Appendix A.  Both compute the
+ * same update in exact arithmetic, with the same error behaviour.
  */
 int lst_step(lst_state* s, int32_t m, int32_t K, const float* H, const int32_t* Y_idx,
              const float* Y_val, float lr, float* loss, float* grad_H);
