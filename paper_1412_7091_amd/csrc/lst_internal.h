@@ -190,7 +190,7 @@ struct StepCtx {
   // shifted spherical loss only (else null): sv = [c | s] (2 d floats) with
   // W = V U + 1 c^T and s = W^T 1; nt = per example [t_i, n_i] = [c^T h_i, s^T h_i],
   // then a copy of [c | s] as the step found them
-  const float* sv;
+  float* sv;
   float* nt;
 };
 static_assert(sizeof(StepCtx) == 336, "StepCtx is a kernel argument of every launch: keep it small");

@@ -82,9 +82,8 @@ __global__ __launch_bounds__(256) void shift_terms_kernel(StepCtx c, int with_c2
         tc += red[0][q][col];
         ts += red[1][q][col];
       }
-      float* sv = const_cast<float*>(c.sv);
-      sv[k] -= c.lr * tc;
-      sv[d + k] -= c.lr * ts;
+      c.sv[k] -= c.lr * tc;
+      c.sv[d + k] -= c.lr * ts;
     }
     return;
   }
