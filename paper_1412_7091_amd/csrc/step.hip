@@ -2117,6 +2117,17 @@ template <bool SMALLM, int W, int LK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SMALLM || LK != 2 ? 1 : 2)))
 void step_kernel(StepCtx c, StepLaunch L) {
   extern __shared__ __attribute__((aligned(16))) unsigned char sraw[];
+  // A GEMM block's decoding reads the task table, then the GEMM header, then
+  // its problem's descriptor: each a kernel-argument line that the one before
+  // selects.  One word of every line it may read is requested up front, so the
+  // lines arrive in one round trip rather than one after another (c2 -0.5 us
+  // per step; the longer tiles of the m > 128 kernels gain nothing from it).
+  if constexpr (SMALLM && ((launch_masks(LK, SMALLM).tasks >> TK_GEMM) & 1u)) {
+    asm volatile("" ::"s"(L.ntask), "s"(L.gemm.np), "s"(L.gemm.x.e1), "s"(L.gemm.x.lde1),
+                 "s"(L.gemm.p[0].M), "s"(L.gemm.p[0].A.ld[0]), "s"(L.gemm.p[0].C),
+                 "s"(L.gemm.p[1].M), "s"(L.gemm.p[1].A.ld[0]), "s"(L.gemm.p[1].C),
+                 "s"(L.gemm.p[2].M), "s"(L.gemm.p[2].A.ld[0]), "s"(L.gemm.p[2].C));
+  }
   const int blk = blockIdx.x;
   int t = 0;
   while (t + 1 < L.ntask && blk >= L.begin[t + 1]) ++t;
