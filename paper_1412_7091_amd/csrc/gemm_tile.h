@@ -394,6 +394,12 @@ enum : unsigned { V_NT = 2, V_NN = 4, V_TN = 8 };
 // EPI_STORE can produce (GemmProblem::dotp, GemmProblem::absp); kernels
 // without it compile neither.
 constexpr unsigned EPX_ROWSUMS = 8;
+// Epilogue-mask bit of kernels whose GEMM blocks test the batch's skip_if flag
+// only before their epilogue (they read their operands either way): the
+// flag's load, which needs the descriptor's pointer first, then overlaps the
+// operand fetch instead of preceding it.  Without it the caller tests the
+// flag before the tile starts.
+constexpr unsigned EPX_LATE_SKIP = 9;
 
 // P.epi == e, folded away when the instantiation does not support e.
 template <unsigned EPIS>
@@ -414,6 +420,8 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   constexpr bool kRowSums = (EPIS >> EPX_ROWSUMS) & 1u;
+  constexpr bool kLateSkip = (EPIS >> EPX_LATE_SKIP) & 1u;
+  const int skip = (kLateSkip && bt.skip_if != nullptr) ? *bt.skip_if : 0;
   const bool dot = kRowSums && X.dotp != nullptr && n0 < X.dot_ncols;
   const bool absr = kRowSums && X.absp != nullptr && n0 + T > X.abs_col0;
   LST_MARK(0);
@@ -523,6 +531,7 @@ __device__ __forceinline__ void panel_run(const GemmBatch& bt, const GemmProblem
       for (int r = 0; r < 4; ++r) asm volatile("" ::"v"(pre1[i][j][r]), "v"(pre2[i][j][r]));
 
   LST_MARK(3);
+  if (kLateSkip && skip != 0) return;  // nothing is written
   // EPI_SCALED: the power-of-two scale from the trace of the previous product
   // (exact, so the vector the products converge to does not depend on it).
   float pscale = 1.f, tsum = 0.f;

@@ -2048,14 +2048,14 @@ constexpr LaunchMasks kLaunchMasks[8] = {
     {(1u << TK_GEMM) | (1u << TK_SOLVE) | (1u << TK_YY) | (1u << TK_SCALARS), V_NN | V_NT,
      (1u << EPI_STORE) | (1u << EPI_STORE_T), TILE32},
     {(1u << TK_GEMM) | (1u << TK_SCATTER), V_NN, 1u << EPI_GRADT, TILE32},
-    {(1u << TK_GEMM) | (1u << TK_CLEAR), V_TN, (1u << EPI_SYM) | (1u << EPI_STORE),
-     TILE32 | TILE64},
+    {(1u << TK_GEMM) | (1u << TK_CLEAR), V_TN,
+     (1u << EPI_SYM) | (1u << EPI_STORE) | (1u << EPX_LATE_SKIP), TILE32 | TILE64},
     // the d x d products of the Appendix C stabilisation
     {1u << TK_GEMM, V_NT | V_NN, 1u << EPI_SCALED, TILE32},
     // launches 3 and 4 of a step whose hot rows are scattered in launch 4
     {(1u << TK_GEMM) | (1u << TK_SCATTER), V_NN, 1u << EPI_GRADT, TILE32, true},
-    {(1u << TK_GEMM) | (1u << TK_CLEAR), V_TN, (1u << EPI_SYM) | (1u << EPI_STORE),
-     TILE32 | TILE64, true},
+    {(1u << TK_GEMM) | (1u << TK_CLEAR), V_TN,
+     (1u << EPI_SYM) | (1u << EPI_STORE) | (1u << EPX_LATE_SKIP), TILE32 | TILE64, true},
 };
 
 // The kernels of launches 1 and 2 built for m > 128 also compile 64 x 64
@@ -2082,7 +2082,9 @@ __device__ __forceinline__ void run_task(const StepCtx& c, const StepLaunch& L, 
   const int kind = L.kind[t];
   if constexpr ((M.tasks >> TK_GEMM) & 1u) {
     if (kind == TK_GEMM) {
-      if (L.gemm.skip_if && *L.gemm.skip_if) return;
+      if constexpr (!((M.epis >> EPX_LATE_SKIP) & 1u)) {
+        if (L.gemm.skip_if && *L.gemm.skip_if) return;
+      }
       panel_tile<M.tiles, W, M.vars, M.epis>(L.gemm, local, reinterpret_cast<float*>(sraw));
       return;
     }
