@@ -74,6 +74,45 @@ def test_shifted_c3_shape_30_steps(gpu_lib):
     _assert(reports, W_rel)
 
 
+def test_shifted_unaligned(gpu_lib):
+    """m = 150 (not a multiple of 4, N formed first) and d = 37 (4-byte loads
+    and DMA): the all-ones terms on ragged shapes."""
+    cfg = _cfg(D=2500, d=37, m=150, lr=2e-3, entropy=315)
+    reports, W_rel, _ = run_parity(cfg, 20, W_every=10, V_check_untouched=True)
+    _assert(reports, W_rel)
+
+
+def test_shifted_with_restores(gpu_lib):
+    """The pristine restore (V <- V U, U <- I) every third step: c and s stay
+    bitwise, W = V U + 1 c^T is kept, and the steps after it follow the oracle."""
+    import paper_1412_7091_amd as lst
+
+    cfg = _cfg(D=1200, d=24, m=16, lr=1e-2, entropy=316)
+    wl = Workload(cfg)
+    dev = torch.device("cuda:0")
+    V0 = wl.init_V()
+    layer = lst.FactoredOutputLayer(torch.from_numpy(V0).to(dev), loss=cfg.loss,
+                                    sph_eps=cfg.sph_eps, m_max=cfg.m, K_max=1)
+    W_ref = V0.astype(np.float64)
+    for s in range(15):
+        H, idx, val = wl.batch(s)
+        loss_t, grad_t = layer.step(*(torch.from_numpy(x).to(dev) for x in (H, idx, val)), cfg.lr)
+        assert layer.sync() == 0
+        loss_r, grad_r, W_ref = explicit.shifted_spherical_step(W_ref, H, idx, cfg.lr, cfg.sph_eps)
+        assert rel(loss_t.cpu().numpy(), loss_r) <= 1e-4 and rel(grad_t.cpu().numpy(), grad_r) <= 1e-4
+        if s % 3 == 2:
+            before = [x.clone() for x in layer.get_shift()]
+            W_before = layer.materialize_W().cpu().numpy()
+            layer.restore()
+            assert layer.sync() == 0
+            for x, y in zip(before, layer.get_shift()):
+                assert torch.equal(x, y)
+            assert rel(layer.materialize_W().cpu().numpy(), W_before) <= 1e-5
+            _, U, Uit = layer.get_state()
+            assert torch.equal(U, torch.eye(cfg.d, device=dev)) and torch.equal(Uit, U)
+    assert rel(layer.materialize_W().cpu().numpy(), W_ref) <= 1e-3
+
+
 @pytest.mark.parametrize("d,entropy", [(16, 305), (37, 312), (1088, 313)])
 def test_shifted_single_example(gpu_lib, d, entropy):
     """m = 1 takes the two-launch single-example form (Algorithm 1 with the
